@@ -1,0 +1,161 @@
+"""Logical per-layer expert cache of the prefetcher (Sec. "Coordination of
+Prefetching and Inference": Alg. 1 prefetch worker, Alg. 2 PushPredictedExperts
+/ PushPreciseExperts, "Reordered Inference"; Sec. "Cache Implementation":
+a standard per-layer LRU in which both prefetch and inference count as
+accesses, and prefetching touches experts that are already cached).
+
+Deterministic reading.  The paper replaces a slot when the worker copies an
+expert's first chunk and counts a hit only once a chunk has arrived; both
+depend on copy timing.  Here the *logical* state (slot assignment, LRU order,
+counters) changes in program order when a plan is made; the physical copies
+follow.  Any slot-assigned expert counts as resident.
+
+State of one layer: slot_expert[C] (-1 free), slot_of[E], stamp[C] from a
+per-layer clock, fetch_seq[C] (order in which slots were (re)filled),
+spec_unused[C] (filled by a prediction and not yet used).
+Warm start: experts 0..C-1 in slots 0..C-1, stamp = slot index, fetch_seq 0.
+
+spec_plan(Q)      -- PushPredictedExperts: for e in Q order, touch it if
+                     resident; else take the lowest free slot or the least
+                     recently stamped one, evict, assign, mark speculative and
+                     queue its three chunks at low priority.
+precise_plan(P)   -- PushPreciseExperts: P = the distinct experts the layer's
+                     tokens chose, ascending.  Low-priority work of the layer is
+                     dropped (physical only).  Order = resident experts by
+                     (fetch_seq, id) ascending -- earliest filled first, which on
+                     one FIFO copy queue is the most-complete-first order of the
+                     paper's sort by ready chunks -- followed by the missing
+                     experts in id order.  Resident ones are touched (hits);
+                     missing ones get a victim slot exactly as above (misses) and
+                     are queued at high priority.  A victim that is itself an
+                     earlier member of this order must finish computing before
+                     its slot is overwritten: its position is recorded as
+                     ``after``.
+"""
+from dataclasses import dataclass
+
+COUNTERS = ("prec_access", "hit", "miss", "spec_issued", "spec_resident", "spec_used", "spec_wasted", "evict")
+
+
+@dataclass
+class SpecEntry:
+    expert: int
+    slot: int
+    new: bool
+    victim: int          # expert evicted (-1 none)
+
+
+@dataclass
+class PreciseEntry:
+    expert: int
+    slot: int            # slot this position computes from
+    miss: bool
+    victim: int          # expert evicted for a miss (-1 none)
+    after: int           # position in the order whose compute must precede the fill (-1 none)
+
+
+class LayerCache:
+    def __init__(self, n_experts: int, slots: int, warm: bool = True):
+        self.E, self.C = n_experts, slots
+        self.slot_expert = [-1] * slots
+        self.slot_of = [-1] * n_experts
+        self.stamp = [0] * slots
+        self.fetch_seq = [0] * slots
+        self.spec_unused = [False] * slots
+        self.clock = slots - 1
+        self.fseq = 0
+        self.count = {c: 0 for c in COUNTERS}
+        if warm:
+            for s in range(min(slots, n_experts)):
+                self.slot_expert[s] = s
+                self.slot_of[s] = s
+                self.stamp[s] = s
+
+    # -- helpers
+    def _victim(self) -> int:
+        for s in range(self.C):
+            if self.slot_expert[s] < 0:
+                return s
+        return min(range(self.C), key=lambda s: self.stamp[s])
+
+    def _evict(self, s: int) -> int:
+        v = self.slot_expert[s]
+        if v >= 0:
+            self.count["evict"] += 1
+            if self.spec_unused[s]:
+                self.count["spec_wasted"] += 1
+            self.slot_of[v] = -1
+            self.slot_expert[s] = -1
+        return v
+
+    def _touch(self, s: int) -> None:
+        self.clock += 1
+        self.stamp[s] = self.clock
+
+    def _fill(self, e: int, s: int, speculative: bool) -> None:
+        self.slot_expert[s] = e
+        self.slot_of[e] = s
+        self.fseq += 1
+        self.fetch_seq[s] = self.fseq
+        self.spec_unused[s] = speculative
+        self._touch(s)
+
+    # -- plans
+    def spec_plan(self, Q):
+        out = []
+        for e in Q:
+            e = int(e)
+            s = self.slot_of[e]
+            if s >= 0:
+                self._touch(s)
+                self.count["spec_resident"] += 1
+                out.append(SpecEntry(e, s, False, -1))
+            else:
+                s = self._victim()
+                v = self._evict(s)
+                self._fill(e, s, True)
+                self.count["spec_issued"] += 1
+                out.append(SpecEntry(e, s, True, v))
+        return out
+
+    def precise_plan(self, P):
+        P = sorted(set(int(e) for e in P))
+        hits = [e for e in P if self.slot_of[e] >= 0]
+        missing = [e for e in P if self.slot_of[e] < 0]
+        hits.sort(key=lambda e: (self.fetch_seq[self.slot_of[e]], e))
+        order = hits + missing
+        pos_of = {e: i for i, e in enumerate(order)}
+        entries = []
+        for e in hits:
+            s = self.slot_of[e]
+            self._touch(s)
+            self.count["hit"] += 1
+            if self.spec_unused[s]:
+                self.count["spec_used"] += 1
+                self.spec_unused[s] = False
+            entries.append(PreciseEntry(e, s, False, -1, -1))
+        for e in missing:
+            s = self._victim()
+            v = self._evict(s)
+            self._fill(e, s, False)
+            self.count["miss"] += 1
+            entries.append(PreciseEntry(e, s, True, v, pos_of.get(v, -1) if v >= 0 else -1))
+        self.count["prec_access"] += len(P)
+        return order, entries
+
+    def resident(self):
+        return {e for e in self.slot_expert if e >= 0}
+
+
+class Cache:
+    """One LayerCache per layer (layers are independent)."""
+
+    def __init__(self, n_layers: int, n_experts: int, slots: int, warm: bool = True):
+        self.layers = [LayerCache(n_experts, slots, warm) for _ in range(n_layers)]
+
+    def totals(self):
+        t = {c: 0 for c in COUNTERS}
+        for lc in self.layers:
+            for c in COUNTERS:
+                t[c] += lc.count[c]
+        return t

@@ -1,0 +1,151 @@
+"""Pins of the oracle's logical cache: the paper's worked example, exhaustive
+replay against an independent log-scanning LRU, invariants and closed forms."""
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+
+from oracle import brute, cache
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def test_paper_worked_example_reorder():
+    g = json.load(open(os.path.join(HERE, "golden", "worked_example_reorder.json")))
+    lc = cache.LayerCache(g["n_experts"], g["slots"], warm=g["warm"])
+    lc.spec_plan(g["prefetched"])
+    order, entries = lc.precise_plan(g["gate_selects"])
+    assert order == g["expected_order"]
+    assert [e.expert for e in entries if e.miss] == g["expected_misses"]
+    assert lc.count["miss"] == 1 and lc.count["hit"] == 3
+    # expert 3 was prefetched but not used: it is the LRU victim of the miss
+    assert entries[-1].victim == 3 and lc.count["spec_wasted"] == 1 and lc.count["spec_used"] == 3
+
+
+def _check_invariants(lc):
+    res = [e for e in lc.slot_expert if e >= 0]
+    assert len(res) == len(set(res)) <= lc.C
+    for s, e in enumerate(lc.slot_expert):
+        if e >= 0:
+            assert lc.slot_of[e] == s
+    for e, s in enumerate(lc.slot_of):
+        if s >= 0:
+            assert lc.slot_expert[s] == e
+    c = lc.count
+    assert c["hit"] + c["miss"] == c["prec_access"]
+    assert c["spec_used"] + c["spec_wasted"] <= c["spec_issued"]
+
+
+def _plans(E, C):
+    out = []
+    for n in range(1, E + 1):
+        for P in itertools.combinations(range(E), n):
+            out.append(("P", list(P)))
+    for n in range(1, min(C, E) + 1):
+        for Q in itertools.permutations(range(E), n):
+            out.append(("Q", list(Q)))
+    return out
+
+
+def _replay(seq, E, C, warm=True):
+    a = cache.LayerCache(E, C, warm)
+    b = brute.NaiveLRU(E, C, warm)
+    for kind, lst in seq:
+        if kind == "Q":
+            ea = a.spec_plan(lst)
+            eb = b.spec(lst)
+            assert [(x.expert, x.slot, x.new) for x in ea] == eb
+        else:
+            order, entries = a.precise_plan(lst)
+            ob, sb = b.precise(lst)
+            assert order == ob
+            assert [x.slot for x in entries] == sb
+            # the `after` dependency names the earlier position whose slot is reused
+            for i, x in enumerate(entries):
+                if x.after >= 0:
+                    assert x.after < i and order[x.after] == x.victim and entries[x.after].slot == x.slot
+                elif x.miss and x.victim >= 0:
+                    assert x.victim not in order
+        _check_invariants(a)
+        assert a.count == b.c
+        assert {e: s for e, s in enumerate(a.slot_of) if s >= 0} == b.where
+
+
+@pytest.mark.parametrize("C", [1, 2, 3])
+def test_exhaustive_replay_up_to_three_plans(C):
+    E = 4
+    plans = _plans(E, C)
+    for n in (1, 2, 3):
+        for seq in itertools.product(plans, repeat=n):
+            _replay(seq, E, C)
+
+
+def test_random_long_replays():
+    rng = np.random.default_rng(11)
+    for trial in range(300):
+        E = int(rng.integers(2, 9))
+        C = int(rng.integers(1, E + 2))
+        warm = bool(rng.integers(0, 2))
+        plans = []
+        for _ in range(int(rng.integers(1, 16))):
+            if rng.random() < 0.5:
+                plans.append(("P", list(rng.choice(E, size=int(rng.integers(1, E + 1)), replace=False))))
+            else:
+                plans.append(("Q", list(rng.choice(E, size=int(rng.integers(1, min(C, E) + 1)), replace=False))))
+        _replay(plans, E, C, warm)
+
+
+def test_capacity_at_least_e_misses_once():
+    rng = np.random.default_rng(2)
+    E, C = 6, 8
+    lc = cache.LayerCache(E, C, warm=True)          # warm set 0..5 = everything
+    for _ in range(50):
+        lc.precise_plan(rng.choice(E, 3, replace=False))
+    assert lc.count["miss"] == 0
+    lc = cache.LayerCache(8, 8, warm=False)
+    seen = set()
+    for _ in range(50):
+        P = set(rng.choice(8, 3, replace=False).tolist())
+        lc.precise_plan(P)
+        seen |= P
+    assert lc.count["miss"] == len(seen)
+
+
+def test_perfect_predictor_gives_no_misses():
+    rng = np.random.default_rng(3)
+    E, C, k = 16, 6, 4
+    lc = cache.LayerCache(E, C)
+    for _ in range(100):
+        P = sorted(rng.choice(E, k, replace=False).tolist())
+        lc.spec_plan(P)              # |Q| = k <= C, exactly the routed experts
+        order, entries = lc.precise_plan(P)
+        assert not any(x.miss for x in entries)
+    assert lc.count["miss"] == 0 and lc.count["spec_used"] == lc.count["spec_issued"]
+
+
+def test_lru_inclusion_property_demand_only():
+    # pure LRU with one access per plan: misses(C+1) <= misses(C)
+    rng = np.random.default_rng(4)
+    E = 10
+    for trial in range(50):
+        seq = rng.integers(0, E, size=200)
+        prev = None
+        for C in range(1, E + 1):
+            lc = cache.LayerCache(E, C, warm=False)
+            for e in seq:
+                lc.precise_plan([int(e)])
+            m = lc.count["miss"]
+            if prev is not None:
+                assert m <= prev
+            prev = m
+
+
+def test_streaming_more_experts_than_slots():
+    lc = cache.LayerCache(8, 2, warm=True)
+    order, entries = lc.precise_plan(range(8))
+    assert order == list(range(8))
+    assert [x.slot for x in entries] == [0, 1, 0, 1, 0, 1, 0, 1]
+    assert [x.after for x in entries] == [-1, -1, 0, 1, 2, 3, 4, 5]
+    assert lc.count["miss"] == 6 and lc.count["hit"] == 2
