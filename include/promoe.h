@@ -1,0 +1,237 @@
+/*
+ * promoe.h -- C ABI of an MI355X (gfx950) proactive expert cache for
+ * Mixture-of-Experts inference, after ProMoE (arXiv 2410.22134, "ProMoE: Fast
+ * MoE-based LLM Serving using Proactive Caching").
+ *
+ * One MoE layer step is   promoe_predict (optional)
+ *                      -> promoe_route
+ *                      -> promoe_expert_ffn
+ * on one stream.  The predictor of layer l scores the experts of layer
+ * l+lookahead and queues their missing chunks as low-priority copies (the
+ * paper's PushPredictedExperts, Alg. 2); the route call gates layer l, drops
+ * the layer's remaining low-priority work, queues its missing experts at high
+ * priority and returns the reordered expert list (PushPreciseExperts, Alg. 2,
+ * "Early Preemption", "Reordered Inference"); the FFN call computes the experts
+ * in that order, each waiting only for its own chunks (the dependency
+ * mechanism of Sec. "System Integration").
+ *
+ * Conventions
+ *  - Every call returns an int: 0 (PROMOE_OK) or a negative promoe_err.
+ *    No C++ exception crosses this boundary.
+ *  - d_* arguments are device pointers, h_* host pointers; a `stream`
+ *    argument is a hipStream_t passed as void* (NULL = the null stream).
+ *  - Matrices are row-major with the reduction dimension contiguous.
+ *    Element type is the config dtype: fp32, or bf16 (raw 16-bit words).
+ *  - A routed expert is stored as [Wg (I x H) | Wu (I x H) | Wd (H x I)],
+ *    3*I*H elements, in pinned host memory and in cache slots alike; the three
+ *    matrices are the expert's three copy chunks (Sec. "Chunked Prefetching").
+ *  - Ownership: the caller owns every d_* / h_* buffer, the cache region and
+ *    the streams; buffers given to set_* calls must outlive the context.  The
+ *    library owns its copy stream, events, worker thread, slot tables,
+ *    counters and scratch buffers (allocated in promoe_create).
+ *  - One context per GPU; calls on a context come from one host thread.
+ *    Asynchronous kernel faults surface as PROMOE_EHIP at the next call that
+ *    synchronises.
+ */
+#ifndef PROMOE_H
+#define PROMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct promoe_ctx promoe_ctx;
+
+typedef enum {
+  PROMOE_OK = 0,
+  PROMOE_EINVAL = -1,  /* bad argument: null pointer, index or size out of range */
+  PROMOE_ENOMEM = -2,  /* a library allocation failed */
+  PROMOE_EHIP = -3,    /* a HIP runtime call failed (see promoe_last_error_string) */
+  PROMOE_ESTATE = -4,  /* call order violated (e.g. expert_ffn without route) */
+  PROMOE_EUNSUP = -5   /* shape outside what the kernels support */
+} promoe_err;
+
+enum { PROMOE_F32 = 0, PROMOE_BF16 = 1 };
+enum { PROMOE_PRIO_LOW = 0, PROMOE_PRIO_HIGH = 1 };
+
+/* flags */
+#define PROMOE_FLAG_PROFILE 1      /* time FFN / GEMM launches and copy stalls with HIP events */
+#define PROMOE_FLAG_NO_PREFETCH 2  /* predictions update nothing: reactive LRU baseline */
+
+typedef struct promoe_config {
+  int32_t n_layers;          /* L */
+  int32_t hidden;            /* H, multiple of 8 */
+  int32_t n_experts;         /* E routed experts per layer, 1..64 */
+  int32_t top_k;             /* k, 1..min(E, 8) */
+  int32_t inter;             /* I of a routed expert, multiple of 8 */
+  int32_t shared_inter;      /* total I of the resident shared expert(s); 0 = none.
+                                Several shared experts are passed as one: gate/up rows
+                                stacked, down columns stacked. */
+  int32_t shared_gate;       /* 0: shared output weight 1; 1: sigmoid(w_sg . x) */
+  int32_t renorm;            /* 1: renormalise the top-k gate weights to sum 1 */
+  int32_t router_bias;       /* 1: an fp32 per-expert bias is added to the gate logits */
+  int32_t slots_per_layer;   /* C cache slots per layer, 1..64 */
+  int32_t lookahead;         /* d: the predictor of layer l targets layer l+d (d >= 0) */
+  int32_t pred_hidden;       /* 0: predictor is one GEMV Wp [E x H];
+                                else a 2-layer MLP: W1 [pred_hidden x H], W2 [E x pred_hidden] */
+  int32_t max_tokens;        /* T limit of every call (1..8192 / top_k) */
+  int32_t dtype;             /* PROMOE_F32 or PROMOE_BF16 */
+  int64_t copy_subchunk_bytes; /* copy issue unit; 0 = 16 MiB */
+  int32_t copy_window;       /* low-priority sub-copies kept in flight; 0 = 2 */
+  int32_t flags;             /* PROMOE_FLAG_* */
+} promoe_config;
+
+typedef struct promoe_stats {
+  /* Logical counters, decided on the device in program order; exact. */
+  int64_t prec_access;    /* distinct experts routed, summed over route calls */
+  int64_t hit;            /* routed experts already slot-assigned */
+  int64_t miss;           /* routed experts given a slot at route time */
+  int64_t spec_issued;    /* predicted experts given a slot */
+  int64_t spec_resident;  /* predicted experts already resident (touched) */
+  int64_t spec_used;      /* speculatively filled slots later hit */
+  int64_t spec_wasted;    /* speculatively filled slots evicted unused */
+  int64_t evict;          /* slot reassignments that displaced an expert */
+  /* Physical counters (host side). */
+  int64_t copies_high, copies_low;  /* sub-copies issued per priority */
+  int64_t bytes_high, bytes_low;    /* bytes issued per priority */
+  int64_t low_purged;               /* queued low-priority sub-copies dropped by route */
+  int64_t deferred;                 /* high copies held until an earlier expert of the
+                                       same layer finished reading the slot */
+  /* Timing, PROMOE_FLAG_PROFILE only (HIP events on the launch stream). */
+  int64_t k_launches[4];  /* [0] FFN gate/up, [1] FFN down, [2] GEMM gate/up, [3] GEMM down */
+  double k_ms[4];         /* summed kernel time */
+  double k_bytes[4];      /* summed algorithmic weight bytes */
+  double k_flops[4];      /* summed algorithmic flops */
+  double stall_ms;        /* compute stream time spent waiting on copies */
+  double copy_ms;         /* copy stream busy time (first issue to last completion, summed per burst) */
+} promoe_stats;
+
+typedef struct promoe_plan {
+  /* The last plan of a layer, as decided on the device.
+     kind 0 (spec):    expert[i], slot[i], flag[i] = 1 if newly assigned, victim[i].
+     kind 1 (precise): expert[i] = order, slot[i] = slot the position computes from,
+                       flag[i] = 1 for a miss, victim[i], after[i] = earlier position whose
+                       compute must finish before the fill (-1 none), count[i] = tokens. */
+  int32_t n;
+  int32_t expert[64], slot[64], flag[64], victim[64], after[64], count[64];
+} promoe_plan;
+
+/* ---- lifetime ------------------------------------------------------------ */
+
+/* Create a context on the current HIP device.  d_cache is the caller's cache
+ * region of at least n_layers*slots_per_layer*expert_bytes bytes (slot s of
+ * layer l at offset (l*C+s)*expert_bytes).  All slots start free.
+ * Errors: EINVAL (null/size), EUNSUP (E > 64, C > 64, k > 8, H or I not a
+ * multiple of 8), ENOMEM, EHIP. */
+int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, promoe_ctx** out);
+
+/* Drain all copies, stop the worker and free library resources. */
+int promoe_destroy(promoe_ctx* ctx);
+
+/* ---- weights ------------------------------------------------------------- */
+
+/* Resident weights of a layer (device pointers, caller-owned):
+ *  d_wgate [E x H]; d_bias [E] fp32 (router_bias only, else NULL);
+ *  d_pw1, d_pw2: predictor owned by this layer, targeting layer+lookahead
+ *    (Sec. "Learning-based Predictor"): Wp [E x H] (pred_hidden == 0, d_pw2 NULL)
+ *    or W1 [pred_hidden x H], W2 [E x pred_hidden]; NULL when the layer has none;
+ *  d_shared: [Wg | Wu | Wd] of the shared expert(s) with I = shared_inter, or NULL;
+ *  d_shared_gate [H] (shared_gate only). */
+int promoe_set_layer(promoe_ctx* ctx, int layer, const void* d_wgate, const float* d_bias,
+                     const void* d_pw1, const void* d_pw2, const void* d_shared,
+                     const void* d_shared_gate);
+
+/* Host copy of routed expert `expert` of `layer`: pinned memory (e.g. from
+ * promoe_host_alloc) holding [Wg | Wu | Wd]. */
+int promoe_set_expert_host(promoe_ctx* ctx, int layer, int expert, const void* h_pinned);
+
+/* Warm start: experts h_experts[0..n) are copied (synchronously) into slots
+ * 0..n) of the layer and become resident with LRU order = slot order.  Not
+ * counted.  Must precede the layer's first plan.  n <= slots_per_layer. */
+int promoe_set_initial_cache(promoe_ctx* ctx, int layer, const int32_t* h_experts, int n);
+
+/* ---- the hot path -------------------------------------------------------- */
+
+/* Look-ahead prediction (Sec. "Learning-based Predictor", "Stride Prefetching";
+ * Alg. 2 PushPredictedExperts).  One fused pass over d_x [T x H] computes the
+ * gate logits of `layer` (reused by the next promoe_route of that layer on the
+ * same d_x) and the predictor of layer+lookahead; per-token top-k of the
+ * predictor output; an integer vote merges the tokens' picks into a list Q of
+ * at most slots_per_layer experts (votes desc, best rank asc, id asc); the
+ * target layer's cache is planned on the device: resident members are
+ * touched, others take the free or least-recently-used slot and their three
+ * chunks are queued at low priority, copied by the library's worker thread.
+ * Optional outputs: d_pred_ids [T x k] per-token predicted ids; h_q/n_q the
+ * list Q (requesting it synchronises the stream).  When layer+lookahead is
+ * past the last layer only the gate logits are computed and *n_q = 0. */
+int promoe_predict(promoe_ctx* ctx, int layer, const void* d_x, int T, int32_t* d_pred_ids,
+                   int32_t* h_q, int32_t* n_q, void* stream);
+
+/* Route `layer` (Background "MoE based LLMs"; "Early Preemption";
+ * "Reordered Inference"; Alg. 2 PushPreciseExperts).  Gate logits
+ * (+bias), softmax, top-k by (logit desc, id asc), weights renormalised over
+ * the k if cfg.renorm -> d_ids [T x k] int32, d_w [T x k] fp32, and for a gated
+ * shared expert d_shared_scale [T] = sigmoid(w_sg . x) (else may be NULL).
+ * Then the precise plan: pending low-priority copies of the layer are dropped,
+ * order = resident experts by fill order then missing experts by id; missing
+ * experts get slots and are copied at high priority.  Synchronises with the
+ * stream once.  h_order [>= E] receives the order, *n_order its length. */
+int promoe_route(promoe_ctx* ctx, int layer, const void* d_x, int T, int32_t* d_ids, float* d_w,
+                 float* d_shared_scale, int32_t* h_order, int32_t* n_order, void* stream);
+
+/* External push of a list of experts for `target_layer` (Alg. 2
+ * PushPredictedExperts with a caller-chosen list): the same device plan as a
+ * prediction; prio selects the copy queue. */
+int promoe_prefetch(promoe_ctx* ctx, int target_layer, const int32_t* h_ids, int n, int prio,
+                    void* stream);
+
+/* Expert FFN of the routed layer (Background; Sec. "Reordered Inference"):
+ * for every (t, r): Y = Wd (bf16|fp32)(silu(Wg x_t) * (Wu x_t)) with the
+ * expert read from its cache slot, experts computed in the route order and
+ * each launch waiting only on its own chunks; plus the shared expert;
+ * d_y [T x H] = sum_r d_w[t,r] Y[t,r] (fixed r order) + s_t Y_shared[t],
+ * rounded once to the config dtype.  d_x, d_ids, d_w, d_shared_scale must be
+ * the ones passed to promoe_route for this layer. */
+int promoe_expert_ffn(promoe_ctx* ctx, int layer, const void* d_x, int T, const int32_t* d_ids,
+                      const float* d_w, const float* d_shared_scale, void* d_y, void* stream);
+
+/* ---- state and statistics ------------------------------------------------ */
+
+/* Counters of one layer, or of all layers summed (layer = -1).  Synchronises. */
+int promoe_cache_stats(promoe_ctx* ctx, int layer, promoe_stats* out);
+int promoe_reset_stats(promoe_ctx* ctx);
+/* h_slot_of [E]: slot of each expert of the layer, -1 if not resident.  Synchronises. */
+int promoe_slot_table(promoe_ctx* ctx, int layer, int32_t* h_slot_of);
+/* Last spec (kind 0) or precise (kind 1) plan of a layer.  Synchronises. */
+int promoe_last_plan(promoe_ctx* ctx, int layer, int kind, promoe_plan* out);
+/* Wait for all queued copies and compute issued through the context. */
+int promoe_sync(promoe_ctx* ctx);
+
+/* ---- harness (the layer around the MoE block) ---------------------------- */
+
+/* Attention surrogate weight Wa [H x H] of a layer. */
+int promoe_set_attn(promoe_ctx* ctx, int layer, const void* d_wattn);
+/* d_h [T x H] fp32 residual stream: h += Wa q(rms(h)); d_x_out = q(rms(h)),
+ * rms(v) = v / sqrt(mean(v^2) + 1e-6), q = dtype rounding. */
+int promoe_attn_surrogate(promoe_ctx* ctx, int layer, float* d_h, int T, void* d_x_out,
+                          void* stream);
+/* d_h [T x H] fp32 += d_y [T x H] (config dtype). */
+int promoe_residual_add(promoe_ctx* ctx, float* d_h, const void* d_y, int T, void* stream);
+
+/* ---- utilities ----------------------------------------------------------- */
+
+/* Pinned host memory for expert weights (hipHostMalloc); free with promoe_host_free. */
+int promoe_host_alloc(size_t bytes, void** out);
+int promoe_host_free(void* p);
+size_t promoe_expert_bytes(const promoe_config* cfg);
+const char* promoe_strerror(int err);
+/* Text of the last HIP error seen by the library in this thread. */
+const char* promoe_last_error_string(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PROMOE_H */

@@ -1,0 +1,114 @@
+// Launch-argument structs and host launchers of the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace promoe {
+
+// Rows GEMV: out[t][o_off + j] (=|+=) sum_k W_j[k] * f(x[t][x_off + k]),
+// rows j from up to three sources (w[i], nrows[i]) concatenated.
+struct RowsArgs {
+  const void* w[3];
+  int nrows[3];
+  int K;
+  const void* x;
+  int ldx, x_off;
+  int T;
+  float* out;
+  int ldo, o_off;
+  int add;      // 1: accumulate into out
+  int relu_in;  // 1: f = relu, else identity
+};
+
+// Expert FFN launch over the positions pos_list[0 .. n) of the route order.
+struct FfnArgs {
+  const uint8_t* cache;
+  int64_t expert_bytes;
+  int layer, slots;
+  const int32_t* order_slot;  // [n_pos] slot each position computes from
+  const int32_t* offsets;     // [n_pos + 1] pair offsets of each position
+  const int32_t* perm;        // [T*k] pair q -> t*k + r
+  uint8_t pos_list[64];       // blockIdx.y -> position of the route order
+  int hidden, inter, top_k, T;
+  const void* x;              // [T x H]
+  void* act;                  // [T*k x I] permuted activations
+  float* Y;                   // [T*k x H] by (t, r)
+  // shared expert (one launch with shared = 1)
+  int shared, shared_inter;
+  const void* shared_w;
+  void* act_sh;               // [T x I_sh]
+  float* Ysh;                 // [T x H]
+};
+
+struct CombineArgs {
+  const float* Y;       // [T*k x H]
+  const float* w;       // [T x k]
+  const float* Ysh;     // [T x H] or null
+  const float* sscale;  // [T] or null (weight 1)
+  void* y;              // [T x H]
+  int hidden, top_k;
+};
+
+// Per-layer logical cache state on the device.
+struct CacheState {
+  int32_t* slot_expert;  // [L*C]
+  int32_t* slot_of;      // [L*E]
+  uint32_t* stamp;       // [L*C]
+  uint32_t* fetch_seq;   // [L*C]
+  int32_t* spec_unused;  // [L*C]
+  uint32_t* clock;       // [L]
+  uint32_t* fseq;        // [L]
+  int64_t* counters;     // [L*8]: prec_access hit miss spec_issued spec_resident spec_used spec_wasted evict
+};
+
+// Plan record written by the plan kernels into host-mapped memory.
+struct PlanRecord {
+  int32_t kind;   // 0 spec, 1 precise
+  int32_t layer;
+  int32_t n;
+  int32_t n_hit;
+  int32_t expert[64], slot[64], flag[64], victim[64], after[64], count[64];
+  int32_t offset[65];
+  int32_t q_in[64];  // host-provided list for promoe_prefetch
+  int32_t n_q_in;
+  int32_t done;
+};
+
+struct TopkArgs {
+  const float* logits;  // [T x ld]; gate logits at column 0..E-1
+  int ld;
+  int E, k, T;
+  const float* bias;    // [E] or null
+  int renorm;
+  int want_weights;     // 0: ids only (predictor)
+  int32_t* ids;         // [T x k]
+  float* w;             // [T x k]
+  int sgate_col;        // column of the shared-gate logit, -1 none
+  float* sscale;        // [T]
+};
+
+struct PlanArgs {
+  CacheState st;
+  int layer, C, E;
+  const int32_t* ids;   // [T x k] (precise) or per-token predicted ids (spec); null = use rec->q_in
+  int T, k;
+  PlanRecord* rec;      // host-mapped
+  int32_t* d_order_slot; // [64]
+  int32_t* d_offsets;    // [65]
+  int32_t* d_perm;       // [T*k]
+  int32_t* d_pos_of;     // [64] scratch
+};
+
+void launch_rows_gemv(const RowsArgs& a, int wdtype, int xdtype, hipStream_t s);
+void launch_ffn(const FfnArgs& a, int pass, int n_pos, int max_tokens_per_pos, int dtype, hipStream_t s);
+void launch_combine(const CombineArgs& a, int T, int dtype, hipStream_t s);
+void launch_rmsnorm_quant(const float* h, void* out, int T, int H, int dtype, hipStream_t s);
+void launch_residual_add(float* h, const void* y, int n, int dtype, hipStream_t s);
+void launch_topk(const TopkArgs& a, hipStream_t s);
+void launch_plan_spec(const PlanArgs& a, hipStream_t s);
+void launch_plan_precise(const PlanArgs& a, hipStream_t s);
+void launch_state_init(CacheState st, int L, int C, int E, hipStream_t s);
+void launch_warm(CacheState st, int layer, int C, int E, const int32_t* d_experts, int n, hipStream_t s);
+
+}  // namespace promoe

@@ -1,0 +1,342 @@
+// Routing and cache-plan kernels for gfx950 (wave64).
+//
+//  * k_topk          -- per token one wave, one lane per expert (E <= 64):
+//                       softmax and top-k by (logit desc, id asc) from k rounds
+//                       of a wave max over 64-bit keys (order-preserving logit
+//                       bits, then 63 - id), renormalised weights, the shared
+//                       expert's sigmoid gate.  Used by the router and, ids
+//                       only, by the predictor.
+//  * k_plan_spec     -- speculative plan of a target layer (Alg. 2
+//                       PushPredictedExperts): integer vote over the tokens'
+//                       predicted ids, then the LRU plan.
+//  * k_plan_precise  -- precise plan of the routed layer (Alg. 2
+//                       PushPreciseExperts, Sec. "Reordered Inference"):
+//                       hit/miss, order, victim slots, counters, followed by the
+//                       token permutation grouping (t, r) pairs by position.
+//
+// Both plans run in one workgroup: the counting phases use all 256 threads,
+// the sequential LRU walk runs in wave 0 with one lane per slot (for slot
+// state) and one lane per expert (for slot_of), so every victim search is one
+// wave-wide argmin.  The plans write a record into host-mapped memory for the
+// copy scheduler.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace promoe {
+
+enum { CNT_PREC = 0, CNT_HIT, CNT_MISS, CNT_SPEC_ISSUED, CNT_SPEC_RESIDENT, CNT_SPEC_USED, CNT_SPEC_WASTED, CNT_EVICT };
+
+// ============================================================ top-k
+__global__ __launch_bounds__(256) void k_topk(TopkArgs a) {
+  const int lane = threadIdx.x % kWave;
+  const int t = blockIdx.x * 4 + threadIdx.x / kWave;
+  if (t >= a.T) return;
+  const bool valid = lane < a.E;
+  float z = -INFINITY;
+  if (valid) z = a.logits[(size_t)t * a.ld + lane] + (a.bias ? a.bias[lane] : 0.0f);
+  uint64_t key = valid ? (((uint64_t)f32_order_key(z) << 32) | (uint32_t)(63 - lane)) : 0ull;
+  int myrank = -1;
+  for (int r = 0; r < a.k; ++r) {
+    const uint64_t kmax = wave_max_u64(key);
+    const int e = 63 - (int)(uint32_t)(kmax & 0xFFFFFFFFu);
+    if (lane == e) { myrank = r; key = 0ull; }
+    if (lane == 0) a.ids[t * a.k + r] = e;
+  }
+  if (a.want_weights) {
+    const float zmax = wave_max(valid ? z : -INFINITY);
+    const float ez = valid ? expf(z - zmax) : 0.0f;
+    const float denom = a.renorm ? wave_sum(myrank >= 0 ? ez : 0.0f) : wave_sum(ez);
+    if (myrank >= 0) a.w[t * a.k + myrank] = ez / denom;
+    if (a.sgate_col >= 0 && lane == 0) {
+      const float u = a.logits[(size_t)t * a.ld + a.sgate_col];
+      a.sscale[t] = 1.0f / (1.0f + expf(-u));
+    }
+  }
+}
+
+// ============================================================ plan helpers
+struct WaveState {
+  int slot_expert;  // lane = slot
+  uint32_t stamp, fetch;
+  int spec_unused;
+  int slot_of;      // lane = expert
+};
+
+__device__ __forceinline__ void load_state(const PlanArgs& a, int lane, WaveState& w, uint32_t& clock, uint32_t& fseq,
+                                           int64_t (&cnt)[8]) {
+  const int bc = a.layer * a.C, be = a.layer * a.E;
+  w.slot_expert = lane < a.C ? a.st.slot_expert[bc + lane] : -1;
+  w.stamp = lane < a.C ? a.st.stamp[bc + lane] : 0u;
+  w.fetch = lane < a.C ? a.st.fetch_seq[bc + lane] : 0u;
+  w.spec_unused = lane < a.C ? a.st.spec_unused[bc + lane] : 0;
+  w.slot_of = lane < a.E ? a.st.slot_of[be + lane] : -1;
+  clock = a.st.clock[a.layer];
+  fseq = a.st.fseq[a.layer];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) cnt[i] = a.st.counters[a.layer * 8 + i];
+}
+
+__device__ __forceinline__ void store_state(const PlanArgs& a, int lane, const WaveState& w, uint32_t clock,
+                                            uint32_t fseq, const int64_t (&cnt)[8]) {
+  const int bc = a.layer * a.C, be = a.layer * a.E;
+  if (lane < a.C) {
+    a.st.slot_expert[bc + lane] = w.slot_expert;
+    a.st.stamp[bc + lane] = w.stamp;
+    a.st.fetch_seq[bc + lane] = w.fetch;
+    a.st.spec_unused[bc + lane] = w.spec_unused;
+  }
+  if (lane < a.E) a.st.slot_of[be + lane] = w.slot_of;
+  if (lane == 0) {
+    a.st.clock[a.layer] = clock;
+    a.st.fseq[a.layer] = fseq;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) a.st.counters[a.layer * 8 + i] = cnt[i];
+  }
+}
+
+// Lowest-index free slot, else the least recently stamped one (stamps are unique).
+__device__ __forceinline__ int victim_slot(const PlanArgs& a, int lane, const WaveState& w) {
+  uint64_t key = ~0ull;
+  if (lane < a.C) key = w.slot_expert < 0 ? (uint64_t)lane : ((1ull << 40) | (uint64_t)w.stamp);
+  key = (key << 6) | (uint64_t)lane;
+  return (int)(wave_min_u64(key) & 63ull);
+}
+
+// Give slot v to expert e: evict its occupant (counted), fill, stamp.
+__device__ __forceinline__ int fill_slot(const PlanArgs& a, int lane, WaveState& w, int e, int v, bool speculative,
+                                         uint32_t& clock, uint32_t& fseq, int64_t (&cnt)[8]) {
+  const int old = __shfl(w.slot_expert, v, kWave);
+  const int old_unused = __shfl(w.spec_unused, v, kWave);
+  if (old >= 0) {
+    cnt[CNT_EVICT]++;
+    if (old_unused) cnt[CNT_SPEC_WASTED]++;
+    if (lane == old) w.slot_of = -1;
+  }
+  ++fseq;
+  ++clock;
+  if (lane == v) {
+    w.slot_expert = e;
+    w.fetch = fseq;
+    w.stamp = clock;
+    w.spec_unused = speculative ? 1 : 0;
+  }
+  if (lane == e) w.slot_of = v;
+  return old;
+}
+
+// ============================================================ spec plan
+__global__ __launch_bounds__(256) void k_plan_spec(PlanArgs a) {
+  __shared__ int votes[kMaxE], best[kMaxE], Q[kMaxE];
+  __shared__ int nq;
+  const int tid = threadIdx.x, lane = tid % kWave;
+  if (tid < kMaxE) { votes[tid] = 0; best[tid] = kMaxK; }
+  __syncthreads();
+  if (a.ids) {
+    const int n = a.T * a.k;
+    for (int i = tid; i < n; i += 256) {
+      const int e = a.ids[i];
+      atomicAdd(&votes[e], 1);
+      atomicMin(&best[e], i % a.k);
+    }
+  }
+  __syncthreads();
+  if (a.ids) {
+    if (tid < a.E && votes[tid] > 0) {
+      const int ve = votes[tid], be = best[tid];
+      int rank = 0;
+      for (int j = 0; j < a.E; ++j) {
+        const int vj = votes[j], bj = best[j];
+        rank += (vj > ve) || (vj == ve && bj < be) || (vj == ve && bj == be && j < tid);
+      }
+      if (rank < a.C) Q[rank] = tid;
+    }
+    if (tid == 0) {
+      int nv = 0;
+      for (int j = 0; j < a.E; ++j) nv += votes[j] > 0;
+      nq = min(nv, a.C);
+    }
+  } else if (tid == 0) {
+    nq = a.rec->n_q_in;
+    for (int i = 0; i < nq; ++i) Q[i] = a.rec->q_in[i];
+  }
+  __syncthreads();
+  if (tid >= kWave) return;
+
+  WaveState w;
+  uint32_t clock, fseq;
+  int64_t cnt[8];
+  load_state(a, lane, w, clock, fseq, cnt);
+  PlanRecord* rec = a.rec;
+  for (int i = 0; i < nq; ++i) {
+    const int e = Q[i];
+    const int s_res = __shfl(w.slot_of, e, kWave);
+    if (s_res >= 0) {
+      ++clock;
+      if (lane == s_res) w.stamp = clock;
+      cnt[CNT_SPEC_RESIDENT]++;
+      if (lane == 0) { rec->expert[i] = e; rec->slot[i] = s_res; rec->flag[i] = 0; rec->victim[i] = -1; rec->after[i] = -1; }
+    } else {
+      const int v = victim_slot(a, lane, w);
+      const int old = fill_slot(a, lane, w, e, v, true, clock, fseq, cnt);
+      cnt[CNT_SPEC_ISSUED]++;
+      if (lane == 0) { rec->expert[i] = e; rec->slot[i] = v; rec->flag[i] = 1; rec->victim[i] = old; rec->after[i] = -1; }
+    }
+  }
+  store_state(a, lane, w, clock, fseq, cnt);
+  if (lane == 0) {
+    rec->kind = 0;
+    rec->layer = a.layer;
+    rec->n = nq;
+    rec->n_hit = 0;
+    __threadfence_system();
+    rec->done = 1;
+  }
+}
+
+// ============================================================ precise plan + permutation
+__global__ __launch_bounds__(256) void k_plan_precise(PlanArgs a) {
+  __shared__ int cnt_e[kMaxE], pos_of[kMaxE], order[kMaxE], offs[kMaxE + 1], fill[kMaxE], tile_cnt[kMaxE];
+  __shared__ int tile_pos[256];
+  __shared__ int n_pos;
+  const int tid = threadIdx.x, lane = tid % kWave;
+  const int npairs = a.T * a.k;
+  if (tid < kMaxE) { cnt_e[tid] = 0; fill[tid] = 0; }
+  __syncthreads();
+  for (int i = tid; i < npairs; i += 256) atomicAdd(&cnt_e[a.ids[i]], 1);
+  __syncthreads();
+
+  WaveState w;
+  uint32_t clock, fseq;
+  int64_t cnt[8];
+  if (tid < kWave) {
+    load_state(a, lane, w, clock, fseq, cnt);
+    const bool used = lane < a.E && cnt_e[lane] > 0;
+    const bool res = used && w.slot_of >= 0;
+    const uint32_t fs = __shfl(w.fetch, w.slot_of >= 0 ? w.slot_of : 0, kWave);
+    const uint64_t hmask = __ballot(res);
+    const uint64_t mmask = __ballot(used && !res);
+    const int nh = __popcll(hmask), np = nh + __popcll(mmask);
+    int rank = -1;
+    if (res) {
+      rank = 0;
+      for (int j = 0; j < kWave; ++j) {
+        const uint32_t fj = __shfl(fs, j, kWave);
+        if (((hmask >> j) & 1ull) && (fj < fs || (fj == fs && j < lane))) ++rank;
+      }
+    } else if (used) {
+      rank = nh + __popcll(mmask & ((1ull << lane) - 1ull));
+    } else {
+      // keep the shuffle loop uniform across the wave
+      for (int j = 0; j < kWave; ++j) (void)__shfl(fs, j, kWave);
+    }
+    pos_of[lane] = rank;
+    if (rank >= 0) order[rank] = lane;
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_wave_barrier();
+
+    PlanRecord* rec = a.rec;
+    for (int pos = 0; pos < np; ++pos) {
+      const int e = order[pos];
+      if (pos < nh) {
+        const int s = __shfl(w.slot_of, e, kWave);
+        ++clock;
+        const int was_spec = __shfl(w.spec_unused, s, kWave);
+        if (lane == s) { w.stamp = clock; w.spec_unused = 0; }
+        cnt[CNT_HIT]++;
+        if (was_spec) cnt[CNT_SPEC_USED]++;
+        if (lane == 0) { rec->expert[pos] = e; rec->slot[pos] = s; rec->flag[pos] = 0; rec->victim[pos] = -1; rec->after[pos] = -1; }
+        if (lane == 0) a.d_order_slot[pos] = s;
+      } else {
+        const int v = victim_slot(a, lane, w);
+        const int old = fill_slot(a, lane, w, e, v, false, clock, fseq, cnt);
+        cnt[CNT_MISS]++;
+        const int after = old >= 0 ? pos_of[old] : -1;
+        if (lane == 0) { rec->expert[pos] = e; rec->slot[pos] = v; rec->flag[pos] = 1; rec->victim[pos] = old; rec->after[pos] = after; }
+        if (lane == 0) a.d_order_slot[pos] = v;
+      }
+    }
+    cnt[CNT_PREC] += np;
+    store_state(a, lane, w, clock, fseq, cnt);
+    if (lane == 0) {
+      int o = 0;
+      for (int pos = 0; pos < np; ++pos) {
+        offs[pos] = o;
+        const int c = cnt_e[order[pos]];
+        rec->count[pos] = c;
+        rec->offset[pos] = o;
+        a.d_offsets[pos] = o;
+        o += c;
+      }
+      offs[np] = o;
+      rec->offset[np] = o;
+      a.d_offsets[np] = o;
+      rec->kind = 1;
+      rec->layer = a.layer;
+      rec->n = np;
+      rec->n_hit = nh;
+      n_pos = np;
+    }
+  }
+  __syncthreads();
+
+  // Permutation: pairs in (t, r) order are placed into their position's range,
+  // keeping (t, r) order inside a range.  Tiles of 256 pairs.
+  for (int base = 0; base < npairs; base += 256) {
+    const int i = base + tid;
+    const int pos = i < npairs ? pos_of[a.ids[i]] : -1;
+    tile_pos[tid] = pos;
+    if (tid < kMaxE) tile_cnt[tid] = 0;
+    __syncthreads();
+    if (pos >= 0) {
+      int r = 0;
+      for (int j = 0; j < tid; ++j) r += tile_pos[j] == pos;
+      a.d_perm[offs[pos] + fill[pos] + r] = i;
+      atomicAdd(&tile_cnt[pos], 1);
+    }
+    __syncthreads();
+    if (tid < kMaxE) fill[tid] += tile_cnt[tid];
+    __syncthreads();
+  }
+  if (tid == 0) {
+    __threadfence_system();
+    a.rec->done = 1;
+  }
+}
+
+// ============================================================ state init / warm start
+__global__ void k_state_init(CacheState st, int L, int C, int E) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < L * C) { st.slot_expert[i] = -1; st.stamp[i] = 0u; st.fetch_seq[i] = 0u; st.spec_unused[i] = 0; }
+  if (i < L * E) st.slot_of[i] = -1;
+  if (i < L) { st.clock[i] = (uint32_t)(C - 1); st.fseq[i] = 0u; }
+  if (i < L * 8) st.counters[i] = 0;
+}
+
+__global__ void k_warm(CacheState st, int layer, int C, int E, const int32_t* experts, int n) {
+  const int s = threadIdx.x;
+  if (s < n) {
+    const int e = experts[s];
+    st.slot_expert[layer * C + s] = e;
+    st.slot_of[layer * E + e] = s;
+    st.stamp[layer * C + s] = (uint32_t)s;
+    st.fetch_seq[layer * C + s] = 0u;
+    st.spec_unused[layer * C + s] = 0;
+  }
+}
+
+// ============================================================ launchers
+void launch_topk(const TopkArgs& a, hipStream_t s) {
+  k_topk<<<(a.T + 3) / 4, 256, 0, s>>>(a);
+}
+void launch_plan_spec(const PlanArgs& a, hipStream_t s) { k_plan_spec<<<1, 256, 0, s>>>(a); }
+void launch_plan_precise(const PlanArgs& a, hipStream_t s) { k_plan_precise<<<1, 256, 0, s>>>(a); }
+void launch_state_init(CacheState st, int L, int C, int E, hipStream_t s) {
+  int n = L * (C > E ? C : E);
+  if (n < L * 8) n = L * 8;
+  k_state_init<<<(n + 255) / 256, 256, 0, s>>>(st, L, C, E);
+}
+void launch_warm(CacheState st, int layer, int C, int E, const int32_t* d_experts, int n, hipStream_t s) {
+  k_warm<<<1, 64, 0, s>>>(st, layer, C, E, d_experts, n);
+}
+
+}  // namespace promoe

@@ -1,0 +1,1046 @@
+// Host runtime and C ABI of the expert cache (see include/promoe.h).
+//
+// Split of responsibilities
+//  * logical cache state (slot tables, LRU stamps, counters) lives on the
+//    device and changes only inside the plan kernels, in stream order;
+//  * the plan kernels write a record per plan into host-mapped memory;
+//  * the host ingests records in program order into the copy scheduler
+//    (Prefetcher), which tracks what each slot physically holds and issues the
+//    copies on the library's copy stream;
+//  * speculative records are ingested by a worker thread (the prefetch worker
+//    of Alg. 1) that waits on the plan's event, so promoe_predict never blocks;
+//    a route synchronises once on its own plan and issues its high-priority
+//    copies itself, in the returned order, right behind at most `window`
+//    in-flight low-priority sub-copies;
+//  * compute waits on copy events only for the chunks it reads (gate/up pass
+//    after chunks 0-1, down pass after chunk 2); copies into a slot wait on the
+//    event of the last launch that read it.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <condition_variable>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "../../include/promoe.h"
+#include "common.hpp"
+#include "kernels.hpp"
+#include "scheduler.hpp"
+
+using namespace promoe;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+constexpr int kRecRing = 64;
+constexpr int kCopyRing = 4096;
+constexpr int kComputeRing = 4096;
+
+struct ProfEntry {
+  hipEvent_t a, b;
+  int cls;  // 0..3 kernels, 4 stall
+  double bytes, flops;
+};
+
+class HipEngine : public CopyEngine {
+ public:
+  hipStream_t stream = nullptr;
+  std::vector<hipEvent_t> ev;
+  std::vector<hipEvent_t>* compute_ev = nullptr;
+  hipError_t err = hipSuccess;
+
+  void issue(int64_t seq, void* dst, const void* src, size_t bytes, int64_t after) override {
+    hipError_t e = hipSuccess;
+    if (after >= 0) e = hipStreamWaitEvent(stream, (*compute_ev)[after % kComputeRing], 0);
+    if (e == hipSuccess) e = hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, stream);
+    if (e == hipSuccess) e = hipEventRecord(ev[seq % kCopyRing], stream);
+    if (e != hipSuccess && err == hipSuccess) err = e;
+  }
+  bool done(int64_t seq) override { return hipEventQuery(ev[seq % kCopyRing]) == hipSuccess; }
+  void wait(int64_t seq) override {
+    hipError_t e = hipEventSynchronize(ev[seq % kCopyRing]);
+    if (e != hipSuccess && err == hipSuccess) err = e;
+  }
+  hipEvent_t event(int64_t seq) { return ev[seq % kCopyRing]; }
+  int64_t capacity() const override { return kCopyRing - 1; }
+};
+
+struct LayerW {
+  const void *wg = nullptr, *pw1 = nullptr, *pw2 = nullptr, *shared = nullptr, *sgate = nullptr, *attn = nullptr;
+  const float* bias = nullptr;
+  bool planned = false;
+};
+
+struct Deferred {
+  int pos, slot, expert, after;
+};
+
+}  // namespace
+
+struct promoe_ctx {
+  promoe_config cfg{};
+  int dev = 0;
+  int L, H, E, K, I, Ish, C, D, Ph, maxT, dt, eb;
+  size_t chunk_bytes, expert_bytes;
+  uint8_t* cache = nullptr;
+
+  // device memory
+  void* dmem = nullptr;
+  CacheState st{};
+  float* d_logits = nullptr;
+  int ld_logits = 0;
+  int pred_col = 0;  // first predictor column of d_logits (after gate and shared-gate columns)
+  float* d_predq = nullptr;
+  int32_t* d_pred_ids = nullptr;
+  int32_t* d_order_slot = nullptr;
+  int32_t* d_offsets = nullptr;
+  int32_t* d_perm = nullptr;
+  int32_t* d_pos_of = nullptr;
+  int32_t* d_warm = nullptr;
+  void* d_act = nullptr;
+  float* d_Y = nullptr;
+  void* d_act_sh = nullptr;
+  float* d_Ysh = nullptr;
+  void* d_u = nullptr;
+
+  std::vector<LayerW> lw;
+
+  // gate logits computed by predict, reused by route
+  int gate_layer = -1;
+  const void* gate_x = nullptr;
+  int gate_T = 0;
+
+  // plan records
+  PlanRecord* rec_h = nullptr;  // host view
+  PlanRecord* rec_d = nullptr;  // device view
+  hipEvent_t rec_ev[kRecRing];
+  int rec_kind[kRecRing];
+  int rec_prio[kRecRing];
+  int64_t rec_next = 0, rec_pub = 0, rec_ingested = 0;  // reserved / event recorded / ingested
+  std::vector<PlanRecord> last_spec, last_precise;
+
+  // route -> ffn hand-over
+  int route_layer = -1;
+  int route_T = 0;
+  PlanRecord route_rec{};
+  std::vector<int64_t> need01, need2;  // copy seq each position waits for (-1 none)
+  std::vector<Deferred> deferred;
+
+  // scheduler and worker
+  HipEngine eng;
+  Prefetcher* pf = nullptr;
+  std::mutex mu;
+  std::condition_variable cv;
+  std::thread worker;
+  bool stop = false;
+
+  std::vector<hipEvent_t> cev;
+  int64_t cnext = 0;
+  hipStream_t last_stream = nullptr;
+
+  // profiling
+  bool profile = false;
+  std::vector<ProfEntry> prof_pending;
+  std::vector<hipEvent_t> prof_free;
+  int64_t k_launches[4] = {0, 0, 0, 0};
+  double k_ms[4] = {0, 0, 0, 0}, k_bytes[4] = {0, 0, 0, 0}, k_flops[4] = {0, 0, 0, 0};
+  double stall_ms = 0.0;
+};
+
+namespace {
+
+int fail_hip(hipError_t e, const char* what) {
+  g_last_error = std::string(what) + ": " + hipGetErrorString(e);
+  return PROMOE_EHIP;
+}
+#define HIPCHK(x)                                 \
+  do {                                            \
+    hipError_t _e = (x);                          \
+    if (_e != hipSuccess) return fail_hip(_e, #x); \
+  } while (0)
+#define LAUNCHCHK(what)                               \
+  do {                                                \
+    hipError_t _e = hipGetLastError();                \
+    if (_e != hipSuccess) return fail_hip(_e, what);  \
+  } while (0)
+
+hipEvent_t prof_event(promoe_ctx* c) {
+  if (!c->prof_free.empty()) {
+    hipEvent_t e = c->prof_free.back();
+    c->prof_free.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  hipEventCreate(&e);
+  return e;
+}
+
+void prof_resolve(promoe_ctx* c) {
+  for (auto& p : c->prof_pending) {
+    hipEventSynchronize(p.b);
+    float ms = 0.0f;
+    hipEventElapsedTime(&ms, p.a, p.b);
+    if (p.cls < 4) {
+      c->k_launches[p.cls]++;
+      c->k_ms[p.cls] += ms;
+      c->k_bytes[p.cls] += p.bytes;
+      c->k_flops[p.cls] += p.flops;
+    } else {
+      c->stall_ms += ms;
+    }
+    c->prof_free.push_back(p.a);
+    c->prof_free.push_back(p.b);
+  }
+  c->prof_pending.clear();
+}
+
+// Ingest record r (spec kind) into the copy scheduler.  Caller holds mu and
+// knows the record's plan kernel has completed.
+void ingest_spec(promoe_ctx* c, int64_t r) {
+  const PlanRecord& rec = c->rec_h[r % kRecRing];
+  const int layer = rec.layer;
+  c->last_spec[layer] = rec;
+  if (!(c->cfg.flags & PROMOE_FLAG_NO_PREFETCH)) {
+    const bool high = c->rec_prio[r % kRecRing] == PROMOE_PRIO_HIGH;
+    for (int i = 0; i < rec.n; ++i) {
+      if (rec.flag[i]) c->pf->assign(layer, rec.slot[i], rec.expert[i]);
+      if (high) c->pf->issue_high(layer, rec.slot[i]);
+      else c->pf->push_low(layer, rec.slot[i]);
+    }
+  }
+  c->rec_ingested = r + 1;
+}
+
+void worker_main(promoe_ctx* c) {
+  hipSetDevice(c->dev);
+  std::unique_lock<std::mutex> lk(c->mu);
+  while (!c->stop) {
+    while (c->rec_ingested < c->rec_pub && c->rec_kind[c->rec_ingested % kRecRing] == 0 &&
+           hipEventQuery(c->rec_ev[c->rec_ingested % kRecRing]) == hipSuccess)
+      ingest_spec(c, c->rec_ingested);
+    c->pf->pump();
+    const bool head_spec = c->rec_ingested < c->rec_pub && c->rec_kind[c->rec_ingested % kRecRing] == 0;
+    if (c->pf->has_low() && c->pf->in_flight() >= c->pf->window()) {
+      const int64_t seq = c->pf->oldest_in_flight();
+      hipEvent_t e = c->eng.event(seq);
+      lk.unlock();
+      hipEventSynchronize(e);
+      lk.lock();
+      continue;
+    }
+    if (head_spec) {
+      hipEvent_t e = c->rec_ev[c->rec_ingested % kRecRing];
+      lk.unlock();
+      hipEventSynchronize(e);
+      lk.lock();
+      continue;
+    }
+    c->cv.wait(lk);
+  }
+}
+
+// Reserve a plan record slot (waiting for / ingesting the oldest if the ring is full).
+int new_record(promoe_ctx* c, int kind, int prio, int64_t* out) {
+  std::unique_lock<std::mutex> lk(c->mu);
+  while (c->rec_next - c->rec_ingested >= kRecRing) {
+    const int64_t r = c->rec_ingested;
+    if (c->rec_kind[r % kRecRing] != 0) {
+      g_last_error = "plan record ring blocked by an unconsumed route";
+      return PROMOE_ESTATE;
+    }
+    if (r >= c->rec_pub) {
+      g_last_error = "plan record ring full of unpublished records";
+      return PROMOE_ESTATE;
+    }
+    hipEvent_t e = c->rec_ev[r % kRecRing];
+    lk.unlock();
+    HIPCHK(hipEventSynchronize(e));
+    lk.lock();
+    if (c->rec_ingested == r) ingest_spec(c, r);
+  }
+  const int64_t r = c->rec_next++;
+  c->rec_kind[r % kRecRing] = kind;
+  c->rec_prio[r % kRecRing] = prio;
+  std::memset(&c->rec_h[r % kRecRing], 0, sizeof(PlanRecord));
+  *out = r;
+  return PROMOE_OK;
+}
+
+// Record r's plan event has been recorded (or the plan was abandoned): the
+// worker may now look at it.
+void publish(promoe_ctx* c, int64_t r) {
+  {
+    std::lock_guard<std::mutex> lk(c->mu);
+    if (c->rec_pub < r + 1) c->rec_pub = r + 1;
+  }
+  c->cv.notify_all();
+}
+
+int64_t record_compute(promoe_ctx* c, hipStream_t s) {
+  const int64_t tok = c->cnext++;
+  hipEventRecord(c->cev[tok % kComputeRing], s);
+  return tok;
+}
+
+PlanArgs plan_args(promoe_ctx* c, int layer, const int32_t* ids, int T, int64_t r) {
+  PlanArgs a{};
+  a.st = c->st;
+  a.layer = layer;
+  a.C = c->C;
+  a.E = c->E;
+  a.ids = ids;
+  a.T = T;
+  a.k = c->K;
+  a.rec = c->rec_d + (r % kRecRing);
+  a.d_order_slot = c->d_order_slot;
+  a.d_offsets = c->d_offsets;
+  a.d_perm = c->d_perm;
+  a.d_pos_of = c->d_pos_of;
+  return a;
+}
+
+int check_tokens(promoe_ctx* c, int T) {
+  if (T < 1 || T > c->maxT) {
+    g_last_error = "T out of range";
+    return PROMOE_EINVAL;
+  }
+  return PROMOE_OK;
+}
+
+// Gate (+ shared-gate row) (+ predictor first layer) rows over x, one launch:
+// columns [0, E) gate logits, E shared-gate logit (if any), then predictor rows.
+int launch_gate_rows(promoe_ctx* c, int layer, const void* d_x, int T, bool with_pred, hipStream_t s) {
+  const LayerW& w = c->lw[layer];
+  RowsArgs a{};
+  a.w[0] = w.wg;
+  a.nrows[0] = c->E;
+  a.w[1] = w.sgate;
+  a.nrows[1] = w.sgate ? 1 : 0;
+  a.w[2] = with_pred ? w.pw1 : nullptr;
+  a.nrows[2] = with_pred ? (c->Ph > 0 ? c->Ph : c->E) : 0;
+  a.K = c->H;
+  a.x = d_x;
+  a.ldx = c->H;
+  a.x_off = 0;
+  a.T = T;
+  a.out = c->d_logits;
+  a.ldo = c->ld_logits;
+  a.o_off = 0;
+  launch_rows_gemv(a, c->dt, c->dt, s);
+  LAUNCHCHK("gate rows");
+  return PROMOE_OK;
+}
+
+}  // namespace
+
+// =====================================================================
+extern "C" {
+
+const char* promoe_strerror(int err) {
+  switch (err) {
+    case PROMOE_OK: return "ok";
+    case PROMOE_EINVAL: return "invalid argument";
+    case PROMOE_ENOMEM: return "out of memory";
+    case PROMOE_EHIP: return "HIP runtime error";
+    case PROMOE_ESTATE: return "call order violated";
+    case PROMOE_EUNSUP: return "unsupported shape";
+    default: return "unknown error";
+  }
+}
+
+const char* promoe_last_error_string(void) { return g_last_error.c_str(); }
+
+size_t promoe_expert_bytes(const promoe_config* cfg) {
+  if (!cfg) return 0;
+  const size_t eb = cfg->dtype == PROMOE_BF16 ? 2 : 4;
+  return 3 * (size_t)cfg->inter * (size_t)cfg->hidden * eb;
+}
+
+int promoe_host_alloc(size_t bytes, void** out) {
+  if (!out || !bytes) return PROMOE_EINVAL;
+  void* p = nullptr;
+  hipError_t e = hipHostMalloc(&p, bytes, hipHostMallocDefault);
+  if (e != hipSuccess) return fail_hip(e, "hipHostMalloc");
+  *out = p;
+  return PROMOE_OK;
+}
+
+int promoe_host_free(void* p) {
+  if (!p) return PROMOE_EINVAL;
+  HIPCHK(hipHostFree(p));
+  return PROMOE_OK;
+}
+
+int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, promoe_ctx** out) {
+  if (!cfg || !d_cache || !out) return PROMOE_EINVAL;
+  const promoe_config& g = *cfg;
+  if (g.n_layers < 1 || g.hidden < 8 || g.inter < 8 || g.n_experts < 1 || g.top_k < 1 ||
+      g.slots_per_layer < 1 || g.max_tokens < 1 || g.lookahead < 0 || g.pred_hidden < 0 || g.shared_inter < 0 ||
+      (g.dtype != PROMOE_F32 && g.dtype != PROMOE_BF16) || g.top_k > g.n_experts) {
+    g_last_error = "invalid config";
+    return PROMOE_EINVAL;
+  }
+  if (g.n_experts > kMaxE || g.slots_per_layer > 64 || g.top_k > kMaxK || g.hidden % 8 || g.inter % 8 ||
+      g.shared_inter % 8 || (int64_t)g.max_tokens * g.top_k > 8192) {
+    g_last_error = "unsupported shape";
+    return PROMOE_EUNSUP;
+  }
+  const size_t ebytes = promoe_expert_bytes(cfg);
+  if (cache_bytes < (size_t)g.n_layers * g.slots_per_layer * ebytes) {
+    g_last_error = "cache region too small";
+    return PROMOE_EINVAL;
+  }
+  promoe_ctx* c = new (std::nothrow) promoe_ctx();
+  if (!c) return PROMOE_ENOMEM;
+  c->cfg = g;
+  c->L = g.n_layers; c->H = g.hidden; c->E = g.n_experts; c->K = g.top_k; c->I = g.inter;
+  c->Ish = g.shared_inter; c->C = g.slots_per_layer; c->D = g.lookahead; c->Ph = g.pred_hidden;
+  c->maxT = g.max_tokens; c->dt = g.dtype; c->eb = g.dtype == PROMOE_BF16 ? 2 : 4;
+  c->chunk_bytes = (size_t)c->I * c->H * c->eb;
+  c->expert_bytes = 3 * c->chunk_bytes;
+  c->cache = static_cast<uint8_t*>(d_cache);
+  c->profile = (g.flags & PROMOE_FLAG_PROFILE) != 0;
+  c->lw.resize(c->L);
+  c->last_spec.resize(c->L);
+  c->last_precise.resize(c->L);
+  hipGetDevice(&c->dev);
+
+  // ---- device memory (one allocation, 256-byte aligned pieces)
+  const int L = c->L, C = c->C, E = c->E, T = c->maxT, Kk = c->K, H = c->H;
+  c->pred_col = E + ((c->Ish > 0 && g.shared_gate) ? 1 : 0);
+  c->ld_logits = c->pred_col + std::max(c->Ph, E);
+  size_t off = 0;
+  auto take = [&](size_t bytes) { size_t o = off; off += (bytes + 255) & ~(size_t)255; return o; };
+  const size_t o_se = take(sizeof(int32_t) * L * C), o_so = take(sizeof(int32_t) * L * E),
+               o_stamp = take(sizeof(uint32_t) * L * C), o_fs = take(sizeof(uint32_t) * L * C),
+               o_su = take(sizeof(int32_t) * L * C), o_clock = take(sizeof(uint32_t) * L),
+               o_fseq = take(sizeof(uint32_t) * L), o_cnt = take(sizeof(int64_t) * L * 8),
+               o_logits = take(sizeof(float) * (size_t)T * c->ld_logits), o_predq = take(sizeof(float) * (size_t)T * E),
+               o_pids = take(sizeof(int32_t) * (size_t)T * Kk), o_oslot = take(sizeof(int32_t) * 64),
+               o_offs = take(sizeof(int32_t) * 65), o_perm = take(sizeof(int32_t) * (size_t)T * Kk),
+               o_posof = take(sizeof(int32_t) * 64), o_warm = take(sizeof(int32_t) * 64),
+               o_act = take((size_t)c->eb * T * Kk * c->I), o_Y = take(sizeof(float) * (size_t)T * Kk * H),
+               o_actsh = take((size_t)c->eb * T * std::max(c->Ish, 1)), o_Ysh = take(sizeof(float) * (size_t)T * H),
+               o_u = take((size_t)c->eb * T * H);
+  hipError_t e = hipMalloc(&c->dmem, off);
+  if (e != hipSuccess) {
+    delete c;
+    return fail_hip(e, "hipMalloc");
+  }
+  uint8_t* b = static_cast<uint8_t*>(c->dmem);
+  c->st.slot_expert = reinterpret_cast<int32_t*>(b + o_se);
+  c->st.slot_of = reinterpret_cast<int32_t*>(b + o_so);
+  c->st.stamp = reinterpret_cast<uint32_t*>(b + o_stamp);
+  c->st.fetch_seq = reinterpret_cast<uint32_t*>(b + o_fs);
+  c->st.spec_unused = reinterpret_cast<int32_t*>(b + o_su);
+  c->st.clock = reinterpret_cast<uint32_t*>(b + o_clock);
+  c->st.fseq = reinterpret_cast<uint32_t*>(b + o_fseq);
+  c->st.counters = reinterpret_cast<int64_t*>(b + o_cnt);
+  c->d_logits = reinterpret_cast<float*>(b + o_logits);
+  c->d_predq = reinterpret_cast<float*>(b + o_predq);
+  c->d_pred_ids = reinterpret_cast<int32_t*>(b + o_pids);
+  c->d_order_slot = reinterpret_cast<int32_t*>(b + o_oslot);
+  c->d_offsets = reinterpret_cast<int32_t*>(b + o_offs);
+  c->d_perm = reinterpret_cast<int32_t*>(b + o_perm);
+  c->d_pos_of = reinterpret_cast<int32_t*>(b + o_posof);
+  c->d_warm = reinterpret_cast<int32_t*>(b + o_warm);
+  c->d_act = b + o_act;
+  c->d_Y = reinterpret_cast<float*>(b + o_Y);
+  c->d_act_sh = b + o_actsh;
+  c->d_Ysh = reinterpret_cast<float*>(b + o_Ysh);
+  c->d_u = b + o_u;
+
+  launch_state_init(c->st, L, C, E, nullptr);
+  e = hipGetLastError();
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    hipFree(c->dmem);
+    delete c;
+    return fail_hip(e, "state init");
+  }
+
+  // ---- plan records in host-mapped memory
+  void* rh = nullptr;
+  e = hipHostMalloc(&rh, sizeof(PlanRecord) * kRecRing, hipHostMallocMapped | hipHostMallocCoherent);
+  if (e != hipSuccess) {
+    hipFree(c->dmem);
+    delete c;
+    return fail_hip(e, "hipHostMalloc(records)");
+  }
+  std::memset(rh, 0, sizeof(PlanRecord) * kRecRing);
+  void* rd = nullptr;
+  e = hipHostGetDevicePointer(&rd, rh, 0);
+  if (e != hipSuccess) {
+    hipHostFree(rh);
+    hipFree(c->dmem);
+    delete c;
+    return fail_hip(e, "hipHostGetDevicePointer");
+  }
+  c->rec_h = static_cast<PlanRecord*>(rh);
+  c->rec_d = static_cast<PlanRecord*>(rd);
+  for (int i = 0; i < kRecRing; ++i) hipEventCreateWithFlags(&c->rec_ev[i], hipEventDisableTiming);
+
+  // ---- copy engine + scheduler
+  hipStreamCreateWithFlags(&c->eng.stream, hipStreamNonBlocking);
+  c->eng.ev.resize(kCopyRing);
+  for (auto& ev : c->eng.ev) hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+  c->cev.resize(kComputeRing);
+  for (auto& ev : c->cev) hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+  c->eng.compute_ev = &c->cev;
+  const size_t sub = g.copy_subchunk_bytes > 0 ? (size_t)g.copy_subchunk_bytes : ((size_t)16 << 20);
+  const int window = g.copy_window > 0 ? g.copy_window : 2;
+  c->pf = new Prefetcher(L, C, E, c->chunk_bytes, sub, window, c->cache, &c->eng);
+  c->worker = std::thread(worker_main, c);
+  *out = c;
+  return PROMOE_OK;
+}
+
+int promoe_sync(promoe_ctx* c) {
+  if (!c) return PROMOE_EINVAL;
+  {
+    std::unique_lock<std::mutex> lk(c->mu);
+    // flush speculative records and low-priority work, then wait for every copy
+    for (;;) {
+      while (c->rec_ingested < c->rec_pub && c->rec_kind[c->rec_ingested % kRecRing] == 0) {
+        hipEvent_t e = c->rec_ev[c->rec_ingested % kRecRing];
+        const int64_t r = c->rec_ingested;
+        lk.unlock();
+        hipEventSynchronize(e);
+        lk.lock();
+        if (c->rec_ingested == r) ingest_spec(c, r);
+      }
+      c->pf->pump();
+      if (!c->pf->has_low() && c->pf->in_flight() == 0) break;
+      const int64_t seq = c->pf->oldest_in_flight();
+      if (seq >= 0) {
+        hipEvent_t e = c->eng.event(seq);
+        lk.unlock();
+        hipEventSynchronize(e);
+        lk.lock();
+      }
+      c->pf->retire();
+    }
+    if (c->eng.err != hipSuccess) return fail_hip(c->eng.err, "copy engine");
+  }
+  if (c->last_stream) HIPCHK(hipStreamSynchronize(c->last_stream));
+  HIPCHK(hipStreamSynchronize(nullptr));
+  if (c->profile) prof_resolve(c);
+  return PROMOE_OK;
+}
+
+int promoe_destroy(promoe_ctx* c) {
+  if (!c) return PROMOE_EINVAL;
+  {
+    std::lock_guard<std::mutex> lk(c->mu);
+    c->stop = true;
+  }
+  c->cv.notify_all();
+  if (c->worker.joinable()) c->worker.join();
+  hipStreamSynchronize(c->eng.stream);
+  hipDeviceSynchronize();
+  if (c->profile) prof_resolve(c);
+  for (auto& e : c->prof_free) hipEventDestroy(e);
+  for (auto& e : c->eng.ev) hipEventDestroy(e);
+  for (auto& e : c->cev) hipEventDestroy(e);
+  for (int i = 0; i < kRecRing; ++i) hipEventDestroy(c->rec_ev[i]);
+  hipStreamDestroy(c->eng.stream);
+  hipHostFree(c->rec_h);
+  hipFree(c->dmem);
+  delete c->pf;
+  delete c;
+  return PROMOE_OK;
+}
+
+int promoe_set_layer(promoe_ctx* c, int layer, const void* d_wgate, const float* d_bias, const void* d_pw1,
+                     const void* d_pw2, const void* d_shared, const void* d_shared_gate) {
+  if (!c || layer < 0 || layer >= c->L || !d_wgate) return PROMOE_EINVAL;
+  if (c->cfg.router_bias && !d_bias) return PROMOE_EINVAL;
+  if (c->Ish > 0 && !d_shared) return PROMOE_EINVAL;
+  if (c->Ish > 0 && c->cfg.shared_gate && !d_shared_gate) return PROMOE_EINVAL;
+  if (d_pw1 && c->Ph > 0 && !d_pw2) return PROMOE_EINVAL;
+  LayerW& w = c->lw[layer];
+  w.wg = d_wgate;
+  w.bias = c->cfg.router_bias ? d_bias : nullptr;
+  w.pw1 = d_pw1;
+  w.pw2 = c->Ph > 0 ? d_pw2 : nullptr;
+  w.shared = c->Ish > 0 ? d_shared : nullptr;
+  w.sgate = (c->Ish > 0 && c->cfg.shared_gate) ? d_shared_gate : nullptr;
+  return PROMOE_OK;
+}
+
+int promoe_set_attn(promoe_ctx* c, int layer, const void* d_wattn) {
+  if (!c || layer < 0 || layer >= c->L || !d_wattn) return PROMOE_EINVAL;
+  c->lw[layer].attn = d_wattn;
+  return PROMOE_OK;
+}
+
+int promoe_set_expert_host(promoe_ctx* c, int layer, int expert, const void* h_pinned) {
+  if (!c || layer < 0 || layer >= c->L || expert < 0 || expert >= c->E || !h_pinned) return PROMOE_EINVAL;
+  std::lock_guard<std::mutex> lk(c->mu);
+  c->pf->set_host(layer, expert, static_cast<const uint8_t*>(h_pinned));
+  return PROMOE_OK;
+}
+
+int promoe_set_initial_cache(promoe_ctx* c, int layer, const int32_t* h_experts, int n) {
+  if (!c || layer < 0 || layer >= c->L || n < 0 || n > c->C || (n && !h_experts)) return PROMOE_EINVAL;
+  if (c->lw[layer].planned) {
+    g_last_error = "initial cache after the first plan";
+    return PROMOE_ESTATE;
+  }
+  std::vector<int> seen(c->E, 0);
+  for (int i = 0; i < n; ++i) {
+    if (h_experts[i] < 0 || h_experts[i] >= c->E || seen[h_experts[i]]++) return PROMOE_EINVAL;
+    if (!c->pf->host(layer, h_experts[i])) {
+      g_last_error = "expert host buffer not set";
+      return PROMOE_ESTATE;
+    }
+  }
+  for (int i = 0; i < n; ++i) {
+    uint8_t* dst = c->cache + ((size_t)layer * c->C + i) * c->expert_bytes;
+    HIPCHK(hipMemcpy(dst, c->pf->host(layer, h_experts[i]), c->expert_bytes, hipMemcpyHostToDevice));
+  }
+  HIPCHK(hipMemcpy(c->d_warm, h_experts, sizeof(int32_t) * n, hipMemcpyHostToDevice));
+  launch_warm(c->st, layer, c->C, c->E, c->d_warm, n, nullptr);
+  LAUNCHCHK("warm");
+  HIPCHK(hipDeviceSynchronize());
+  std::lock_guard<std::mutex> lk(c->mu);
+  for (int i = 0; i < n; ++i) c->pf->mark_resident(layer, i, h_experts[i]);
+  return PROMOE_OK;
+}
+
+int promoe_predict(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_pred_ids, int32_t* h_q,
+                   int32_t* n_q, void* stream) {
+  if (!c || layer < 0 || layer >= c->L || !d_x || !c->lw[layer].wg) return PROMOE_EINVAL;
+  int rc = check_tokens(c, T);
+  if (rc) return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  c->last_stream = s;
+  const int target = layer + c->D;
+  const bool has_pred = target < c->L && c->lw[layer].pw1 != nullptr;
+  if (has_pred && c->route_layer == target) {
+    g_last_error = "prediction for a layer whose route is not consumed";
+    return PROMOE_ESTATE;
+  }
+  rc = launch_gate_rows(c, layer, d_x, T, has_pred, s);
+  if (rc) return rc;
+  c->gate_layer = layer;
+  c->gate_x = d_x;
+  c->gate_T = T;
+  if (n_q) *n_q = 0;
+  if (!has_pred) return PROMOE_OK;
+  int32_t* pids = d_pred_ids ? d_pred_ids : c->d_pred_ids;
+  TopkArgs tk{};
+  if (c->Ph > 0) {
+    RowsArgs a{};
+    a.w[0] = c->lw[layer].pw2;
+    a.nrows[0] = c->E;
+    a.K = c->Ph;
+    a.x = c->d_logits;
+    a.ldx = c->ld_logits;
+    a.x_off = c->pred_col;
+    a.T = T;
+    a.out = c->d_predq;
+    a.ldo = c->E;
+    a.relu_in = 1;
+    launch_rows_gemv(a, c->dt, PROMOE_F32, s);
+    tk.logits = c->d_predq;
+    tk.ld = c->E;
+  } else {
+    tk.logits = c->d_logits + c->pred_col;
+    tk.ld = c->ld_logits;
+  }
+  tk.E = c->E;
+  tk.k = c->K;
+  tk.T = T;
+  tk.ids = pids;
+  tk.want_weights = 0;
+  tk.sgate_col = -1;
+  launch_topk(tk, s);
+  LAUNCHCHK("predictor");
+  if (c->cfg.flags & PROMOE_FLAG_NO_PREFETCH) return PROMOE_OK;
+  int64_t r;
+  rc = new_record(c, 0, PROMOE_PRIO_LOW, &r);
+  if (rc) return rc;
+  launch_plan_spec(plan_args(c, target, pids, T, r), s);
+  hipError_t le = hipGetLastError();
+  if (le == hipSuccess) le = hipEventRecord(c->rec_ev[r % kRecRing], s);
+  publish(c, r);
+  if (le != hipSuccess) return fail_hip(le, "plan_spec");
+  c->lw[target].planned = true;
+  if (h_q || n_q) {
+    HIPCHK(hipEventSynchronize(c->rec_ev[r % kRecRing]));
+    const PlanRecord& rec = c->rec_h[r % kRecRing];
+    if (n_q) *n_q = rec.n;
+    if (h_q)
+      for (int i = 0; i < rec.n; ++i) h_q[i] = rec.expert[i];
+  }
+  return PROMOE_OK;
+}
+
+int promoe_prefetch(promoe_ctx* c, int target_layer, const int32_t* h_ids, int n, int prio, void* stream) {
+  if (!c || target_layer < 0 || target_layer >= c->L || n < 0 || n > c->C || (n && !h_ids)) return PROMOE_EINVAL;
+  if (prio != PROMOE_PRIO_LOW && prio != PROMOE_PRIO_HIGH) return PROMOE_EINVAL;
+  std::vector<int> seen(c->E, 0);
+  for (int i = 0; i < n; ++i)
+    if (h_ids[i] < 0 || h_ids[i] >= c->E || seen[h_ids[i]]++) return PROMOE_EINVAL;
+  if (c->route_layer == target_layer) {
+    g_last_error = "prefetch for a layer whose route is not consumed";
+    return PROMOE_ESTATE;
+  }
+  if (c->cfg.flags & PROMOE_FLAG_NO_PREFETCH) return PROMOE_OK;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  c->last_stream = s;
+  int64_t r;
+  int rc = new_record(c, 0, prio, &r);
+  if (rc) return rc;
+  PlanRecord& rec = c->rec_h[r % kRecRing];
+  rec.n_q_in = n;
+  for (int i = 0; i < n; ++i) rec.q_in[i] = h_ids[i];
+  launch_plan_spec(plan_args(c, target_layer, nullptr, 0, r), s);
+  hipError_t le = hipGetLastError();
+  if (le == hipSuccess) le = hipEventRecord(c->rec_ev[r % kRecRing], s);
+  publish(c, r);
+  if (le != hipSuccess) return fail_hip(le, "plan_spec");
+  c->lw[target_layer].planned = true;
+  return PROMOE_OK;
+}
+
+int promoe_route(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_ids, float* d_w,
+                 float* d_shared_scale, int32_t* h_order, int32_t* n_order, void* stream) {
+  if (!c || layer < 0 || layer >= c->L || !d_x || !d_ids || !d_w || !c->lw[layer].wg) return PROMOE_EINVAL;
+  if (c->cfg.shared_gate && c->Ish > 0 && !d_shared_scale) return PROMOE_EINVAL;
+  int rc = check_tokens(c, T);
+  if (rc) return rc;
+  if (c->route_layer >= 0) {
+    g_last_error = "previous route not consumed by promoe_expert_ffn";
+    return PROMOE_ESTATE;
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  c->last_stream = s;
+  if (!(c->gate_layer == layer && c->gate_x == d_x && c->gate_T == T)) {
+    rc = launch_gate_rows(c, layer, d_x, T, false, s);
+    if (rc) return rc;
+  }
+  c->gate_layer = -1;
+  TopkArgs tk{};
+  tk.logits = c->d_logits;
+  tk.ld = c->ld_logits;
+  tk.E = c->E;
+  tk.k = c->K;
+  tk.T = T;
+  tk.bias = c->lw[layer].bias;
+  tk.renorm = c->cfg.renorm;
+  tk.want_weights = 1;
+  tk.ids = d_ids;
+  tk.w = d_w;
+  const bool sg = c->cfg.shared_gate && c->Ish > 0;
+  tk.sgate_col = sg ? c->E : -1;
+  tk.sscale = sg ? d_shared_scale : nullptr;
+  launch_topk(tk, s);
+  LAUNCHCHK("route topk");
+  int64_t r;
+  rc = new_record(c, 1, PROMOE_PRIO_HIGH, &r);
+  if (rc) return rc;
+  launch_plan_precise(plan_args(c, layer, d_ids, T, r), s);
+  hipError_t le = hipGetLastError();
+  if (le == hipSuccess) le = hipEventRecord(c->rec_ev[r % kRecRing], s);
+  if (le == hipSuccess) le = hipEventSynchronize(c->rec_ev[r % kRecRing]);
+  publish(c, r);
+  if (le != hipSuccess) return fail_hip(le, "plan_precise");
+  c->lw[layer].planned = true;
+
+  std::unique_lock<std::mutex> lk(c->mu);
+  while (c->rec_ingested < r) {  // earlier plans on the same stream: complete
+    HIPCHK(hipEventSynchronize(c->rec_ev[c->rec_ingested % kRecRing]));
+    ingest_spec(c, c->rec_ingested);
+  }
+  const PlanRecord rec = c->rec_h[r % kRecRing];
+  c->rec_ingested = r + 1;
+  c->last_precise[layer] = rec;
+  c->pf->purge_low(layer);
+  c->need01.assign(rec.n, -1);
+  c->need2.assign(rec.n, -1);
+  c->deferred.clear();
+  for (int pos = 0; pos < rec.n; ++pos) {
+    const int slot = rec.slot[pos];
+    if (rec.flag[pos]) {
+      if (rec.after[pos] >= 0) {
+        c->deferred.push_back(Deferred{pos, slot, rec.expert[pos], rec.after[pos]});
+        continue;
+      }
+      c->pf->assign(layer, slot, rec.expert[pos]);
+    }
+    c->pf->issue_high(layer, slot);
+    c->need01[pos] = c->pf->ready_seq(layer, slot, 1);
+    c->need2[pos] = c->pf->ready_seq(layer, slot, 2);
+  }
+  if (c->eng.err != hipSuccess) return fail_hip(c->eng.err, "copy engine");
+  lk.unlock();
+  c->cv.notify_all();
+  c->route_layer = layer;
+  c->route_T = T;
+  c->route_rec = rec;
+  if (h_order)
+    for (int i = 0; i < rec.n; ++i) h_order[i] = rec.expert[i];
+  if (n_order) *n_order = rec.n;
+  return PROMOE_OK;
+}
+
+namespace {
+
+// Launch gate/up and down passes for a list of positions.
+int ffn_launch(promoe_ctx* c, FfnArgs a, const std::vector<int>& plist, hipStream_t s, int64_t wait01,
+               int64_t wait2) {
+  const PlanRecord& rec = c->route_rec;
+  int maxc = 1;
+  for (size_t i = 0; i < plist.size(); ++i) {
+    a.pos_list[i] = (uint8_t)plist[i];
+    maxc = std::max(maxc, rec.count[plist[i]]);
+  }
+  const double wbytes = (double)c->chunk_bytes * plist.size();
+  double pairs = 0;  // token-expert pairs in the launch
+  for (int p : plist) pairs += rec.count[p];
+  const double melems = (double)c->I * c->H;  // elements of one expert matrix
+  for (int pass = 0; pass < 2; ++pass) {
+    const int64_t w = pass == 0 ? wait01 : wait2;
+    if (w >= 0) {
+      hipEvent_t pa = nullptr, pb = nullptr;
+      if (c->profile) { pa = prof_event(c); pb = prof_event(c); hipEventRecord(pa, s); }
+      HIPCHK(hipStreamWaitEvent(s, c->eng.event(w), 0));
+      if (c->profile) { hipEventRecord(pb, s); c->prof_pending.push_back(ProfEntry{pa, pb, 4, 0, 0}); }
+    }
+    hipEvent_t ka = nullptr, kb = nullptr;
+    if (c->profile) { ka = prof_event(c); kb = prof_event(c); hipEventRecord(ka, s); }
+    launch_ffn(a, pass, (int)plist.size(), maxc, c->dt, s);
+    LAUNCHCHK("ffn");
+    if (c->profile) {
+      hipEventRecord(kb, s);
+      const double by = pass == 0 ? 2 * wbytes : wbytes;
+      c->prof_pending.push_back(ProfEntry{ka, kb, pass, by, 2.0 * pairs * melems * (pass == 0 ? 2 : 1)});
+    }
+  }
+  return PROMOE_OK;
+}
+
+}  // namespace
+
+int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const int32_t* d_ids, const float* d_w,
+                      const float* d_shared_scale, void* d_y, void* stream) {
+  if (!c || layer < 0 || layer >= c->L || !d_x || !d_ids || !d_w || !d_y) return PROMOE_EINVAL;
+  if (c->route_layer != layer || c->route_T != T) {
+    g_last_error = "expert_ffn without a matching route";
+    return PROMOE_ESTATE;
+  }
+  if (c->cfg.shared_gate && c->Ish > 0 && !d_shared_scale) return PROMOE_EINVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  c->last_stream = s;
+  const PlanRecord& rec = c->route_rec;
+  FfnArgs a{};
+  a.cache = c->cache;
+  a.expert_bytes = (int64_t)c->expert_bytes;
+  a.layer = layer;
+  a.slots = c->C;
+  a.order_slot = c->d_order_slot;
+  a.offsets = c->d_offsets;
+  a.perm = c->d_perm;
+  a.hidden = c->H;
+  a.inter = c->I;
+  a.top_k = c->K;
+  a.T = T;
+  a.x = d_x;
+  a.act = c->d_act;
+  a.Y = c->d_Y;
+  a.shared_inter = c->Ish;
+  a.act_sh = c->d_act_sh;
+  a.Ysh = c->d_Ysh;
+
+  // shared expert first: resident, never waits
+  if (c->Ish > 0) {
+    FfnArgs sa = a;
+    sa.shared = 1;
+    sa.shared_w = c->lw[layer].shared;
+    const int mt = std::min(T, 8);
+    for (int pass = 0; pass < 2; ++pass) {
+      hipEvent_t ka = nullptr, kb = nullptr;
+      if (c->profile) { ka = prof_event(c); kb = prof_event(c); hipEventRecord(ka, s); }
+      sa.pos_list[0] = 0;
+      launch_ffn(sa, pass, 1, mt, c->dt, s);
+      LAUNCHCHK("ffn shared");
+      if (c->profile) {
+        hipEventRecord(kb, s);
+        const double by = (double)c->Ish * c->H * c->eb * (pass == 0 ? 2 : 1);
+        c->prof_pending.push_back(ProfEntry{ka, kb, pass, by, 2.0 * T * (by / c->eb)});  // T tokens x weights
+      }
+    }
+  }
+
+  std::unique_lock<std::mutex> lk(c->mu);
+  const int n = rec.n;
+  std::vector<char> done(n, 0);
+  std::vector<int> ready;
+  std::vector<char> is_def(n, 0);
+  for (const auto& d : c->deferred) is_def[d.pos] = 1;
+  for (int p = 0; p < n; ++p)
+    if (!is_def[p] && c->need01[p] < 0 && c->need2[p] < 0) ready.push_back(p);
+
+  auto after_launch = [&](const std::vector<int>& plist) {
+    const int64_t tok = record_compute(c, s);
+    for (int p : plist) {
+      c->pf->set_last_read(layer, rec.slot[p], tok);
+      done[p] = 1;
+    }
+    // release fills that waited for these positions' reads
+    for (const auto& d : c->deferred) {
+      if (std::find(plist.begin(), plist.end(), d.after) == plist.end()) continue;
+      c->pf->assign(layer, d.slot, d.expert);
+      c->pf->issue_high_after(layer, d.slot, tok);
+      c->need01[d.pos] = c->pf->ready_seq(layer, d.slot, 1);
+      c->need2[d.pos] = c->pf->ready_seq(layer, d.slot, 2);
+    }
+  };
+
+  int rc = PROMOE_OK;
+  if (!ready.empty()) {
+    rc = ffn_launch(c, a, ready, s, -1, -1);
+    if (rc) return rc;
+    after_launch(ready);
+  }
+  for (int p = 0; p < n; ++p) {
+    if (done[p]) continue;
+    std::vector<int> one(1, p);
+    rc = ffn_launch(c, a, one, s, c->need01[p], c->need2[p]);
+    if (rc) return rc;
+    after_launch(one);
+  }
+  if (c->eng.err != hipSuccess) return fail_hip(c->eng.err, "copy engine");
+  lk.unlock();
+  c->cv.notify_all();
+
+  CombineArgs ca{};
+  ca.Y = c->d_Y;
+  ca.w = d_w;
+  ca.Ysh = c->Ish > 0 ? c->d_Ysh : nullptr;
+  ca.sscale = (c->Ish > 0 && c->cfg.shared_gate) ? d_shared_scale : nullptr;
+  ca.y = d_y;
+  ca.hidden = c->H;
+  ca.top_k = c->K;
+  launch_combine(ca, T, c->dt, s);
+  LAUNCHCHK("combine");
+  c->route_layer = -1;
+  if (c->profile && c->prof_pending.size() > 4096) {
+    HIPCHK(hipStreamSynchronize(s));
+    prof_resolve(c);
+  }
+  return PROMOE_OK;
+}
+
+int promoe_cache_stats(promoe_ctx* c, int layer, promoe_stats* out) {
+  if (!c || !out || layer < -1 || layer >= c->L) return PROMOE_EINVAL;
+  int rc = promoe_sync(c);
+  if (rc) return rc;
+  std::vector<int64_t> cnt((size_t)c->L * 8);
+  HIPCHK(hipMemcpy(cnt.data(), c->st.counters, sizeof(int64_t) * cnt.size(), hipMemcpyDeviceToHost));
+  std::memset(out, 0, sizeof(*out));
+  int64_t* dst = &out->prec_access;
+  for (int l = 0; l < c->L; ++l) {
+    if (layer >= 0 && l != layer) continue;
+    for (int i = 0; i < 8; ++i) dst[i] += cnt[(size_t)l * 8 + i];
+  }
+  std::lock_guard<std::mutex> lk(c->mu);
+  const PhysStats& ps = c->pf->stats();
+  out->copies_low = ps.copies[0];
+  out->copies_high = ps.copies[1];
+  out->bytes_low = ps.bytes[0];
+  out->bytes_high = ps.bytes[1];
+  out->low_purged = ps.low_purged;
+  out->deferred = ps.deferred;
+  for (int i = 0; i < 4; ++i) {
+    out->k_launches[i] = c->k_launches[i];
+    out->k_ms[i] = c->k_ms[i];
+    out->k_bytes[i] = c->k_bytes[i];
+    out->k_flops[i] = c->k_flops[i];
+  }
+  out->stall_ms = c->stall_ms;
+  return PROMOE_OK;
+}
+
+int promoe_reset_stats(promoe_ctx* c) {
+  if (!c) return PROMOE_EINVAL;
+  int rc = promoe_sync(c);
+  if (rc) return rc;
+  std::lock_guard<std::mutex> lk(c->mu);
+  c->pf->reset_stats();
+  for (int i = 0; i < 4; ++i) c->k_launches[i] = 0, c->k_ms[i] = c->k_bytes[i] = c->k_flops[i] = 0.0;
+  c->stall_ms = 0.0;
+  return PROMOE_OK;
+}
+
+int promoe_slot_table(promoe_ctx* c, int layer, int32_t* h_slot_of) {
+  if (!c || !h_slot_of || layer < 0 || layer >= c->L) return PROMOE_EINVAL;
+  int rc = promoe_sync(c);
+  if (rc) return rc;
+  HIPCHK(hipMemcpy(h_slot_of, c->st.slot_of + (size_t)layer * c->E, sizeof(int32_t) * c->E, hipMemcpyDeviceToHost));
+  return PROMOE_OK;
+}
+
+int promoe_last_plan(promoe_ctx* c, int layer, int kind, promoe_plan* out) {
+  if (!c || !out || layer < 0 || layer >= c->L || (kind != 0 && kind != 1)) return PROMOE_EINVAL;
+  int rc = promoe_sync(c);
+  if (rc) return rc;
+  std::lock_guard<std::mutex> lk(c->mu);
+  const PlanRecord& r = kind == 0 ? c->last_spec[layer] : c->last_precise[layer];
+  out->n = r.n;
+  for (int i = 0; i < 64; ++i) {
+    out->expert[i] = r.expert[i];
+    out->slot[i] = r.slot[i];
+    out->flag[i] = r.flag[i];
+    out->victim[i] = r.victim[i];
+    out->after[i] = r.after[i];
+    out->count[i] = r.count[i];
+  }
+  return PROMOE_OK;
+}
+
+int promoe_attn_surrogate(promoe_ctx* c, int layer, float* d_h, int T, void* d_x_out, void* stream) {
+  if (!c || layer < 0 || layer >= c->L || !d_h || !d_x_out) return PROMOE_EINVAL;
+  int rc = check_tokens(c, T);
+  if (rc) return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  c->last_stream = s;
+  if (c->lw[layer].attn) {
+    launch_rmsnorm_quant(d_h, c->d_u, T, c->H, c->dt, s);
+    RowsArgs a{};
+    a.w[0] = c->lw[layer].attn;
+    a.nrows[0] = c->H;
+    a.K = c->H;
+    a.x = c->d_u;
+    a.ldx = c->H;
+    a.T = T;
+    a.out = d_h;
+    a.ldo = c->H;
+    a.add = 1;
+    launch_rows_gemv(a, c->dt, c->dt, s);
+  }
+  launch_rmsnorm_quant(d_h, d_x_out, T, c->H, c->dt, s);
+  LAUNCHCHK("attn surrogate");
+  return PROMOE_OK;
+}
+
+int promoe_residual_add(promoe_ctx* c, float* d_h, const void* d_y, int T, void* stream) {
+  if (!c || !d_h || !d_y) return PROMOE_EINVAL;
+  int rc = check_tokens(c, T);
+  if (rc) return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  c->last_stream = s;
+  launch_residual_add(d_h, d_y, T * c->H, c->dt, s);
+  LAUNCHCHK("residual");
+  return PROMOE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,153 @@
+#include "scheduler.hpp"
+
+#include <algorithm>
+
+namespace promoe {
+
+Prefetcher::Prefetcher(int n_layers, int slots, int n_experts, size_t chunk_bytes, size_t sub_bytes,
+                       int window, uint8_t* cache_base, CopyEngine* engine)
+    : L_(n_layers), C_(slots), E_(n_experts), chunk_bytes_(chunk_bytes),
+      sub_bytes_(std::min(sub_bytes, chunk_bytes)), window_(window < 1 ? 1 : window), cache_(cache_base),
+      eng_(engine), host_((size_t)n_layers * n_experts, nullptr), slots_((size_t)n_layers * slots) {
+  n_sub_ = (int)((chunk_bytes_ + sub_bytes_ - 1) / sub_bytes_);
+}
+
+void Prefetcher::set_host(int layer, int expert, const uint8_t* p) { host_[layer * E_ + expert] = p; }
+
+void Prefetcher::assign(int layer, int slot, int expert) {
+  Slot& s = slot_(layer, slot);
+  // cancel queued low-priority work aimed at this slot (it belongs to the old expert)
+  for (auto it = low_.begin(); it != low_.end();) {
+    if (it->layer == layer && it->slot == slot) it = low_.erase(it);
+    else ++it;
+  }
+  s.expert = expert;
+  for (auto& c : s.ch) c = Chunk();
+}
+
+void Prefetcher::mark_resident(int layer, int slot, int expert) {
+  assign(layer, slot, expert);
+  for (auto& c : slot_(layer, slot).ch) {
+    c.n_issued = n_sub_;
+    c.last = -1;
+  }
+}
+
+void Prefetcher::push_low(int layer, int slot) {
+  Slot& s = slot_(layer, slot);
+  if (s.expert < 0) return;
+  for (int c = 0; c < kChunks; ++c) {
+    Chunk& ch = s.ch[c];
+    if (ch.queued || ch.n_issued == n_sub_) continue;  // dedupe: queued, in flight or copied
+    ch.queued = true;
+    low_.push_back(LowTask{layer, slot, c, s.expert});
+  }
+}
+
+void Prefetcher::purge_low(int layer) {
+  for (auto it = low_.begin(); it != low_.end();) {
+    if (it->layer == layer) {
+      Chunk& ch = slot_(it->layer, it->slot).ch[it->chunk];
+      st_.low_purged += n_sub_ - ch.n_issued;
+      ch.queued = false;
+      it = low_.erase(it);
+    } else {
+      ++it;
+    }
+  }
+}
+
+void Prefetcher::issue_sub(int layer, int slot, int chunk, Prio prio, int64_t after_compute) {
+  Slot& s = slot_(layer, slot);
+  Chunk& ch = s.ch[chunk];
+  const size_t off = (size_t)ch.n_issued * sub_bytes_;
+  const size_t bytes = std::min(sub_bytes_, chunk_bytes_ - off);
+  const size_t slot_off = ((size_t)layer * C_ + slot) * (kChunks * chunk_bytes_) + chunk * chunk_bytes_ + off;
+  const uint8_t* src = host_[layer * E_ + s.expert] + chunk * chunk_bytes_ + off;
+  // write-after-read: the fill must follow every compute that read the old contents
+  int64_t after = std::max(after_compute, s.last_read);
+  while (next_seq_ - retired_ >= eng_->capacity()) {  // keep the engine's event ring from wrapping
+    eng_->wait(retired_);
+    retire();
+  }
+  int64_t seq = next_seq_++;
+  eng_->issue(seq, cache_ + slot_off, src, bytes, after);
+  ch.n_issued++;
+  ch.last = seq;
+  st_.copies[prio]++;
+  st_.bytes[prio] += (int64_t)bytes;
+}
+
+void Prefetcher::issue_high(int layer, int slot) {
+  Slot& s = slot_(layer, slot);
+  if (s.expert < 0) return;
+  for (int c = 0; c < kChunks; ++c) {
+    Chunk& ch = s.ch[c];
+    if (ch.queued) {
+      // promote: drop the queued low-priority task for this chunk
+      for (auto it = low_.begin(); it != low_.end(); ++it)
+        if (it->layer == layer && it->slot == slot && it->chunk == c) { low_.erase(it); break; }
+      ch.queued = false;
+    }
+    while (ch.n_issued < n_sub_) issue_sub(layer, slot, c, HIGH, -1);
+  }
+}
+
+void Prefetcher::issue_high_after(int layer, int slot, int64_t after_compute) {
+  Slot& s = slot_(layer, slot);
+  if (s.expert < 0) return;
+  st_.deferred++;
+  bool first = true;
+  for (int c = 0; c < kChunks; ++c) {
+    Chunk& ch = s.ch[c];
+    ch.queued = false;
+    while (ch.n_issued < n_sub_) {
+      issue_sub(layer, slot, c, HIGH, first ? after_compute : -1);
+      first = false;
+    }
+  }
+}
+
+int Prefetcher::pump() {
+  int n = 0;
+  retire();
+  while (!low_.empty() && in_flight() < window_) {
+    LowTask t = low_.front();
+    Slot& s = slot_(t.layer, t.slot);
+    Chunk& ch = s.ch[t.chunk];
+    if (s.expert != t.expert || ch.n_issued == n_sub_) {  // stale or already served
+      ch.queued = false;
+      low_.pop_front();
+      continue;
+    }
+    issue_sub(t.layer, t.slot, t.chunk, LOW, -1);
+    ++n;
+    if (ch.n_issued == n_sub_) {
+      ch.queued = false;
+      low_.pop_front();
+    }
+  }
+  return n;
+}
+
+void Prefetcher::retire() {
+  while (retired_ < next_seq_ && eng_->done(retired_)) ++retired_;
+}
+
+int64_t Prefetcher::ready_seq(int layer, int slot, int upto_chunk) const {
+  const Slot& s = slot_(layer, slot);
+  int64_t need = -1;
+  for (int c = 0; c <= upto_chunk; ++c) {
+    const Chunk& ch = s.ch[c];
+    if (ch.n_issued < n_sub_) return -2;
+    if (ch.last >= retired_) need = std::max(need, ch.last);
+  }
+  return need;
+}
+
+void Prefetcher::set_last_read(int layer, int slot, int64_t tok) {
+  Slot& s = slot_(layer, slot);
+  s.last_read = std::max(s.last_read, tok);
+}
+
+}  // namespace promoe

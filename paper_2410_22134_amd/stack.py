@@ -1,0 +1,47 @@
+"""Stack driver: the transformer-layer loop around the MoE block for the
+synthetic configs (prefill or decode steps), calling the library per layer:
+attention surrogate -> predict -> route -> expert_ffn -> residual add."""
+from __future__ import annotations
+
+from .model import SyntheticModel
+
+
+class Stack:
+    def __init__(self, model: SyntheticModel, T: int):
+        import torch
+        cfg = model.cfg
+        self.m, self.T = model, T
+        dev = model.device
+        xdt = torch.int16 if cfg.dtype == "bf16" else torch.float32
+        H, k = cfg.hidden, cfg.top_k
+        self.h = torch.zeros(T, H, dtype=torch.float32, device=dev)
+        self.x = torch.zeros(T, H, dtype=xdt, device=dev)
+        self.y = torch.zeros(T, H, dtype=xdt, device=dev)
+        self.ids = torch.zeros(T, k, dtype=torch.int32, device=dev)
+        self.w = torch.zeros(T, k, dtype=torch.float32, device=dev)
+        self.s = torch.zeros(T, dtype=torch.float32, device=dev)
+        self.pred_ids = torch.zeros(T, k, dtype=torch.int32, device=dev)
+
+    def moe_layer(self, l: int, predict: bool = True, want_q: bool = False, stream=None):
+        """predict -> route -> ffn on self.x; returns (order, q)."""
+        ctx, T = self.m.ctx, self.T
+        q = ctx.predict(l, self.x, T, self.pred_ids, want_q=want_q, stream=stream) if predict else None
+        order = ctx.route(l, self.x, T, self.ids, self.w, self.s, stream=stream)
+        ctx.expert_ffn(l, self.x, T, self.ids, self.w, self.s, self.y, stream=stream)
+        return order, q
+
+    def step(self, h0, predict: bool = True, record=None, stream=None):
+        """One step over all layers from residual input h0 [T, H] (fp32, device)."""
+        ctx, T = self.m.ctx, self.T
+        self.h.copy_(h0)
+        for l in range(self.m.cfg.n_layers):
+            if record is not None:
+                record("h", l, self)
+            ctx.attn_surrogate(l, self.h, T, self.x, stream=stream)
+            if record is not None:
+                record("x", l, self)
+            order, q = self.moe_layer(l, predict, want_q=record is not None, stream=stream)
+            if record is not None:
+                record("moe", l, self, order=order, q=q)
+            ctx.residual_add(self.h, self.y, T, stream=stream)
+        return self.h

@@ -1,0 +1,191 @@
+"""Helpers for GPU-vs-oracle parity tests (teacher-forced per layer).
+
+The GPU path runs through the C ABI; every layer's inputs and outputs are
+copied back and checked against the oracle computed on the same inputs:
+  * routing ids exactly where the oracle's logit margin exceeds 1e-3, weights
+    within 1e-4 (fp32), evaluated on the GPU's own ids;
+  * predictor ids exactly where margins exceed 1e-3; the merged list Q exactly,
+    given the GPU's per-token ids;
+  * plans (order, slots, misses, victims, fill dependencies, token counts),
+    slot tables and counters exactly, by replaying the oracle's cache with the
+    GPU's routing;
+  * MoE outputs within the stated tolerances (bf16: max-abs <= 2e-2 and
+    rel-L2 < 1e-2; fp32: max-abs <= 1e-4).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle
+from oracle import bf16 as obf16
+from oracle import cache as ocache
+from oracle import ffn as offn
+from oracle import predictor as opred
+from oracle import router as orouter
+from oracle import stack as ostack
+from synth import model as sm
+
+MARGIN = 1e-3
+TOL_BF16_MAXABS, TOL_BF16_RELL2, TOL_F32 = 2e-2, 1e-2, 1e-4
+
+
+def to_np(t):
+    import torch
+    a = t.detach().cpu()
+    if a.dtype == torch.int16:
+        return a.numpy().view(np.uint16)
+    return a.numpy()
+
+
+def f64(a, dtype):
+    return obf16.to_f64(a, dtype)
+
+
+class LayerRecord:
+    def __init__(self):
+        self.h_in = None
+        self.x = None
+        self.ids = self.w = self.s = self.y = self.pred_ids = None
+        self.order = self.q = None
+        self.spec_plan = self.precise_plan = None
+
+
+def recorder(model, records):
+    """Record callback for Stack.step."""
+    ctx = model.ctx
+    cfg = model.cfg
+
+    def cb(stage, l, st, order=None, q=None):
+        if stage == "h":
+            records.setdefault(l, LayerRecord()).h_in = to_np(st.h).astype(np.float64)
+        elif stage == "x":
+            records.setdefault(l, LayerRecord()).x = to_np(st.x).copy()
+        else:
+            r = records.setdefault(l, LayerRecord())
+            r.ids, r.w, r.s, r.y = to_np(st.ids).copy(), to_np(st.w).copy(), to_np(st.s).copy(), to_np(st.y).copy()
+            r.pred_ids = to_np(st.pred_ids).copy()
+            r.order, r.q = order, q
+            r.precise_plan = ctx.last_plan(l, 1)
+            tgt = sm.predictor_target(cfg, l)
+            if q is not None and tgt is not None:
+                r.spec_plan = ctx.last_plan(tgt, 0)
+    return cb
+
+
+def check_route(cfg, model, l, x64, rec, ids_ok_frac=None):
+    """Route: ids where margins allow, weights on the GPU's ids, shared scale."""
+    E, k = cfg.n_experts, cfg.top_k
+    wg = f64(model.np_gate[l], cfg.dtype)
+    z = orouter.gate_logits(x64, wg, model.np_bias[l])
+    ids_o, w_o, p = orouter.route(z, k, bool(cfg.renorm))
+    bnd, inner = orouter.margins(z, k)
+    clear = bnd > MARGIN
+    g_ids = rec.ids.astype(np.int64)
+    assert np.all((g_ids >= 0) & (g_ids < E))
+    for t in np.nonzero(clear)[0]:
+        assert set(g_ids[t]) == set(ids_o[t]), (l, t, g_ids[t], ids_o[t])
+        if inner[t] > MARGIN:
+            assert list(g_ids[t]) == list(ids_o[t]), (l, t)
+    # every token: ids distinct, and each selected logit >= every unselected one - margin
+    for t in range(x64.shape[0]):
+        assert len(set(g_ids[t])) == k
+        sel = z[t, g_ids[t]]
+        rest = np.delete(z[t], g_ids[t])
+        assert sel.min() >= (rest.max() if rest.size else -np.inf) - MARGIN
+    w_ref = orouter.weights_for(p, g_ids, bool(cfg.renorm))
+    assert np.max(np.abs(rec.w - w_ref)) <= TOL_F32, np.max(np.abs(rec.w - w_ref))
+    if cfg.renorm:
+        assert np.allclose(rec.w.sum(1), 1.0, atol=1e-6)
+    s_ref = None
+    if cfg.n_shared and cfg.shared_gate:
+        s_ref = orouter.shared_scale(x64, f64(model.np_sgate[l], cfg.dtype))
+        assert np.max(np.abs(rec.s - s_ref)) <= TOL_F32
+    return g_ids, w_ref, s_ref, clear.mean()
+
+
+def check_predictor(cfg, model, l, x64, rec):
+    pred = model.np_pred[l]
+    if pred is None or rec.q is None:
+        return None
+    w1 = f64(pred[0], cfg.dtype)
+    w2 = None if pred[1] is None else f64(pred[1], cfg.dtype)
+    q = opred.logits(x64, w1, w2)
+    k = cfg.top_k
+    ids_o = opred.per_token(q, k)
+    bnd, inner = orouter.margins(q, k)
+    g = rec.pred_ids.astype(np.int64)
+    for t in np.nonzero(bnd > MARGIN)[0]:
+        assert set(g[t]) == set(ids_o[t]), (l, t)
+        if inner[t] > MARGIN:
+            assert list(g[t]) == list(ids_o[t])
+    Q, _, _ = opred.vote(g, cfg.n_experts, cfg.slots)
+    assert rec.q == Q, (l, rec.q, Q)
+    return Q
+
+
+def check_ffn(cfg, model, l, x64, g_ids, w_ref, s_ref, y_gpu, tokens=None):
+    """MoE output on the GPU's routing; tokens = optional sample of rows."""
+    if tokens is not None:
+        x64, g_ids, w_ref = x64[tokens], g_ids[tokens], w_ref[tokens]
+        s_ref = None if s_ref is None else s_ref[tokens]
+        y_gpu = y_gpu[tokens]
+    def expert_fn(e):  # called once per distinct expert
+        wg, wu, wd = sm.expert_from_bytes(cfg, model.expert_host(l, e))
+        return f64(wg, cfg.dtype), f64(wu, cfg.dtype), f64(wd, cfg.dtype)
+
+    parts = None
+    if cfg.n_shared:
+        parts = [tuple(f64(m, cfg.dtype) for m in p) for p in sm.shared_parts(cfg, l)]
+    act_bf16 = cfg.dtype == "bf16"
+    y = offn.moe_forward(x64, g_ids, w_ref, expert_fn, act_bf16, parts, s_ref)
+    y_ref = offn.round_out(y, cfg.dtype)
+    yg = f64(y_gpu, cfg.dtype)
+    err = np.abs(yg - y_ref)
+    if cfg.dtype == "bf16":
+        rel = np.linalg.norm(yg - y) / max(np.linalg.norm(y), 1e-30)
+        assert err.max() <= TOL_BF16_MAXABS and rel < TOL_BF16_RELL2, (l, err.max(), rel)
+        return err.max(), rel
+    assert err.max() <= TOL_F32, (l, err.max())
+    return err.max(), None
+
+
+def check_plan_precise(lc: ocache.LayerCache, g_ids, gpu_plan):
+    P = np.unique(g_ids)
+    order, entries = lc.precise_plan(P.tolist())
+    assert gpu_plan["expert"] == order, (gpu_plan["expert"], order)
+    assert gpu_plan["slot"] == [e.slot for e in entries]
+    assert gpu_plan["flag"] == [int(e.miss) for e in entries]
+    assert gpu_plan["victim"] == [e.victim for e in entries]
+    assert gpu_plan["after"] == [e.after for e in entries]
+    counts = [int((g_ids == e).sum()) for e in order]
+    assert gpu_plan["count"] == counts
+    return order
+
+
+def check_plan_spec(lc: ocache.LayerCache, Q, gpu_plan):
+    entries = lc.spec_plan(Q)
+    assert gpu_plan["expert"] == [e.expert for e in entries]
+    assert gpu_plan["slot"] == [e.slot for e in entries]
+    assert gpu_plan["flag"] == [int(e.new) for e in entries]
+    assert gpu_plan["victim"] == [e.victim for e in entries]
+
+
+def check_counters(model, lc_by_layer):
+    for l, lc in lc_by_layer.items():
+        st = model.ctx.stats(l)
+        for c in ocache.COUNTERS:
+            assert st[c] == lc.count[c], (l, c, st[c], lc.count[c])
+        slot_of = model.ctx.slot_table(l)
+        assert slot_of == lc.slot_of, (l, slot_of, lc.slot_of)
+
+
+def check_harness(cfg, model, l, rec):
+    """x = q(rms(h + Wa q(rms(h)))) on the GPU's h."""
+    if rec.h_in is None:
+        return
+    wa = f64(sm.attn(cfg, l), cfg.dtype)
+    h1 = ostack.attn_surrogate(rec.h_in, wa, cfg.dtype)
+    x_ref = ostack.moe_input(h1, cfg.dtype)
+    xg = f64(rec.x, cfg.dtype)
+    # at most one bf16 ulp apart (rounding of values that differ in the last fp32 bits)
+    assert np.all(np.abs(xg - x_ref) <= np.abs(x_ref) * 2.0 ** -7 + 1e-6), np.max(np.abs(xg - x_ref))

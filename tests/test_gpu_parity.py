@@ -1,0 +1,131 @@
+"""GPU parity through the C ABI against the CPU oracle (teacher-forced per layer).
+
+Workload shapes are the five synthetic configs; stacks are cut to the layers a
+look-ahead needs (d + 2) so every plan kind is exercised at the full per-layer
+shape.  Large prefill outputs are checked on a seeded sample of tokens."""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import parity_util as pu  # noqa: E402
+from oracle import cache as ocache  # noqa: E402
+from synth import configs, model as sm  # noqa: E402
+
+from paper_2410_22134_amd import FLAG_NO_PREFETCH  # noqa: E402
+from paper_2410_22134_amd.model import SyntheticModel  # noqa: E402
+from paper_2410_22134_amd.stack import Stack  # noqa: E402
+
+
+def _log(*a):
+    print(*a, flush=True)
+
+
+def _moe_layer_check(cfg, m, st, l, lcs, x_np, sample=None):
+    """Run predict/route/ffn of layer l on x and check everything against the oracle."""
+    st.x.copy_(torch.from_numpy(x_np.view(np.int16) if x_np.dtype == np.uint16 else x_np).cuda())
+    order, q = st.moe_layer(l, predict=True, want_q=True)
+    rec = pu.LayerRecord()
+    rec.x = x_np
+    rec.ids, rec.w, rec.s, rec.y = (pu.to_np(t).copy() for t in (st.ids, st.w, st.s, st.y))
+    rec.pred_ids = pu.to_np(st.pred_ids).copy()
+    rec.order, rec.q = order, q
+    x64 = pu.f64(x_np, cfg.dtype)
+    tgt = sm.predictor_target(cfg, l)
+    if tgt is not None and m.np_pred[l] is not None:
+        Q = pu.check_predictor(cfg, m, l, x64, rec)
+        pu.check_plan_spec(lcs[tgt], Q, m.ctx.last_plan(tgt, 0))
+    g_ids, w_ref, s_ref, clear = pu.check_route(cfg, m, l, x64, rec)
+    pu.check_plan_precise(lcs[l], g_ids, m.ctx.last_plan(l, 1))
+    assert rec.order == m.ctx.last_plan(l, 1)["expert"]
+    err = pu.check_ffn(cfg, m, l, x64, g_ids, w_ref, s_ref, rec.y, tokens=sample)
+    return rec, err
+
+
+# ------------------------------------------------------------------ tiny fp32 config
+@pytest.fixture(scope="module")
+def c1():
+    m = SyntheticModel(configs.C1, max_tokens=16)
+    yield m
+    m.close()
+
+
+def test_c1_batch_and_decode_steps(c1):
+    cfg = configs.C1
+    lcs = {0: ocache.LayerCache(cfg.n_experts, cfg.slots)}
+    st16 = Stack(c1, 16)
+    x = sm.layer_input(cfg, 0, 16, tag=0)
+    _log("c1 batch T=16")
+    _moe_layer_check(cfg, c1, st16, 0, lcs, x)
+    st1 = Stack(c1, 1)
+    for step in range(16):
+        _log("c1 decode step", step)
+        _moe_layer_check(cfg, c1, st1, 0, lcs, sm.layer_input(cfg, 0, 1, tag=1 + step))
+    pu.check_counters(c1, lcs)
+
+
+def test_c1_output_invariant_to_cache_size_and_prefetch():
+    cfg = configs.C1
+    x = torch.from_numpy(sm.layer_input(cfg, 0, 16, tag=0)).cuda()
+    outs = []
+    for C, flags in ((1, 0), (2, 0), (4, 0), (8, 0), (4, FLAG_NO_PREFETCH), (1, FLAG_NO_PREFETCH)):
+        _log("c1 invariance C", C, "flags", flags)
+        m = SyntheticModel(cfg.with_(slots=C), max_tokens=16, flags=flags)
+        st = Stack(m, 16)
+        ys = []
+        for rep in range(3):   # repeated calls: the cache state differs, the output must not
+            st.x.copy_(x)
+            st.moe_layer(0, predict=True)
+            ys.append(st.y.cpu().numpy().copy())
+        m.close()
+        for y in ys[1:]:
+            assert np.array_equal(y, ys[0])
+        outs.append(ys[0])
+    for y in outs[1:]:
+        assert np.array_equal(y, outs[0])
+
+
+# ------------------------------------------------------------------ full per-layer shapes
+CASES = [
+    ("c2_decode", configs.C2, 1, 3),
+    ("c3_prefill", configs.C3, 512, 1),
+    ("c3_decode", configs.C3, 1, 2),
+    ("c4_prefill", configs.C4, 256, 1),
+    ("c4_decode", configs.C4, 1, 2),
+    ("c5_prefill", configs.C5, 1024, 1),
+    ("c5_decode_b8", configs.C5, 8, 2),
+]
+
+
+@pytest.mark.parametrize("name,base,T,steps", CASES, ids=[c[0] for c in CASES])
+def test_stack_layers_full_shape(name, base, T, steps):
+    cfg = base.with_(n_layers=min(base.n_layers, base.lookahead + 2))
+    _log("case", name, "layers", cfg.n_layers, "T", T)
+    m = SyntheticModel(cfg, max_tokens=T)
+    st = Stack(m, T)
+    lcs = {l: ocache.LayerCache(cfg.n_experts, cfg.slots) for l in range(cfg.n_layers)}
+    rng = np.random.default_rng(hash(name) % 2**32)
+    sample = None if T <= 16 else np.sort(rng.choice(T, 24, replace=False))
+    try:
+        for step in range(steps):
+            records = {}
+            h0 = torch.from_numpy(sm.stack_input(cfg, step, T)).cuda()
+            st.step(h0, predict=True, record=pu.recorder(m, records))
+            for l in range(cfg.n_layers):
+                _log("  check", name, "step", step, "layer", l)
+                rec = records[l]
+                pu.check_harness(cfg, m, l, rec)
+                x64 = pu.f64(rec.x, cfg.dtype)
+                if rec.spec_plan is not None:
+                    Q = pu.check_predictor(cfg, m, l, x64, rec)
+                    pu.check_plan_spec(lcs[sm.predictor_target(cfg, l)], Q, rec.spec_plan)
+                g_ids, w_ref, s_ref, _ = pu.check_route(cfg, m, l, x64, rec)
+                pu.check_plan_precise(lcs[l], g_ids, rec.precise_plan)
+                pu.check_ffn(cfg, m, l, x64, g_ids, w_ref, s_ref, rec.y, tokens=sample)
+        pu.check_counters(m, lcs)
+    finally:
+        m.close()
