@@ -7,7 +7,7 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libpromoe.so")
+LIB_PATH = os.environ.get("PROMOE_LIB", os.path.join(HERE, "libpromoe.so"))
 
 PROMOE_F32, PROMOE_BF16 = 0, 1
 PRIO_LOW, PRIO_HIGH = 0, 1

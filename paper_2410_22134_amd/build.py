@@ -14,8 +14,8 @@ from concurrent.futures import ThreadPoolExecutor
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 ROOT = os.path.dirname(HERE)
-LIB = os.path.join(HERE, "libpromoe.so")
-BUILD_DIR = os.path.join(ROOT, "_build")
+LIB = os.environ.get("PROMOE_BUILD_OUT", os.path.join(HERE, "libpromoe.so"))
+BUILD_DIR = os.environ.get("PROMOE_BUILD_DIR", os.path.join(ROOT, "_build"))
 
 SOURCES = ["promoe.cpp", "scheduler.cpp", "kernels_gemv.hip", "kernels_route.hip", "kernels_gemm.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -23,6 +23,7 @@ ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-I" + os.path.join(ROOT, "include"), "-Wno-unused-result", "-Wno-unused-value"]
+FLAGS += os.environ.get("PROMOE_EXTRA_FLAGS", "").split()
 
 
 def _compile(src: str) -> str:

@@ -21,7 +21,16 @@ struct RowsArgs {
   int relu_in;  // 1: f = relu, else identity
 };
 
-// Expert FFN launch over the positions pos_list[0 .. n) of the route order.
+// Expert FFN launch: a list of jobs (route positions, or the shared expert),
+// each job split into row tiles; block b runs tile b - job_tile0[j] of the job
+// j with job_tile0[j] <= b < job_tile0[j + 1].
+constexpr int kMaxJobs = 65;
+// Launch clock slot: word 0 = max of ~start over the first blocks (so ~word0 is
+// the earliest start), then kTclkLines 128-byte lines whose first words hold
+// the latest wave end seen by the waves hashed to that line.
+constexpr int kTclkLines = 32;
+constexpr int kTclkWords = 16 * (kTclkLines + 1);
+constexpr uint8_t kSharedJob = 255;
 struct FfnArgs {
   const uint8_t* cache;
   int64_t expert_bytes;
@@ -29,16 +38,21 @@ struct FfnArgs {
   const int32_t* order_slot;  // [n_pos] slot each position computes from
   const int32_t* offsets;     // [n_pos + 1] pair offsets of each position
   const int32_t* perm;        // [T*k] pair q -> t*k + r
-  uint8_t pos_list[64];       // blockIdx.y -> position of the route order
   int hidden, inter, top_k, T;
   const void* x;              // [T x H]
   void* act;                  // [T*k x I] permuted activations
   float* Y;                   // [T*k x H] by (t, r)
-  // shared expert (one launch with shared = 1)
-  int shared, shared_inter;
-  const void* shared_w;
+  int shared_inter;
+  const void* shared_w;       // resident shared expert [Wg | Wu | Wd], I = shared_inter
   void* act_sh;               // [T x I_sh]
   float* Ysh;                 // [T x H]
+  int n_jobs;
+  uint8_t job_pos[kMaxJobs];  // route position, or kSharedJob
+  int32_t job_tile0[kMaxJobs + 1];
+  unsigned long long* tclock;   // optional launch clock slot (see kTclkWords), zero-initialised
+  const void* job_w[kMaxJobs];  // expert weights [Wg | Wu | Wd] of each job (slot or shared)
+  int32_t job_q0[kMaxJobs];     // pair range [q0, q1) of each job (tokens for the shared job)
+  int32_t job_q1[kMaxJobs];
 };
 
 struct CombineArgs {
@@ -101,7 +115,10 @@ struct PlanArgs {
 };
 
 void launch_rows_gemv(const RowsArgs& a, int wdtype, int xdtype, hipStream_t s);
-void launch_ffn(const FfnArgs& a, int pass, int n_pos, int max_tokens_per_pos, int dtype, hipStream_t s);
+// Fills job_tile0 for the pass and launches.  max_tokens = most pairs of any job.
+// With ev0/ev1 set, the launch records them itself (kernel execution time).
+void launch_ffn(FfnArgs& a, int pass, int max_tokens, int dtype, hipStream_t s, hipEvent_t ev0 = nullptr,
+                hipEvent_t ev1 = nullptr);
 void launch_combine(const CombineArgs& a, int T, int dtype, hipStream_t s);
 void launch_rmsnorm_quant(const float* h, void* out, int T, int H, int dtype, hipStream_t s);
 void launch_residual_add(float* h, const void* y, int n, int dtype, hipStream_t s);

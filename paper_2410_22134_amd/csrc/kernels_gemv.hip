@@ -13,6 +13,8 @@
 // fp32 in K-slabs shared by the block's four waves; each lane accumulates in
 // fp32 and the wave reduces at the end.  Weight bytes are read once per token
 // group of up to MT tokens, which is what bounds decode (HBM) throughput.
+#include <hip/hip_ext.h>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -143,143 +145,212 @@ __global__ __launch_bounds__(kThreads) void k_rows_gemv(RowsArgs a) {
 }
 
 // ============================================================ expert FFN
-// Token pairs of position p: q in [off[p], off[p+1]) of the permuted pair list
-// (pair q is token perm[q] / k, rank perm[q] % k).  The shared expert uses
-// q = token.
-template <typename TW>
-__device__ __forceinline__ const TW* expert_weights(const FfnArgs& a, int p) {
-  if (a.shared) return reinterpret_cast<const TW*>(a.shared_w);
-  const int slot = a.order_slot[p];
-  return reinterpret_cast<const TW*>(a.cache + ((size_t)a.layer * a.slots + slot) * a.expert_bytes);
+// Decode-shaped expert GEMVs.  No LDS and no block barrier: every lane holds the
+// token vectors' 16-byte pieces for its own k positions in registers and issues
+// all of its weight loads (RWxNCH rows x 16 B, about 16 per lane) before the
+// first FMA, so each wave keeps ~16 KiB of weights in flight.  A block is four
+// independent waves; the grid is a flat list of (job, row tile) blocks over
+// all experts of the launch (route positions and the shared expert).
+constexpr int kBlockWaves = 4;
+
+__device__ __forceinline__ int find_job(const FfnArgs& a, int bid) {
+  int lo = 0, hi = a.n_jobs - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.job_tile0[mid] <= bid) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
 }
 
-template <typename TW, int MT>
-__global__ __launch_bounds__(kThreads) void k_ffn_gateup(FfnArgs a) {
-  constexpr int RP = 2, R = 2 * RP, U = 2;  // RP (gate, up) row pairs per wave
-  __shared__ __attribute__((aligned(16))) float xs[kSlabFloats];
-  const int ks_max = kSlabFloats / MT;
-  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-  const int p = a.shared ? 0 : a.pos_list[blockIdx.y];
-  const int I = a.shared ? a.shared_inter : a.inter;
-  const int H = a.hidden;
-  const TW* W = expert_weights<TW>(a, p);
-  const int q0 = a.shared ? 0 : a.offsets[p];
-  const int q1 = a.shared ? a.T : a.offsets[p + 1];
-  const int i0 = (blockIdx.x * kWaves + wave) * RP;
-  const TW* rbase[R];
-  bool rvalid[R];
-#pragma unroll
-  for (int j = 0; j < RP; ++j) {
-    const bool v = i0 + j < I;
-    rvalid[2 * j] = rvalid[2 * j + 1] = v;
-    rbase[2 * j] = v ? W + (size_t)(i0 + j) * H : nullptr;            // gate row
-    rbase[2 * j + 1] = v ? W + (size_t)(I + i0 + j) * H : nullptr;    // up row
+template <typename TW>
+struct Job {
+  const TW* W;
+  int I, q0, q1;
+  bool shared;
+};
+
+template <typename TW>
+__device__ __forceinline__ Job<TW> job_of(const FfnArgs& a, int j) {
+  Job<TW> jb;
+  jb.shared = a.job_pos[j] == kSharedJob;
+  jb.W = reinterpret_cast<const TW*>(a.job_w[j]);
+  jb.I = jb.shared ? a.shared_inter : a.inter;
+  jb.q0 = a.job_q0[j];
+  jb.q1 = a.job_q1[j];
+  return jb;
+}
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+// Weights are streamed once per launch: non-temporal loads keep them from
+// displacing the token vectors and activations in the caches (measured faster
+// on gfx950 for the decode GEMVs).
+template <typename TW>
+__device__ __forceinline__ uint4 ld16_stream(const TW* p) {
+  const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+template <typename TW>
+__device__ __forceinline__ uint4 ld16(const TW* p) {
+  return *reinterpret_cast<const uint4*>(p);
+}
+
+// Launch timing on the device's constant-rate clock (profiling only): the
+// earliest block start and the latest wave end of the launch.
+// Blocks start in index order, so the first blocks carry the start; wave ends
+// are spread over separate cache lines so the atomics do not serialise.
+__device__ __forceinline__ void tclock_start(const FfnArgs& a) {
+  if (a.tclock && threadIdx.x == 0 && blockIdx.x < 8) atomicMax(a.tclock, ~(unsigned long long)wall_clock64());
+}
+__device__ __forceinline__ void tclock_end(const FfnArgs& a, int lane) {
+  if (a.tclock && lane == 0) {
+    const int line = 1 + (blockIdx.x * kBlockWaves + threadIdx.x / kWave) % kTclkLines;
+    atomicMax(a.tclock + 16 * line, (unsigned long long)wall_clock64());
   }
-  using TX = TW;
-  for (int g = q0; g < q1; g += MT) {
-    const int mt = min(MT, q1 - g);
-    const TX* xrow[MT];
+}
+
+// acc[r][m] += <rows[r], xs[m]> over k; rows/xs point at element 0 of the row
+// (xs at the token's vector).  nch = K / EPC chunks of 16 bytes.
+template <typename TW, int R, int MT, int NCH>
+__device__ __forceinline__ void wave_rows_dot(const TW* const (&rows)[R], const bool (&rv)[R],
+                                              const TW* const (&xs)[MT], int mt, int nch, int lane,
+                                              float (&acc)[R][MT]) {
+  constexpr int EPC = Elem<TW>::kPer16B;
+  for (int cb = 0; cb < nch; cb += kWave * NCH) {
+    uint4 wr[R][NCH];
+    uint4 xr[MT][NCH];
 #pragma unroll
-    for (int m = 0; m < MT; ++m) {
-      const int q = g + min(m, mt - 1);
-      const int t = a.shared ? q : a.perm[q] / a.top_k;
-      xrow[m] = reinterpret_cast<const TX*>(a.x) + (size_t)t * H;
-    }
-    float acc[R][MT];
+    for (int u = 0; u < NCH; ++u) {
+      const int c = cb + lane + u * kWave;
 #pragma unroll
-    for (int r = 0; r < R; ++r)
+      for (int r = 0; r < R; ++r) wr[r][u] = (c < nch && rv[r]) ? ld16_stream(rows[r] + (size_t)c * EPC) : make_uint4(0, 0, 0, 0);
 #pragma unroll
-      for (int m = 0; m < MT; ++m) acc[r][m] = 0.0f;
-    for (int k0 = 0; k0 < H; k0 += ks_max) {
-      const int ks = min(ks_max, H - k0);
-      __syncthreads();
-      stage_slab<TX, MT>(xs, ks_max, xrow, mt, k0, ks, false);
-      __syncthreads();
-      const TW* rows[R];
-#pragma unroll
-      for (int r = 0; r < R; ++r) rows[r] = rvalid[r] ? rbase[r] + k0 : nullptr;
-      wave_dot_slab<TW, R, MT, U>(rows, rvalid, xs, ks_max, mt, ks / Elem<TW>::kPer16B, lane, acc);
+      for (int m = 0; m < MT; ++m) xr[m][u] = (c < nch && m < mt) ? ld16(xs[m] + (size_t)c * EPC) : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
-    for (int r = 0; r < R; ++r)
+    for (int u = 0; u < NCH; ++u) {
+      float xf[MT][EPC];
 #pragma unroll
-      for (int m = 0; m < MT; ++m) acc[r][m] = wave_sum(acc[r][m]);
-    if (lane < RP * MT) {
-      const int j = lane % RP, m = lane / RP;
-      float ga = 0.0f, ub = 0.0f;
+      for (int m = 0; m < MT; ++m) unpack16(xr[m][u], xf[m]);
 #pragma unroll
-      for (int jj = 0; jj < RP; ++jj)
+      for (int r = 0; r < R; ++r) {
+        float wf[EPC];
+        unpack16(wr[r][u], wf);
 #pragma unroll
-        for (int mm = 0; mm < MT; ++mm)
-          if (jj == j && mm == m) { ga = acc[2 * jj][mm]; ub = acc[2 * jj + 1][mm]; }
-      if (m < mt && i0 + j < I) {
-        TW* act = reinterpret_cast<TW*>(a.shared ? a.act_sh : a.act);
-        Elem<TW>::store(act, (g + m) * I + i0 + j, silu(ga) * ub);
+        for (int m = 0; m < MT; ++m)
+#pragma unroll
+          for (int e = 0; e < EPC; ++e) acc[r][m] = fmaf(wf[e], xf[m][e], acc[r][m]);
       }
     }
   }
 }
 
-template <typename TW, int MT>
-__global__ __launch_bounds__(kThreads) void k_ffn_down(FfnArgs a) {
-  constexpr int R = 4, U = 2;
-  __shared__ __attribute__((aligned(16))) float xs[kSlabFloats];
-  const int ks_max = kSlabFloats / MT;
+// pass 1: act[q][i] = q(silu(Wg[i] . x_t) * (Wu[i] . x_t)) for the wave's RW rows i
+template <typename TW, int MT, int NCH, int RW>
+__global__ __launch_bounds__(kThreads) void k_ffn_gateup(FfnArgs a) {
+  constexpr int R = 2 * RW;
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-  const int p = a.shared ? 0 : a.pos_list[blockIdx.y];
-  const int I = a.shared ? a.shared_inter : a.inter;
-  const int H = a.hidden;
-  const TW* Wd = expert_weights<TW>(a, p) + (size_t)2 * I * H;
-  const int q0 = a.shared ? 0 : a.offsets[p];
-  const int q1 = a.shared ? a.T : a.offsets[p + 1];
-  const int n0 = (blockIdx.x * kWaves + wave) * R;
-  const TW* rbase[R];
-  bool rvalid[R];
+  tclock_start(a);
+  const int j = find_job(a, blockIdx.x);
+  const Job<TW> jb = job_of<TW>(a, j);
+  const int i0 = ((blockIdx.x - a.job_tile0[j]) * kBlockWaves + wave) * RW;
+  if (i0 >= jb.I) return;
+  const int H = a.hidden, I = jb.I;
+  const TW* rows[R];
+  bool rv[R];
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    rvalid[r] = n0 + r < H;
-    rbase[r] = rvalid[r] ? Wd + (size_t)(n0 + r) * I : nullptr;
+  for (int r = 0; r < RW; ++r) {
+    const bool v = i0 + r < I;
+    rv[2 * r] = rv[2 * r + 1] = v;
+    rows[2 * r] = jb.W + (size_t)(v ? i0 + r : 0) * H;          // gate row
+    rows[2 * r + 1] = jb.W + (size_t)(v ? I + i0 + r : 0) * H;  // up row
   }
-  const TW* actb = reinterpret_cast<const TW*>(a.shared ? a.act_sh : a.act);
-  for (int g = q0; g < q1; g += MT) {
-    const int mt = min(MT, q1 - g);
-    const TW* xrow[MT];
+  TW* act = reinterpret_cast<TW*>(jb.shared ? a.act_sh : a.act);
+  const TW* xb = reinterpret_cast<const TW*>(a.x);
+  for (int g = jb.q0; g < jb.q1; g += MT) {
+    const int mt = min(MT, jb.q1 - g);
+    const TW* xs[MT];
 #pragma unroll
-    for (int m = 0; m < MT; ++m) xrow[m] = actb + (size_t)(g + min(m, mt - 1)) * I;
+    for (int m = 0; m < MT; ++m) {
+      const int q = g + min(m, mt - 1);
+      const int t = (jb.shared || a.T == 1) ? (jb.shared ? q : 0) : a.perm[q] / a.top_k;
+      xs[m] = xb + (size_t)t * H;
+    }
     float acc[R][MT];
 #pragma unroll
     for (int r = 0; r < R; ++r)
 #pragma unroll
       for (int m = 0; m < MT; ++m) acc[r][m] = 0.0f;
-    for (int k0 = 0; k0 < I; k0 += ks_max) {
-      const int ks = min(ks_max, I - k0);
-      __syncthreads();
-      stage_slab<TW, MT>(xs, ks_max, xrow, mt, k0, ks, false);
-      __syncthreads();
-      const TW* rows[R];
-#pragma unroll
-      for (int r = 0; r < R; ++r) rows[r] = rvalid[r] ? rbase[r] + k0 : nullptr;
-      wave_dot_slab<TW, R, MT, U>(rows, rvalid, xs, ks_max, mt, ks / Elem<TW>::kPer16B, lane, acc);
-    }
+    wave_rows_dot<TW, R, MT, NCH>(rows, rv, xs, mt, H / Elem<TW>::kPer16B, lane, acc);
 #pragma unroll
     for (int r = 0; r < R; ++r)
 #pragma unroll
       for (int m = 0; m < MT; ++m) acc[r][m] = wave_sum(acc[r][m]);
-    if (lane < R * MT) {
-      const int r = lane % R, m = lane / R;
+    if (lane < RW * MT) {
+      const int r = lane % RW, m = lane / RW;
+      float ga = 0.0f, ub = 0.0f;
+#pragma unroll
+      for (int rr = 0; rr < RW; ++rr)
+#pragma unroll
+        for (int mm = 0; mm < MT; ++mm)
+          if (rr == r && mm == m) { ga = acc[2 * rr][mm]; ub = acc[2 * rr + 1][mm]; }
+      if (m < mt && i0 + r < I) Elem<TW>::store(act, (g + m) * I + i0 + r, silu(ga) * ub);
+    }
+  }
+  tclock_end(a, lane);
+}
+
+// pass 2: Y[pair][n] = Wd[n] . act[q] for the wave's RW rows n
+template <typename TW, int MT, int NCH, int RW>
+__global__ __launch_bounds__(kThreads) void k_ffn_down(FfnArgs a) {
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  tclock_start(a);
+  const int j = find_job(a, blockIdx.x);
+  const Job<TW> jb = job_of<TW>(a, j);
+  const int H = a.hidden, I = jb.I;
+  const int n0 = ((blockIdx.x - a.job_tile0[j]) * kBlockWaves + wave) * RW;
+  if (n0 >= H) return;
+  const TW* Wd = jb.W + (size_t)2 * I * H;
+  const TW* rows[RW];
+  bool rv[RW];
+#pragma unroll
+  for (int r = 0; r < RW; ++r) {
+    rv[r] = n0 + r < H;
+    rows[r] = Wd + (size_t)(rv[r] ? n0 + r : 0) * I;
+  }
+  const TW* actb = reinterpret_cast<const TW*>(jb.shared ? a.act_sh : a.act);
+  for (int g = jb.q0; g < jb.q1; g += MT) {
+    const int mt = min(MT, jb.q1 - g);
+    const TW* xs[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) xs[m] = actb + (size_t)(g + min(m, mt - 1)) * I;
+    float acc[RW][MT];
+#pragma unroll
+    for (int r = 0; r < RW; ++r)
+#pragma unroll
+      for (int m = 0; m < MT; ++m) acc[r][m] = 0.0f;
+    wave_rows_dot<TW, RW, MT, NCH>(rows, rv, xs, mt, I / Elem<TW>::kPer16B, lane, acc);
+#pragma unroll
+    for (int r = 0; r < RW; ++r)
+#pragma unroll
+      for (int m = 0; m < MT; ++m) acc[r][m] = wave_sum(acc[r][m]);
+    if (lane < RW * MT) {
+      const int r = lane % RW, m = lane / RW;
       float v = 0.0f;
 #pragma unroll
-      for (int rr = 0; rr < R; ++rr)
+      for (int rr = 0; rr < RW; ++rr)
 #pragma unroll
         for (int mm = 0; mm < MT; ++mm)
           if (rr == r && mm == m) v = acc[rr][mm];
-      if (m < mt && rvalid[r]) {
+      if (m < mt && rv[r]) {
         const int q = g + m;
-        float* Y = a.shared ? a.Ysh + (size_t)q * H : a.Y + (size_t)a.perm[q] * H;
+        float* Y = jb.shared ? a.Ysh + (size_t)q * H : a.Y + (size_t)a.perm[q] * H;
         Y[n0 + r] = v;
       }
     }
   }
+  tclock_end(a, lane);
 }
 
 // ============================================================ combine
@@ -339,30 +410,44 @@ void launch_rows_gemv(const RowsArgs& a, int wdtype, int xdtype, hipStream_t s) 
   else rows_dispatch<float, float>(a, s);
 }
 
+// (MT, NCH) pairs keep the registers per lane bounded: MT x NCH x 16 B of token
+// pieces plus R x NCH x 16 B of weights in flight.
 template <typename TW, int MT>
-static void ffn_dispatch(const FfnArgs& a, int pass, int n_pos, hipStream_t s) {
-  const int I = a.shared ? a.shared_inter : a.inter;
-  if (pass == 0) {
-    dim3 grid((I + kWaves * 2 - 1) / (kWaves * 2), n_pos);
-    k_ffn_gateup<TW, MT><<<grid, kThreads, 0, s>>>(a);
+static void ffn_dispatch(FfnArgs& a, int pass, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  constexpr int NCH = MT <= 2 ? 4 : (MT == 4 ? 2 : 1);
+  constexpr int RWG = 2, RWD = 4;
+  const int rows_per_block = kBlockWaves * (pass == 0 ? RWG : RWD);
+  int tiles = 0;
+  for (int j = 0; j < a.n_jobs; ++j) {
+    a.job_tile0[j] = tiles;
+    const int I = a.job_pos[j] == kSharedJob ? a.shared_inter : a.inter;
+    const int rows = pass == 0 ? I : a.hidden;
+    tiles += (rows + rows_per_block - 1) / rows_per_block;
+  }
+  a.job_tile0[a.n_jobs] = tiles;
+  if (tiles == 0) return;
+  if (ev0) {
+    if (pass == 0) hipExtLaunchKernelGGL(k_ffn_gateup<TW, MT, NCH, RWG>, dim3(tiles), dim3(kThreads), 0, s, ev0, ev1, 0, a);
+    else hipExtLaunchKernelGGL(k_ffn_down<TW, MT, NCH, RWD>, dim3(tiles), dim3(kThreads), 0, s, ev0, ev1, 0, a);
+  } else if (pass == 0) {
+    k_ffn_gateup<TW, MT, NCH, RWG><<<tiles, kThreads, 0, s>>>(a);
   } else {
-    dim3 grid((a.hidden + kWaves * 4 - 1) / (kWaves * 4), n_pos);
-    k_ffn_down<TW, MT><<<grid, kThreads, 0, s>>>(a);
+    k_ffn_down<TW, MT, NCH, RWD><<<tiles, kThreads, 0, s>>>(a);
   }
 }
 
-void launch_ffn(const FfnArgs& a, int pass, int n_pos, int max_tokens_per_pos, int dtype, hipStream_t s) {
-  const int mt = max_tokens_per_pos >= 8 ? 8 : (max_tokens_per_pos >= 4 ? 4 : (max_tokens_per_pos >= 2 ? 2 : 1));
+void launch_ffn(FfnArgs& a, int pass, int max_tokens, int dtype, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  const int mt = max_tokens >= 8 ? 8 : (max_tokens >= 4 ? 4 : (max_tokens >= 2 ? 2 : 1));
   if (dtype == 1) {
-    if (mt == 8) ffn_dispatch<bf16_t, 8>(a, pass, n_pos, s);
-    else if (mt == 4) ffn_dispatch<bf16_t, 4>(a, pass, n_pos, s);
-    else if (mt == 2) ffn_dispatch<bf16_t, 2>(a, pass, n_pos, s);
-    else ffn_dispatch<bf16_t, 1>(a, pass, n_pos, s);
+    if (mt == 8) ffn_dispatch<bf16_t, 8>(a, pass, s, ev0, ev1);
+    else if (mt == 4) ffn_dispatch<bf16_t, 4>(a, pass, s, ev0, ev1);
+    else if (mt == 2) ffn_dispatch<bf16_t, 2>(a, pass, s, ev0, ev1);
+    else ffn_dispatch<bf16_t, 1>(a, pass, s, ev0, ev1);
   } else {
-    if (mt == 8) ffn_dispatch<float, 8>(a, pass, n_pos, s);
-    else if (mt == 4) ffn_dispatch<float, 4>(a, pass, n_pos, s);
-    else if (mt == 2) ffn_dispatch<float, 2>(a, pass, n_pos, s);
-    else ffn_dispatch<float, 1>(a, pass, n_pos, s);
+    if (mt == 8) ffn_dispatch<float, 8>(a, pass, s, ev0, ev1);
+    else if (mt == 4) ffn_dispatch<float, 4>(a, pass, s, ev0, ev1);
+    else if (mt == 2) ffn_dispatch<float, 2>(a, pass, s, ev0, ev1);
+    else ffn_dispatch<float, 1>(a, pass, s, ev0, ev1);
   }
 }
 

@@ -144,8 +144,14 @@ struct promoe_ctx {
   int64_t cnext = 0;
   hipStream_t last_stream = nullptr;
 
-  // profiling
+  // profiling: FFN launches timed on the device clock (d_tclock ring of
+  // [start, end] pairs), copy-wait stalls with HIP events
   bool profile = false;
+  unsigned long long* d_tclock = nullptr;
+  int64_t tclk_next = 0, tclk_resolved = 0;
+  struct TclkMeta { int cls; double bytes, flops; };
+  std::vector<TclkMeta> tclk_meta;
+  double wall_khz = 100000.0;
   std::vector<ProfEntry> prof_pending;
   std::vector<hipEvent_t> prof_free;
   int64_t k_launches[4] = {0, 0, 0, 0};
@@ -176,12 +182,53 @@ hipEvent_t prof_event(promoe_ctx* c) {
     c->prof_free.pop_back();
     return e;
   }
+  // timing-only events: no system-scope fence on completion (it would add a
+  // cache writeback/invalidate to every measured interval)
   hipEvent_t e = nullptr;
-  hipEventCreate(&e);
+  hipEventCreateWithFlags(&e, hipEventDisableSystemFence);
   return e;
 }
 
+constexpr int kTclkRing = 8192;
+
+// Read back finished launch clocks (caller has synchronised the launch stream)
+// and clear the slots.
+void tclock_resolve(promoe_ctx* c) {
+  const int64_t from = c->tclk_resolved, to = c->tclk_next;
+  if (to == from) return;
+  std::vector<unsigned long long> v((size_t)kTclkWords * kTclkRing);
+  hipMemcpy(v.data(), c->d_tclock, sizeof(unsigned long long) * v.size(), hipMemcpyDeviceToHost);
+  for (int64_t i = from; i < to; ++i) {
+    const int64_t slot = i % kTclkRing;
+    const unsigned long long* w = v.data() + (size_t)kTclkWords * slot;
+    const unsigned long long t0 = ~w[0];
+    unsigned long long t1 = 0;
+    for (int l = 1; l <= kTclkLines; ++l) t1 = std::max(t1, w[16 * l]);
+    const promoe_ctx::TclkMeta& m = c->tclk_meta[slot];
+    if (w[0] == 0 || t1 < t0) continue;  // launch without blocks
+    c->k_launches[m.cls]++;
+    c->k_ms[m.cls] += (double)(t1 - t0) / c->wall_khz;
+    c->k_bytes[m.cls] += m.bytes;
+    c->k_flops[m.cls] += m.flops;
+  }
+  hipMemset(c->d_tclock, 0, sizeof(unsigned long long) * v.size());
+  c->tclk_resolved = to;
+}
+
+// Slot of the next timed launch; resolves (synchronising) when the ring is full.
+unsigned long long* tclock_slot(promoe_ctx* c, hipStream_t s, int cls, double bytes, double flops) {
+  if (!c->d_tclock) return nullptr;
+  if (c->tclk_next - c->tclk_resolved >= kTclkRing) {
+    hipStreamSynchronize(s);
+    tclock_resolve(c);
+  }
+  const int64_t slot = c->tclk_next++ % kTclkRing;
+  c->tclk_meta[slot] = promoe_ctx::TclkMeta{cls, bytes, flops};
+  return c->d_tclock + (size_t)kTclkWords * slot;
+}
+
 void prof_resolve(promoe_ctx* c) {
+  tclock_resolve(c);
   for (auto& p : c->prof_pending) {
     hipEventSynchronize(p.b);
     float ms = 0.0f;
@@ -496,6 +543,17 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   const size_t sub = g.copy_subchunk_bytes > 0 ? (size_t)g.copy_subchunk_bytes : ((size_t)16 << 20);
   const int window = g.copy_window > 0 ? g.copy_window : 2;
   c->pf = new Prefetcher(L, C, E, c->chunk_bytes, sub, window, c->cache, &c->eng);
+  if (c->profile) {
+    int khz = 0;
+    if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, c->dev) == hipSuccess && khz > 0)
+      c->wall_khz = khz;
+    const size_t tb = sizeof(unsigned long long) * kTclkWords * kTclkRing;
+    if (hipMalloc(&c->d_tclock, tb) == hipSuccess && hipMemset(c->d_tclock, 0, tb) == hipSuccess) {
+      c->tclk_meta.resize(kTclkRing);
+    } else {
+      c->d_tclock = nullptr;
+    }
+  }
   c->worker = std::thread(worker_main, c);
   *out = c;
   return PROMOE_OK;
@@ -551,6 +609,7 @@ int promoe_destroy(promoe_ctx* c) {
   for (int i = 0; i < kRecRing; ++i) hipEventDestroy(c->rec_ev[i]);
   hipStreamDestroy(c->eng.stream);
   hipHostFree(c->rec_h);
+  if (c->d_tclock) hipFree(c->d_tclock);
   hipFree(c->dmem);
   delete c->pf;
   delete c;
@@ -794,19 +853,33 @@ int promoe_route(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_id
 
 namespace {
 
-// Launch gate/up and down passes for a list of positions.
-int ffn_launch(promoe_ctx* c, FfnArgs a, const std::vector<int>& plist, hipStream_t s, int64_t wait01,
+// Launch the gate/up and down passes over a list of jobs (route positions, or
+// kSharedJob), waiting first for copy `wait01` (chunks 0-1 of every job) and
+// then `wait2` (chunk 2).
+int ffn_launch(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipStream_t s, int64_t wait01,
                int64_t wait2) {
   const PlanRecord& rec = c->route_rec;
   int maxc = 1;
-  for (size_t i = 0; i < plist.size(); ++i) {
-    a.pos_list[i] = (uint8_t)plist[i];
-    maxc = std::max(maxc, rec.count[plist[i]]);
+  double wbytes = 0, flops = 0;  // per pass 0 (gate/up) and 1 (down), scaled below
+  a.n_jobs = (int)jobs.size();
+  for (size_t i = 0; i < jobs.size(); ++i) {
+    const bool sh = jobs[i] == kSharedJob;
+    a.job_pos[i] = (uint8_t)jobs[i];
+    if (sh) {
+      a.job_w[i] = a.shared_w;
+      a.job_q0[i] = 0;
+      a.job_q1[i] = a.T;
+    } else {
+      a.job_w[i] = c->cache + ((size_t)a.layer * c->C + rec.slot[jobs[i]]) * c->expert_bytes;
+      a.job_q0[i] = rec.offset[jobs[i]];
+      a.job_q1[i] = rec.offset[jobs[i] + 1];
+    }
+    const int cnt = sh ? a.T : rec.count[jobs[i]];
+    const double melems = (double)(sh ? c->Ish : c->I) * c->H;
+    maxc = std::max(maxc, cnt);
+    wbytes += melems * c->eb;
+    flops += 2.0 * cnt * melems;
   }
-  const double wbytes = (double)c->chunk_bytes * plist.size();
-  double pairs = 0;  // token-expert pairs in the launch
-  for (int p : plist) pairs += rec.count[p];
-  const double melems = (double)c->I * c->H;  // elements of one expert matrix
   for (int pass = 0; pass < 2; ++pass) {
     const int64_t w = pass == 0 ? wait01 : wait2;
     if (w >= 0) {
@@ -815,15 +888,10 @@ int ffn_launch(promoe_ctx* c, FfnArgs a, const std::vector<int>& plist, hipStrea
       HIPCHK(hipStreamWaitEvent(s, c->eng.event(w), 0));
       if (c->profile) { hipEventRecord(pb, s); c->prof_pending.push_back(ProfEntry{pa, pb, 4, 0, 0}); }
     }
-    hipEvent_t ka = nullptr, kb = nullptr;
-    if (c->profile) { ka = prof_event(c); kb = prof_event(c); hipEventRecord(ka, s); }
-    launch_ffn(a, pass, (int)plist.size(), maxc, c->dt, s);
+    const double k = pass == 0 ? 2.0 : 1.0;  // gate and up, or down
+    a.tclock = c->profile ? tclock_slot(c, s, pass, k * wbytes, k * flops) : nullptr;
+    launch_ffn(a, pass, maxc, c->dt, s);
     LAUNCHCHK("ffn");
-    if (c->profile) {
-      hipEventRecord(kb, s);
-      const double by = pass == 0 ? 2 * wbytes : wbytes;
-      c->prof_pending.push_back(ProfEntry{ka, kb, pass, by, 2.0 * pairs * melems * (pass == 0 ? 2 : 1)});
-    }
   }
   return PROMOE_OK;
 }
@@ -857,67 +925,70 @@ int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const in
   a.act = c->d_act;
   a.Y = c->d_Y;
   a.shared_inter = c->Ish;
+  a.shared_w = c->lw[layer].shared;
   a.act_sh = c->d_act_sh;
   a.Ysh = c->d_Ysh;
 
-  // shared expert first: resident, never waits
-  if (c->Ish > 0) {
-    FfnArgs sa = a;
-    sa.shared = 1;
-    sa.shared_w = c->lw[layer].shared;
-    const int mt = std::min(T, 8);
-    for (int pass = 0; pass < 2; ++pass) {
-      hipEvent_t ka = nullptr, kb = nullptr;
-      if (c->profile) { ka = prof_event(c); kb = prof_event(c); hipEventRecord(ka, s); }
-      sa.pos_list[0] = 0;
-      launch_ffn(sa, pass, 1, mt, c->dt, s);
-      LAUNCHCHK("ffn shared");
-      if (c->profile) {
-        hipEventRecord(kb, s);
-        const double by = (double)c->Ish * c->H * c->eb * (pass == 0 ? 2 : 1);
-        c->prof_pending.push_back(ProfEntry{ka, kb, pass, by, 2.0 * T * (by / c->eb)});  // T tokens x weights
-      }
-    }
-  }
-
   std::unique_lock<std::mutex> lk(c->mu);
   const int n = rec.n;
-  std::vector<char> done(n, 0);
-  std::vector<int> ready;
-  std::vector<char> is_def(n, 0);
+  std::vector<char> done(n, 0), is_def(n, 0);
   for (const auto& d : c->deferred) is_def[d.pos] = 1;
-  for (int p = 0; p < n; ++p)
-    if (!is_def[p] && c->need01[p] < 0 && c->need2[p] < 0) ready.push_back(p);
 
-  auto after_launch = [&](const std::vector<int>& plist) {
+  auto after_launch = [&](const std::vector<int>& jobs) {
     const int64_t tok = record_compute(c, s);
-    for (int p : plist) {
+    for (int p : jobs) {
+      if (p == kSharedJob) continue;
       c->pf->set_last_read(layer, rec.slot[p], tok);
       done[p] = 1;
     }
     // release fills that waited for these positions' reads
     for (const auto& d : c->deferred) {
-      if (std::find(plist.begin(), plist.end(), d.after) == plist.end()) continue;
+      if (std::find(jobs.begin(), jobs.end(), d.after) == jobs.end()) continue;
       c->pf->assign(layer, d.slot, d.expert);
       c->pf->issue_high_after(layer, d.slot, tok);
       c->need01[d.pos] = c->pf->ready_seq(layer, d.slot, 1);
       c->need2[d.pos] = c->pf->ready_seq(layer, d.slot, 2);
+      is_def[d.pos] = 0;
     }
   };
 
+  // 1. the shared expert and every routed expert whose chunks are already in HBM
+  std::vector<int> jobs;
+  if (c->Ish > 0) jobs.push_back(kSharedJob);
+  for (int p = 0; p < n; ++p)
+    if (!is_def[p] && c->need01[p] < 0 && c->need2[p] < 0) jobs.push_back(p);
   int rc = PROMOE_OK;
-  if (!ready.empty()) {
-    rc = ffn_launch(c, a, ready, s, -1, -1);
+  if (!jobs.empty()) {
+    rc = ffn_launch(c, a, jobs, s, -1, -1);
     if (rc) return rc;
-    after_launch(ready);
+    after_launch(jobs);
   }
-  for (int p = 0; p < n; ++p) {
-    if (done[p]) continue;
-    std::vector<int> one(1, p);
-    rc = ffn_launch(c, a, one, s, c->need01[p], c->need2[p]);
+  // 2. experts still arriving.  Decode-sized steps batch them into one launch
+  // behind the last copy (a GEMV is ~1% of a copy, so per-expert launches buy no
+  // overlap); larger steps launch per expert in the route order so compute
+  // follows the copies expert by expert.  Fills deferred behind an earlier
+  // expert's read are released as that expert is launched.
+  const bool batch = (int64_t)T * c->K <= 64;
+  for (;;) {
+    jobs.clear();
+    int64_t w01 = -1, w2 = -1;
+    for (int p = 0; p < n; ++p) {
+      if (done[p] || is_def[p]) continue;
+      jobs.push_back(p);
+      w01 = std::max(w01, c->need01[p]);
+      w2 = std::max(w2, c->need2[p]);
+      if (!batch) break;
+    }
+    if (jobs.empty()) break;
+    rc = ffn_launch(c, a, jobs, s, w01, w2);
     if (rc) return rc;
-    after_launch(one);
+    after_launch(jobs);
   }
+  for (int p = 0; p < n; ++p)
+    if (!done[p]) {
+      g_last_error = "expert_ffn: unreleased position";
+      return PROMOE_ESTATE;
+    }
   if (c->eng.err != hipSuccess) return fail_hip(c->eng.err, "copy engine");
   lk.unlock();
   c->cv.notify_all();
@@ -974,6 +1045,9 @@ int promoe_reset_stats(promoe_ctx* c) {
   if (!c) return PROMOE_EINVAL;
   int rc = promoe_sync(c);
   if (rc) return rc;
+  if (c->profile) prof_resolve(c);
+  HIPCHK(hipMemset(c->st.counters, 0, sizeof(int64_t) * 8 * c->L));
+  HIPCHK(hipDeviceSynchronize());
   std::lock_guard<std::mutex> lk(c->mu);
   c->pf->reset_stats();
   for (int i = 0; i < 4; ++i) c->k_launches[i] = 0, c->k_ms[i] = c->k_bytes[i] = c->k_flops[i] = 0.0;
