@@ -49,6 +49,8 @@ struct FfnArgs {
   int n_jobs;
   uint8_t job_pos[kMaxJobs];  // route position, or kSharedJob
   int32_t job_tile0[kMaxJobs + 1];
+  int ksplit;                   // split-K slices of the shared expert's down GEMM (>= 1)
+  int64_t ysh_split_stride;     // elements between the slices' partial outputs in Ysh
   unsigned long long* tclock;   // optional launch clock slot (see kTclkWords), zero-initialised
   const void* job_w[kMaxJobs];  // expert weights [Wg | Wu | Wd] of each job (slot or shared)
   int32_t job_q0[kMaxJobs];     // pair range [q0, q1) of each job (tokens for the shared job)
@@ -58,7 +60,9 @@ struct FfnArgs {
 struct CombineArgs {
   const float* Y;       // [T*k x H]
   const float* w;       // [T x k]
-  const float* Ysh;     // [T x H] or null
+  const float* Ysh;     // [ysh_split x T x H] partial outputs, summed in slice order, or null
+  int ysh_split;
+  int64_t ysh_split_stride;
   const float* sscale;  // [T] or null (weight 1)
   void* y;              // [T x H]
   int hidden, top_k;
@@ -114,11 +118,38 @@ struct PlanArgs {
   int32_t* d_pos_of;     // [64] scratch
 };
 
+// Launch timing on the device's constant-rate clock (profiling only): the
+// first blocks carry the launch start (blocks start in index order), and wave
+// ends are spread over kTclkLines cache lines so the atomics do not serialise.
+__device__ __forceinline__ void tclock_start(const FfnArgs& a) {
+  if (a.tclock && threadIdx.x == 0 && blockIdx.x < 8) atomicMax(a.tclock, ~(unsigned long long)wall_clock64());
+}
+__device__ __forceinline__ void tclock_end(const FfnArgs& a) {
+  if (a.tclock && (threadIdx.x & 63) == 0) {
+    const int line = 1 + (blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) % kTclkLines;
+    atomicMax(a.tclock + 16 * line, (unsigned long long)wall_clock64());
+  }
+}
+
 void launch_rows_gemv(const RowsArgs& a, int wdtype, int xdtype, hipStream_t s);
 // Fills job_tile0 for the pass and launches.  max_tokens = most pairs of any job.
 // With ev0/ev1 set, the launch records them itself (kernel execution time).
 void launch_ffn(FfnArgs& a, int pass, int max_tokens, int dtype, hipStream_t s, hipEvent_t ev0 = nullptr,
                 hipEvent_t ev1 = nullptr);
+// Grouped MFMA GEMM (bf16) for the same passes; needs N % 128 == 0 and K % 64 == 0.
+bool gemm_supported(int N, int K);
+int gemm_tiles_shared_down(int T, int H);
+// MFMA rows product: out[t][o_off + n] (=|+=) sum_k W[n][k] x[t][k], bf16 in, fp32 out; K % 64 == 0.
+struct RowsGemmArgs {
+  const void* w;
+  int N, K;
+  const void* x;
+  int ldx, T;
+  float* out;
+  int ldo, o_off, add;
+};
+void launch_gemm_rows(const RowsGemmArgs& a, hipStream_t s);
+void launch_gemm(FfnArgs& a, int pass, int max_tokens, hipStream_t s);
 void launch_combine(const CombineArgs& a, int T, int dtype, hipStream_t s);
 void launch_rmsnorm_quant(const float* h, void* out, int T, int H, int dtype, hipStream_t s);
 void launch_residual_add(float* h, const void* y, int n, int dtype, hipStream_t s);

@@ -1,0 +1,348 @@
+// Grouped expert GEMMs for prefill on gfx950 MFMA (bf16 in, fp32 accumulate).
+//
+// Both passes are "NT" products C[m][n] = sum_k A[m][k] B[n][k] with the
+// reduction dimension contiguous in both operands:
+//   gate/up: A = token rows of x (gathered through the pair permutation),
+//            B = Wg rows and Wu rows of the expert (dual B), epilogue
+//            act = bf16(silu(A.Wg^T) * (A.Wu^T));
+//   down:    A = activation rows, B = Wd rows, epilogue writes fp32 rows of Y
+//            scattered back to (token, rank).
+// One launch covers a list of jobs (route positions or the shared expert);
+// block b takes tile b of the flat job x m-tile x n-tile list, remapped so the
+// m-tiles that share an n-tile (the same weight rows) run on the same XCD and
+// meet in its L2.
+//
+// Block = 4 or 8 waves, tile BM x 128 x 64 (k).  A and B tiles go global -> LDS
+// directly (global_load_lds_dwordx4: each wave instruction fills 8 rows of
+// 128 bytes, no staging registers) through a 3-stage ring, so the loads of two
+// later k-tiles are in flight while one feeds v_mfma_f32_16x16x32_bf16; one
+// barrier per k-tile.  LDS rows are unpadded and their 16-byte chunks are
+// XOR-swizzled by (row >> 1) & 7, so the 16 rows read by one ds_read_b128 phase
+// fall in distinct banks.  Lane l of an MFMA supplies A[l % 16][8*(l/16)..+8]
+// and B[l % 16][8*(l/16)..+8] and receives C[4*(l/16) + i][l % 16], i < 4.
+#include "common.hpp"
+#include "kernels.hpp"
+
+namespace promoe {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+typedef unsigned int gu32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kBN = 128;
+constexpr int kBK = 64;
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& v) {
+  return __builtin_bit_cast(bf16x8_t, v);
+}
+
+__device__ __forceinline__ uint4 gload16_stream(const bf16_t* p) {
+  const gu32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const gu32x4_t*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+__device__ __forceinline__ int gemm_find_job(const FfnArgs& a, int bid) {
+  int lo = 0, hi = a.n_jobs - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.job_tile0[mid] <= bid) lo = mid;
+    else hi = mid - 1;
+  }
+  return lo;
+}
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef __attribute__((address_space(1))) void* gbl_ptr_t;
+
+// Chunk (16 bytes) swizzle of LDS row r: logical chunk c lives at c ^ swz(r).
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding:
+// vmcnt bits [3:0] and [15:14], expcnt [6:4] = 7, lgkmcnt [11:8] = 15).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Main loop shared by the expert and rows GEMMs: C[BM x 128] (+= NB of them)
+// over k-tiles [kt0, kt1) of 64.  src[i] is this lane's DMA source row pointer
+// (already offset to its swizzled 16-byte chunk) for DMA load i; LDS rows
+// 0..BM-1 hold A, then NB x 128 rows of B.
+template <int BM, int WM, int WN, int NB, int STAGES>
+struct GemmTile {
+  static constexpr int NW = WM * WN;
+  static constexpr int WTM = BM / WM, WTN = kBN / WN;
+  static constexpr int TM = WTM / 16, TN = WTN / 16;
+  static constexpr int ROWS = BM + NB * kBN;
+  static constexpr int STAGE = ROWS * kBK;
+  static constexpr int NLD = ROWS / 8 / NW;
+  static_assert(ROWS % (8 * NW) == 0 && BM % 16 == 0 && TM >= 1 && TN >= 1, "tile shape");
+  static_assert(STAGES == 2 || STAGES == 3, "stages");
+
+  __device__ static void run(const bf16_t* const (&src)[NLD], int kt0, int kt1, bf16_t* lds,
+                             f32x4_t (&acc)[NB][TM][TN], int wave, int lane) {
+    const int wm = wave / WN, wn = wave % WN;
+    const int lr = lane % 16, lg = lane / 16;
+#pragma unroll
+    for (int h = 0; h < NB; ++h)
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int jn = 0; jn < TN; ++jn) acc[h][i][jn] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    auto issue = [&](int stage, int k0) {
+      bf16_t* dst = lds + stage * STAGE;
+#pragma unroll
+      for (int i = 0; i < NLD; ++i)
+        __builtin_amdgcn_global_load_lds((gbl_ptr_t)(src[i] + k0), (lds_ptr_t)(dst + 8 * (NW * i + wave) * kBK),
+                                         16, 0, 0);
+    };
+    // All fragment reads of a k-tile (both 32-wide k steps) are issued before
+    // the first MFMA so LDS latency overlaps the first step's MFMAs.
+    auto compute = [&](int stage) {
+      const bf16_t* L = lds + stage * STAGE;
+      bf16x8_t fa[2][TM], fb[2][NB][TN];
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const int c = s2 * 4 + lg;  // logical 16-byte chunk of this lane
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+          const int r = wm * WTM + i * 16 + lr;
+          fa[s2][i] = as_bf16x8(*reinterpret_cast<const uint4*>(&L[r * kBK + (c ^ swz(r)) * 8]));
+        }
+#pragma unroll
+        for (int h = 0; h < NB; ++h)
+#pragma unroll
+          for (int jn = 0; jn < TN; ++jn) {
+            const int r = BM + h * kBN + wn * WTN + jn * 16 + lr;
+            fb[s2][h][jn] = as_bf16x8(*reinterpret_cast<const uint4*>(&L[r * kBK + (c ^ swz(r)) * 8]));
+          }
+      }
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2)
+#pragma unroll
+        for (int h = 0; h < NB; ++h)
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int jn = 0; jn < TN; ++jn)
+              acc[h][i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[s2][i], fb[s2][h][jn], acc[h][i][jn], 0, 0, 0);
+    };
+    // k-tile kt lives in stage (kt - kt0) % STAGES; the next STAGES-1 tiles are in
+    // flight while kt is computed.  Before computing kt a wave waits until only
+    // the loads of later tiles remain outstanding, then a bare s_barrier makes
+    // every wave's tile visible (__syncthreads() would also drain the later
+    // tiles' DMA) and guarantees the stage overwritten next has been read.
+    const int nk = kt1 - kt0;
+#pragma unroll
+    for (int st = 0; st < STAGES - 1; ++st)
+      if (st < nk) issue(st, (kt0 + st) * kBK);
+    for (int t = 0; t < nk; ++t) {
+      if (STAGES == 3 && t + 1 < nk) wait_vmcnt<NLD>();
+      else wait_vmcnt<0>();
+      __asm__ volatile("" ::: "memory");
+      __builtin_amdgcn_s_barrier();
+      __asm__ volatile("" ::: "memory");
+      if (t + STAGES - 1 < nk) issue((t + STAGES - 1) % STAGES, (kt0 + t + STAGES - 1) * kBK);
+      compute(t % STAGES);
+    }
+  }
+};
+
+__device__ __forceinline__ int xcd_grouped(int b, int nblk) {
+  // block b runs on XCD b % 8: give each XCD a contiguous range of tiles
+  return (nblk & 7) == 0 ? (b & 7) * (nblk >> 3) + (b >> 3) : b;
+}
+
+// PASS 0: gate/up (dual B), PASS 1: down.  WM x WN waves per block.
+template <int BM, int WM, int WN, int PASS, int STAGES>
+__global__ __launch_bounds__(64 * WM * WN) void k_gemm_ffn(FfnArgs a) {
+  constexpr bool DUAL = PASS == 0;
+  constexpr int NB = DUAL ? 2 : 1;
+  using G = GemmTile<BM, WM, WN, NB, STAGES>;
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[STAGES * G::STAGE];
+
+  const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+  const int wm = wave / WN, wn = wave % WN;
+  tclock_start(a);
+
+  const int b = xcd_grouped(blockIdx.x, gridDim.x);
+  const int j = gemm_find_job(a, b);
+  int jt = b - a.job_tile0[j];
+  const bool shared = a.job_pos[j] == kSharedJob;
+  const int I = shared ? a.shared_inter : a.inter;
+  const int H = a.hidden;
+  const int N = PASS == 0 ? I : H;
+  const int K = PASS == 0 ? H : I;
+  const int q0 = a.job_q0[j], M = a.job_q1[j] - q0;
+  const int mtiles = (M + BM - 1) / BM;
+  const int ntiles = N / kBN;
+  // split-K (shared down pass only): slice ks of S writes its own partial output
+  const int S = (PASS == 1 && shared) ? a.ksplit : 1;
+  const int ks = jt / (mtiles * ntiles);
+  jt -= ks * mtiles * ntiles;
+  const int m0 = (jt % mtiles) * BM;
+  const int n0 = (jt / mtiles) * kBN;
+  const int nk = K / kBK;
+  const int kt0 = ks * nk / S, kt1 = (ks + 1) * nk / S;
+  const bf16_t* W = reinterpret_cast<const bf16_t*>(a.job_w[j]);
+
+  // DMA sources.  Load i of this wave fills LDS rows 8*(NW*i + wave) .. +8;
+  // lane L writes row 8*(NW*i + wave) + L/8, physical chunk L%8, so it fetches
+  // logical chunk (L%8) ^ swz(row) of that row.
+  const bf16_t* src[G::NLD];
+#pragma unroll
+  for (int i = 0; i < G::NLD; ++i) {
+    const int r = 8 * (G::NW * i + wave) + lane / 8;
+    const int c = (lane % 8) ^ swz(r);
+    if (r < BM) {
+      const int m = min(m0 + r, M - 1);  // rows past M load a valid row; results are discarded
+      const bf16_t* row;
+      if (PASS == 0) {
+        const int q = q0 + m;
+        const int t = shared ? q : a.perm[q] / a.top_k;
+        row = reinterpret_cast<const bf16_t*>(a.x) + (size_t)t * H;
+      } else {
+        row = reinterpret_cast<const bf16_t*>(shared ? a.act_sh : a.act) + (size_t)(q0 + m) * I;
+      }
+      src[i] = row + c * 8;
+    } else {
+      const int rb = r - BM;
+      const int which = rb / kBN, n = n0 + rb % kBN;
+      const bf16_t* base = PASS == 0 ? W + (size_t)which * I * H : W + (size_t)2 * I * H;  // Wg | Wu, or Wd
+      src[i] = base + (size_t)n * K + c * 8;
+    }
+  }
+  f32x4_t acc[NB][G::TM][G::TN];
+  G::run(src, kt0, kt1, lds, acc, wave, lane);
+
+  // ---- epilogue
+  const int lr = lane % 16, row_in = 4 * (lane / 16);
+#pragma unroll
+  for (int i = 0; i < G::TM; ++i) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = m0 + wm * G::WTM + i * 16 + row_in + r;
+      if (m >= M) continue;
+      const int q = q0 + m;
+      if (PASS == 0) {
+        bf16_t* act = reinterpret_cast<bf16_t*>(shared ? a.act_sh : a.act);
+#pragma unroll
+        for (int jn = 0; jn < G::TN; ++jn) {
+          const int n = n0 + wn * G::WTN + jn * 16 + lr;
+          act[(size_t)q * I + n] = f32_to_bf16(silu(acc[0][i][jn][r]) * acc[DUAL ? 1 : 0][i][jn][r]);
+        }
+      } else {
+        float* Y = shared ? a.Ysh + (size_t)ks * a.ysh_split_stride + (size_t)q * H : a.Y + (size_t)a.perm[q] * H;
+#pragma unroll
+        for (int jn = 0; jn < G::TN; ++jn) Y[n0 + wn * G::WTN + jn * 16 + lr] = acc[0][i][jn][r];
+      }
+    }
+  }
+  tclock_end(a);
+}
+
+// out[t][o_off + n] (=|+=) sum_k W[n][k] x[t][k] for n < N (rows past N load the
+// last row; their results are discarded).
+template <int BM, int WM, int WN, int STAGES>
+__global__ __launch_bounds__(64 * WM * WN) void k_gemm_rows(RowsGemmArgs a) {
+  using G = GemmTile<BM, WM, WN, 1, STAGES>;
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[STAGES * G::STAGE];
+  const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+  const int wm = wave / WN, wn = wave % WN;
+  const int b = xcd_grouped(blockIdx.x, gridDim.x);
+  const int mtiles = (a.T + BM - 1) / BM;
+  const int m0 = (b % mtiles) * BM;
+  const int n0 = (b / mtiles) * kBN;
+  const bf16_t* X = reinterpret_cast<const bf16_t*>(a.x);
+  const bf16_t* W = reinterpret_cast<const bf16_t*>(a.w);
+  const bf16_t* src[G::NLD];
+#pragma unroll
+  for (int i = 0; i < G::NLD; ++i) {
+    const int r = 8 * (G::NW * i + wave) + lane / 8;
+    const int c = (lane % 8) ^ swz(r);
+    if (r < BM) src[i] = X + (size_t)min(m0 + r, a.T - 1) * a.ldx + c * 8;
+    else src[i] = W + (size_t)min(n0 + r - BM, a.N - 1) * a.K + c * 8;
+  }
+  f32x4_t acc[1][G::TM][G::TN];
+  G::run(src, 0, a.K / kBK, lds, acc, wave, lane);
+  const int lr = lane % 16, row_in = 4 * (lane / 16);
+#pragma unroll
+  for (int i = 0; i < G::TM; ++i)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int m = m0 + wm * G::WTM + i * 16 + row_in + r;
+      if (m >= a.T) continue;
+#pragma unroll
+      for (int jn = 0; jn < G::TN; ++jn) {
+        const int n = n0 + wn * G::WTN + jn * 16 + lr;
+        if (n >= a.N) continue;
+        float* o = a.out + (size_t)m * a.ldo + a.o_off + n;
+        *o = a.add ? *o + acc[0][i][jn][r] : acc[0][i][jn][r];
+      }
+    }
+}
+
+template <int BM, int WM, int WN, int S>
+static void gemm_dispatch(FfnArgs& a, int pass, hipStream_t s) {
+  int tiles = 0;
+  for (int j = 0; j < a.n_jobs; ++j) {
+    a.job_tile0[j] = tiles;
+    const bool sh = a.job_pos[j] == kSharedJob;
+    const int I = sh ? a.shared_inter : a.inter;
+    const int N = pass == 0 ? I : a.hidden;
+    const int M = a.job_q1[j] - a.job_q0[j];
+    const int split = (pass == 1 && sh) ? a.ksplit : 1;
+    tiles += ((M + BM - 1) / BM) * (N / kBN) * split;
+  }
+  a.job_tile0[a.n_jobs] = tiles;
+  if (tiles == 0) return;
+  if (pass == 0) k_gemm_ffn<BM, WM, WN, 0, S><<<tiles, 64 * WM * WN, 0, s>>>(a);
+  else k_gemm_ffn<BM, WM, WN, 1, S><<<tiles, 64 * WM * WN, 0, s>>>(a);
+}
+
+bool gemm_supported(int N, int K) { return N % kBN == 0 && K % kBK == 0; }
+
+// Tile height: the tallest of 256 / 128 / 64 rows whose tile count still covers
+// the 256 CUs (most reuse of each weight tile while filling the machine).
+static int pick_bm(const FfnArgs& a, int pass, int max_tokens) {
+  const int cands[3] = {256, 128, 64};
+  for (int ci = 0; ci < 3; ++ci) {
+    const int bm = cands[ci];
+    if (bm == 256 && max_tokens < 512) continue;
+    if (bm == 128 && max_tokens <= 64) continue;
+    int tiles = 0;
+    for (int j = 0; j < a.n_jobs; ++j) {
+      const bool sh = a.job_pos[j] == kSharedJob;
+      const int I = sh ? a.shared_inter : a.inter;
+      const int N = pass == 0 ? I : a.hidden;
+      const int M = a.job_q1[j] - a.job_q0[j];
+      tiles += ((M + bm - 1) / bm) * (N / kBN) * ((pass == 1 && sh) ? a.ksplit : 1);
+    }
+    if (tiles >= 256 || bm == 64) return bm;
+  }
+  return 64;
+}
+
+int gemm_tiles_shared_down(int T, int H) {
+  const int bm = T >= 512 ? 256 : (T > 64 ? 128 : 64);
+  return ((T + bm - 1) / bm) * (H / kBN);
+}
+
+void launch_gemm_rows(const RowsGemmArgs& a, hipStream_t s) {
+  const int ntiles = (a.N + kBN - 1) / kBN;
+  if (a.T >= 256) {
+    k_gemm_rows<128, 2, 4, 3><<<((a.T + 127) / 128) * ntiles, 512, 0, s>>>(a);
+  } else {
+    k_gemm_rows<64, 1, 4, 3><<<((a.T + 63) / 64) * ntiles, 256, 0, s>>>(a);
+  }
+}
+
+void launch_gemm(FfnArgs& a, int pass, int max_tokens, hipStream_t s) {
+  const int bm = pick_bm(a, pass, max_tokens);
+  if (bm == 256) gemm_dispatch<256, 2, 4, 2>(a, pass, s);
+  else if (bm == 128) gemm_dispatch<128, 2, 4, 3>(a, pass, s);
+  else gemm_dispatch<64, 1, 4, 3>(a, pass, s);
+}
+
+}  // namespace promoe

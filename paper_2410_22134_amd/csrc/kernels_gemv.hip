@@ -196,20 +196,6 @@ __device__ __forceinline__ uint4 ld16(const TW* p) {
   return *reinterpret_cast<const uint4*>(p);
 }
 
-// Launch timing on the device's constant-rate clock (profiling only): the
-// earliest block start and the latest wave end of the launch.
-// Blocks start in index order, so the first blocks carry the start; wave ends
-// are spread over separate cache lines so the atomics do not serialise.
-__device__ __forceinline__ void tclock_start(const FfnArgs& a) {
-  if (a.tclock && threadIdx.x == 0 && blockIdx.x < 8) atomicMax(a.tclock, ~(unsigned long long)wall_clock64());
-}
-__device__ __forceinline__ void tclock_end(const FfnArgs& a, int lane) {
-  if (a.tclock && lane == 0) {
-    const int line = 1 + (blockIdx.x * kBlockWaves + threadIdx.x / kWave) % kTclkLines;
-    atomicMax(a.tclock + 16 * line, (unsigned long long)wall_clock64());
-  }
-}
-
 // acc[r][m] += <rows[r], xs[m]> over k; rows/xs point at element 0 of the row
 // (xs at the token's vector).  nch = K / EPC chunks of 16 bytes.
 template <typename TW, int R, int MT, int NCH>
@@ -298,7 +284,7 @@ __global__ __launch_bounds__(kThreads) void k_ffn_gateup(FfnArgs a) {
       if (m < mt && i0 + r < I) Elem<TW>::store(act, (g + m) * I + i0 + r, silu(ga) * ub);
     }
   }
-  tclock_end(a, lane);
+  tclock_end(a);
 }
 
 // pass 2: Y[pair][n] = Wd[n] . act[q] for the wave's RW rows n
@@ -350,7 +336,7 @@ __global__ __launch_bounds__(kThreads) void k_ffn_down(FfnArgs a) {
       }
     }
   }
-  tclock_end(a, lane);
+  tclock_end(a);
 }
 
 // ============================================================ combine
@@ -362,8 +348,10 @@ __global__ __launch_bounds__(kThreads) void k_combine(CombineArgs a) {
   float y = 0.0f;
   for (int r = 0; r < a.top_k; ++r) y += a.w[t * a.top_k + r] * a.Y[((size_t)t * a.top_k + r) * a.hidden + n];
   if (a.Ysh) {
+    float ysh = 0.0f;
+    for (int k = 0; k < a.ysh_split; ++k) ysh += a.Ysh[(size_t)k * a.ysh_split_stride + (size_t)t * a.hidden + n];
     const float s = a.sscale ? a.sscale[t] : 1.0f;
-    y += s * a.Ysh[(size_t)t * a.hidden + n];
+    y += s * ysh;
   }
   Elem<TY>::store(reinterpret_cast<TY*>(a.y), t * a.hidden + n, y);
 }

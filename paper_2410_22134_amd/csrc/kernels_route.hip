@@ -195,8 +195,7 @@ __global__ __launch_bounds__(256) void k_plan_spec(PlanArgs a) {
 
 // ============================================================ precise plan + permutation
 __global__ __launch_bounds__(256) void k_plan_precise(PlanArgs a) {
-  __shared__ int cnt_e[kMaxE], pos_of[kMaxE], order[kMaxE], offs[kMaxE + 1], fill[kMaxE], tile_cnt[kMaxE];
-  __shared__ int tile_pos[256];
+  __shared__ int cnt_e[kMaxE], pos_of[kMaxE], order[kMaxE], offs[kMaxE + 1], fill[kMaxE];
   __shared__ int n_pos;
   const int tid = threadIdx.x, lane = tid % kWave;
   const int npairs = a.T * a.k;
@@ -280,21 +279,35 @@ __global__ __launch_bounds__(256) void k_plan_precise(PlanArgs a) {
   __syncthreads();
 
   // Permutation: pairs in (t, r) order are placed into their position's range,
-  // keeping (t, r) order inside a range.  Tiles of 256 pairs.
+  // keeping (t, r) order inside a range.  Tiles of 256 pairs; inside a wave the
+  // lanes with the same position are found with six ballots (one per bit of the
+  // position), which gives each pair its rank among the earlier lanes; the waves'
+  // counts are then prefixed through LDS.
+  __shared__ int wave_cnt[4][kMaxE];
+  const int wave = tid / kWave;
+  const uint64_t lt_mask = (1ull << lane) - 1ull;
   for (int base = 0; base < npairs; base += 256) {
     const int i = base + tid;
     const int pos = i < npairs ? pos_of[a.ids[i]] : -1;
-    tile_pos[tid] = pos;
-    if (tid < kMaxE) tile_cnt[tid] = 0;
+    for (int e = tid; e < 4 * kMaxE; e += 256) (&wave_cnt[0][0])[e] = 0;
+    uint64_t same = __ballot(pos >= 0);
+#pragma unroll
+    for (int bit = 0; bit < 6; ++bit) {
+      const bool on = pos >= 0 && ((pos >> bit) & 1);
+      const uint64_t bal = __ballot(on);
+      same &= on ? bal : ~bal;
+    }
+    const int rank_in_wave = __popcll(same & lt_mask);
+    __syncthreads();
+    if (pos >= 0 && rank_in_wave == 0) wave_cnt[wave][pos] = __popcll(same);
     __syncthreads();
     if (pos >= 0) {
-      int r = 0;
-      for (int j = 0; j < tid; ++j) r += tile_pos[j] == pos;
-      a.d_perm[offs[pos] + fill[pos] + r] = i;
-      atomicAdd(&tile_cnt[pos], 1);
+      int before = fill[pos];
+      for (int w = 0; w < wave; ++w) before += wave_cnt[w][pos];
+      a.d_perm[offs[pos] + before + rank_in_wave] = i;
     }
     __syncthreads();
-    if (tid < kMaxE) fill[tid] += tile_cnt[tid];
+    if (tid < kMaxE) fill[tid] += wave_cnt[0][tid] + wave_cnt[1][tid] + wave_cnt[2][tid] + wave_cnt[3][tid];
     __syncthreads();
   }
   if (tid == 0) {

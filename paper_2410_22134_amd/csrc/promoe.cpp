@@ -39,6 +39,7 @@ namespace {
 thread_local std::string g_last_error;
 
 constexpr int kRecRing = 64;
+constexpr int kMaxSplit = 8;  // split-K slices of the shared expert's down GEMM
 constexpr int kCopyRing = 4096;
 constexpr int kComputeRing = 4096;
 
@@ -379,7 +380,35 @@ int launch_gate_rows(promoe_ctx* c, int layer, const void* d_x, int T, bool with
   a.out = c->d_logits;
   a.ldo = c->ld_logits;
   a.o_off = 0;
-  launch_rows_gemv(a, c->dt, c->dt, s);
+  if (c->dt == PROMOE_BF16 && T >= 64 && c->H % 64 == 0) {
+    // prefill-sized: gate and predictor rows on MFMA, the single shared-gate row as a GEMV
+    RowsGemmArgs g{};
+    g.w = w.wg;
+    g.N = c->E;
+    g.K = c->H;
+    g.x = d_x;
+    g.ldx = c->H;
+    g.T = T;
+    g.out = c->d_logits;
+    g.ldo = c->ld_logits;
+    launch_gemm_rows(g, s);
+    if (a.nrows[1]) {
+      RowsArgs r = a;
+      r.w[0] = w.sgate;
+      r.nrows[0] = 1;
+      r.nrows[1] = r.nrows[2] = 0;
+      r.o_off = c->E;
+      launch_rows_gemv(r, c->dt, c->dt, s);
+    }
+    if (with_pred) {
+      g.w = w.pw1;
+      g.N = a.nrows[2];
+      g.o_off = c->pred_col;
+      launch_gemm_rows(g, s);
+    }
+  } else {
+    launch_rows_gemv(a, c->dt, c->dt, s);
+  }
   LAUNCHCHK("gate rows");
   return PROMOE_OK;
 }
@@ -473,7 +502,8 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
                o_offs = take(sizeof(int32_t) * 65), o_perm = take(sizeof(int32_t) * (size_t)T * Kk),
                o_posof = take(sizeof(int32_t) * 64), o_warm = take(sizeof(int32_t) * 64),
                o_act = take((size_t)c->eb * T * Kk * c->I), o_Y = take(sizeof(float) * (size_t)T * Kk * H),
-               o_actsh = take((size_t)c->eb * T * std::max(c->Ish, 1)), o_Ysh = take(sizeof(float) * (size_t)T * H),
+               o_actsh = take((size_t)c->eb * T * std::max(c->Ish, 1)),
+               o_Ysh = take(sizeof(float) * (size_t)kMaxSplit * T * H),
                o_u = take((size_t)c->eb * T * H);
   hipError_t e = hipMalloc(&c->dmem, off);
   if (e != hipSuccess) {
@@ -855,12 +885,15 @@ namespace {
 
 // Launch the gate/up and down passes over a list of jobs (route positions, or
 // kSharedJob), waiting first for copy `wait01` (chunks 0-1 of every job) and
-// then `wait2` (chunk 2).
-int ffn_launch(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipStream_t s, int64_t wait01,
-               int64_t wait2) {
+// then `wait2` (chunk 2).  Jobs with >= kGemmMinTokens pairs go to the MFMA
+// GEMM (bf16, tile-aligned shapes), the rest to the GEMV kernels.
+constexpr int kGemmMinTokens = 16;
+
+int ffn_launch_one(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipStream_t s, int64_t wait01,
+                   int64_t wait2, bool gemm) {
   const PlanRecord& rec = c->route_rec;
   int maxc = 1;
-  double wbytes = 0, flops = 0;  // per pass 0 (gate/up) and 1 (down), scaled below
+  double wbytes = 0, flops = 0;
   a.n_jobs = (int)jobs.size();
   for (size_t i = 0; i < jobs.size(); ++i) {
     const bool sh = jobs[i] == kSharedJob;
@@ -889,10 +922,37 @@ int ffn_launch(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipStream
       if (c->profile) { hipEventRecord(pb, s); c->prof_pending.push_back(ProfEntry{pa, pb, 4, 0, 0}); }
     }
     const double k = pass == 0 ? 2.0 : 1.0;  // gate and up, or down
-    a.tclock = c->profile ? tclock_slot(c, s, pass, k * wbytes, k * flops) : nullptr;
-    launch_ffn(a, pass, maxc, c->dt, s);
+    const int cls = (gemm ? 2 : 0) + pass;
+    a.tclock = c->profile ? tclock_slot(c, s, cls, k * wbytes, k * flops) : nullptr;
+    if (gemm) launch_gemm(a, pass, maxc, s);
+    else launch_ffn(a, pass, maxc, c->dt, s);
     LAUNCHCHK("ffn");
   }
+  return PROMOE_OK;
+}
+
+bool use_gemm(promoe_ctx* c, int tokens, bool shared) {
+  if (c->dt != PROMOE_BF16 || tokens < kGemmMinTokens) return false;
+  const int I = shared ? c->Ish : c->I;
+  return gemm_supported(I, c->H) && gemm_supported(c->H, I);
+}
+
+int ffn_launch(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipStream_t s, int64_t wait01,
+               int64_t wait2) {
+  // split by kernel family; the shared expert (M = T) gets its own GEMM launch
+  // so the routed groups can use the small-M tile
+  std::vector<int> gv, gm, sh;
+  for (int p : jobs) {
+    const bool is_sh = p == kSharedJob;
+    const int cnt = is_sh ? a.T : c->route_rec.count[p];
+    if (!use_gemm(c, cnt, is_sh)) gv.push_back(p);
+    else if (is_sh) sh.push_back(p);
+    else gm.push_back(p);
+  }
+  int rc = PROMOE_OK;
+  if (!sh.empty() && (rc = ffn_launch_one(c, a, sh, s, wait01, wait2, true))) return rc;
+  if (!gm.empty() && (rc = ffn_launch_one(c, a, gm, s, wait01, wait2, true))) return rc;
+  if (!gv.empty() && (rc = ffn_launch_one(c, a, gv, s, wait01, wait2, false))) return rc;
   return PROMOE_OK;
 }
 
@@ -928,6 +988,17 @@ int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const in
   a.shared_w = c->lw[layer].shared;
   a.act_sh = c->d_act_sh;
   a.Ysh = c->d_Ysh;
+  // The shared expert's down GEMM has only (T / BM) x (H / 128) output tiles;
+  // split its reduction so the launch covers the CUs.  Slices write separate
+  // partial outputs that the combine adds in slice order (deterministic).
+  a.ksplit = 1;
+  a.ysh_split_stride = (int64_t)T * c->H;
+  if (c->Ish > 0 && use_gemm(c, T, true)) {
+    const int tiles = gemm_tiles_shared_down(T, c->H);
+    int sp = (256 + tiles - 1) / tiles;
+    sp = std::max(1, std::min(std::min(sp, kMaxSplit), c->Ish / 64 / 4));
+    a.ksplit = sp;
+  }
 
   std::unique_lock<std::mutex> lk(c->mu);
   const int n = rec.n;
@@ -997,6 +1068,8 @@ int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const in
   ca.Y = c->d_Y;
   ca.w = d_w;
   ca.Ysh = c->Ish > 0 ? c->d_Ysh : nullptr;
+  ca.ysh_split = a.ksplit;
+  ca.ysh_split_stride = a.ysh_split_stride;
   ca.sscale = (c->Ish > 0 && c->cfg.shared_gate) ? d_shared_scale : nullptr;
   ca.y = d_y;
   ca.hidden = c->H;
@@ -1099,7 +1172,21 @@ int promoe_attn_surrogate(promoe_ctx* c, int layer, float* d_h, int T, void* d_x
     a.out = d_h;
     a.ldo = c->H;
     a.add = 1;
-    launch_rows_gemv(a, c->dt, c->dt, s);
+    if (c->dt == PROMOE_BF16 && T >= 64 && c->H % 64 == 0) {
+      RowsGemmArgs g{};
+      g.w = c->lw[layer].attn;
+      g.N = c->H;
+      g.K = c->H;
+      g.x = c->d_u;
+      g.ldx = c->H;
+      g.T = T;
+      g.out = d_h;
+      g.ldo = c->H;
+      g.add = 1;
+      launch_gemm_rows(g, s);
+    } else {
+      launch_rows_gemv(a, c->dt, c->dt, s);
+    }
   }
   launch_rmsnorm_quant(d_h, d_x_out, T, c->H, c->dt, s);
   LAUNCHCHK("attn surrogate");
