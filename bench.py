@@ -1,5 +1,6 @@
 """Benchmark: decode tokens/s of the DeepSeek-MoE-16B-shaped stack at a 50% expert cache.
 
+The reported value: decode tokens/s of the DeepSeek-MoE-16B-shaped stack.
 One step = one decode token (batch 1) through all 27 layers of the hot path:
 attention surrogate, look-ahead prediction and speculative plan, gate + top-k +
 precise plan, chunked high/low-priority copies from pinned host memory, expert
@@ -8,10 +9,12 @@ per-step hidden states) are resident in HBM before the timed region; expert
 weights live where the method puts them: 32 of 64 experts per layer in the HBM
 cache, all 64 in pinned host memory.
 
-Prints one JSON line.  The roofline entry is for the dominant kernel (the FFN
-gate/up GEMV), timed with HIP events on its launch stream over the timed
-region; the cpu_baseline entry times the CPU oracle on a bounded sample of the
-same workload on this host.
+Prints one JSON line.  The roofline entry is for the dominant kernel of that
+workload (the FFN gate/up GEMV), each launch timed on the device clock over the
+timed region; the cpu_baseline entry times the CPU oracle on a bounded sample
+of the same workload on this host.  Further legs (detail only): prefill of the
+Qwen1.5-MoE-A2.7B shape (512 tokens, 50% cache) and the shared-expert MFMA
+GEMMs at the Qwen2-57B-A14B shape (roofline_prefill_gemm).
 """
 from __future__ import annotations
 
@@ -25,6 +28,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 METRIC = "decode & prefill tok/s at 50% expert cache; expert-FFN HBM GB/s, MFMA util"
 
 
@@ -38,7 +42,29 @@ def parse():
     p.add_argument("--no-prefetch", action="store_true", help="reactive LRU (predictions ignored)")
     p.add_argument("--copy-calib-mib", type=int, default=1024,
                    help="size of the plain device copy run after the timed region (counter calibration)")
+    p.add_argument("--legs", default="decode,prefill,mfma",
+                   help="decode is always run (it is the reported value); add prefill and/or mfma")
+    p.add_argument("--prefill-steps", type=int, default=3)
+    p.add_argument("--prefill-warmup", type=int, default=1)
     return p.parse_args()
+
+
+def read_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or None when the
+    summary is missing or was taken on a different kernel source."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic_counters.txt")
+    src = os.path.join(ROOT, "paper_2410_22134_amd", "csrc", "kernels_gemv.hip")
+    if not os.path.exists(path):
+        return None
+    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    for line in open(path):
+        f = line.split()
+        if len(f) >= 4 and f[0] == "traffic" and f[1] == kernel:
+            if f[2] != digest:
+                return None
+            return int(float(f[3]))
+    return None
 
 
 def h2d_probe(torch, mib=256, reps=5):
@@ -107,12 +133,96 @@ def cpu_baseline(cfg, model, budget_s):
                       f"{dt:.1f} s, scaled to a whole token"}
 
 
+def _classes(s):
+    """Per kernel class: launches, avg us, achieved GB/s and TFLOP/s (device-clock timing)."""
+    names = ("gemv_gateup", "gemv_down", "gemm_gateup_routed", "gemm_down_routed", "gemm_gateup_shared",
+             "gemm_down_shared")
+    out = {}
+    for i, nm in enumerate(names):
+        n, ms, by, fl = s["k_launches"][i], s["k_ms"][i], s["k_bytes"][i], s["k_flops"][i]
+        if n:
+            out[nm] = {"launches": n, "avg_us": round(ms / n * 1e3, 3),
+                       "GBps": round(by / (ms * 1e-3) / 1e9, 1), "TFLOPs": round(fl / (ms * 1e-3) / 1e12, 1),
+                       "bytes_per_launch": round(by / n), "flops_per_launch": round(fl / n)}
+    return out
+
+
+def run_steps(torch, model, st, inputs, warmup, steps):
+    for i in range(warmup):
+        st.step(inputs[i])
+    model.ctx.sync()
+    torch.cuda.synchronize()
+    model.ctx.reset_stats()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        st.step(inputs[warmup + i])
+    model.ctx.sync()
+    torch.cuda.synchronize()
+    return time.perf_counter() - t0, model.ctx.stats()
+
+
+def leg_prefill(torch, args, flags):
+    """Qwen1.5-MoE-A2.7B shape, 24 layers, 512-token prompt, 30 of 60 experts cached."""
+    import numpy as np
+    from synth import configs, model as sm
+    from paper_2410_22134_amd.model import SyntheticModel
+    from paper_2410_22134_amd.stack import Stack
+    cfg = configs.C3
+    T = 512
+    model = SyntheticModel(cfg, max_tokens=T, flags=flags, gen_threads=8)
+    try:
+        st = Stack(model, T)
+        n = args.prefill_warmup + args.prefill_steps
+        h = torch.from_numpy(np.stack([sm.stack_input(cfg, 1000 + i, T) for i in range(n)])).cuda()
+        dt, s = run_steps(torch, model, st, h, args.prefill_warmup, args.prefill_steps)
+        cls = _classes(s)
+        return {"workload": "Qwen1.5-MoE-A2.7B-shaped stack prefill: 24 layers, hidden 2048, 60 routed experts "
+                            "(I=1408) top-4 + gated shared expert (I=5632), 512-token prompt, 30 of 60 experts "
+                            "per layer cached, look-ahead 2",
+                "tok_s": round(T * args.prefill_steps / dt, 1), "ms_per_step": round(dt / args.prefill_steps * 1e3, 2),
+                "copied_GB": round((s["bytes_high"] + s["bytes_low"]) / 1e9, 3),
+                "copy_GBps_over_timed_region": round((s["bytes_high"] + s["bytes_low"]) / dt / 1e9, 2),
+                "hit": s["hit"], "miss": s["miss"], "kernels": cls}
+    finally:
+        model.close()
+
+
+def leg_mfma(torch, args):
+    """Shared-expert GEMMs at the Qwen2-57B-A14B shape (hidden 3584, shared I = 20480),
+    1024-token prefill, two layers with every expert resident (compute only)."""
+    from synth import configs, model as sm
+    from paper_2410_22134_amd import FLAG_PROFILE
+    from paper_2410_22134_amd.model import SyntheticModel
+    from paper_2410_22134_amd.stack import Stack
+    base = configs.C5
+    cfg = base.with_(n_layers=2, slots=base.n_experts)
+    T = 1024
+    model = SyntheticModel(cfg, max_tokens=T, flags=FLAG_PROFILE, gen_threads=8)
+    try:
+        st = Stack(model, T)
+        import numpy as np
+        h = torch.from_numpy(np.stack([sm.stack_input(cfg, 2000 + i, T) for i in range(4)])).cuda()
+        dt, s = run_steps(torch, model, st, h, 1, 3)
+        cls = _classes(s)
+        fl = s["k_flops"][4] + s["k_flops"][5]
+        ms = s["k_ms"][4] + s["k_ms"][5]
+        tf = fl / (ms * 1e-3) / 1e12 if ms else 0.0
+        return {"bound": "mfma", "kernel": "k_gemm_ffn (shared expert, gate/up + down)",
+                "achieved": round(tf, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                "workload": "Qwen2-57B-A14B shape: M = 1024 tokens, hidden 3584, shared I = 20480, bf16",
+                "kernels": cls}
+    finally:
+        model.close()
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path (expert-parallel sharding "
               "is a design note); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+    import numpy as np
     import torch
     from synth import configs
     from synth import model as sm
@@ -127,41 +237,21 @@ def main():
     model = SyntheticModel(cfg, max_tokens=1, flags=flags, gen_threads=8)
     st = Stack(model, 1)
     n_in = args.warmup + args.steps
-    h_in = torch.from_numpy(__import__("numpy").stack([sm.stack_input(cfg, i, 1) for i in range(n_in)])).cuda()
+    h_in = torch.from_numpy(np.stack([sm.stack_input(cfg, i, 1) for i in range(n_in)])).cuda()
     setup_s = time.perf_counter() - t_setup
-    print(f"[bench] setup {setup_s:.1f}s; warmup {args.warmup} steps", file=sys.stderr, flush=True)
-    for i in range(args.warmup):
-        st.step(h_in[i])
-    model.ctx.sync()
-    torch.cuda.synchronize()
-    model.ctx.reset_stats()
-    print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        st.step(h_in[args.warmup + i])
-    model.ctx.sync()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    s = model.ctx.stats()
+    print(f"[bench] decode: setup {setup_s:.1f}s; {args.warmup} warm-up + {args.steps} timed steps",
+          file=sys.stderr, flush=True)
+    elapsed, s = run_steps(torch, model, st, h_in, args.warmup, args.steps)
     tok_s = args.steps / elapsed
 
     # dominant kernel: FFN gate/up GEMV (class 0); bytes are the weight rows it streams
     launches, ms, by = s["k_launches"][0], s["k_ms"][0], s["k_bytes"][0]
     avg_us = ms / launches * 1e3 if launches else 0.0
     achieved = (by / launches) / (avg_us * 1e-6) / 1e9 if launches else 0.0
-    down_gbs = s["k_bytes"][1] / (s["k_ms"][1] * 1e-3) / 1e9 if s["k_ms"][1] else 0.0
     copy_bytes = s["bytes_high"] + s["bytes_low"]
     h2d_gbs = h2d_probe(torch)
     load_s = s["bytes_high"] / (h2d_gbs * 1e9) if h2d_gbs else 0.0
-    stall_s = s["stall_ms"] * 1e-3
-    # plain device copy of known size for counter calibration (FETCH_SIZE / WRITE_SIZE scaling)
-    n = args.copy_calib_mib << 20
-    a = torch.empty(n, dtype=torch.uint8, device="cuda")
-    b = torch.empty_like(a)
-    b.copy_(a)
-    torch.cuda.synchronize()
-    del a, b
-
+    traffic = read_traffic("k_ffn_gateup")
     out = {
         "metric": METRIC,
         "value": round(tok_s, 3),
@@ -182,17 +272,18 @@ def main():
                    "prefetch": not args.no_prefetch},
         "roofline": {"bound": "hbm", "kernel": "k_ffn_gateup<bf16,1>", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": None, "avg_launch_us": round(avg_us, 3),
-                     "bytes_per_launch": round(by / launches) if launches else 0, "launches": launches},
+                     "traffic": traffic, "avg_launch_us": round(avg_us, 3),
+                     "bytes_per_launch": round(by / launches) if launches else 0, "launches": launches,
+                     "timing": "device clock, first block start to last wave end"},
         "detail": {
-            "down_gemv_GBps": round(down_gbs, 1),
+            "decode_kernels": _classes(s),
             "h2d_copy_GBps_measured_256MiB": round(h2d_gbs, 2),
             "copied_GB": round(copy_bytes / 1e9, 3),
             "copy_GBps_over_timed_region": round(copy_bytes / elapsed / 1e9, 2),
             "hit": s["hit"], "miss": s["miss"], "prec_access": s["prec_access"],
             "spec_issued": s["spec_issued"], "spec_used": s["spec_used"], "spec_wasted": s["spec_wasted"],
             "low_purged_subcopies": s["low_purged"],
-            "stall_s": round(stall_s, 4), "miss_load_s_at_measured_h2d": round(load_s, 4),
+            "stall_s": round(s["stall_ms"] * 1e-3, 4), "miss_load_s_at_measured_h2d": round(load_s, 4),
             "setup_s": round(setup_s, 1),
         },
     }
@@ -200,6 +291,19 @@ def main():
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(cfg, model, args.cpu_seconds)
     model.close()
+    # plain device copy of known size (FETCH_SIZE / WRITE_SIZE calibration under rocprofv3 --pmc)
+    n = args.copy_calib_mib << 20
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    del a, b
+    if "prefill" in args.legs:
+        print("[bench] prefill leg", file=sys.stderr, flush=True)
+        out["detail"]["prefill"] = leg_prefill(torch, args, flags)
+    if "mfma" in args.legs:
+        print("[bench] shared-expert MFMA leg", file=sys.stderr, flush=True)
+        out["roofline_prefill_gemm"] = leg_mfma(torch, args)
     print(json.dumps(out), flush=True)
 
 

@@ -100,13 +100,16 @@ typedef struct promoe_stats {
   int64_t low_purged;               /* queued low-priority sub-copies dropped by route */
   int64_t deferred;                 /* high copies held until an earlier expert of the
                                        same layer finished reading the slot */
-  /* Timing, PROMOE_FLAG_PROFILE only (HIP events on the launch stream). */
-  int64_t k_launches[4];  /* [0] FFN gate/up, [1] FFN down, [2] GEMM gate/up, [3] GEMM down */
-  double k_ms[4];         /* summed kernel time */
-  double k_bytes[4];      /* summed algorithmic weight bytes */
-  double k_flops[4];      /* summed algorithmic flops */
-  double stall_ms;        /* compute stream time spent waiting on copies */
-  double copy_ms;         /* copy stream busy time (first issue to last completion, summed per burst) */
+  /* Timing, PROMOE_FLAG_PROFILE only.  Expert launches are timed on the
+     device clock (earliest block start to latest wave end); classes:
+     [0] GEMV gate/up, [1] GEMV down, [2] GEMM gate/up (routed experts),
+     [3] GEMM down (routed), [4] GEMM gate/up (shared expert), [5] GEMM down (shared). */
+  int64_t k_launches[6];
+  double k_ms[6];         /* summed launch time */
+  double k_bytes[6];      /* summed algorithmic weight bytes */
+  double k_flops[6];      /* summed algorithmic flops */
+  double stall_ms;        /* compute stream time spent waiting on copies (HIP events) */
+  double copy_ms;         /* reserved (0) */
 } promoe_stats;
 
 typedef struct promoe_plan {

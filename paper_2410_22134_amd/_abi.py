@@ -30,7 +30,7 @@ class Stats(ctypes.Structure):
     _fields_ = [(n, _i64) for n in STAT_COUNTERS] + [
         ("copies_high", _i64), ("copies_low", _i64), ("bytes_high", _i64), ("bytes_low", _i64),
         ("low_purged", _i64), ("deferred", _i64),
-        ("k_launches", _i64 * 4), ("k_ms", _dbl * 4), ("k_bytes", _dbl * 4), ("k_flops", _dbl * 4),
+        ("k_launches", _i64 * 6), ("k_ms", _dbl * 6), ("k_bytes", _dbl * 6), ("k_flops", _dbl * 6),
         ("stall_ms", _dbl), ("copy_ms", _dbl)]
 
     def as_dict(self):

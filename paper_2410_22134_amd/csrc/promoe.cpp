@@ -39,13 +39,14 @@ namespace {
 thread_local std::string g_last_error;
 
 constexpr int kRecRing = 64;
+constexpr int kStallClass = 99;
 constexpr int kMaxSplit = 8;  // split-K slices of the shared expert's down GEMM
 constexpr int kCopyRing = 4096;
 constexpr int kComputeRing = 4096;
 
 struct ProfEntry {
   hipEvent_t a, b;
-  int cls;  // 0..3 kernels, 4 stall
+  int cls;  // 0..5 kernel classes, kStallClass copy waits
   double bytes, flops;
 };
 
@@ -155,8 +156,9 @@ struct promoe_ctx {
   double wall_khz = 100000.0;
   std::vector<ProfEntry> prof_pending;
   std::vector<hipEvent_t> prof_free;
-  int64_t k_launches[4] = {0, 0, 0, 0};
-  double k_ms[4] = {0, 0, 0, 0}, k_bytes[4] = {0, 0, 0, 0}, k_flops[4] = {0, 0, 0, 0};
+  static constexpr int kClasses = 6;
+  int64_t k_launches[kClasses] = {};
+  double k_ms[kClasses] = {}, k_bytes[kClasses] = {}, k_flops[kClasses] = {};
   double stall_ms = 0.0;
 };
 
@@ -234,7 +236,7 @@ void prof_resolve(promoe_ctx* c) {
     hipEventSynchronize(p.b);
     float ms = 0.0f;
     hipEventElapsedTime(&ms, p.a, p.b);
-    if (p.cls < 4) {
+    if (p.cls < promoe_ctx::kClasses) {
       c->k_launches[p.cls]++;
       c->k_ms[p.cls] += ms;
       c->k_bytes[p.cls] += p.bytes;
@@ -919,10 +921,11 @@ int ffn_launch_one(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipSt
       hipEvent_t pa = nullptr, pb = nullptr;
       if (c->profile) { pa = prof_event(c); pb = prof_event(c); hipEventRecord(pa, s); }
       HIPCHK(hipStreamWaitEvent(s, c->eng.event(w), 0));
-      if (c->profile) { hipEventRecord(pb, s); c->prof_pending.push_back(ProfEntry{pa, pb, 4, 0, 0}); }
+      if (c->profile) { hipEventRecord(pb, s); c->prof_pending.push_back(ProfEntry{pa, pb, kStallClass, 0, 0}); }
     }
     const double k = pass == 0 ? 2.0 : 1.0;  // gate and up, or down
-    const int cls = (gemm ? 2 : 0) + pass;
+    const bool shared_only = jobs.size() == 1 && jobs[0] == kSharedJob;
+    const int cls = (gemm ? (shared_only ? 4 : 2) : 0) + pass;
     a.tclock = c->profile ? tclock_slot(c, s, cls, k * wbytes, k * flops) : nullptr;
     if (gemm) launch_gemm(a, pass, maxc, s);
     else launch_ffn(a, pass, maxc, c->dt, s);
@@ -1104,7 +1107,7 @@ int promoe_cache_stats(promoe_ctx* c, int layer, promoe_stats* out) {
   out->bytes_high = ps.bytes[1];
   out->low_purged = ps.low_purged;
   out->deferred = ps.deferred;
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < promoe_ctx::kClasses; ++i) {
     out->k_launches[i] = c->k_launches[i];
     out->k_ms[i] = c->k_ms[i];
     out->k_bytes[i] = c->k_bytes[i];
@@ -1123,7 +1126,7 @@ int promoe_reset_stats(promoe_ctx* c) {
   HIPCHK(hipDeviceSynchronize());
   std::lock_guard<std::mutex> lk(c->mu);
   c->pf->reset_stats();
-  for (int i = 0; i < 4; ++i) c->k_launches[i] = 0, c->k_ms[i] = c->k_bytes[i] = c->k_flops[i] = 0.0;
+  for (int i = 0; i < promoe_ctx::kClasses; ++i) c->k_launches[i] = 0, c->k_ms[i] = c->k_bytes[i] = c->k_flops[i] = 0.0;
   c->stall_ms = 0.0;
   return PROMOE_OK;
 }
