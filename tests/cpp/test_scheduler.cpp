@@ -1,0 +1,246 @@
+// CPU tests of the copy scheduler (Prefetcher) against a copy engine with a
+// simulated clock: one FIFO queue, copies take bytes / bandwidth time units,
+// a copy may wait for a compute token that completes at a given time.
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "../../paper_2410_22134_amd/csrc/scheduler.hpp"
+
+using namespace promoe;
+
+namespace {
+
+int failures = 0;
+#define CHECK(cond)                                                        \
+  do {                                                                     \
+    if (!(cond)) {                                                         \
+      std::printf("FAIL %s:%d: %s\n", __FILE__, __LINE__, #cond);          \
+      ++failures;                                                          \
+    }                                                                      \
+  } while (0)
+
+struct FakeEngine : CopyEngine {
+  double now = 0.0;
+  double bw = 1.0;  // bytes per time unit
+  int64_t cap = INT64_MAX;
+  struct Copy {
+    double start, end;
+    uint8_t* dst;
+    size_t bytes;
+    int64_t after;
+  };
+  std::vector<Copy> log;
+  std::map<int64_t, double> compute_done;  // compute token -> completion time
+  void issue(int64_t seq, void* dst, const void*, size_t bytes, int64_t after) override {
+    double start = now;
+    if (!log.empty()) start = std::max(start, log.back().end);
+    if (after >= 0) {
+      auto it = compute_done.find(after);
+      start = std::max(start, it == compute_done.end() ? 1e30 : it->second);
+    }
+    if ((int64_t)log.size() != seq) std::abort();
+    log.push_back({start, start + (double)bytes / bw, static_cast<uint8_t*>(dst), bytes, after});
+  }
+  bool done(int64_t seq) override { return log[seq].end <= now + 1e-12; }
+  void wait(int64_t seq) override { now = std::max(now, log[seq].end); }
+  int64_t capacity() const override { return cap; }
+  void advance(double t) { now = std::max(now, t); }
+};
+
+// Memory layout helpers: one layer, C slots, experts of 3 chunks.
+struct Rig {
+  FakeEngine eng;
+  std::vector<uint8_t> host, cache;
+  Prefetcher* pf;
+  size_t chunk;
+  Rig(int L, int C, int E, size_t chunk_bytes, size_t sub, int window) : chunk(chunk_bytes) {
+    host.resize((size_t)L * E * 3 * chunk_bytes);
+    cache.resize((size_t)L * C * 3 * chunk_bytes);
+    pf = new Prefetcher(L, C, E, chunk_bytes, sub, window, cache.data(), &eng);
+    for (int l = 0; l < L; ++l)
+      for (int e = 0; e < E; ++e) pf->set_host(l, e, host.data() + ((size_t)l * E + e) * 3 * chunk_bytes);
+  }
+  ~Rig() { delete pf; }
+  // start time of the first copy into (layer, slot) issued at or after log index `from`
+  double first_start_into(int layer, int slot, int C, size_t from = 0) {
+    uint8_t* lo = cache.data() + ((size_t)layer * C + slot) * 3 * chunk;
+    for (size_t i = from; i < eng.log.size(); ++i)
+      if (eng.log[i].dst >= lo && eng.log[i].dst < lo + 3 * chunk) return eng.log[i].start;
+    return -1.0;
+  }
+  // the worker's behaviour between host events: issue, wait for the oldest, repeat, up to time t
+  void worker_until(double t) {
+    for (;;) {
+      pf->pump();
+      const int64_t o = pf->oldest_in_flight();
+      if (o < 0 || eng.log[o].end > t) break;
+      eng.wait(o);
+      pf->retire();
+    }
+    eng.advance(t);
+    pf->retire();
+    pf->pump();
+  }
+};
+
+// Chunked prefetching and early preemption, the paper's worked example
+// (expert of three chunks copied at low priority; a miss arrives during the
+// second chunk, or -- with early preemption -- while the first one copies).
+void example(double* chunked, double* unchunked, double* early) {
+  for (int variant = 0; variant < 3; ++variant) {
+    const bool chunking = variant != 1;
+    const size_t unit = 100;  // bytes of one matrix; bw 100 B / unit time -> 1 time unit per chunk
+    // without chunking the whole expert is one copy task: emulate with a single 3-unit sub-copy stream
+    Rig r(1, 4, 8, chunking ? unit : 3 * unit, chunking ? unit : 3 * unit, 1);
+    r.eng.bw = chunking ? 100.0 : 100.0;
+    r.pf->assign(0, 0, 1);  // predicted expert 1 -> slot 0
+    r.pf->push_low(0, 0);
+    const double miss_at = variant == 2 ? 0.5 : 1.5;  // during chunk 0 (gate end) or chunk 1 (access)
+    r.worker_until(miss_at);
+    const size_t mark = r.eng.log.size();
+    r.pf->purge_low(0);
+    r.pf->assign(0, 1, 2);  // missing expert 2 -> slot 1, high priority
+    r.pf->issue_high(0, 1);
+    double start = r.first_start_into(0, 1, 4, mark);
+    if (variant == 0) *chunked = start;
+    if (variant == 1) *unchunked = start;
+    if (variant == 2) *early = start;
+  }
+}
+
+void test_example() {
+  double a, b, c;
+  example(&a, &b, &c);
+  CHECK(std::fabs(a - 2.0) < 1e-9);  // right after the second chunk
+  CHECK(std::fabs(b - 3.0) < 1e-9);  // after the whole expert without chunking
+  CHECK(std::fabs(c - 1.0) < 1e-9);  // early preemption: before the second chunk starts
+}
+
+// A high-priority copy waits for at most `window` already-issued low-priority
+// sub-copies (earlier high-priority copies are drained before each miss).
+void test_window_bound() {
+  for (int window = 1; window <= 3; ++window) {
+    Rig r(2, 8, 16, 1600, 100, window);  // 16 sub-copies per chunk of 1 time unit each
+    r.eng.bw = 100.0;
+    for (int s = 0; s < 8; ++s) {
+      r.pf->assign(1, s, 8 + s);
+      r.pf->push_low(1, s);
+    }
+    double t = 0.37;
+    double max_delay = 0.0;
+    for (int trial = 0; trial < 4; ++trial) {
+      r.worker_until(t);
+      const size_t mark = r.eng.log.size();
+      const int slot = trial;
+      r.pf->assign(0, slot, slot);
+      r.pf->issue_high(0, slot);
+      const double start = r.first_start_into(0, slot, 8, mark);
+      max_delay = std::max(max_delay, start - r.eng.now);
+      CHECK(start - r.eng.now <= window * 1.0 + 1e-9);
+      t = r.eng.log.back().end + 0.61;  // next miss after this one's copies are done
+    }
+    CHECK(max_delay > 0.0);  // low-priority work really was in flight
+  }
+}
+
+void test_purge_dedupe_and_priority() {
+  Rig r(3, 4, 8, 100, 100, 1);
+  r.eng.bw = 100.0;
+  r.pf->assign(1, 0, 5);
+  r.pf->push_low(1, 0);
+  r.pf->push_low(1, 0);  // dedupe: chunks already queued
+  r.pf->assign(2, 0, 6);
+  r.pf->push_low(2, 0);
+  r.pf->pump();  // window 1: only the first LOW sub-copy issues
+  CHECK(r.eng.log.size() == 1);
+  r.pf->purge_low(1);  // drops layer 1's remaining two chunks only
+  CHECK(r.pf->stats().low_purged == 2);
+  CHECK(r.pf->has_low());
+  // high priority goes next, in issue order, regardless of queued low work
+  r.pf->assign(0, 1, 3);
+  r.pf->issue_high(0, 1);
+  CHECK(r.eng.log.size() == 4);
+  r.worker_until(100.0);
+  CHECK(r.eng.log.size() == 7);  // layer 2's three chunks follow
+  CHECK(r.pf->stats().copies[LOW] == 4 && r.pf->stats().copies[HIGH] == 3);
+  // re-push after a purge continues from what was issued (no duplicate bytes)
+  r.pf->issue_high(1, 0);
+  CHECK(r.eng.log.size() == 9);
+}
+
+void test_ready_and_war() {
+  Rig r(1, 2, 4, 100, 50, 2);  // 2 sub-copies per chunk
+  r.eng.bw = 100.0;
+  r.pf->mark_resident(0, 0, 0);
+  CHECK(r.pf->ready_seq(0, 0, 2) == -1);  // warm slot: nothing to wait for
+  // a reader of slot 0 (compute token 7, completes at t = 5)
+  r.pf->set_last_read(0, 0, 7);
+  r.eng.compute_done[7] = 5.0;
+  r.pf->assign(0, 0, 3);
+  CHECK(r.pf->ready_seq(0, 0, 0) == -2);  // not issued yet
+  r.pf->issue_high(0, 0);
+  CHECK(r.eng.log[0].after == 7 && r.eng.log[0].start >= 5.0);  // write-after-read
+  const int64_t need01 = r.pf->ready_seq(0, 0, 1), need2 = r.pf->ready_seq(0, 0, 2);
+  CHECK(need01 == 3 && need2 == 5);  // last sub-copy of chunk 1 / chunk 2
+  r.worker_until(100.0);
+  CHECK(r.pf->ready_seq(0, 0, 2) == -1);
+}
+
+void test_deferred_fill() {
+  // streaming through a too-small cache: the fill into slot 0 waits for the
+  // compute that reads slot 0's previous expert (token 3 completes at t = 9)
+  Rig r(1, 1, 8, 100, 100, 2);
+  r.eng.bw = 100.0;
+  r.pf->mark_resident(0, 0, 0);
+  r.eng.compute_done[3] = 9.0;
+  r.pf->assign(0, 0, 4);
+  r.pf->issue_high_after(0, 0, 3);
+  CHECK(r.eng.log.size() == 3 && r.eng.log[0].start >= 9.0 && r.pf->stats().deferred == 1);
+}
+
+void test_assign_cancels_stale_low() {
+  Rig r(1, 2, 8, 100, 100, 1);
+  r.pf->assign(0, 0, 1);
+  r.pf->push_low(0, 0);
+  r.pf->assign(0, 0, 2);  // the slot changes hands before its low tasks ran
+  r.pf->pump();
+  CHECK(r.eng.log.empty());
+  CHECK(!r.pf->has_low());
+}
+
+void test_capacity_wrap() {
+  Rig r(1, 4, 8, 100, 10, 1);
+  r.eng.cap = 4;
+  for (int s = 0; s < 3; ++s) {
+    r.pf->assign(0, s, s);
+    r.pf->issue_high(0, s);  // 3 chunks x 10 sub-copies each, at most 4 outstanding
+  }
+  CHECK(r.pf->in_flight() <= 4);
+  CHECK(r.eng.log.size() == 90);
+}
+
+}  // namespace
+
+int main(int argc, char** argv) {
+  if (argc > 1 && std::strcmp(argv[1], "example") == 0) {
+    double a, b, c;
+    example(&a, &b, &c);
+    std::printf("%.6f %.6f %.6f\n", a, b, c);
+    return 0;
+  }
+  test_example();
+  test_window_bound();
+  test_purge_dedupe_and_priority();
+  test_ready_and_war();
+  test_deferred_fill();
+  test_assign_cancels_stale_low();
+  test_capacity_wrap();
+  std::printf(failures ? "FAILED %d\n" : "ALL OK\n", failures);
+  return failures ? 1 : 0;
+}

@@ -212,3 +212,28 @@ def check_harness(cfg, model, l, rec):
         check_bf16_output(xg, ostack.rms(h1), ("harness", l))
     else:
         assert err.max() <= TOL_F32, (l, err.max())
+
+
+def moe_layer_check(cfg, m, st, l, lcs, x_np, sample=None, predict=True):
+    """Run predict (optional) -> route -> ffn of layer l on x through the C ABI and check
+    every output against the oracle, replaying the cache plans on lcs."""
+    import torch
+    from synth import model as sm
+    st.x.copy_(torch.from_numpy(x_np.view(np.int16) if x_np.dtype == np.uint16 else x_np).cuda())
+    order, q = st.moe_layer(l, predict=predict, want_q=predict)
+    rec = LayerRecord()
+    rec.x = x_np
+    rec.ids, rec.w, rec.s, rec.y = (to_np(t).copy() for t in (st.ids, st.w, st.s, st.y))
+    rec.pred_ids = to_np(st.pred_ids).copy()
+    rec.order, rec.q = order, q
+    x64 = f64(x_np, cfg.dtype)
+    tgt = sm.predictor_target(cfg, l)
+    if predict and tgt is not None and m.np_pred[l] is not None and lcs is not None:
+        Q = check_predictor(cfg, m, l, x64, rec)
+        check_plan_spec(lcs[tgt], Q, m.ctx.last_plan(tgt, 0))
+    g_ids, w_ref, s_ref, clear = check_route(cfg, m, l, x64, rec)
+    if lcs is not None:
+        check_plan_precise(lcs[l], g_ids, m.ctx.last_plan(l, 1))
+        assert rec.order == m.ctx.last_plan(l, 1)["expert"]
+    err = check_ffn(cfg, m, l, x64, g_ids, w_ref, s_ref, rec.y, tokens=sample)
+    return rec, err
