@@ -40,6 +40,7 @@ thread_local std::string g_last_error;
 
 constexpr int kRecRing = 64;
 constexpr int kStallClass = 99;
+constexpr size_t kHighMergeBytes = (size_t)64 << 20;  // high-priority copies coalesce up to this size
 constexpr int kMaxSplit = 8;  // split-K slices of the shared expert's down GEMM
 constexpr int kCopyRing = 4096;
 constexpr int kComputeRing = 4096;
@@ -574,7 +575,7 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   c->eng.compute_ev = &c->cev;
   const size_t sub = g.copy_subchunk_bytes > 0 ? (size_t)g.copy_subchunk_bytes : ((size_t)16 << 20);
   const int window = g.copy_window > 0 ? g.copy_window : 2;
-  c->pf = new Prefetcher(L, C, E, c->chunk_bytes, sub, window, c->cache, &c->eng);
+  c->pf = new Prefetcher(L, C, E, c->chunk_bytes, sub, window, c->cache, &c->eng, std::max(sub, kHighMergeBytes));
   if (c->profile) {
     int khz = 0;
     if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, c->dev) == hipSuccess && khz > 0)

@@ -5,10 +5,11 @@
 namespace promoe {
 
 Prefetcher::Prefetcher(int n_layers, int slots, int n_experts, size_t chunk_bytes, size_t sub_bytes,
-                       int window, uint8_t* cache_base, CopyEngine* engine)
+                       int window, uint8_t* cache_base, CopyEngine* engine, size_t high_merge_bytes)
     : L_(n_layers), C_(slots), E_(n_experts), chunk_bytes_(chunk_bytes),
-      sub_bytes_(std::min(sub_bytes, chunk_bytes)), window_(window < 1 ? 1 : window), cache_(cache_base),
-      eng_(engine), host_((size_t)n_layers * n_experts, nullptr), slots_((size_t)n_layers * slots) {
+      sub_bytes_(std::min(sub_bytes, chunk_bytes)), window_(window < 1 ? 1 : window), merge_(high_merge_bytes),
+      cache_(cache_base), eng_(engine), host_((size_t)n_layers * n_experts, nullptr),
+      slots_((size_t)n_layers * slots) {
   n_sub_ = (int)((chunk_bytes_ + sub_bytes_ - 1) / sub_bytes_);
 }
 
@@ -78,34 +79,88 @@ void Prefetcher::issue_sub(int layer, int slot, int chunk, Prio prio, int64_t af
   st_.bytes[prio] += (int64_t)bytes;
 }
 
-void Prefetcher::issue_high(int layer, int slot) {
+void Prefetcher::issue_pending_high(int layer, int slot, int64_t after_compute) {
   Slot& s = slot_(layer, slot);
-  if (s.expert < 0) return;
-  for (int c = 0; c < kChunks; ++c) {
+  const size_t expert_bytes = kChunks * chunk_bytes_;
+  bool first = true;
+  for (int c = 0; c < kChunks;) {
     Chunk& ch = s.ch[c];
-    if (ch.queued) {
-      // promote: drop the queued low-priority task for this chunk
+    if (ch.queued) {  // promote: drop the queued low-priority task for this chunk
       for (auto it = low_.begin(); it != low_.end(); ++it)
         if (it->layer == layer && it->slot == slot && it->chunk == c) { low_.erase(it); break; }
       ch.queued = false;
     }
-    while (ch.n_issued < n_sub_) issue_sub(layer, slot, c, HIGH, -1);
+    if (ch.n_issued == n_sub_) { ++c; continue; }
+    if (merge_ == 0) {
+      issue_sub(layer, slot, c, HIGH, first ? after_compute : -1);
+      first = false;
+      continue;
+    }
+    // one copy from the first pending byte of chunk c over every following pending
+    // sub-copy that is contiguous with it (a later chunk joins only if none of it
+    // was issued yet), in whole sub-copies, up to merge_ bytes
+    const size_t start = (size_t)c * chunk_bytes_ + (size_t)ch.n_issued * sub_bytes_;
+    size_t end = start;
+    for (int cc = c; cc < kChunks; ++cc) {
+      Chunk& k = s.ch[cc];
+      if (k.n_issued == n_sub_) break;
+      if (k.queued) {
+        for (auto it = low_.begin(); it != low_.end(); ++it)
+          if (it->layer == layer && it->slot == slot && it->chunk == cc) { low_.erase(it); break; }
+        k.queued = false;
+      }
+      const size_t cend = (size_t)(cc + 1) * chunk_bytes_;
+      const size_t cstart = (size_t)cc * chunk_bytes_ + (size_t)k.n_issued * sub_bytes_;
+      if (cstart != end) break;  // not contiguous with the run
+      const size_t budget = start + merge_ - end;
+      size_t take = cend - cstart;
+      if (take > budget) {
+        take = budget / sub_bytes_ * sub_bytes_;
+        if (take == 0) {
+          if (end != start) break;
+          take = std::min(sub_bytes_, cend - cstart);
+        }
+        end = cstart + take;
+        break;
+      }
+      end = cend;
+    }
+    const int64_t after = std::max(first ? after_compute : -1, s.last_read);
+    while (next_seq_ - retired_ >= eng_->capacity()) {
+      eng_->wait(retired_);
+      retire();
+    }
+    const int64_t seq = next_seq_++;
+    const size_t slot_off = ((size_t)layer * C_ + slot) * expert_bytes;
+    eng_->issue(seq, cache_ + slot_off + start, host_[layer * E_ + s.expert] + start, end - start, after);
+    st_.copies[HIGH]++;
+    st_.bytes[HIGH] += (int64_t)(end - start);
+    first = false;
+    // mark the covered sub-copies of every chunk in [start, end)
+    for (int k = 0; k < kChunks; ++k) {
+      const size_t c0 = (size_t)k * chunk_bytes_;
+      if (end <= c0 || start >= c0 + chunk_bytes_) continue;
+      Chunk& kk = s.ch[k];
+      const size_t upto = std::min(end, c0 + chunk_bytes_) - c0;
+      const int n_done = upto >= chunk_bytes_ ? n_sub_ : (int)(upto / sub_bytes_);
+      if (n_done > kk.n_issued) {
+        kk.n_issued = n_done;
+        kk.last = seq;
+      }
+    }
   }
+}
+
+void Prefetcher::issue_high(int layer, int slot) {
+  if (slot_(layer, slot).expert < 0) return;
+  issue_pending_high(layer, slot, -1);
 }
 
 void Prefetcher::issue_high_after(int layer, int slot, int64_t after_compute) {
   Slot& s = slot_(layer, slot);
   if (s.expert < 0) return;
   st_.deferred++;
-  bool first = true;
-  for (int c = 0; c < kChunks; ++c) {
-    Chunk& ch = s.ch[c];
-    ch.queued = false;
-    while (ch.n_issued < n_sub_) {
-      issue_sub(layer, slot, c, HIGH, first ? after_compute : -1);
-      first = false;
-    }
-  }
+  issue_pending_high(layer, slot, after_compute);
 }
 
 int Prefetcher::pump() {

@@ -53,8 +53,11 @@ class Prefetcher {
  public:
   static constexpr int kChunks = 3;
 
+  // high_merge_bytes > 0: high-priority copies of a slot coalesce contiguous
+  // pending sub-copies into copies of up to that many bytes (nothing preempts
+  // them, and larger DMA transfers run closer to the link rate).
   Prefetcher(int n_layers, int slots, int n_experts, size_t chunk_bytes, size_t sub_bytes, int window,
-             uint8_t* cache_base, CopyEngine* engine);
+             uint8_t* cache_base, CopyEngine* engine, size_t high_merge_bytes = 0);
 
   void set_host(int layer, int expert, const uint8_t* p);
   const uint8_t* host(int layer, int expert) const { return host_[layer * E_ + expert]; }
@@ -117,10 +120,13 @@ class Prefetcher {
   Slot& slot_(int l, int s) { return slots_[l * C_ + s]; }
   const Slot& slot_(int l, int s) const { return slots_[l * C_ + s]; }
   void issue_sub(int layer, int slot, int chunk, Prio prio, int64_t after_compute);
+  // Issue every pending sub-copy of the slot at high priority, coalesced.
+  void issue_pending_high(int layer, int slot, int64_t after_compute);
 
   int L_, C_, E_;
   size_t chunk_bytes_, sub_bytes_;
   int n_sub_, window_;
+  size_t merge_;
   uint8_t* cache_;
   CopyEngine* eng_;
   std::vector<const uint8_t*> host_;

@@ -225,6 +225,94 @@ void test_capacity_wrap() {
   CHECK(r.eng.log.size() == 90);
 }
 
+void test_high_merge() {
+  // chunk 100 B, sub 25 B: a fresh slot at high priority is one 300 B copy (merge 1000)
+  {
+    FakeEngine eng;
+    std::vector<uint8_t> host(8 * 300), cache(2 * 300);
+    Prefetcher pf(1, 2, 8, 100, 25, 2, cache.data(), &eng, 1000);
+    for (int e = 0; e < 8; ++e) pf.set_host(0, e, host.data() + e * 300);
+    pf.assign(0, 1, 3);
+    pf.issue_high(0, 1);
+    CHECK(eng.log.size() == 1 && eng.log[0].bytes == 300 && eng.log[0].dst == cache.data() + 300);
+    CHECK(pf.ready_seq(0, 1, 0) == 0 && pf.ready_seq(0, 1, 2) == 0);
+  }
+  // partial low progress: chunk 0 half issued at low priority, the rest merges
+  // into one run from the first pending byte; merge cap splits at sub boundaries
+  {
+    FakeEngine eng;
+    eng.bw = 1.0;
+    std::vector<uint8_t> host(8 * 300), cache(2 * 300);
+    Prefetcher pf(1, 2, 8, 100, 25, 2, cache.data(), &eng, 120);
+    for (int e = 0; e < 8; ++e) pf.set_host(0, e, host.data() + e * 300);
+    pf.assign(0, 0, 5);
+    pf.push_low(0, 0);
+    pf.pump();  // window 2: two 25 B low sub-copies of chunk 0
+    CHECK(eng.log.size() == 2);
+    pf.purge_low(0);
+    pf.issue_high(0, 0);
+    // pending bytes [50, 300) in runs of <= 120 B cut at 25 B boundaries
+    size_t covered = 0;
+    for (size_t i = 2; i < eng.log.size(); ++i) {
+      CHECK(eng.log[i].bytes <= 120 && eng.log[i].bytes % 25 == 0);
+      CHECK(eng.log[i].dst == cache.data() + 50 + covered);
+      covered += eng.log[i].bytes;
+    }
+    CHECK(covered == 250);
+    CHECK(pf.ready_seq(0, 0, 2) == (int64_t)eng.log.size() - 1);
+    CHECK(pf.stats().bytes[HIGH] == 250 && pf.stats().bytes[LOW] == 50);
+  }
+}
+
+// Every combination of chunk / sub-copy / merge size and low-priority progress:
+// the high-priority runs copy each remaining byte of the slot exactly once,
+// stay inside the slot, respect the merge cap, and leave every chunk ready.
+void test_high_merge_exhaustive() {
+  struct Rec : CopyEngine {
+    struct C { size_t off, bytes; };
+    std::vector<C> log;
+    uint8_t* base = nullptr;
+    void issue(int64_t, void* d, const void*, size_t b, int64_t) override {
+      log.push_back({(size_t)(static_cast<uint8_t*>(d) - base), b});
+    }
+    bool done(int64_t) override { return true; }
+    void wait(int64_t) override {}
+  };
+  for (size_t chunk : {7, 30, 100, 128})
+    for (size_t sub : {1, 3, 25, 30, 64, 200})
+      for (size_t merge : {0, 1, 29, 64, 120, 1000})
+        for (int pre0 = 0; pre0 < 5; ++pre0)
+          for (int pre1 = 0; pre1 < 3; ++pre1) {
+            const size_t sb = std::min(sub, chunk);
+            const int nsub = (int)((chunk + sb - 1) / sb);
+            if (merge && merge < sb) continue;
+            const int p0 = std::min(pre0, nsub), p1 = std::min(pre1, nsub);
+            const int low = p0 + (p0 == nsub ? p1 : 0);
+            Rec e;
+            std::vector<uint8_t> host(4 * 3 * chunk), cache(2 * 3 * chunk);
+            e.base = cache.data();
+            Prefetcher pf(1, 2, 4, chunk, sub, std::max(1, low), cache.data(), &e, merge);
+            for (int x = 0; x < 4; ++x) pf.set_host(0, x, host.data() + x * 3 * chunk);
+            pf.assign(0, 1, 2);
+            pf.push_low(0, 1);
+            if (low) pf.pump();
+            const size_t n_low = e.log.size();
+            pf.purge_low(0);
+            pf.issue_high(0, 1);
+            std::vector<int> cov(3 * chunk, 0);
+            bool ok = true;
+            for (size_t i = 0; i < e.log.size(); ++i) {
+              const auto& c = e.log[i];
+              if (c.off < 3 * chunk || c.off + c.bytes > 6 * chunk) { ok = false; break; }
+              for (size_t b = 0; b < c.bytes; ++b) cov[c.off - 3 * chunk + b]++;
+              if (i >= n_low && merge && c.bytes > std::max(merge, sb)) ok = false;
+            }
+            for (int v : cov) ok = ok && v == 1;
+            ok = ok && pf.ready_seq(0, 1, 2) != -2;
+            CHECK(ok);
+          }
+}
+
 }  // namespace
 
 int main(int argc, char** argv) {
@@ -241,6 +329,8 @@ int main(int argc, char** argv) {
   test_deferred_fill();
   test_assign_cancels_stale_low();
   test_capacity_wrap();
+  test_high_merge();
+  test_high_merge_exhaustive();
   std::printf(failures ? "FAILED %d\n" : "ALL OK\n", failures);
   return failures ? 1 : 0;
 }
