@@ -40,6 +40,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="bound on the oracle sample")
     p.add_argument("--no-prefetch", action="store_true", help="reactive LRU (predictions ignored)")
+    p.add_argument("--spec-fill-limit", type=int, default=0,
+                   help="slots a predicted plan may fill: 0 no limit, n>0 the first n, -1 none")
     p.add_argument("--copy-calib-mib", type=int, default=1024,
                    help="size of the plain device copy run after the timed region (counter calibration)")
     p.add_argument("--legs", default="decode,prefill,mfma",
@@ -161,7 +163,7 @@ def run_steps(torch, model, st, inputs, warmup, steps):
     return time.perf_counter() - t0, model.ctx.stats()
 
 
-def leg_prefill(torch, args, flags):
+def leg_prefill(torch, args, flags, limit):
     """Qwen1.5-MoE-A2.7B shape, 24 layers, 512-token prompt, 30 of 60 experts cached."""
     import numpy as np
     from synth import configs, model as sm
@@ -169,7 +171,7 @@ def leg_prefill(torch, args, flags):
     from paper_2410_22134_amd.stack import Stack
     cfg = configs.C3
     T = 512
-    model = SyntheticModel(cfg, max_tokens=T, flags=flags, gen_threads=8)
+    model = SyntheticModel(cfg, max_tokens=T, flags=flags, gen_threads=8, spec_fill_limit=limit)
     try:
         st = Stack(model, T)
         n = args.prefill_warmup + args.prefill_steps
@@ -234,7 +236,7 @@ def main():
     cfg = configs.C2
     flags = FLAG_PROFILE | (FLAG_NO_PREFETCH if args.no_prefetch else 0)
     t_setup = time.perf_counter()
-    model = SyntheticModel(cfg, max_tokens=1, flags=flags, gen_threads=8)
+    model = SyntheticModel(cfg, max_tokens=1, flags=flags, gen_threads=8, spec_fill_limit=args.spec_fill_limit)
     st = Stack(model, 1)
     n_in = args.warmup + args.steps
     h_in = torch.from_numpy(np.stack([sm.stack_input(cfg, i, 1) for i in range(n_in)])).cuda()
@@ -269,7 +271,7 @@ def main():
                                "experts (I=1408) top-6 + 2 shared, 32 of 64 experts per layer cached in HBM, "
                                "the rest in pinned host memory, look-ahead 1, 2-layer MLP predictor",
                    "global_batch": 1, "seq_len": 1, "parallelism": "none (1 GPU)",
-                   "prefetch": not args.no_prefetch},
+                   "prefetch": not args.no_prefetch, "spec_fill_limit": args.spec_fill_limit},
         "roofline": {"bound": "hbm", "kernel": "k_ffn_gateup<bf16,1>", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic, "avg_launch_us": round(avg_us, 3),
@@ -300,7 +302,7 @@ def main():
     del a, b
     if "prefill" in args.legs:
         print("[bench] prefill leg", file=sys.stderr, flush=True)
-        out["detail"]["prefill"] = leg_prefill(torch, args, flags)
+        out["detail"]["prefill"] = leg_prefill(torch, args, flags, args.spec_fill_limit)
     if "mfma" in args.legs:
         print("[bench] shared-expert MFMA leg", file=sys.stderr, flush=True)
         out["roofline_prefill_gemm"] = leg_mfma(torch, args)

@@ -82,6 +82,17 @@ typedef struct promoe_config {
   int64_t copy_subchunk_bytes; /* copy issue unit; 0 = 16 MiB */
   int32_t copy_window;       /* low-priority sub-copies kept in flight; 0 = 2 */
   int32_t flags;             /* PROMOE_FLAG_* */
+  int32_t spec_fill_limit;   /* Slots a predictor-driven plan (promoe_predict) may fill
+                                (Alg. 2 PushPredictedExperts).  0: no limit, every
+                                predicted expert that is not resident takes a slot;
+                                n > 0: only the first n non-resident experts of the
+                                vote order take one, the rest are skipped; -1: none,
+                                the plan only refreshes the LRU stamps of resident
+                                predicted experts.  The paper's worker replaces a slot
+                                only when a copy starts; a limit models how few
+                                low-priority copies start before the layer's route
+                                when the host link is the bottleneck.  Lists passed to
+                                promoe_prefetch are never limited.  -1..64. */
 } promoe_config;
 
 typedef struct promoe_stats {

@@ -83,14 +83,18 @@ class NaiveLRU:
             self.spec_pending.discard(e)
         return s, v
 
-    def spec(self, Q):
+    def spec(self, Q, budget=-1):
         out = []
+        brought = 0
         for e in Q:
             if e in self.where:
                 self.log.append(("touch", e))
                 self.c["spec_resident"] += 1
                 out.append((e, self.where[e], False))
+            elif budget >= 0 and brought >= budget:
+                out.append((e, -1, False))
             else:
+                brought += 1
                 s, _ = self._bring(e, True)
                 self.c["spec_issued"] += 1
                 out.append((e, s, True))

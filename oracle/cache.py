@@ -18,7 +18,12 @@ Warm start: experts 0..C-1 in slots 0..C-1, stamp = slot index, fetch_seq 0.
 spec_plan(Q)      -- PushPredictedExperts: for e in Q order, touch it if
                      resident; else take the lowest free slot or the least
                      recently stamped one, evict, assign, mark speculative and
-                     queue its three chunks at low priority.
+                     queue its three chunks at low priority.  With a budget
+                     b >= 0 at most b experts per plan are filled (later
+                     non-resident members are skipped): the paper's worker
+                     replaces a slot only when a copy starts, and when copies
+                     are the bottleneck only the first few predicted experts of
+                     a layer start before the layer's route drops the rest.
 precise_plan(P)   -- PushPreciseExperts: P = the distinct experts the layer's
                      tokens chose, ascending.  Low-priority work of the layer is
                      dropped (physical only).  Order = resident experts by
@@ -40,9 +45,10 @@ COUNTERS = ("prec_access", "hit", "miss", "spec_issued", "spec_resident", "spec_
 @dataclass
 class SpecEntry:
     expert: int
-    slot: int
+    slot: int            # -1 when skipped
     new: bool
     victim: int          # expert evicted (-1 none)
+    skipped: bool = False  # non-resident, over the fill budget
 
 
 @dataclass
@@ -101,8 +107,9 @@ class LayerCache:
         self._touch(s)
 
     # -- plans
-    def spec_plan(self, Q):
+    def spec_plan(self, Q, budget: int = -1):
         out = []
+        fills = 0
         for e in Q:
             e = int(e)
             s = self.slot_of[e]
@@ -110,7 +117,10 @@ class LayerCache:
                 self._touch(s)
                 self.count["spec_resident"] += 1
                 out.append(SpecEntry(e, s, False, -1))
+            elif 0 <= budget <= fills:
+                out.append(SpecEntry(e, -1, False, -1, True))
             else:
+                fills += 1
                 s = self._victim()
                 v = self._evict(s)
                 self._fill(e, s, True)

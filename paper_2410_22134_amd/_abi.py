@@ -20,7 +20,8 @@ class Config(ctypes.Structure):
     _fields_ = [("n_layers", _i32), ("hidden", _i32), ("n_experts", _i32), ("top_k", _i32), ("inter", _i32),
                 ("shared_inter", _i32), ("shared_gate", _i32), ("renorm", _i32), ("router_bias", _i32),
                 ("slots_per_layer", _i32), ("lookahead", _i32), ("pred_hidden", _i32), ("max_tokens", _i32),
-                ("dtype", _i32), ("copy_subchunk_bytes", _i64), ("copy_window", _i32), ("flags", _i32)]
+                ("dtype", _i32), ("copy_subchunk_bytes", _i64), ("copy_window", _i32), ("flags", _i32),
+                ("spec_fill_limit", _i32)]
 
 
 STAT_COUNTERS = ("prec_access", "hit", "miss", "spec_issued", "spec_resident", "spec_used", "spec_wasted", "evict")

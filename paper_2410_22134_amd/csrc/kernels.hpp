@@ -111,6 +111,7 @@ struct PlanArgs {
   int layer, C, E;
   const int32_t* ids;   // [T x k] (precise) or per-token predicted ids (spec); null = use rec->q_in
   int T, k;
+  int fill_budget;      // spec plan from ids: most slots filled, -1 = no limit
   PlanRecord* rec;      // host-mapped
   int32_t* d_order_slot; // [64]
   int32_t* d_offsets;    // [65]

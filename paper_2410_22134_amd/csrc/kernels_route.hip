@@ -8,7 +8,8 @@
 //                       only, by the predictor.
 //  * k_plan_spec     -- speculative plan of a target layer (Alg. 2
 //                       PushPredictedExperts): integer vote over the tokens'
-//                       predicted ids, then the LRU plan.
+//                       predicted ids, then the LRU plan (optionally filling
+//                       only the first few non-resident experts).
 //  * k_plan_precise  -- precise plan of the routed layer (Alg. 2
 //                       PushPreciseExperts, Sec. "Reordered Inference"):
 //                       hit/miss, order, victim slots, counters, followed by the
@@ -167,6 +168,9 @@ __global__ __launch_bounds__(256) void k_plan_spec(PlanArgs a) {
   int64_t cnt[8];
   load_state(a, lane, w, clock, fseq, cnt);
   PlanRecord* rec = a.rec;
+  // Host-given lists are never limited; a predicted plan fills at most fill_budget slots.
+  const int budget = a.ids ? a.fill_budget : -1;
+  int fills = 0;
   for (int i = 0; i < nq; ++i) {
     const int e = Q[i];
     const int s_res = __shfl(w.slot_of, e, kWave);
@@ -175,7 +179,10 @@ __global__ __launch_bounds__(256) void k_plan_spec(PlanArgs a) {
       if (lane == s_res) w.stamp = clock;
       cnt[CNT_SPEC_RESIDENT]++;
       if (lane == 0) { rec->expert[i] = e; rec->slot[i] = s_res; rec->flag[i] = 0; rec->victim[i] = -1; rec->after[i] = -1; }
+    } else if (budget >= 0 && fills >= budget) {
+      if (lane == 0) { rec->expert[i] = e; rec->slot[i] = -1; rec->flag[i] = 0; rec->victim[i] = -1; rec->after[i] = -1; }
     } else {
+      ++fills;
       const int v = victim_slot(a, lane, w);
       const int old = fill_slot(a, lane, w, e, v, true, clock, fseq, cnt);
       cnt[CNT_SPEC_ISSUED]++;

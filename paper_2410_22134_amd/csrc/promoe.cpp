@@ -260,6 +260,7 @@ void ingest_spec(promoe_ctx* c, int64_t r) {
   if (!(c->cfg.flags & PROMOE_FLAG_NO_PREFETCH)) {
     const bool high = c->rec_prio[r % kRecRing] == PROMOE_PRIO_HIGH;
     for (int i = 0; i < rec.n; ++i) {
+      if (rec.slot[i] < 0) continue;  // skipped: over the fill limit
       if (rec.flag[i]) c->pf->assign(layer, rec.slot[i], rec.expert[i]);
       if (high) c->pf->issue_high(layer, rec.slot[i]);
       else c->pf->push_low(layer, rec.slot[i]);
@@ -348,6 +349,9 @@ PlanArgs plan_args(promoe_ctx* c, int layer, const int32_t* ids, int T, int64_t 
   a.ids = ids;
   a.T = T;
   a.k = c->K;
+  // fills allowed in a predictor-driven speculative plan (-1: no limit)
+  const int lim = c->cfg.spec_fill_limit;
+  a.fill_budget = lim == 0 ? -1 : (lim < 0 ? 0 : lim);
   a.rec = c->rec_d + (r % kRecRing);
   a.d_order_slot = c->d_order_slot;
   a.d_offsets = c->d_offsets;
@@ -461,7 +465,8 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   const promoe_config& g = *cfg;
   if (g.n_layers < 1 || g.hidden < 8 || g.inter < 8 || g.n_experts < 1 || g.top_k < 1 ||
       g.slots_per_layer < 1 || g.max_tokens < 1 || g.lookahead < 0 || g.pred_hidden < 0 || g.shared_inter < 0 ||
-      (g.dtype != PROMOE_F32 && g.dtype != PROMOE_BF16) || g.top_k > g.n_experts) {
+      (g.dtype != PROMOE_F32 && g.dtype != PROMOE_BF16) || g.top_k > g.n_experts || g.spec_fill_limit < -1 ||
+      g.spec_fill_limit > 64) {
     g_last_error = "invalid config";
     return PROMOE_EINVAL;
   }

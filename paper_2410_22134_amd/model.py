@@ -14,7 +14,8 @@ from synth.configs import MoEConfig
 from ._abi import PROMOE_BF16, PROMOE_F32, Config, Context, HostBuffer
 
 
-def lib_config(cfg: MoEConfig, max_tokens: int, flags: int = 0, window: int = 0, subchunk: int = 0) -> Config:
+def lib_config(cfg: MoEConfig, max_tokens: int, flags: int = 0, window: int = 0, subchunk: int = 0,
+               spec_fill_limit: int = 0) -> Config:
     c = Config()
     c.n_layers, c.hidden, c.n_experts, c.top_k, c.inter = cfg.n_layers, cfg.hidden, cfg.n_experts, cfg.top_k, cfg.inter
     c.shared_inter, c.shared_gate = cfg.shared_total, cfg.shared_gate if cfg.n_shared else 0
@@ -23,6 +24,7 @@ def lib_config(cfg: MoEConfig, max_tokens: int, flags: int = 0, window: int = 0,
     c.max_tokens = max_tokens
     c.dtype = PROMOE_BF16 if cfg.dtype == "bf16" else PROMOE_F32
     c.copy_subchunk_bytes, c.copy_window, c.flags = subchunk, window, flags
+    c.spec_fill_limit = spec_fill_limit
     return c
 
 
@@ -35,7 +37,7 @@ def _dev(arr: np.ndarray, device):
 
 
 class SyntheticModel:
-    def __init__(self, cfg: MoEConfig, device="cuda", max_tokens=None, flags=0, window=0, subchunk=0,
+    def __init__(self, cfg: MoEConfig, device="cuda", max_tokens=None, flags=0, window=0, subchunk=0, spec_fill_limit=0,
                  warm=True, gen_threads=4):
         import torch
         self.cfg = cfg
@@ -64,7 +66,7 @@ class SyntheticModel:
         self.d_sgate = [None if v is None else _dev(v, device) for v in self.np_sgate]
         self.d_attn = [None if not cfg.attn_surrogate else _dev(sm.attn(cfg, l), device) for l in range(L)]
         self.cache = torch.empty(L * cfg.slots * eb, dtype=torch.uint8, device=device)
-        self.ctx = Context(lib_config(cfg, self.max_tokens, flags, window, subchunk), self.cache.data_ptr(),
+        self.ctx = Context(lib_config(cfg, self.max_tokens, flags, window, subchunk, spec_fill_limit), self.cache.data_ptr(),
                            self.cache.numel())
         for l in range(L):
             p1, p2 = self.d_pred[l]

@@ -177,8 +177,13 @@ def check_plan_precise(lc: ocache.LayerCache, g_ids, gpu_plan):
     return order
 
 
-def check_plan_spec(lc: ocache.LayerCache, Q, gpu_plan):
-    entries = lc.spec_plan(Q)
+def fill_budget(spec_fill_limit: int) -> int:
+    """The oracle's spec-plan budget for a library spec_fill_limit (0 = no limit)."""
+    return -1 if spec_fill_limit == 0 else (0 if spec_fill_limit < 0 else spec_fill_limit)
+
+
+def check_plan_spec(lc: ocache.LayerCache, Q, gpu_plan, budget: int = -1):
+    entries = lc.spec_plan(Q, budget)
     assert gpu_plan["expert"] == [e.expert for e in entries]
     assert gpu_plan["slot"] == [e.slot for e in entries]
     assert gpu_plan["flag"] == [int(e.new) for e in entries]
@@ -214,7 +219,7 @@ def check_harness(cfg, model, l, rec):
         assert err.max() <= TOL_F32, (l, err.max())
 
 
-def moe_layer_check(cfg, m, st, l, lcs, x_np, sample=None, predict=True):
+def moe_layer_check(cfg, m, st, l, lcs, x_np, sample=None, predict=True, budget=-1):
     """Run predict (optional) -> route -> ffn of layer l on x through the C ABI and check
     every output against the oracle, replaying the cache plans on lcs."""
     import torch
@@ -230,7 +235,7 @@ def moe_layer_check(cfg, m, st, l, lcs, x_np, sample=None, predict=True):
     tgt = sm.predictor_target(cfg, l)
     if predict and tgt is not None and m.np_pred[l] is not None and lcs is not None:
         Q = check_predictor(cfg, m, l, x64, rec)
-        check_plan_spec(lcs[tgt], Q, m.ctx.last_plan(tgt, 0))
+        check_plan_spec(lcs[tgt], Q, m.ctx.last_plan(tgt, 0), budget)
     g_ids, w_ref, s_ref, clear = check_route(cfg, m, l, x64, rec)
     if lcs is not None:
         check_plan_precise(lcs[l], g_ids, m.ctx.last_plan(l, 1))

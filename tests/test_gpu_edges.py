@@ -84,6 +84,29 @@ def test_reactive_mode_matches_demand_only_lru():
         m.close()
 
 
+@pytest.mark.parametrize("limit,T", [(1, 1), (2, 6), (-1, 3)])
+def test_spec_fill_limit(limit, T):
+    # predicted plans fill at most `limit` slots (-1: none); host pushes are not limited
+    cfg = SMALL
+    _log("spec fill limit", limit, "T", T)
+    m = SyntheticModel(cfg, max_tokens=T, spec_fill_limit=limit)
+    try:
+        st = Stack(m, T)
+        lcs = {l: ocache.LayerCache(cfg.n_experts, cfg.slots) for l in range(cfg.n_layers)}
+        b = pu.fill_budget(limit)
+        for step in range(4):
+            for l in range(cfg.n_layers):
+                pu.moe_layer_check(cfg, m, st, l, lcs, sm.layer_input(cfg, l, T, tag=400 + step), budget=b)
+        m.ctx.prefetch(0, [0, 1, 2, 3], PRIO_LOW)
+        pu.check_plan_spec(lcs[0], [0, 1, 2, 3], m.ctx.last_plan(0, 0))
+        pu.moe_layer_check(cfg, m, st, 0, lcs, sm.layer_input(cfg, 0, T, tag=499), predict=False)
+        pu.check_counters(m, lcs)
+        if limit < 0:
+            assert m.ctx.stats(1)["spec_issued"] == 0
+    finally:
+        m.close()
+
+
 def test_external_pushes_low_and_high():
     cfg = SMALL.with_(n_layers=1, lookahead=0)
     m = SyntheticModel(cfg, max_tokens=2)
@@ -143,3 +166,5 @@ def test_error_returns():
     assert _abi.lib().promoe_create(ctypes.byref(c), buf.data_ptr(), buf.numel(), ctypes.byref(h)) == -5
     c.hidden = 256
     assert _abi.lib().promoe_create(ctypes.byref(c), buf.data_ptr(), 100, ctypes.byref(h)) == -1
+    c.spec_fill_limit = -2
+    assert _abi.lib().promoe_create(ctypes.byref(c), buf.data_ptr(), buf.numel(), ctypes.byref(h)) == -1

@@ -49,13 +49,13 @@ def _plans(E, C):
     return out
 
 
-def _replay(seq, E, C, warm=True):
+def _replay(seq, E, C, warm=True, budget=-1):
     a = cache.LayerCache(E, C, warm)
     b = brute.NaiveLRU(E, C, warm)
     for kind, lst in seq:
         if kind == "Q":
-            ea = a.spec_plan(lst)
-            eb = b.spec(lst)
+            ea = a.spec_plan(lst, budget)
+            eb = b.spec(lst, budget)
             assert [(x.expert, x.slot, x.new) for x in ea] == eb
         else:
             order, entries = a.precise_plan(lst)
@@ -80,6 +80,46 @@ def test_exhaustive_replay_up_to_three_plans(C):
     for n in (1, 2, 3):
         for seq in itertools.product(plans, repeat=n):
             _replay(seq, E, C)
+
+
+@pytest.mark.parametrize("budget", [0, 1, 2])
+def test_exhaustive_replay_with_fill_budget(budget):
+    E, C = 4, 2
+    plans = _plans(E, C)
+    for n in (1, 2, 3):
+        for seq in itertools.product(plans, repeat=n):
+            _replay(seq, E, C, budget=budget)
+
+
+def test_fill_budget_closed_forms():
+    rng = np.random.default_rng(9)
+    E, C = 16, 8
+    # budget 0: predictions only refresh residents, so fills happen only on misses
+    a = cache.LayerCache(E, C)
+    for _ in range(200):
+        Q = rng.choice(E, 4, replace=False).tolist()
+        P = rng.choice(E, 3, replace=False).tolist()
+        ea = a.spec_plan(Q, budget=0)
+        assert not any(x.new for x in ea) and a.count["spec_issued"] == 0
+        a.precise_plan(P)
+    # a budget of at least |Q| equals no budget
+    c1, c2 = cache.LayerCache(E, C), cache.LayerCache(E, C)
+    for _ in range(200):
+        Q = rng.choice(E, 4, replace=False).tolist()
+        P = rng.choice(E, 3, replace=False).tolist()
+        e1 = c1.spec_plan(Q, budget=4)
+        e2 = c2.spec_plan(Q)
+        assert [(x.expert, x.slot, x.new) for x in e1] == [(x.expert, x.slot, x.new) for x in e2]
+        assert c1.precise_plan(P)[0] == c2.precise_plan(P)[0]
+    assert c1.count == c2.count
+    # fills per plan never exceed the budget
+    d = cache.LayerCache(E, C)
+    for _ in range(200):
+        Q = rng.choice(E, 6, replace=False).tolist()
+        before = d.count["spec_issued"]
+        d.spec_plan(Q, budget=2)
+        assert d.count["spec_issued"] - before <= 2
+        d.precise_plan(rng.choice(E, 3, replace=False).tolist())
 
 
 def test_random_long_replays():
