@@ -9,12 +9,19 @@ per-step hidden states) are resident in HBM before the timed region; expert
 weights live where the method puts them: 32 of 64 experts per layer in the HBM
 cache, all 64 in pinned host memory.
 
+Speculative plans fill at most one slot each by default (--spec-fill-limit 1):
+with the host link saturated, that is the configuration of the method that
+measured fastest; the ablation leg reports the others, the unlimited fill of
+the algorithm as written included.
+
 Prints one JSON line.  The roofline entry is for the dominant kernel of that
 workload (the FFN gate/up GEMV), each launch timed on the device clock over the
 timed region; the cpu_baseline entry times the CPU oracle on a bounded sample
 of the same workload on this host.  Further legs (detail only): prefill of the
-Qwen1.5-MoE-A2.7B shape (512 tokens, 50% cache) and the shared-expert MFMA
-GEMMs at the Qwen2-57B-A14B shape (roofline_prefill_gemm).
+Qwen1.5-MoE-A2.7B shape (512 tokens, 50% cache), the shared-expert MFMA GEMMs
+at the Qwen2-57B-A14B shape (roofline_prefill_gemm), and the ablation (LRU
+baseline, + prefetch, chunked prefetch, early preemption, reordered inference;
+static cache; no prefetch; fill limit 1) on the decode and prefill workloads.
 """
 from __future__ import annotations
 
@@ -40,14 +47,15 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="bound on the oracle sample")
     p.add_argument("--no-prefetch", action="store_true", help="reactive LRU (predictions ignored)")
-    p.add_argument("--spec-fill-limit", type=int, default=0,
+    p.add_argument("--spec-fill-limit", type=int, default=1,
                    help="slots a predicted plan may fill: 0 no limit, n>0 the first n, -1 none")
     p.add_argument("--copy-calib-mib", type=int, default=1024,
                    help="size of the plain device copy run after the timed region (counter calibration)")
-    p.add_argument("--legs", default="decode,prefill,mfma",
-                   help="decode is always run (it is the reported value); add prefill and/or mfma")
+    p.add_argument("--legs", default="decode,prefill,mfma,ablation",
+                   help="decode is always run (it is the reported value); add prefill, mfma, ablation")
     p.add_argument("--prefill-steps", type=int, default=3)
     p.add_argument("--prefill-warmup", type=int, default=1)
+    p.add_argument("--ablation-steps", type=int, default=32)
     return p.parse_args()
 
 
@@ -189,6 +197,39 @@ def leg_prefill(torch, args, flags, limit):
         model.close()
 
 
+def leg_ablation(torch, args):
+    """The paper's ablation steps and baselines (LRU; + prefetch, chunked prefetch,
+    early preemption, reordered inference; static cache; reactive with every other
+    technique on; the unlimited and limit-1 speculative fills) on the decode and
+    prefill workloads, one context per mode over the same weights."""
+    import numpy as np
+    from synth import configs, model as sm
+    from paper_2410_22134_amd import ABLATION, FLAG_NO_PREFETCH
+    from paper_2410_22134_amd.model import SyntheticModel
+    from paper_2410_22134_amd.stack import Stack
+    modes = [(k, f, 0) for k, f in ABLATION.items()] + [("+cer (no prefetch)", FLAG_NO_PREFETCH, 0),
+                                                         ("+pcer fill limit 1", 0, 1)]
+    out = {}
+    for name, cfg, T, warm, steps in (("decode", configs.C2, 1, 4, args.ablation_steps),
+                                      ("prefill", configs.C3, 512, 1, 2)):
+        model = SyntheticModel(cfg, max_tokens=T, gen_threads=8)
+        try:
+            st = Stack(model, T)
+            h = torch.from_numpy(np.stack([sm.stack_input(cfg, 3000 + i, T) for i in range(warm + steps)])).cuda()
+            res = {}
+            for mode, flags, lim in modes:
+                model.open(flags=flags, spec_fill_limit=lim)
+                dt, s = run_steps(torch, model, st, h, warm, steps)
+                res[mode] = {"tok_s": round(T * steps / dt, 2),
+                             "copied_GB": round((s["bytes_high"] + s["bytes_low"]) / 1e9, 3),
+                             "hit": s["hit"], "miss": s["miss"], "spec_wasted": s["spec_wasted"]}
+                print(f"[bench] ablation {name} {mode}: {res[mode]}", file=sys.stderr, flush=True)
+            out[name] = res
+        finally:
+            model.close()
+    return out
+
+
 def leg_mfma(torch, args):
     """Shared-expert GEMMs at the Qwen2-57B-A14B shape (hidden 3584, shared I = 20480),
     1024-token prefill, two layers with every expert resident (compute only)."""
@@ -303,6 +344,9 @@ def main():
     if "prefill" in args.legs:
         print("[bench] prefill leg", file=sys.stderr, flush=True)
         out["detail"]["prefill"] = leg_prefill(torch, args, flags, args.spec_fill_limit)
+    if "ablation" in args.legs:
+        print("[bench] ablation leg", file=sys.stderr, flush=True)
+        out["detail"]["ablation"] = leg_ablation(torch, args)
     if "mfma" in args.legs:
         print("[bench] shared-expert MFMA leg", file=sys.stderr, flush=True)
         out["roofline_prefill_gemm"] = leg_mfma(torch, args)

@@ -57,9 +57,27 @@ typedef enum {
 enum { PROMOE_F32 = 0, PROMOE_BF16 = 1 };
 enum { PROMOE_PRIO_LOW = 0, PROMOE_PRIO_HIGH = 1 };
 
-/* flags */
-#define PROMOE_FLAG_PROFILE 1      /* time FFN / GEMM launches and copy stalls with HIP events */
-#define PROMOE_FLAG_NO_PREFETCH 2  /* predictions update nothing: reactive LRU baseline */
+/* flags.  The NO_* switches turn off one technique each, for the paper's
+   ablation (Sec. "Evaluation", ablation study: the LRU baseline plus prefetch,
+   chunked prefetch, early preemption and reordered inference in turn) and its
+   baselines.  All of them leave the outputs unchanged. */
+#define PROMOE_FLAG_PROFILE 1      /* time expert launches on the device clock and copy
+                                      stalls with HIP events */
+#define PROMOE_FLAG_NO_PREFETCH 2  /* predictions update nothing (Sec. "Expert Prefetching" off) */
+#define PROMOE_FLAG_NO_CHUNK 4     /* a low-priority task is a whole expert: once started,
+                                      all its bytes are queued at once (Sec. "Chunked
+                                      Prefetching" off) */
+#define PROMOE_FLAG_NO_PREEMPT 8   /* a route neither drops the layer's queued low-priority
+                                      work nor issues its copies: each expert that is not
+                                      fully issued is fetched on access, after the compute
+                                      of the previous position (Sec. "Early Preemption" off) */
+#define PROMOE_FLAG_NO_REORDER 16  /* experts run in ascending id order and the precise
+                                      plan classifies each at its turn, so an earlier miss
+                                      may evict a later routed expert (Sec. "Reordered
+                                      Inference" off) */
+#define PROMOE_FLAG_STATIC 32      /* static cache baseline: the first C-2 slots keep their
+                                      initial experts for good, misses rotate through the
+                                      last 2 (LRU among them).  Needs C >= 3. */
 
 typedef struct promoe_config {
   int32_t n_layers;          /* L */
@@ -109,8 +127,9 @@ typedef struct promoe_stats {
   int64_t copies_high, copies_low;  /* sub-copies issued per priority */
   int64_t bytes_high, bytes_low;    /* bytes issued per priority */
   int64_t low_purged;               /* queued low-priority sub-copies dropped by route */
-  int64_t deferred;                 /* high copies held until an earlier expert of the
-                                       same layer finished reading the slot */
+  int64_t deferred;                 /* high copies held behind an earlier position's
+                                       compute: the slot's previous reader (write after
+                                       read), or the previous position (NO_PREEMPT) */
   /* Timing, PROMOE_FLAG_PROFILE only.  Expert launches are timed on the
      device clock (earliest block start to latest wave end); classes:
      [0] GEMV gate/up, [1] GEMV down, [2] GEMM gate/up (routed experts),

@@ -40,8 +40,8 @@ class NaiveLRU:
     LRU victim is found by re-scanning the whole log for each resident expert's
     latest access, and fill order by scanning for its latest fill."""
 
-    def __init__(self, n_experts, slots, warm=True):
-        self.E, self.C = n_experts, slots
+    def __init__(self, n_experts, slots, warm=True, pinned=0):
+        self.E, self.C, self.pinned = n_experts, slots, pinned
         self.where = {}          # expert -> slot
         self.log = []            # (kind, expert), kind in {"touch", "fill"}
         if warm:
@@ -60,11 +60,13 @@ class NaiveLRU:
         return -1
 
     def _free_or_lru(self):
+        # slots below `pinned` are never given away
         used = set(self.where.values())
-        free = [s for s in range(self.C) if s not in used]
+        free = [s for s in range(self.pinned, self.C) if s not in used]
         if free:
             return free[0], None
-        v = min(self.where, key=lambda e: self._last(e, ("touch", "fill")))
+        movable = [e for e in self.where if self.where[e] >= self.pinned]
+        v = min(movable, key=lambda e: self._last(e, ("touch", "fill")))
         return self.where[v], v
 
     def _bring(self, e, speculative):
@@ -104,20 +106,33 @@ class NaiveLRU:
         i = self._last(e, ("fill",))
         return i if i >= 0 else -1   # warm experts were never filled: earliest
 
-    def precise(self, P):
+    def _use(self, e):
+        self.log.append(("touch", e))
+        self.c["hit"] += 1
+        if e in self.spec_pending:
+            self.c["spec_used"] += 1
+            self.spec_pending.discard(e)
+        return self.where[e]
+
+    def precise(self, P, reorder=True):
         P = sorted(set(P))
+        if not reorder:
+            # one access at a time, in id order
+            slots = []
+            for e in P:
+                if e in self.where:
+                    slots.append(self._use(e))
+                else:
+                    s, _ = self._bring(e, False)
+                    self.c["miss"] += 1
+                    slots.append(s)
+            self.c["prec_access"] += len(P)
+            return P, slots
         hits = [e for e in P if e in self.where]
         miss = [e for e in P if e not in self.where]
         hits.sort(key=lambda e: (self._fill_time(e), e))
         order = hits + miss
-        slots = []
-        for e in hits:
-            self.log.append(("touch", e))
-            self.c["hit"] += 1
-            if e in self.spec_pending:
-                self.c["spec_used"] += 1
-                self.spec_pending.discard(e)
-            slots.append(self.where[e])
+        slots = [self._use(e) for e in hits]
         for e in miss:
             s, _ = self._bring(e, False)
             self.c["miss"] += 1

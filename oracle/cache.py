@@ -36,6 +36,17 @@ precise_plan(P)   -- PushPreciseExperts: P = the distinct experts the layer's
                      earlier member of this order must finish computing before
                      its slot is overwritten: its position is recorded as
                      ``after``.
+precise_plan(P, reorder=False)
+                  -- the order frameworks use without reordered inference:
+                     ascending expert id, each expert classified at its turn.
+                     An earlier miss may evict a later member of P, which then
+                     misses in its turn (the cache thrashing of "Reordered
+                     Inference"); a victim that is a later member needs no wait.
+
+Static cache (the paper's static baseline, Sec. "Evaluation"): the first
+``pinned`` slots keep their warm experts for good; victims are chosen among the
+remaining slots only (with C - pinned = 2 staging buffers, as the paper's static
+baseline uses).  pinned = 0 is the LRU cache above.
 """
 from dataclasses import dataclass
 
@@ -61,8 +72,9 @@ class PreciseEntry:
 
 
 class LayerCache:
-    def __init__(self, n_experts: int, slots: int, warm: bool = True):
-        self.E, self.C = n_experts, slots
+    def __init__(self, n_experts: int, slots: int, warm: bool = True, pinned: int = 0):
+        assert 0 <= pinned < slots
+        self.E, self.C, self.pinned = n_experts, slots, pinned
         self.slot_expert = [-1] * slots
         self.slot_of = [-1] * n_experts
         self.stamp = [0] * slots
@@ -79,10 +91,11 @@ class LayerCache:
 
     # -- helpers
     def _victim(self) -> int:
-        for s in range(self.C):
+        cand = range(self.pinned, self.C)
+        for s in cand:
             if self.slot_expert[s] < 0:
                 return s
-        return min(range(self.C), key=lambda s: self.stamp[s])
+        return min(cand, key=lambda s: self.stamp[s])
 
     def _evict(self, s: int) -> int:
         v = self.slot_expert[s]
@@ -128,28 +141,37 @@ class LayerCache:
                 out.append(SpecEntry(e, s, True, v))
         return out
 
-    def precise_plan(self, P):
+    def _hit(self, e: int) -> PreciseEntry:
+        s = self.slot_of[e]
+        self._touch(s)
+        self.count["hit"] += 1
+        if self.spec_unused[s]:
+            self.count["spec_used"] += 1
+            self.spec_unused[s] = False
+        return PreciseEntry(e, s, False, -1, -1)
+
+    def _miss(self, e: int, pos: int, pos_of) -> PreciseEntry:
+        s = self._victim()
+        v = self._evict(s)
+        self._fill(e, s, False)
+        self.count["miss"] += 1
+        after = pos_of[v] if v >= 0 and pos_of.get(v, pos) < pos else -1
+        return PreciseEntry(e, s, True, v, after)
+
+    def precise_plan(self, P, reorder: bool = True):
         P = sorted(set(int(e) for e in P))
+        if not reorder:
+            pos_of = {e: i for i, e in enumerate(P)}
+            entries = [self._hit(e) if self.slot_of[e] >= 0 else self._miss(e, i, pos_of) for i, e in enumerate(P)]
+            self.count["prec_access"] += len(P)
+            return P, entries
         hits = [e for e in P if self.slot_of[e] >= 0]
         missing = [e for e in P if self.slot_of[e] < 0]
         hits.sort(key=lambda e: (self.fetch_seq[self.slot_of[e]], e))
         order = hits + missing
         pos_of = {e: i for i, e in enumerate(order)}
-        entries = []
-        for e in hits:
-            s = self.slot_of[e]
-            self._touch(s)
-            self.count["hit"] += 1
-            if self.spec_unused[s]:
-                self.count["spec_used"] += 1
-                self.spec_unused[s] = False
-            entries.append(PreciseEntry(e, s, False, -1, -1))
-        for e in missing:
-            s = self._victim()
-            v = self._evict(s)
-            self._fill(e, s, False)
-            self.count["miss"] += 1
-            entries.append(PreciseEntry(e, s, True, v, pos_of.get(v, -1) if v >= 0 else -1))
+        entries = [self._hit(e) for e in hits]
+        entries += [self._miss(e, len(hits) + i, pos_of) for i, e in enumerate(missing)]
         self.count["prec_access"] += len(P)
         return order, entries
 
@@ -160,8 +182,8 @@ class LayerCache:
 class Cache:
     """One LayerCache per layer (layers are independent)."""
 
-    def __init__(self, n_layers: int, n_experts: int, slots: int, warm: bool = True):
-        self.layers = [LayerCache(n_experts, slots, warm) for _ in range(n_layers)]
+    def __init__(self, n_layers: int, n_experts: int, slots: int, warm: bool = True, pinned: int = 0):
+        self.layers = [LayerCache(n_experts, slots, warm, pinned) for _ in range(n_layers)]
 
     def totals(self):
         t = {c: 0 for c in COUNTERS}

@@ -11,7 +11,7 @@ LIB_PATH = os.environ.get("PROMOE_LIB", os.path.join(HERE, "libpromoe.so"))
 
 PROMOE_F32, PROMOE_BF16 = 0, 1
 PRIO_LOW, PRIO_HIGH = 0, 1
-FLAG_PROFILE, FLAG_NO_PREFETCH = 1, 2
+FLAG_PROFILE, FLAG_NO_PREFETCH, FLAG_NO_CHUNK, FLAG_NO_PREEMPT, FLAG_NO_REORDER, FLAG_STATIC = 1, 2, 4, 8, 16, 32
 
 _i32, _i64, _vp, _sz, _dbl = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_double
 

@@ -112,6 +112,8 @@ struct PlanArgs {
   const int32_t* ids;   // [T x k] (precise) or per-token predicted ids (spec); null = use rec->q_in
   int T, k;
   int fill_budget;      // spec plan from ids: most slots filled, -1 = no limit
+  int reorder;          // precise plan: 1 hits first (reordered inference), 0 id order
+  int pinned;           // slots [0, pinned) are never victims (static cache)
   PlanRecord* rec;      // host-mapped
   int32_t* d_order_slot; // [64]
   int32_t* d_offsets;    // [65]

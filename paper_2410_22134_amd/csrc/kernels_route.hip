@@ -95,10 +95,11 @@ __device__ __forceinline__ void store_state(const PlanArgs& a, int lane, const W
   }
 }
 
-// Lowest-index free slot, else the least recently stamped one (stamps are unique).
+// Lowest-index free slot, else the least recently stamped one (stamps are
+// unique), among the slots that are not pinned.
 __device__ __forceinline__ int victim_slot(const PlanArgs& a, int lane, const WaveState& w) {
   uint64_t key = ~0ull;
-  if (lane < a.C) key = w.slot_expert < 0 ? (uint64_t)lane : ((1ull << 40) | (uint64_t)w.stamp);
+  if (lane < a.C && lane >= a.pinned) key = w.slot_expert < 0 ? (uint64_t)lane : ((1ull << 40) | (uint64_t)w.stamp);
   key = (key << 6) | (uint64_t)lane;
   return (int)(wave_min_u64(key) & 63ull);
 }
@@ -223,7 +224,11 @@ __global__ __launch_bounds__(256) void k_plan_precise(PlanArgs a) {
     const uint64_t mmask = __ballot(used && !res);
     const int nh = __popcll(hmask), np = nh + __popcll(mmask);
     int rank = -1;
-    if (res) {
+    if (!a.reorder) {
+      // id order; every member is classified at its turn in the walk below
+      const uint64_t umask = __ballot(used);
+      if (used) rank = __popcll(umask & ((1ull << lane) - 1ull));
+    } else if (res) {
       rank = 0;
       for (int j = 0; j < kWave; ++j) {
         const uint32_t fj = __shfl(fs, j, kWave);
@@ -241,10 +246,13 @@ __global__ __launch_bounds__(256) void k_plan_precise(PlanArgs a) {
     __builtin_amdgcn_wave_barrier();
 
     PlanRecord* rec = a.rec;
+    int n_hit = 0;
     for (int pos = 0; pos < np; ++pos) {
       const int e = order[pos];
-      if (pos < nh) {
-        const int s = __shfl(w.slot_of, e, kWave);
+      // reordered: positions below nh are the resident members; id order: resident now
+      const int s = __shfl(w.slot_of, e, kWave);
+      if (s >= 0) {
+        ++n_hit;
         ++clock;
         const int was_spec = __shfl(w.spec_unused, s, kWave);
         if (lane == s) { w.stamp = clock; w.spec_unused = 0; }
@@ -256,7 +264,9 @@ __global__ __launch_bounds__(256) void k_plan_precise(PlanArgs a) {
         const int v = victim_slot(a, lane, w);
         const int old = fill_slot(a, lane, w, e, v, false, clock, fseq, cnt);
         cnt[CNT_MISS]++;
-        const int after = old >= 0 ? pos_of[old] : -1;
+        // an earlier member must finish reading the slot; a later one was never read
+        const int po = old >= 0 ? pos_of[old] : -1;
+        const int after = po < pos ? po : -1;
         if (lane == 0) { rec->expert[pos] = e; rec->slot[pos] = v; rec->flag[pos] = 1; rec->victim[pos] = old; rec->after[pos] = after; }
         if (lane == 0) a.d_order_slot[pos] = v;
       }
@@ -279,7 +289,7 @@ __global__ __launch_bounds__(256) void k_plan_precise(PlanArgs a) {
       rec->kind = 1;
       rec->layer = a.layer;
       rec->n = np;
-      rec->n_hit = nh;
+      rec->n_hit = n_hit;
       n_pos = np;
     }
   }

@@ -80,8 +80,12 @@ struct LayerW {
   bool planned = false;
 };
 
+// A position whose copies wait for an earlier position's compute: a fill of a
+// slot that an earlier position reads (write after read), or, without early
+// preemption, any copy still to issue when the position is reached.
 struct Deferred {
   int pos, slot, expert, after;
+  bool fill;  // the slot changes expert (else only pending chunks are issued)
 };
 
 }  // namespace
@@ -352,6 +356,8 @@ PlanArgs plan_args(promoe_ctx* c, int layer, const int32_t* ids, int T, int64_t 
   // fills allowed in a predictor-driven speculative plan (-1: no limit)
   const int lim = c->cfg.spec_fill_limit;
   a.fill_budget = lim == 0 ? -1 : (lim < 0 ? 0 : lim);
+  a.reorder = (c->cfg.flags & PROMOE_FLAG_NO_REORDER) ? 0 : 1;
+  a.pinned = (c->cfg.flags & PROMOE_FLAG_STATIC) ? c->C - 2 : 0;
   a.rec = c->rec_d + (r % kRecRing);
   a.d_order_slot = c->d_order_slot;
   a.d_offsets = c->d_offsets;
@@ -466,7 +472,7 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   if (g.n_layers < 1 || g.hidden < 8 || g.inter < 8 || g.n_experts < 1 || g.top_k < 1 ||
       g.slots_per_layer < 1 || g.max_tokens < 1 || g.lookahead < 0 || g.pred_hidden < 0 || g.shared_inter < 0 ||
       (g.dtype != PROMOE_F32 && g.dtype != PROMOE_BF16) || g.top_k > g.n_experts || g.spec_fill_limit < -1 ||
-      g.spec_fill_limit > 64) {
+      g.spec_fill_limit > 64 || ((g.flags & PROMOE_FLAG_STATIC) && g.slots_per_layer < 3)) {
     g_last_error = "invalid config";
     return PROMOE_EINVAL;
   }
@@ -581,6 +587,7 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   const size_t sub = g.copy_subchunk_bytes > 0 ? (size_t)g.copy_subchunk_bytes : ((size_t)16 << 20);
   const int window = g.copy_window > 0 ? g.copy_window : 2;
   c->pf = new Prefetcher(L, C, E, c->chunk_bytes, sub, window, c->cache, &c->eng, std::max(sub, kHighMergeBytes));
+  c->pf->set_whole_expert_low((g.flags & PROMOE_FLAG_NO_CHUNK) != 0);
   if (c->profile) {
     int khz = 0;
     if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, c->dev) == hipSuccess && khz > 0)
@@ -860,19 +867,26 @@ int promoe_route(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_id
   const PlanRecord rec = c->rec_h[r % kRecRing];
   c->rec_ingested = r + 1;
   c->last_precise[layer] = rec;
-  c->pf->purge_low(layer);
+  const bool early = !(c->cfg.flags & PROMOE_FLAG_NO_PREEMPT);
+  if (early) c->pf->purge_low(layer);
   c->need01.assign(rec.n, -1);
   c->need2.assign(rec.n, -1);
   c->deferred.clear();
   for (int pos = 0; pos < rec.n; ++pos) {
     const int slot = rec.slot[pos];
-    if (rec.flag[pos]) {
-      if (rec.after[pos] >= 0) {
-        c->deferred.push_back(Deferred{pos, slot, rec.expert[pos], rec.after[pos]});
-        continue;
-      }
-      c->pf->assign(layer, slot, rec.expert[pos]);
+    const bool fill = rec.flag[pos] != 0;
+    // Without early preemption a copy starts when its position is reached, after
+    // the previous position's compute (positions then run in order, so this also
+    // follows any earlier reader of the slot).
+    if (!early && pos > 0 && (fill || c->pf->ready_seq(layer, slot, 2) == -2)) {
+      c->deferred.push_back(Deferred{pos, slot, rec.expert[pos], pos - 1, fill});
+      continue;
     }
+    if (fill && rec.after[pos] >= 0) {
+      c->deferred.push_back(Deferred{pos, slot, rec.expert[pos], rec.after[pos], true});
+      continue;
+    }
+    if (fill) c->pf->assign(layer, slot, rec.expert[pos]);
     c->pf->issue_high(layer, slot);
     c->need01[pos] = c->pf->ready_seq(layer, slot, 1);
     c->need2[pos] = c->pf->ready_seq(layer, slot, 2);
@@ -1024,7 +1038,7 @@ int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const in
     // release fills that waited for these positions' reads
     for (const auto& d : c->deferred) {
       if (std::find(jobs.begin(), jobs.end(), d.after) == jobs.end()) continue;
-      c->pf->assign(layer, d.slot, d.expert);
+      if (d.fill) c->pf->assign(layer, d.slot, d.expert);
       c->pf->issue_high_after(layer, d.slot, tok);
       c->need01[d.pos] = c->pf->ready_seq(layer, d.slot, 1);
       c->need2[d.pos] = c->pf->ready_seq(layer, d.slot, 2);
@@ -1032,11 +1046,17 @@ int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const in
     }
   };
 
+  // Reordered inference runs every ready expert first; without it (or without
+  // early preemption, where a later position's copy starts only when it is
+  // reached) positions run strictly in the route order.
+  const bool in_order = (c->cfg.flags & (PROMOE_FLAG_NO_REORDER | PROMOE_FLAG_NO_PREEMPT)) != 0;
   // 1. the shared expert and every routed expert whose chunks are already in HBM
   std::vector<int> jobs;
   if (c->Ish > 0) jobs.push_back(kSharedJob);
-  for (int p = 0; p < n; ++p)
+  for (int p = 0; p < n; ++p) {
     if (!is_def[p] && c->need01[p] < 0 && c->need2[p] < 0) jobs.push_back(p);
+    else if (in_order) break;
+  }
   int rc = PROMOE_OK;
   if (!jobs.empty()) {
     rc = ffn_launch(c, a, jobs, s, -1, -1);
@@ -1053,7 +1073,11 @@ int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const in
     jobs.clear();
     int64_t w01 = -1, w2 = -1;
     for (int p = 0; p < n; ++p) {
-      if (done[p] || is_def[p]) continue;
+      if (done[p]) continue;
+      if (is_def[p]) {
+        if (in_order) break;
+        continue;
+      }
       jobs.push_back(p);
       w01 = std::max(w01, c->need01[p]);
       w2 = std::max(w2, c->need2[p]);

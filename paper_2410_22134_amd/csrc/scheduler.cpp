@@ -79,7 +79,7 @@ void Prefetcher::issue_sub(int layer, int slot, int chunk, Prio prio, int64_t af
   st_.bytes[prio] += (int64_t)bytes;
 }
 
-void Prefetcher::issue_pending_high(int layer, int slot, int64_t after_compute) {
+void Prefetcher::issue_pending(int layer, int slot, int64_t after_compute, Prio prio) {
   Slot& s = slot_(layer, slot);
   const size_t expert_bytes = kChunks * chunk_bytes_;
   bool first = true;
@@ -92,7 +92,7 @@ void Prefetcher::issue_pending_high(int layer, int slot, int64_t after_compute) 
     }
     if (ch.n_issued == n_sub_) { ++c; continue; }
     if (merge_ == 0) {
-      issue_sub(layer, slot, c, HIGH, first ? after_compute : -1);
+      issue_sub(layer, slot, c, prio, first ? after_compute : -1);
       first = false;
       continue;
     }
@@ -133,8 +133,8 @@ void Prefetcher::issue_pending_high(int layer, int slot, int64_t after_compute) 
     const int64_t seq = next_seq_++;
     const size_t slot_off = ((size_t)layer * C_ + slot) * expert_bytes;
     eng_->issue(seq, cache_ + slot_off + start, host_[layer * E_ + s.expert] + start, end - start, after);
-    st_.copies[HIGH]++;
-    st_.bytes[HIGH] += (int64_t)(end - start);
+    st_.copies[prio]++;
+    st_.bytes[prio] += (int64_t)(end - start);
     first = false;
     // mark the covered sub-copies of every chunk in [start, end)
     for (int k = 0; k < kChunks; ++k) {
@@ -153,14 +153,14 @@ void Prefetcher::issue_pending_high(int layer, int slot, int64_t after_compute) 
 
 void Prefetcher::issue_high(int layer, int slot) {
   if (slot_(layer, slot).expert < 0) return;
-  issue_pending_high(layer, slot, -1);
+  issue_pending(layer, slot, -1, HIGH);
 }
 
 void Prefetcher::issue_high_after(int layer, int slot, int64_t after_compute) {
   Slot& s = slot_(layer, slot);
   if (s.expert < 0) return;
   st_.deferred++;
-  issue_pending_high(layer, slot, after_compute);
+  issue_pending(layer, slot, after_compute, HIGH);
 }
 
 int Prefetcher::pump() {
@@ -173,6 +173,11 @@ int Prefetcher::pump() {
     if (s.expert != t.expert || ch.n_issued == n_sub_) {  // stale or already served
       ch.queued = false;
       low_.pop_front();
+      continue;
+    }
+    if (whole_low_) {  // drops every queued task of the slot, this one included
+      issue_pending(t.layer, t.slot, -1, LOW);
+      ++n;
       continue;
     }
     issue_sub(t.layer, t.slot, t.chunk, LOW, -1);

@@ -78,8 +78,13 @@ class Prefetcher {
   // Issue the slot's chunks at high priority after compute token `after`.
   void issue_high_after(int layer, int slot, int64_t after_compute);
 
+  // Without chunked prefetching a low-priority task is the whole expert: once
+  // started, every pending sub-copy of the slot is issued at once (so a
+  // high-priority copy may wait for a whole expert).
+  void set_whole_expert_low(bool on) { whole_low_ = on; }
+
   // Issue low-priority sub-copies while fewer than `window` copies are in
-  // flight.  Returns the number issued.
+  // flight.  Returns the number of tasks started.
   int pump();
   // Note completed copies (in FIFO order).
   void retire();
@@ -120,13 +125,15 @@ class Prefetcher {
   Slot& slot_(int l, int s) { return slots_[l * C_ + s]; }
   const Slot& slot_(int l, int s) const { return slots_[l * C_ + s]; }
   void issue_sub(int layer, int slot, int chunk, Prio prio, int64_t after_compute);
-  // Issue every pending sub-copy of the slot at high priority, coalesced.
-  void issue_pending_high(int layer, int slot, int64_t after_compute);
+  // Issue every pending sub-copy of the slot (coalesced when merge_ > 0),
+  // dropping its queued low-priority tasks.
+  void issue_pending(int layer, int slot, int64_t after_compute, Prio prio);
 
   int L_, C_, E_;
   size_t chunk_bytes_, sub_bytes_;
   int n_sub_, window_;
   size_t merge_;
+  bool whole_low_ = false;
   uint8_t* cache_;
   CopyEngine* eng_;
   std::vector<const uint8_t*> host_;

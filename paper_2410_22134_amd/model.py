@@ -66,8 +66,17 @@ class SyntheticModel:
         self.d_sgate = [None if v is None else _dev(v, device) for v in self.np_sgate]
         self.d_attn = [None if not cfg.attn_surrogate else _dev(sm.attn(cfg, l), device) for l in range(L)]
         self.cache = torch.empty(L * cfg.slots * eb, dtype=torch.uint8, device=device)
-        self.ctx = Context(lib_config(cfg, self.max_tokens, flags, window, subchunk, spec_fill_limit), self.cache.data_ptr(),
-                           self.cache.numel())
+        self.ctx = None
+        self.open(flags, window, subchunk, spec_fill_limit, warm)
+
+    def open(self, flags=0, window=0, subchunk=0, spec_fill_limit=0, warm=True):
+        """(Re)create the context over the same weights and cache region, e.g. to
+        run another cache policy; the cache starts over from the warm set."""
+        cfg, L, E, eb = self.cfg, self.cfg.n_layers, self.cfg.n_experts, self.cfg.expert_bytes
+        if self.ctx is not None:
+            self.ctx.close()
+        self.ctx = Context(lib_config(cfg, self.max_tokens, flags, window, subchunk, spec_fill_limit),
+                           self.cache.data_ptr(), self.cache.numel())
         for l in range(L):
             p1, p2 = self.d_pred[l]
             self.ctx.set_layer(l, self.d_gate[l], self.d_bias[l], p1, p2, self.d_shared[l], self.d_sgate[l])

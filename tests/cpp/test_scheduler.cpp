@@ -59,10 +59,10 @@ struct Rig {
   std::vector<uint8_t> host, cache;
   Prefetcher* pf;
   size_t chunk;
-  Rig(int L, int C, int E, size_t chunk_bytes, size_t sub, int window) : chunk(chunk_bytes) {
+  Rig(int L, int C, int E, size_t chunk_bytes, size_t sub, int window, size_t merge = 0) : chunk(chunk_bytes) {
     host.resize((size_t)L * E * 3 * chunk_bytes);
     cache.resize((size_t)L * C * 3 * chunk_bytes);
-    pf = new Prefetcher(L, C, E, chunk_bytes, sub, window, cache.data(), &eng);
+    pf = new Prefetcher(L, C, E, chunk_bytes, sub, window, cache.data(), &eng, merge);
     for (int l = 0; l < L; ++l)
       for (int e = 0; e < E; ++e) pf->set_host(l, e, host.data() + ((size_t)l * E + e) * 3 * chunk_bytes);
   }
@@ -96,9 +96,9 @@ void example(double* chunked, double* unchunked, double* early) {
   for (int variant = 0; variant < 3; ++variant) {
     const bool chunking = variant != 1;
     const size_t unit = 100;  // bytes of one matrix; bw 100 B / unit time -> 1 time unit per chunk
-    // without chunking the whole expert is one copy task: emulate with a single 3-unit sub-copy stream
-    Rig r(1, 4, 8, chunking ? unit : 3 * unit, chunking ? unit : 3 * unit, 1);
-    r.eng.bw = chunking ? 100.0 : 100.0;
+    Rig r(1, 4, 8, unit, unit, 1);
+    r.pf->set_whole_expert_low(!chunking);  // without chunking the low task is the whole expert
+    r.eng.bw = 100.0;
     r.pf->assign(0, 0, 1);  // predicted expert 1 -> slot 0
     r.pf->push_low(0, 0);
     const double miss_at = variant == 2 ? 0.5 : 1.5;  // during chunk 0 (gate end) or chunk 1 (access)
@@ -120,6 +120,32 @@ void test_example() {
   CHECK(std::fabs(a - 2.0) < 1e-9);  // right after the second chunk
   CHECK(std::fabs(b - 3.0) < 1e-9);  // after the whole expert without chunking
   CHECK(std::fabs(c - 1.0) < 1e-9);  // early preemption: before the second chunk starts
+}
+
+// Whole-expert low-priority tasks: a started task issues all of its expert's
+// sub-copies at once (past the window), coalesced when merging is on, and a
+// task dropped by a route never starts.
+void test_whole_expert_low() {
+  for (size_t merge : {(size_t)0, (size_t)1000}) {
+    Rig r(2, 4, 8, 100, 50, 1, merge);  // 2 sub-copies per chunk
+    r.eng.bw = 100.0;
+    r.pf->set_whole_expert_low(true);
+    r.pf->assign(1, 0, 3);
+    r.pf->push_low(1, 0);
+    r.pf->assign(1, 1, 4);
+    r.pf->push_low(1, 1);
+    CHECK(r.pf->pump() == 1);                       // one task: expert 3 whole
+    CHECK(r.eng.log.size() == (merge ? 1u : 6u));
+    size_t bytes = 0;
+    for (auto& c : r.eng.log) bytes += c.bytes;
+    CHECK(bytes == 300);
+    CHECK(r.pf->ready_seq(1, 0, 2) >= 0);          // every chunk issued
+    CHECK(r.pf->ready_seq(1, 1, 0) == -2);         // the next task has not started
+    r.pf->purge_low(1);
+    CHECK(r.pf->stats().low_purged == 6);          // expert 4: 3 chunks x 2 sub-copies
+    r.worker_until(100.0);
+    CHECK(r.pf->stats().bytes[LOW] == 300 && r.pf->stats().copies[HIGH] == 0);
+  }
 }
 
 // A high-priority copy waits for at most `window` already-issued low-priority
@@ -323,6 +349,7 @@ int main(int argc, char** argv) {
     return 0;
   }
   test_example();
+  test_whole_expert_low();
   test_window_bound();
   test_purge_dedupe_and_priority();
   test_ready_and_war();

@@ -164,9 +164,9 @@ def check_ffn(cfg, model, l, x64, g_ids, w_ref, s_ref, y_gpu, tokens=None):
     return err.max(), None
 
 
-def check_plan_precise(lc: ocache.LayerCache, g_ids, gpu_plan):
+def check_plan_precise(lc: ocache.LayerCache, g_ids, gpu_plan, reorder: bool = True):
     P = np.unique(g_ids)
-    order, entries = lc.precise_plan(P.tolist())
+    order, entries = lc.precise_plan(P.tolist(), reorder)
     assert gpu_plan["expert"] == order, (gpu_plan["expert"], order)
     assert gpu_plan["slot"] == [e.slot for e in entries]
     assert gpu_plan["flag"] == [int(e.miss) for e in entries]
@@ -219,7 +219,7 @@ def check_harness(cfg, model, l, rec):
         assert err.max() <= TOL_F32, (l, err.max())
 
 
-def moe_layer_check(cfg, m, st, l, lcs, x_np, sample=None, predict=True, budget=-1):
+def moe_layer_check(cfg, m, st, l, lcs, x_np, sample=None, predict=True, budget=-1, reorder=True):
     """Run predict (optional) -> route -> ffn of layer l on x through the C ABI and check
     every output against the oracle, replaying the cache plans on lcs."""
     import torch
@@ -238,7 +238,7 @@ def moe_layer_check(cfg, m, st, l, lcs, x_np, sample=None, predict=True, budget=
         check_plan_spec(lcs[tgt], Q, m.ctx.last_plan(tgt, 0), budget)
     g_ids, w_ref, s_ref, clear = check_route(cfg, m, l, x64, rec)
     if lcs is not None:
-        check_plan_precise(lcs[l], g_ids, m.ctx.last_plan(l, 1))
+        check_plan_precise(lcs[l], g_ids, m.ctx.last_plan(l, 1), reorder)
         assert rec.order == m.ctx.last_plan(l, 1)["expert"]
     err = check_ffn(cfg, m, l, x64, g_ids, w_ref, s_ref, rec.y, tokens=sample)
     return rec, err

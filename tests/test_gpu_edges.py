@@ -17,7 +17,8 @@ from oracle import cache as ocache  # noqa: E402
 from synth import configs, model as sm  # noqa: E402
 from synth.configs import MoEConfig, Workload  # noqa: E402
 
-from paper_2410_22134_amd import FLAG_NO_PREFETCH, PRIO_HIGH, PRIO_LOW, PromoeError  # noqa: E402
+from paper_2410_22134_amd import ABLATION, FLAG_NO_PREFETCH, FLAG_NO_REORDER, FLAG_STATIC  # noqa: E402
+from paper_2410_22134_amd import PRIO_HIGH, PRIO_LOW, PromoeError  # noqa: E402
 from paper_2410_22134_amd import _abi  # noqa: E402
 from paper_2410_22134_amd.model import SyntheticModel  # noqa: E402
 from paper_2410_22134_amd.stack import Stack  # noqa: E402
@@ -107,6 +108,31 @@ def test_spec_fill_limit(limit, T):
         m.close()
 
 
+@pytest.mark.parametrize("T", [1, 77])
+@pytest.mark.parametrize("mode", list(ABLATION))
+def test_ablation_modes(mode, T):
+    # every ablation step and the static baseline: plans, counters and outputs
+    flags = ABLATION[mode]
+    cfg = SMALL.with_(slots=5)
+    _log("ablation", mode, "T", T)
+    m = SyntheticModel(cfg, max_tokens=T, flags=flags)
+    try:
+        st = Stack(m, T)
+        pinned = cfg.slots - 2 if flags & FLAG_STATIC else 0
+        lcs = {l: ocache.LayerCache(cfg.n_experts, cfg.slots, pinned=pinned) for l in range(cfg.n_layers)}
+        predict = not flags & FLAG_NO_PREFETCH
+        for step in range(3):
+            for l in range(cfg.n_layers):
+                pu.moe_layer_check(cfg, m, st, l, lcs, sm.layer_input(cfg, l, T, tag=500 + step), predict=predict,
+                                   reorder=not flags & FLAG_NO_REORDER)
+        pu.check_counters(m, lcs)
+        if pinned:
+            for l in range(cfg.n_layers):
+                assert m.ctx.slot_table(l)[:pinned] == list(range(pinned))
+    finally:
+        m.close()
+
+
 def test_external_pushes_low_and_high():
     cfg = SMALL.with_(n_layers=1, lookahead=0)
     m = SyntheticModel(cfg, max_tokens=2)
@@ -167,4 +193,6 @@ def test_error_returns():
     c.hidden = 256
     assert _abi.lib().promoe_create(ctypes.byref(c), buf.data_ptr(), 100, ctypes.byref(h)) == -1
     c.spec_fill_limit = -2
+    assert _abi.lib().promoe_create(ctypes.byref(c), buf.data_ptr(), buf.numel(), ctypes.byref(h)) == -1
+    c.spec_fill_limit, c.flags, c.slots_per_layer = 0, FLAG_STATIC, 2   # static needs C >= 3
     assert _abi.lib().promoe_create(ctypes.byref(c), buf.data_ptr(), buf.numel(), ctypes.byref(h)) == -1

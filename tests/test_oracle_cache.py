@@ -49,25 +49,31 @@ def _plans(E, C):
     return out
 
 
-def _replay(seq, E, C, warm=True, budget=-1):
-    a = cache.LayerCache(E, C, warm)
-    b = brute.NaiveLRU(E, C, warm)
+def _replay(seq, E, C, warm=True, budget=-1, reorder=True, pinned=0):
+    a = cache.LayerCache(E, C, warm, pinned)
+    b = brute.NaiveLRU(E, C, warm, pinned)
     for kind, lst in seq:
         if kind == "Q":
             ea = a.spec_plan(lst, budget)
             eb = b.spec(lst, budget)
             assert [(x.expert, x.slot, x.new) for x in ea] == eb
         else:
-            order, entries = a.precise_plan(lst)
-            ob, sb = b.precise(lst)
+            order, entries = a.precise_plan(lst, reorder)
+            ob, sb = b.precise(lst, reorder)
             assert order == ob
             assert [x.slot for x in entries] == sb
-            # the `after` dependency names the earlier position whose slot is reused
+            # the `after` dependency names the earlier position whose slot is reused;
+            # a victim that is a member of the order is an earlier one (reordered) or
+            # one not yet used (id order)
             for i, x in enumerate(entries):
                 if x.after >= 0:
                     assert x.after < i and order[x.after] == x.victim and entries[x.after].slot == x.slot
                 elif x.miss and x.victim >= 0:
-                    assert x.victim not in order
+                    assert x.victim not in order[:i]
+                    if reorder:
+                        assert x.victim not in order
+            if pinned and warm:
+                assert a.slot_expert[:pinned] == list(range(pinned))
         _check_invariants(a)
         assert a.count == b.c
         assert {e: s for e, s in enumerate(a.slot_of) if s >= 0} == b.where
@@ -89,6 +95,74 @@ def test_exhaustive_replay_with_fill_budget(budget):
     for n in (1, 2, 3):
         for seq in itertools.product(plans, repeat=n):
             _replay(seq, E, C, budget=budget)
+
+
+@pytest.mark.parametrize("reorder,pinned", [(False, 0), (True, 1), (False, 1)])
+def test_exhaustive_replay_id_order_and_static(reorder, pinned):
+    E, C = 4, 2
+    plans = _plans(E, C)
+    for n in (1, 2, 3):
+        for seq in itertools.product(plans, repeat=n):
+            _replay(seq, E, C, reorder=reorder, pinned=pinned)
+
+
+def test_random_replays_id_order_and_static():
+    rng = np.random.default_rng(12)
+    for trial in range(300):
+        E = int(rng.integers(2, 9))
+        C = int(rng.integers(2, E + 2))
+        warm = bool(rng.integers(0, 2))
+        pinned = int(rng.integers(0, C))
+        plans = []
+        for _ in range(int(rng.integers(1, 16))):
+            if rng.random() < 0.5:
+                plans.append(("P", list(rng.choice(E, size=int(rng.integers(1, E + 1)), replace=False))))
+            else:
+                plans.append(("Q", list(rng.choice(E, size=int(rng.integers(1, min(C, E) + 1)), replace=False))))
+        _replay(plans, E, C, warm, reorder=bool(rng.integers(0, 2)), pinned=pinned)
+
+
+def test_id_order_cyclic_scan_thrashes():
+    # every expert routed each time, C < E: in id order LRU misses every access after
+    # the first scan; reordered, the resident half hits
+    E, C, n = 8, 4, 5
+    a, b = cache.LayerCache(E, C), cache.LayerCache(E, C)
+    for _ in range(n):
+        a.precise_plan(range(E), reorder=False)
+        b.precise_plan(range(E))
+    assert a.count["miss"] == (E - C) + E * (n - 1) and a.count["hit"] == C
+    assert b.count["miss"] == (E - C) * n and b.count["hit"] == C * n
+
+
+def test_paper_example_without_reorder_keeps_id_order():
+    g = json.load(open(os.path.join(HERE, "golden", "worked_example_reorder.json")))
+    lc = cache.LayerCache(g["n_experts"], g["slots"], warm=g["warm"])
+    lc.spec_plan(g["prefetched"])
+    order, entries = lc.precise_plan(g["gate_selects"], reorder=False)
+    assert order == sorted(g["gate_selects"])
+    assert [e.expert for e in entries if e.miss] == g["expected_misses"]
+
+
+def test_static_cache_closed_form():
+    # pinned experts always hit; the two staging slots hold the latest two misses
+    rng = np.random.default_rng(13)
+    E, C = 12, 6
+    lc = cache.LayerCache(E, C, pinned=C - 2)
+    staging = [C - 2, C - 1]
+    for _ in range(300):
+        P = sorted(rng.choice(E, int(rng.integers(1, 5)), replace=False).tolist())
+        resident = set(lc.slot_expert)
+        before = dict(lc.count)
+        order, entries = lc.precise_plan(P, reorder=False)
+        # misses: at least the non-resident members, at most every non-pinned member
+        m = lc.count["miss"] - before["miss"]
+        assert len(set(P) - resident) <= m <= len([e for e in P if e >= C - 2])
+        for x in entries:
+            if x.expert < C - 2:
+                assert not x.miss and x.slot == x.expert
+            if x.miss:
+                assert x.slot in staging
+        assert lc.slot_expert[:C - 2] == list(range(C - 2))
 
 
 def test_fill_budget_closed_forms():
