@@ -77,6 +77,35 @@ def read_traffic(kernel):
     return None
 
 
+def prediction_metrics(s):
+    """GoodPred = Accuracy x FetchRate (Sec. "A New Prediction Metric: GoodPred").
+    Accuracy: predicted experts that the target layer routes (exact, device counters);
+    FetchRate: of those, the ones whose bytes had all landed when the route ran;
+    proactive coverage: fetched experts that a prediction brought in before the route."""
+    acc = s["pred_correct"] / s["pred_n"] if s["pred_n"] else None
+    fetch = s["pred_in_time"] / s["pred_correct"] if s["pred_correct"] else None
+    fetched = s["spec_used"] + s["miss"]
+    return {"accuracy": None if acc is None else round(acc, 4),
+            "fetch_rate": None if fetch is None else round(fetch, 4),
+            "goodpred": None if acc is None or fetch is None else round(acc * fetch, 4),
+            "proactive_coverage": round(s["spec_used"] / fetched, 4) if fetched else None,
+            "pred_n": s["pred_n"], "pred_correct": s["pred_correct"], "pred_in_time": s["pred_in_time"]}
+
+
+def overlap_metrics(s, elapsed, h2d_gbs):
+    """Share of copy time hidden behind compute: H_time = 1 - stall / load, where stall is
+    the compute stream's measured wait on copies and load = copied bytes at the measured
+    single-copy rate; H_max = min(1, (elapsed - stall) / load) bounds it."""
+    load = (s["bytes_high"] + s["bytes_low"]) / (h2d_gbs * 1e9) if h2d_gbs else 0.0
+    stall = s["stall_ms"] * 1e-3
+    if load <= 0:
+        return None
+    h_time = 1.0 - stall / load
+    h_max = min(1.0, max(elapsed - stall, 0.0) / load)
+    return {"load_s": round(load, 4), "stall_s": round(stall, 4), "H_time": round(h_time, 4),
+            "H_max": round(h_max, 4), "H_time_over_H_max": round(h_time / h_max, 4) if h_max > 0 else None}
+
+
 def h2d_probe(torch, mib=256, reps=5):
     """Pinned host -> device copy bandwidth (GB/s) of one large async copy."""
     n = mib << 20
@@ -326,6 +355,8 @@ def main():
             "hit": s["hit"], "miss": s["miss"], "prec_access": s["prec_access"],
             "spec_issued": s["spec_issued"], "spec_used": s["spec_used"], "spec_wasted": s["spec_wasted"],
             "low_purged_subcopies": s["low_purged"],
+            "prediction": prediction_metrics(s),
+            "overlap": overlap_metrics(s, elapsed, h2d_gbs),
             "stall_s": round(s["stall_ms"] * 1e-3, 4), "miss_load_s_at_measured_h2d": round(load_s, 4),
             "setup_s": round(setup_s, 1),
         },

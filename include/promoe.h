@@ -123,6 +123,10 @@ typedef struct promoe_stats {
   int64_t spec_used;      /* speculatively filled slots later hit */
   int64_t spec_wasted;    /* speculatively filled slots evicted unused */
   int64_t evict;          /* slot reassignments that displaced an expert */
+  int64_t pred_n;         /* experts in predictor-driven plans (|Q| summed) */
+  int64_t pred_correct;   /* of those, routed at the layer's next route: accuracy =
+                             pred_correct / pred_n (Sec. "A New Prediction Metric:
+                             GoodPred"; per token when T = 1) */
   /* Physical counters (host side). */
   int64_t copies_high, copies_low;  /* sub-copies issued per priority */
   int64_t bytes_high, bytes_low;    /* bytes issued per priority */
@@ -130,6 +134,9 @@ typedef struct promoe_stats {
   int64_t deferred;                 /* high copies held behind an earlier position's
                                        compute: the slot's previous reader (write after
                                        read), or the previous position (NO_PREEMPT) */
+  int64_t pred_in_time;             /* correctly predicted experts whose bytes had all
+                                       landed in HBM when the route ran: FetchRate =
+                                       pred_in_time / pred_correct */
   /* Timing, PROMOE_FLAG_PROFILE only.  Expert launches are timed on the
      device clock (earliest block start to latest wave end); classes:
      [0] GEMV gate/up, [1] GEMV down, [2] GEMM gate/up (routed experts),
@@ -233,7 +240,8 @@ int promoe_expert_ffn(promoe_ctx* ctx, int layer, const void* d_x, int T, const 
 
 /* ---- state and statistics ------------------------------------------------ */
 
-/* Counters of one layer, or of all layers summed (layer = -1).  Synchronises. */
+/* Logical counters of one layer, or of all layers summed (layer = -1); the
+ * physical counters and timings always cover all layers.  Synchronises. */
 int promoe_cache_stats(promoe_ctx* ctx, int layer, promoe_stats* out);
 int promoe_reset_stats(promoe_ctx* ctx);
 /* h_slot_of [E]: slot of each expert of the layer, -1 if not resident.  Synchronises. */

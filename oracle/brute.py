@@ -51,7 +51,8 @@ class NaiveLRU:
         self.warm_set = set(self.where)
         self.spec_pending = set()
         self.c = {k: 0 for k in ("prec_access", "hit", "miss", "spec_issued", "spec_resident",
-                                 "spec_used", "spec_wasted", "evict")}
+                                 "spec_used", "spec_wasted", "evict", "pred_n", "pred_correct")}
+        self.predicted = []      # the last prediction not yet followed by a route
 
     def _last(self, e, kinds):
         for i in range(len(self.log) - 1, -1, -1):
@@ -85,7 +86,10 @@ class NaiveLRU:
             self.spec_pending.discard(e)
         return s, v
 
-    def spec(self, Q, budget=-1):
+    def spec(self, Q, budget=-1, predicted=True):
+        if predicted:
+            self.predicted = list(Q)
+            self.c["pred_n"] += len(Q)
         out = []
         brought = 0
         for e in Q:
@@ -116,6 +120,8 @@ class NaiveLRU:
 
     def precise(self, P, reorder=True):
         P = sorted(set(P))
+        self.c["pred_correct"] += sum(1 for e in self.predicted if e in P)
+        self.predicted = []
         if not reorder:
             # one access at a time, in id order
             slots = []

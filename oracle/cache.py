@@ -43,6 +43,14 @@ precise_plan(P, reorder=False)
                      misses in its turn (the cache thrashing of "Reordered
                      Inference"); a victim that is a later member needs no wait.
 
+Prediction accuracy (Sec. "A New Prediction Metric: GoodPred": the share of
+predicted experts that are correct).  A predictor-driven spec plan of a layer
+records its list Q (pred_n += |Q|); the layer's next precise plan counts
+pred_correct += |Q & P| and forgets Q.  With one token, Q is the token's k
+predicted experts, so pred_correct / pred_n is exactly the per-token accuracy;
+with several tokens it is the accuracy of the merged list.  Lists pushed by the
+caller are not predictions and are not counted.
+
 Static cache (the paper's static baseline, Sec. "Evaluation"): the first
 ``pinned`` slots keep their warm experts for good; victims are chosen among the
 remaining slots only (with C - pinned = 2 staging buffers, as the paper's static
@@ -50,7 +58,8 @@ baseline uses).  pinned = 0 is the LRU cache above.
 """
 from dataclasses import dataclass
 
-COUNTERS = ("prec_access", "hit", "miss", "spec_issued", "spec_resident", "spec_used", "spec_wasted", "evict")
+COUNTERS = ("prec_access", "hit", "miss", "spec_issued", "spec_resident", "spec_used", "spec_wasted", "evict",
+            "pred_n", "pred_correct")
 
 
 @dataclass
@@ -82,6 +91,7 @@ class LayerCache:
         self.spec_unused = [False] * slots
         self.clock = slots - 1
         self.fseq = 0
+        self.pred_set = set()
         self.count = {c: 0 for c in COUNTERS}
         if warm:
             for s in range(min(slots, n_experts)):
@@ -120,7 +130,10 @@ class LayerCache:
         self._touch(s)
 
     # -- plans
-    def spec_plan(self, Q, budget: int = -1):
+    def spec_plan(self, Q, budget: int = -1, predicted: bool = True):
+        if predicted:
+            self.pred_set = set(int(e) for e in Q)
+            self.count["pred_n"] += len(self.pred_set)
         out = []
         fills = 0
         for e in Q:
@@ -160,6 +173,8 @@ class LayerCache:
 
     def precise_plan(self, P, reorder: bool = True):
         P = sorted(set(int(e) for e in P))
+        self.count["pred_correct"] += len(self.pred_set & set(P))
+        self.pred_set = set()
         if not reorder:
             pos_of = {e: i for i, e in enumerate(P)}
             entries = [self._hit(e) if self.slot_of[e] >= 0 else self._miss(e, i, pos_of) for i, e in enumerate(P)]

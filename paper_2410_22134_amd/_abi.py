@@ -24,19 +24,20 @@ class Config(ctypes.Structure):
                 ("spec_fill_limit", _i32)]
 
 
-STAT_COUNTERS = ("prec_access", "hit", "miss", "spec_issued", "spec_resident", "spec_used", "spec_wasted", "evict")
+STAT_COUNTERS = ("prec_access", "hit", "miss", "spec_issued", "spec_resident", "spec_used", "spec_wasted", "evict",
+                 "pred_n", "pred_correct")
 
 
 class Stats(ctypes.Structure):
     _fields_ = [(n, _i64) for n in STAT_COUNTERS] + [
         ("copies_high", _i64), ("copies_low", _i64), ("bytes_high", _i64), ("bytes_low", _i64),
-        ("low_purged", _i64), ("deferred", _i64),
+        ("low_purged", _i64), ("deferred", _i64), ("pred_in_time", _i64),
         ("k_launches", _i64 * 6), ("k_ms", _dbl * 6), ("k_bytes", _dbl * 6), ("k_flops", _dbl * 6),
         ("stall_ms", _dbl), ("copy_ms", _dbl)]
 
     def as_dict(self):
         d = {n: int(getattr(self, n)) for n in STAT_COUNTERS}
-        for n in ("copies_high", "copies_low", "bytes_high", "bytes_low", "low_purged", "deferred"):
+        for n in ("copies_high", "copies_low", "bytes_high", "bytes_low", "low_purged", "deferred", "pred_in_time"):
             d[n] = int(getattr(self, n))
         for n in ("k_launches", "k_ms", "k_bytes", "k_flops"):
             d[n] = list(getattr(self, n))

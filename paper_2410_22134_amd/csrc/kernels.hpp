@@ -68,6 +68,8 @@ struct CombineArgs {
   int hidden, top_k;
 };
 
+constexpr int kCounters = 10;
+
 // Per-layer logical cache state on the device.
 struct CacheState {
   int32_t* slot_expert;  // [L*C]
@@ -77,7 +79,9 @@ struct CacheState {
   int32_t* spec_unused;  // [L*C]
   uint32_t* clock;       // [L]
   uint32_t* fseq;        // [L]
-  int64_t* counters;     // [L*8]: prec_access hit miss spec_issued spec_resident spec_used spec_wasted evict
+  int64_t* counters;     // [L*kCounters]: prec_access hit miss spec_issued spec_resident spec_used
+                         // spec_wasted evict pred_n pred_correct
+  uint64_t* pred_mask;   // [L]: experts of the layer's last prediction not yet routed
 };
 
 // Plan record written by the plan kernels into host-mapped memory.
@@ -86,6 +90,7 @@ struct PlanRecord {
   int32_t layer;
   int32_t n;
   int32_t n_hit;
+  int32_t predicted;  // spec plan from the predictor (not a caller's list)
   int32_t expert[64], slot[64], flag[64], victim[64], after[64], count[64];
   int32_t offset[65];
   int32_t q_in[64];  // host-provided list for promoe_prefetch

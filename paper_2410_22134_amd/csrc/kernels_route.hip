@@ -25,7 +25,10 @@
 
 namespace promoe {
 
-enum { CNT_PREC = 0, CNT_HIT, CNT_MISS, CNT_SPEC_ISSUED, CNT_SPEC_RESIDENT, CNT_SPEC_USED, CNT_SPEC_WASTED, CNT_EVICT };
+enum {
+  CNT_PREC = 0, CNT_HIT, CNT_MISS, CNT_SPEC_ISSUED, CNT_SPEC_RESIDENT, CNT_SPEC_USED, CNT_SPEC_WASTED, CNT_EVICT,
+  CNT_PRED_N, CNT_PRED_CORRECT
+};
 
 // ============================================================ top-k
 __global__ __launch_bounds__(256) void k_topk(TopkArgs a) {
@@ -64,7 +67,7 @@ struct WaveState {
 };
 
 __device__ __forceinline__ void load_state(const PlanArgs& a, int lane, WaveState& w, uint32_t& clock, uint32_t& fseq,
-                                           int64_t (&cnt)[8]) {
+                                           int64_t (&cnt)[kCounters]) {
   const int bc = a.layer * a.C, be = a.layer * a.E;
   w.slot_expert = lane < a.C ? a.st.slot_expert[bc + lane] : -1;
   w.stamp = lane < a.C ? a.st.stamp[bc + lane] : 0u;
@@ -74,11 +77,11 @@ __device__ __forceinline__ void load_state(const PlanArgs& a, int lane, WaveStat
   clock = a.st.clock[a.layer];
   fseq = a.st.fseq[a.layer];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) cnt[i] = a.st.counters[a.layer * 8 + i];
+  for (int i = 0; i < kCounters; ++i) cnt[i] = a.st.counters[a.layer * kCounters + i];
 }
 
 __device__ __forceinline__ void store_state(const PlanArgs& a, int lane, const WaveState& w, uint32_t clock,
-                                            uint32_t fseq, const int64_t (&cnt)[8]) {
+                                            uint32_t fseq, const int64_t (&cnt)[kCounters]) {
   const int bc = a.layer * a.C, be = a.layer * a.E;
   if (lane < a.C) {
     a.st.slot_expert[bc + lane] = w.slot_expert;
@@ -91,7 +94,7 @@ __device__ __forceinline__ void store_state(const PlanArgs& a, int lane, const W
     a.st.clock[a.layer] = clock;
     a.st.fseq[a.layer] = fseq;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) a.st.counters[a.layer * 8 + i] = cnt[i];
+    for (int i = 0; i < kCounters; ++i) a.st.counters[a.layer * kCounters + i] = cnt[i];
   }
 }
 
@@ -106,7 +109,7 @@ __device__ __forceinline__ int victim_slot(const PlanArgs& a, int lane, const Wa
 
 // Give slot v to expert e: evict its occupant (counted), fill, stamp.
 __device__ __forceinline__ int fill_slot(const PlanArgs& a, int lane, WaveState& w, int e, int v, bool speculative,
-                                         uint32_t& clock, uint32_t& fseq, int64_t (&cnt)[8]) {
+                                         uint32_t& clock, uint32_t& fseq, int64_t (&cnt)[kCounters]) {
   const int old = __shfl(w.slot_expert, v, kWave);
   const int old_unused = __shfl(w.spec_unused, v, kWave);
   if (old >= 0) {
@@ -166,11 +169,17 @@ __global__ __launch_bounds__(256) void k_plan_spec(PlanArgs a) {
 
   WaveState w;
   uint32_t clock, fseq;
-  int64_t cnt[8];
+  int64_t cnt[kCounters];
   load_state(a, lane, w, clock, fseq, cnt);
   PlanRecord* rec = a.rec;
   // Host-given lists are never limited; a predicted plan fills at most fill_budget slots.
   const int budget = a.ids ? a.fill_budget : -1;
+  if (a.ids) {  // a prediction: remembered until the layer's route scores it
+    uint64_t m = 0;
+    for (int i = 0; i < nq; ++i) m |= 1ull << Q[i];
+    if (lane == 0) a.st.pred_mask[a.layer] = m;
+    cnt[CNT_PRED_N] += nq;
+  }
   int fills = 0;
   for (int i = 0; i < nq; ++i) {
     const int e = Q[i];
@@ -196,6 +205,7 @@ __global__ __launch_bounds__(256) void k_plan_spec(PlanArgs a) {
     rec->layer = a.layer;
     rec->n = nq;
     rec->n_hit = 0;
+    rec->predicted = a.ids ? 1 : 0;
     __threadfence_system();
     rec->done = 1;
   }
@@ -214,7 +224,7 @@ __global__ __launch_bounds__(256) void k_plan_precise(PlanArgs a) {
 
   WaveState w;
   uint32_t clock, fseq;
-  int64_t cnt[8];
+  int64_t cnt[kCounters];
   if (tid < kWave) {
     load_state(a, lane, w, clock, fseq, cnt);
     const bool used = lane < a.E && cnt_e[lane] > 0;
@@ -222,6 +232,7 @@ __global__ __launch_bounds__(256) void k_plan_precise(PlanArgs a) {
     const uint32_t fs = __shfl(w.fetch, w.slot_of >= 0 ? w.slot_of : 0, kWave);
     const uint64_t hmask = __ballot(res);
     const uint64_t mmask = __ballot(used && !res);
+    cnt[CNT_PRED_CORRECT] += __popcll(a.st.pred_mask[a.layer] & (hmask | mmask));
     const int nh = __popcll(hmask), np = nh + __popcll(mmask);
     int rank = -1;
     if (!a.reorder) {
@@ -273,6 +284,7 @@ __global__ __launch_bounds__(256) void k_plan_precise(PlanArgs a) {
     }
     cnt[CNT_PREC] += np;
     store_state(a, lane, w, clock, fseq, cnt);
+    if (lane == 0) a.st.pred_mask[a.layer] = 0ull;
     if (lane == 0) {
       int o = 0;
       for (int pos = 0; pos < np; ++pos) {
@@ -338,8 +350,8 @@ __global__ void k_state_init(CacheState st, int L, int C, int E) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < L * C) { st.slot_expert[i] = -1; st.stamp[i] = 0u; st.fetch_seq[i] = 0u; st.spec_unused[i] = 0; }
   if (i < L * E) st.slot_of[i] = -1;
-  if (i < L) { st.clock[i] = (uint32_t)(C - 1); st.fseq[i] = 0u; }
-  if (i < L * 8) st.counters[i] = 0;
+  if (i < L) { st.clock[i] = (uint32_t)(C - 1); st.fseq[i] = 0u; st.pred_mask[i] = 0ull; }
+  if (i < L * kCounters) st.counters[i] = 0;
 }
 
 __global__ void k_warm(CacheState st, int layer, int C, int E, const int32_t* experts, int n) {
@@ -362,7 +374,7 @@ void launch_plan_spec(const PlanArgs& a, hipStream_t s) { k_plan_spec<<<1, 256, 
 void launch_plan_precise(const PlanArgs& a, hipStream_t s) { k_plan_precise<<<1, 256, 0, s>>>(a); }
 void launch_state_init(CacheState st, int L, int C, int E, hipStream_t s) {
   int n = L * (C > E ? C : E);
-  if (n < L * 8) n = L * 8;
+  if (n < L * kCounters) n = L * kCounters;
   k_state_init<<<(n + 255) / 256, 256, 0, s>>>(st, L, C, E);
 }
 void launch_warm(CacheState st, int layer, int C, int E, const int32_t* d_experts, int n, hipStream_t s) {

@@ -137,6 +137,8 @@ struct promoe_ctx {
   int route_T = 0;
   PlanRecord route_rec{};
   std::vector<int64_t> need01, need2;  // copy seq each position waits for (-1 none)
+  std::vector<uint64_t> pred_host;     // per layer: experts of the last ingested prediction
+  int64_t pred_in_time = 0;
   std::vector<Deferred> deferred;
 
   // scheduler and worker
@@ -261,6 +263,11 @@ void ingest_spec(promoe_ctx* c, int64_t r) {
   const PlanRecord& rec = c->rec_h[r % kRecRing];
   const int layer = rec.layer;
   c->last_spec[layer] = rec;
+  if (rec.predicted) {
+    uint64_t m = 0;
+    for (int i = 0; i < rec.n; ++i) m |= 1ull << rec.expert[i];
+    c->pred_host[layer] = m;
+  }
   if (!(c->cfg.flags & PROMOE_FLAG_NO_PREFETCH)) {
     const bool high = c->rec_prio[r % kRecRing] == PROMOE_PRIO_HIGH;
     for (int i = 0; i < rec.n; ++i) {
@@ -498,6 +505,7 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   c->profile = (g.flags & PROMOE_FLAG_PROFILE) != 0;
   c->lw.resize(c->L);
   c->last_spec.resize(c->L);
+  c->pred_host.assign(c->L, 0ull);
   c->last_precise.resize(c->L);
   hipGetDevice(&c->dev);
 
@@ -510,7 +518,8 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   const size_t o_se = take(sizeof(int32_t) * L * C), o_so = take(sizeof(int32_t) * L * E),
                o_stamp = take(sizeof(uint32_t) * L * C), o_fs = take(sizeof(uint32_t) * L * C),
                o_su = take(sizeof(int32_t) * L * C), o_clock = take(sizeof(uint32_t) * L),
-               o_fseq = take(sizeof(uint32_t) * L), o_cnt = take(sizeof(int64_t) * L * 8),
+               o_fseq = take(sizeof(uint32_t) * L), o_cnt = take(sizeof(int64_t) * L * kCounters),
+               o_pmask = take(sizeof(uint64_t) * L),
                o_logits = take(sizeof(float) * (size_t)T * c->ld_logits), o_predq = take(sizeof(float) * (size_t)T * E),
                o_pids = take(sizeof(int32_t) * (size_t)T * Kk), o_oslot = take(sizeof(int32_t) * 64),
                o_offs = take(sizeof(int32_t) * 65), o_perm = take(sizeof(int32_t) * (size_t)T * Kk),
@@ -533,6 +542,7 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   c->st.clock = reinterpret_cast<uint32_t*>(b + o_clock);
   c->st.fseq = reinterpret_cast<uint32_t*>(b + o_fseq);
   c->st.counters = reinterpret_cast<int64_t*>(b + o_cnt);
+  c->st.pred_mask = reinterpret_cast<uint64_t*>(b + o_pmask);
   c->d_logits = reinterpret_cast<float*>(b + o_logits);
   c->d_predq = reinterpret_cast<float*>(b + o_predq);
   c->d_pred_ids = reinterpret_cast<int32_t*>(b + o_pids);
@@ -869,6 +879,9 @@ int promoe_route(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_id
   c->last_precise[layer] = rec;
   const bool early = !(c->cfg.flags & PROMOE_FLAG_NO_PREEMPT);
   if (early) c->pf->purge_low(layer);
+  c->pf->retire();  // completions so far, for the in-time count below
+  const uint64_t predicted = c->pred_host[layer];
+  c->pred_host[layer] = 0ull;
   c->need01.assign(rec.n, -1);
   c->need2.assign(rec.n, -1);
   c->deferred.clear();
@@ -890,6 +903,7 @@ int promoe_route(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_id
     c->pf->issue_high(layer, slot);
     c->need01[pos] = c->pf->ready_seq(layer, slot, 1);
     c->need2[pos] = c->pf->ready_seq(layer, slot, 2);
+    if (((predicted >> rec.expert[pos]) & 1ull) && c->need01[pos] == -1 && c->need2[pos] == -1) c->pred_in_time++;
   }
   if (c->eng.err != hipSuccess) return fail_hip(c->eng.err, "copy engine");
   lk.unlock();
@@ -1121,13 +1135,13 @@ int promoe_cache_stats(promoe_ctx* c, int layer, promoe_stats* out) {
   if (!c || !out || layer < -1 || layer >= c->L) return PROMOE_EINVAL;
   int rc = promoe_sync(c);
   if (rc) return rc;
-  std::vector<int64_t> cnt((size_t)c->L * 8);
+  std::vector<int64_t> cnt((size_t)c->L * kCounters);
   HIPCHK(hipMemcpy(cnt.data(), c->st.counters, sizeof(int64_t) * cnt.size(), hipMemcpyDeviceToHost));
   std::memset(out, 0, sizeof(*out));
   int64_t* dst = &out->prec_access;
   for (int l = 0; l < c->L; ++l) {
     if (layer >= 0 && l != layer) continue;
-    for (int i = 0; i < 8; ++i) dst[i] += cnt[(size_t)l * 8 + i];
+    for (int i = 0; i < kCounters; ++i) dst[i] += cnt[(size_t)l * kCounters + i];
   }
   std::lock_guard<std::mutex> lk(c->mu);
   const PhysStats& ps = c->pf->stats();
@@ -1137,6 +1151,7 @@ int promoe_cache_stats(promoe_ctx* c, int layer, promoe_stats* out) {
   out->bytes_high = ps.bytes[1];
   out->low_purged = ps.low_purged;
   out->deferred = ps.deferred;
+  out->pred_in_time = c->pred_in_time;
   for (int i = 0; i < promoe_ctx::kClasses; ++i) {
     out->k_launches[i] = c->k_launches[i];
     out->k_ms[i] = c->k_ms[i];
@@ -1152,10 +1167,11 @@ int promoe_reset_stats(promoe_ctx* c) {
   int rc = promoe_sync(c);
   if (rc) return rc;
   if (c->profile) prof_resolve(c);
-  HIPCHK(hipMemset(c->st.counters, 0, sizeof(int64_t) * 8 * c->L));
+  HIPCHK(hipMemset(c->st.counters, 0, sizeof(int64_t) * kCounters * c->L));
   HIPCHK(hipDeviceSynchronize());
   std::lock_guard<std::mutex> lk(c->mu);
   c->pf->reset_stats();
+  c->pred_in_time = 0;
   for (int i = 0; i < promoe_ctx::kClasses; ++i) c->k_launches[i] = 0, c->k_ms[i] = c->k_bytes[i] = c->k_flops[i] = 0.0;
   c->stall_ms = 0.0;
   return PROMOE_OK;

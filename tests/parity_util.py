@@ -182,8 +182,8 @@ def fill_budget(spec_fill_limit: int) -> int:
     return -1 if spec_fill_limit == 0 else (0 if spec_fill_limit < 0 else spec_fill_limit)
 
 
-def check_plan_spec(lc: ocache.LayerCache, Q, gpu_plan, budget: int = -1):
-    entries = lc.spec_plan(Q, budget)
+def check_plan_spec(lc: ocache.LayerCache, Q, gpu_plan, budget: int = -1, predicted: bool = True):
+    entries = lc.spec_plan(Q, budget, predicted)
     assert gpu_plan["expert"] == [e.expert for e in entries]
     assert gpu_plan["slot"] == [e.slot for e in entries]
     assert gpu_plan["flag"] == [int(e.new) for e in entries]

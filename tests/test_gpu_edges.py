@@ -99,7 +99,7 @@ def test_spec_fill_limit(limit, T):
             for l in range(cfg.n_layers):
                 pu.moe_layer_check(cfg, m, st, l, lcs, sm.layer_input(cfg, l, T, tag=400 + step), budget=b)
         m.ctx.prefetch(0, [0, 1, 2, 3], PRIO_LOW)
-        pu.check_plan_spec(lcs[0], [0, 1, 2, 3], m.ctx.last_plan(0, 0))
+        pu.check_plan_spec(lcs[0], [0, 1, 2, 3], m.ctx.last_plan(0, 0), predicted=False)
         pu.moe_layer_check(cfg, m, st, 0, lcs, sm.layer_input(cfg, 0, T, tag=499), predict=False)
         pu.check_counters(m, lcs)
         if limit < 0:
@@ -141,7 +141,7 @@ def test_external_pushes_low_and_high():
         lc = ocache.LayerCache(cfg.n_experts, cfg.slots)
         for i, (ids, prio) in enumerate((([5, 6], PRIO_LOW), ([7, 1, 4], PRIO_HIGH), ([0], PRIO_LOW))):
             m.ctx.prefetch(0, ids, prio)
-            pu.check_plan_spec(lc, ids, m.ctx.last_plan(0, 0))
+            pu.check_plan_spec(lc, ids, m.ctx.last_plan(0, 0), predicted=False)
             pu.moe_layer_check(cfg, m, st, 0, {0: lc}, sm.layer_input(cfg, 0, 2, tag=300 + i), predict=False)
         pu.check_counters(m, {0: lc})
         assert m.ctx.stats()["bytes_high"] > 0

@@ -165,6 +165,26 @@ def test_static_cache_closed_form():
         assert lc.slot_expert[:C - 2] == list(range(C - 2))
 
 
+def test_prediction_accuracy_counts():
+    lc = cache.LayerCache(8, 4)
+    lc.spec_plan([5, 6, 1])                 # predicted
+    lc.precise_plan([1, 2, 6])              # 1 and 6 correct
+    assert (lc.count["pred_n"], lc.count["pred_correct"]) == (3, 2)
+    lc.precise_plan([5])                    # the prediction was consumed by the route
+    assert lc.count["pred_correct"] == 2
+    lc.spec_plan([7], predicted=False)      # a caller's push is not a prediction
+    lc.precise_plan([7])
+    assert (lc.count["pred_n"], lc.count["pred_correct"]) == (3, 2)
+    # a perfect predictor of one token scores k of k
+    rng = np.random.default_rng(14)
+    p = cache.LayerCache(16, 6)
+    for _ in range(50):
+        P = rng.choice(16, 4, replace=False).tolist()
+        p.spec_plan(P)
+        p.precise_plan(P)
+    assert p.count["pred_correct"] == p.count["pred_n"] == 200
+
+
 def test_fill_budget_closed_forms():
     rng = np.random.default_rng(9)
     E, C = 16, 8
