@@ -24,13 +24,26 @@ struct RowsArgs {
 // Expert FFN launch: a list of jobs (route positions, or the shared expert),
 // each job split into row tiles; block b runs tile b - job_tile0[j] of the job
 // j with job_tile0[j] <= b < job_tile0[j + 1].
-constexpr int kMaxJobs = 65;
+constexpr int kMaxJobs = 80;  // 64 route positions + pieces of the shared expert
 // Launch clock slot: word 0 = max of ~start over the first blocks (so ~word0 is
 // the earliest start), then kTclkLines 128-byte lines whose first words hold
 // the latest wave end seen by the waves hashed to that line.
 constexpr int kTclkLines = 32;
 constexpr int kTclkWords = 16 * (kTclkLines + 1);
 constexpr uint8_t kSharedJob = 255;
+// One expert job of an FFN launch (a route position, the shared expert, or a
+// piece of the shared expert's rows), 32 bytes: a block reads it with one
+// scalar load.
+struct alignas(16) FfnJob {
+  const void* w;   // expert weights [Wg | Wu | Wd] (slot or resident shared expert)
+  int32_t q0, q1;  // pair range [q0, q1) (token range for the shared expert)
+  int32_t I;       // intermediate size of the expert
+  int32_t r0;      // GEMV: first row of the job's piece
+  int32_t pos;     // route position, or kSharedJob
+  int32_t pad;
+};
+static_assert(sizeof(FfnJob) == 32, "FfnJob layout");
+
 struct FfnArgs {
   const uint8_t* cache;
   int64_t expert_bytes;
@@ -47,14 +60,12 @@ struct FfnArgs {
   void* act_sh;               // [T x I_sh]
   float* Ysh;                 // [T x H]
   int n_jobs;
-  uint8_t job_pos[kMaxJobs];  // route position, or kSharedJob
-  int32_t job_tile0[kMaxJobs + 1];
+  int piece_rows;             // GEMV: rows per piece; the shared expert spans several pieces
   int ksplit;                   // split-K slices of the shared expert's down GEMM (>= 1)
   int64_t ysh_split_stride;     // elements between the slices' partial outputs in Ysh
   unsigned long long* tclock;   // optional launch clock slot (see kTclkWords), zero-initialised
-  const void* job_w[kMaxJobs];  // expert weights [Wg | Wu | Wd] of each job (slot or shared)
-  int32_t job_q0[kMaxJobs];     // pair range [q0, q1) of each job (tokens for the shared job)
-  int32_t job_q1[kMaxJobs];
+  int32_t job_tile0[kMaxJobs + 1];  // GEMM: first block of each job in the 1-D grid
+  FfnJob jobs[kMaxJobs];
 };
 
 struct CombineArgs {
@@ -130,7 +141,7 @@ struct PlanArgs {
 // first blocks carry the launch start (blocks start in index order), and wave
 // ends are spread over kTclkLines cache lines so the atomics do not serialise.
 __device__ __forceinline__ void tclock_start(const FfnArgs& a) {
-  if (a.tclock && threadIdx.x == 0 && blockIdx.x < 8) atomicMax(a.tclock, ~(unsigned long long)wall_clock64());
+  if (a.tclock && threadIdx.x == 0 && blockIdx.x < 8 && blockIdx.y == 0) atomicMax(a.tclock, ~(unsigned long long)wall_clock64());
 }
 __device__ __forceinline__ void tclock_end(const FfnArgs& a) {
   if (a.tclock && (threadIdx.x & 63) == 0) {
@@ -140,9 +151,10 @@ __device__ __forceinline__ void tclock_end(const FfnArgs& a) {
 }
 
 void launch_rows_gemv(const RowsArgs& a, int wdtype, int xdtype, hipStream_t s);
-// Fills job_tile0 for the pass and launches.  max_tokens = most pairs of any job.
+// Launches one pass of the GEMV kernels over the jobs (a copy of `a` is
+// adjusted per pass; `a` is unchanged).  max_tokens = most pairs of any job.
 // With ev0/ev1 set, the launch records them itself (kernel execution time).
-void launch_ffn(FfnArgs& a, int pass, int max_tokens, int dtype, hipStream_t s, hipEvent_t ev0 = nullptr,
+void launch_ffn(const FfnArgs& a, int pass, int max_tokens, int dtype, hipStream_t s, hipEvent_t ev0 = nullptr,
                 hipEvent_t ev1 = nullptr);
 // Grouped MFMA GEMM (bf16) for the same passes; needs N % 128 == 0 and K % 64 == 0.
 bool gemm_supported(int N, int K);

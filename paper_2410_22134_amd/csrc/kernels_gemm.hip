@@ -169,12 +169,13 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_ffn(FfnArgs a) {
   const int b = xcd_grouped(blockIdx.x, gridDim.x);
   const int j = gemm_find_job(a, b);
   int jt = b - a.job_tile0[j];
-  const bool shared = a.job_pos[j] == kSharedJob;
-  const int I = shared ? a.shared_inter : a.inter;
+  const FfnJob jd = a.jobs[j];
+  const bool shared = jd.pos == kSharedJob;
+  const int I = jd.I;
   const int H = a.hidden;
   const int N = PASS == 0 ? I : H;
   const int K = PASS == 0 ? H : I;
-  const int q0 = a.job_q0[j], M = a.job_q1[j] - q0;
+  const int q0 = jd.q0, M = jd.q1 - q0;
   const int mtiles = (M + BM - 1) / BM;
   const int ntiles = N / kBN;
   // split-K (shared down pass only): slice ks of S writes its own partial output
@@ -185,7 +186,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_ffn(FfnArgs a) {
   const int n0 = (jt / mtiles) * kBN;
   const int nk = K / kBK;
   const int kt0 = ks * nk / S, kt1 = (ks + 1) * nk / S;
-  const bf16_t* W = reinterpret_cast<const bf16_t*>(a.job_w[j]);
+  const bf16_t* W = reinterpret_cast<const bf16_t*>(jd.w);
 
   // DMA sources.  Load i of this wave fills LDS rows 8*(NW*i + wave) .. +8;
   // lane L writes row 8*(NW*i + wave) + L/8, physical chunk L%8, so it fetches
@@ -288,10 +289,9 @@ static void gemm_dispatch(FfnArgs& a, int pass, hipStream_t s) {
   int tiles = 0;
   for (int j = 0; j < a.n_jobs; ++j) {
     a.job_tile0[j] = tiles;
-    const bool sh = a.job_pos[j] == kSharedJob;
-    const int I = sh ? a.shared_inter : a.inter;
-    const int N = pass == 0 ? I : a.hidden;
-    const int M = a.job_q1[j] - a.job_q0[j];
+    const bool sh = a.jobs[j].pos == kSharedJob;
+    const int N = pass == 0 ? a.jobs[j].I : a.hidden;
+    const int M = a.jobs[j].q1 - a.jobs[j].q0;
     const int split = (pass == 1 && sh) ? a.ksplit : 1;
     tiles += ((M + BM - 1) / BM) * (N / kBN) * split;
   }
@@ -313,10 +313,9 @@ static int pick_bm(const FfnArgs& a, int pass, int max_tokens) {
     if (bm == 128 && max_tokens <= 64) continue;
     int tiles = 0;
     for (int j = 0; j < a.n_jobs; ++j) {
-      const bool sh = a.job_pos[j] == kSharedJob;
-      const int I = sh ? a.shared_inter : a.inter;
-      const int N = pass == 0 ? I : a.hidden;
-      const int M = a.job_q1[j] - a.job_q0[j];
+      const bool sh = a.jobs[j].pos == kSharedJob;
+      const int N = pass == 0 ? a.jobs[j].I : a.hidden;
+      const int M = a.jobs[j].q1 - a.jobs[j].q0;
       tiles += ((M + bm - 1) / bm) * (N / kBN) * ((pass == 1 && sh) ? a.ksplit : 1);
     }
     if (tiles >= 256 || bm == 64) return bm;

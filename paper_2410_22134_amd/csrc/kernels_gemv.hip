@@ -149,35 +149,34 @@ __global__ __launch_bounds__(kThreads) void k_rows_gemv(RowsArgs a) {
 // token vectors' 16-byte pieces for its own k positions in registers and issues
 // all of its weight loads (RWxNCH rows x 16 B, about 16 per lane) before the
 // first FMA, so each wave keeps ~16 KiB of weights in flight.  A block is four
-// independent waves; the grid is a flat list of (job, row tile) blocks over
-// all experts of the launch (route positions and the shared expert).
+// independent waves.  The grid is (row tile, job): every job -- a route
+// position, or a piece of the shared expert's rows -- spans the same number of
+// row tiles, and a block finds its job's fields with independent scalar loads
+// from the kernel arguments, so its first weight load waits for one round trip
+// only (a search over the jobs, or a byte-sized field read through the vector
+// memory path, would chain several before any weight is requested).
 constexpr int kBlockWaves = 4;
-
-__device__ __forceinline__ int find_job(const FfnArgs& a, int bid) {
-  int lo = 0, hi = a.n_jobs - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (a.job_tile0[mid] <= bid) lo = mid;
-    else hi = mid - 1;
-  }
-  return lo;
-}
 
 template <typename TW>
 struct Job {
   const TW* W;
-  int I, q0, q1;
+  int I, q0, q1, r0, r1;  // rows [r0, r1) of this job's piece
   bool shared;
 };
 
+// Everything a block needs from the kernel arguments, read before any branch so
+// the scalar loads issue together.
 template <typename TW>
-__device__ __forceinline__ Job<TW> job_of(const FfnArgs& a, int j) {
+__device__ __forceinline__ Job<TW> job_of(const FfnArgs& a, int nrows) {
+  const FfnJob jd = a.jobs[blockIdx.y];
   Job<TW> jb;
-  jb.shared = a.job_pos[j] == kSharedJob;
-  jb.W = reinterpret_cast<const TW*>(a.job_w[j]);
-  jb.I = jb.shared ? a.shared_inter : a.inter;
-  jb.q0 = a.job_q0[j];
-  jb.q1 = a.job_q1[j];
+  jb.shared = jd.pos == kSharedJob;
+  jb.W = reinterpret_cast<const TW*>(jd.w);
+  jb.I = jd.I;
+  jb.q0 = jd.q0;
+  jb.q1 = jd.q1;
+  jb.r0 = jd.r0;
+  jb.r1 = min(jd.r0 + a.piece_rows, nrows < 0 ? jd.I : nrows);
   return jb;
 }
 
@@ -237,30 +236,35 @@ template <typename TW, int MT, int NCH, int RW>
 __global__ __launch_bounds__(kThreads) void k_ffn_gateup(FfnArgs a) {
   constexpr int R = 2 * RW;
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const Job<TW> jb = job_of<TW>(a, -1);
+  const int H = a.hidden, I = jb.I, T = a.T, top_k = a.top_k;
+  const int32_t* perm = a.perm;
+  void* act_r = a.act;
+  void* act_s = a.act_sh;
+  const TW* xb = reinterpret_cast<const TW*>(a.x);
+  // materialise every argument here, so all of their loads issue together
+  asm volatile("" ::"s"(H), "s"(T), "s"(top_k), "s"(perm), "s"(act_r), "s"(act_s), "s"(xb), "s"(jb.W), "s"(jb.I),
+               "s"(jb.q0), "s"(jb.q1), "s"(jb.r1), "s"((int)jb.shared));
+  TW* act = reinterpret_cast<TW*>(jb.shared ? act_s : act_r);
   tclock_start(a);
-  const int j = find_job(a, blockIdx.x);
-  const Job<TW> jb = job_of<TW>(a, j);
-  const int i0 = ((blockIdx.x - a.job_tile0[j]) * kBlockWaves + wave) * RW;
-  if (i0 >= jb.I) return;
-  const int H = a.hidden, I = jb.I;
+  const int i0 = jb.r0 + (blockIdx.x * kBlockWaves + wave) * RW;
+  if (i0 >= jb.r1) return;
   const TW* rows[R];
   bool rv[R];
 #pragma unroll
   for (int r = 0; r < RW; ++r) {
-    const bool v = i0 + r < I;
+    const bool v = i0 + r < jb.r1;
     rv[2 * r] = rv[2 * r + 1] = v;
     rows[2 * r] = jb.W + (size_t)(v ? i0 + r : 0) * H;          // gate row
     rows[2 * r + 1] = jb.W + (size_t)(v ? I + i0 + r : 0) * H;  // up row
   }
-  TW* act = reinterpret_cast<TW*>(jb.shared ? a.act_sh : a.act);
-  const TW* xb = reinterpret_cast<const TW*>(a.x);
   for (int g = jb.q0; g < jb.q1; g += MT) {
     const int mt = min(MT, jb.q1 - g);
     const TW* xs[MT];
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
       const int q = g + min(m, mt - 1);
-      const int t = (jb.shared || a.T == 1) ? (jb.shared ? q : 0) : a.perm[q] / a.top_k;
+      const int t = (jb.shared || T == 1) ? (jb.shared ? q : 0) : perm[q] / top_k;
       xs[m] = xb + (size_t)t * H;
     }
     float acc[R][MT];
@@ -281,7 +285,7 @@ __global__ __launch_bounds__(kThreads) void k_ffn_gateup(FfnArgs a) {
 #pragma unroll
         for (int mm = 0; mm < MT; ++mm)
           if (rr == r && mm == m) { ga = acc[2 * rr][mm]; ub = acc[2 * rr + 1][mm]; }
-      if (m < mt && i0 + r < I) Elem<TW>::store(act, (g + m) * I + i0 + r, silu(ga) * ub);
+      if (m < mt && i0 + r < jb.r1) Elem<TW>::store(act, (g + m) * I + i0 + r, silu(ga) * ub);
     }
   }
   tclock_end(a);
@@ -291,21 +295,29 @@ __global__ __launch_bounds__(kThreads) void k_ffn_gateup(FfnArgs a) {
 template <typename TW, int MT, int NCH, int RW>
 __global__ __launch_bounds__(kThreads) void k_ffn_down(FfnArgs a) {
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-  tclock_start(a);
-  const int j = find_job(a, blockIdx.x);
-  const Job<TW> jb = job_of<TW>(a, j);
+  const Job<TW> jb = job_of<TW>(a, a.hidden);
   const int H = a.hidden, I = jb.I;
-  const int n0 = ((blockIdx.x - a.job_tile0[j]) * kBlockWaves + wave) * RW;
-  if (n0 >= H) return;
+  const void* act_r = a.act;
+  const void* act_s = a.act_sh;
+  float* y_r = a.Y;
+  float* y_s = a.Ysh;
+  const int32_t* perm = a.perm;
+  // materialise every argument here, so all of their loads issue together
+  asm volatile("" ::"s"(H), "s"(act_r), "s"(act_s), "s"(y_r), "s"(y_s), "s"(perm), "s"(jb.W), "s"(jb.I), "s"(jb.q0),
+               "s"(jb.q1), "s"(jb.r1), "s"((int)jb.shared));
+  const TW* actb = reinterpret_cast<const TW*>(jb.shared ? act_s : act_r);
+  float* Yb = jb.shared ? y_s : y_r;
+  tclock_start(a);
+  const int n0 = jb.r0 + (blockIdx.x * kBlockWaves + wave) * RW;
+  if (n0 >= jb.r1) return;
   const TW* Wd = jb.W + (size_t)2 * I * H;
   const TW* rows[RW];
   bool rv[RW];
 #pragma unroll
   for (int r = 0; r < RW; ++r) {
-    rv[r] = n0 + r < H;
+    rv[r] = n0 + r < jb.r1;
     rows[r] = Wd + (size_t)(rv[r] ? n0 + r : 0) * I;
   }
-  const TW* actb = reinterpret_cast<const TW*>(jb.shared ? a.act_sh : a.act);
   for (int g = jb.q0; g < jb.q1; g += MT) {
     const int mt = min(MT, jb.q1 - g);
     const TW* xs[MT];
@@ -331,7 +343,7 @@ __global__ __launch_bounds__(kThreads) void k_ffn_down(FfnArgs a) {
           if (rr == r && mm == m) v = acc[rr][mm];
       if (m < mt && rv[r]) {
         const int q = g + m;
-        float* Y = jb.shared ? a.Ysh + (size_t)q * H : a.Y + (size_t)a.perm[q] * H;
+        float* Y = Yb + (size_t)(jb.shared ? q : perm[q]) * H;
         Y[n0 + r] = v;
       }
     }
@@ -400,31 +412,57 @@ void launch_rows_gemv(const RowsArgs& a, int wdtype, int xdtype, hipStream_t s) 
 
 // (MT, NCH) pairs keep the registers per lane bounded: MT x NCH x 16 B of token
 // pieces plus R x NCH x 16 B of weights in flight.
+// Every job of a GEMV launch covers `piece_rows` rows: in pass 1 all H output
+// rows; in pass 0 the routed expert's I rows, the shared expert being split into
+// as many pieces of that size as the job table allows.
+static int gemv_jobs(const FfnArgs& in, int pass, FfnArgs& a) {
+  a = in;
+  if (pass == 1) {
+    for (int j = 0; j < a.n_jobs; ++j) a.jobs[j].r0 = 0;
+    a.piece_rows = a.hidden;
+    return a.n_jobs;
+  }
+  int n_routed = 0;
+  for (int j = 0; j < in.n_jobs; ++j) n_routed += in.jobs[j].pos != kSharedJob;
+  const bool has_shared = n_routed < in.n_jobs;
+  int P = n_routed ? in.inter : in.shared_inter;
+  int pieces = has_shared ? (in.shared_inter + P - 1) / P : 0;
+  if (pieces > kMaxJobs - n_routed) {
+    pieces = kMaxJobs - n_routed;
+    P = (in.shared_inter + pieces - 1) / pieces;
+  }
+  int n = 0;
+  for (int j = 0; j < in.n_jobs; ++j) {
+    const int np = in.jobs[j].pos == kSharedJob ? pieces : 1;
+    for (int p = 0; p < np; ++p, ++n) {
+      a.jobs[n] = in.jobs[j];
+      a.jobs[n].r0 = p * P;
+    }
+  }
+  a.n_jobs = n;
+  a.piece_rows = P;
+  return n;
+}
+
 template <typename TW, int MT>
-static void ffn_dispatch(FfnArgs& a, int pass, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+static void ffn_dispatch(const FfnArgs& in, int pass, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   constexpr int NCH = MT <= 2 ? 4 : (MT == 4 ? 2 : 1);
   constexpr int RWG = 2, RWD = 4;
   const int rows_per_block = kBlockWaves * (pass == 0 ? RWG : RWD);
-  int tiles = 0;
-  for (int j = 0; j < a.n_jobs; ++j) {
-    a.job_tile0[j] = tiles;
-    const int I = a.job_pos[j] == kSharedJob ? a.shared_inter : a.inter;
-    const int rows = pass == 0 ? I : a.hidden;
-    tiles += (rows + rows_per_block - 1) / rows_per_block;
-  }
-  a.job_tile0[a.n_jobs] = tiles;
-  if (tiles == 0) return;
+  FfnArgs a;
+  if (gemv_jobs(in, pass, a) == 0 || a.piece_rows <= 0) return;
+  const dim3 grid((a.piece_rows + rows_per_block - 1) / rows_per_block, a.n_jobs);
   if (ev0) {
-    if (pass == 0) hipExtLaunchKernelGGL(k_ffn_gateup<TW, MT, NCH, RWG>, dim3(tiles), dim3(kThreads), 0, s, ev0, ev1, 0, a);
-    else hipExtLaunchKernelGGL(k_ffn_down<TW, MT, NCH, RWD>, dim3(tiles), dim3(kThreads), 0, s, ev0, ev1, 0, a);
+    if (pass == 0) hipExtLaunchKernelGGL(k_ffn_gateup<TW, MT, NCH, RWG>, grid, dim3(kThreads), 0, s, ev0, ev1, 0, a);
+    else hipExtLaunchKernelGGL(k_ffn_down<TW, MT, NCH, RWD>, grid, dim3(kThreads), 0, s, ev0, ev1, 0, a);
   } else if (pass == 0) {
-    k_ffn_gateup<TW, MT, NCH, RWG><<<tiles, kThreads, 0, s>>>(a);
+    k_ffn_gateup<TW, MT, NCH, RWG><<<grid, kThreads, 0, s>>>(a);
   } else {
-    k_ffn_down<TW, MT, NCH, RWD><<<tiles, kThreads, 0, s>>>(a);
+    k_ffn_down<TW, MT, NCH, RWD><<<grid, kThreads, 0, s>>>(a);
   }
 }
 
-void launch_ffn(FfnArgs& a, int pass, int max_tokens, int dtype, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+void launch_ffn(const FfnArgs& a, int pass, int max_tokens, int dtype, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   const int mt = max_tokens >= 8 ? 8 : (max_tokens >= 4 ? 4 : (max_tokens >= 2 ? 2 : 1));
   if (dtype == 1) {
     if (mt == 8) ffn_dispatch<bf16_t, 8>(a, pass, s, ev0, ev1);

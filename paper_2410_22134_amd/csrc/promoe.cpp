@@ -933,15 +933,20 @@ int ffn_launch_one(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipSt
   a.n_jobs = (int)jobs.size();
   for (size_t i = 0; i < jobs.size(); ++i) {
     const bool sh = jobs[i] == kSharedJob;
-    a.job_pos[i] = (uint8_t)jobs[i];
+    FfnJob& jb = a.jobs[i];
+    jb.pos = jobs[i];
+    jb.r0 = 0;
+    jb.pad = 0;
     if (sh) {
-      a.job_w[i] = a.shared_w;
-      a.job_q0[i] = 0;
-      a.job_q1[i] = a.T;
+      jb.w = a.shared_w;
+      jb.q0 = 0;
+      jb.q1 = a.T;
+      jb.I = c->Ish;
     } else {
-      a.job_w[i] = c->cache + ((size_t)a.layer * c->C + rec.slot[jobs[i]]) * c->expert_bytes;
-      a.job_q0[i] = rec.offset[jobs[i]];
-      a.job_q1[i] = rec.offset[jobs[i] + 1];
+      jb.w = c->cache + ((size_t)a.layer * c->C + rec.slot[jobs[i]]) * c->expert_bytes;
+      jb.q0 = rec.offset[jobs[i]];
+      jb.q1 = rec.offset[jobs[i] + 1];
+      jb.I = c->I;
     }
     const int cnt = sh ? a.T : rec.count[jobs[i]];
     const double melems = (double)(sh ? c->Ish : c->I) * c->H;
