@@ -161,7 +161,7 @@ template <typename TW>
 struct Job {
   const TW* W;
   int I, q0, q1, r0, r1;  // rows [r0, r1) of this job's piece
-  bool shared;
+  int pos;                // route position, or kSharedJob
 };
 
 // Everything a block needs from the kernel arguments, read before any branch so
@@ -170,7 +170,7 @@ template <typename TW>
 __device__ __forceinline__ Job<TW> job_of(const FfnArgs& a, int nrows) {
   const FfnJob jd = a.jobs[blockIdx.y];
   Job<TW> jb;
-  jb.shared = jd.pos == kSharedJob;
+  jb.pos = jd.pos;
   jb.W = reinterpret_cast<const TW*>(jd.w);
   jb.I = jd.I;
   jb.q0 = jd.q0;
@@ -244,8 +244,9 @@ __global__ __launch_bounds__(kThreads) void k_ffn_gateup(FfnArgs a) {
   const TW* xb = reinterpret_cast<const TW*>(a.x);
   // materialise every argument here, so all of their loads issue together
   asm volatile("" ::"s"(H), "s"(T), "s"(top_k), "s"(perm), "s"(act_r), "s"(act_s), "s"(xb), "s"(jb.W), "s"(jb.I),
-               "s"(jb.q0), "s"(jb.q1), "s"(jb.r1), "s"((int)jb.shared));
-  TW* act = reinterpret_cast<TW*>(jb.shared ? act_s : act_r);
+               "s"(jb.q0), "s"(jb.q1), "s"(jb.r1), "s"(jb.pos));
+  const bool shared = jb.pos == kSharedJob;
+  TW* act = reinterpret_cast<TW*>(shared ? act_s : act_r);
   tclock_start(a);
   const int i0 = jb.r0 + (blockIdx.x * kBlockWaves + wave) * RW;
   if (i0 >= jb.r1) return;
@@ -264,7 +265,7 @@ __global__ __launch_bounds__(kThreads) void k_ffn_gateup(FfnArgs a) {
 #pragma unroll
     for (int m = 0; m < MT; ++m) {
       const int q = g + min(m, mt - 1);
-      const int t = (jb.shared || T == 1) ? (jb.shared ? q : 0) : perm[q] / top_k;
+      const int t = (shared || T == 1) ? (shared ? q : 0) : perm[q] / top_k;
       xs[m] = xb + (size_t)t * H;
     }
     float acc[R][MT];
@@ -304,9 +305,10 @@ __global__ __launch_bounds__(kThreads) void k_ffn_down(FfnArgs a) {
   const int32_t* perm = a.perm;
   // materialise every argument here, so all of their loads issue together
   asm volatile("" ::"s"(H), "s"(act_r), "s"(act_s), "s"(y_r), "s"(y_s), "s"(perm), "s"(jb.W), "s"(jb.I), "s"(jb.q0),
-               "s"(jb.q1), "s"(jb.r1), "s"((int)jb.shared));
-  const TW* actb = reinterpret_cast<const TW*>(jb.shared ? act_s : act_r);
-  float* Yb = jb.shared ? y_s : y_r;
+               "s"(jb.q1), "s"(jb.r1), "s"(jb.pos));
+  const bool shared = jb.pos == kSharedJob;
+  const TW* actb = reinterpret_cast<const TW*>(shared ? act_s : act_r);
+  float* Yb = shared ? y_s : y_r;
   tclock_start(a);
   const int n0 = jb.r0 + (blockIdx.x * kBlockWaves + wave) * RW;
   if (n0 >= jb.r1) return;
@@ -343,7 +345,7 @@ __global__ __launch_bounds__(kThreads) void k_ffn_down(FfnArgs a) {
           if (rr == r && mm == m) v = acc[rr][mm];
       if (m < mt && rv[r]) {
         const int q = g + m;
-        float* Y = Yb + (size_t)(jb.shared ? q : perm[q]) * H;
+        float* Y = Yb + (size_t)(shared ? q : perm[q]) * H;
         Y[n0 + r] = v;
       }
     }
@@ -447,7 +449,7 @@ static int gemv_jobs(const FfnArgs& in, int pass, FfnArgs& a) {
 template <typename TW, int MT>
 static void ffn_dispatch(const FfnArgs& in, int pass, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   constexpr int NCH = MT <= 2 ? 4 : (MT == 4 ? 2 : 1);
-  constexpr int RWG = 2, RWD = 4;
+  constexpr int RWG = 1, RWD = 2;
   const int rows_per_block = kBlockWaves * (pass == 0 ? RWG : RWD);
   FfnArgs a;
   if (gemv_jobs(in, pass, a) == 0 || a.piece_rows <= 0) return;
