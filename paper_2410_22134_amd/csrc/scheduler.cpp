@@ -72,7 +72,7 @@ void Prefetcher::issue_sub(int layer, int slot, int chunk, Prio prio, int64_t af
     retire();
   }
   int64_t seq = next_seq_++;
-  eng_->issue(seq, cache_ + slot_off, src, bytes, after);
+  eng_->issue(seq, cache_ + slot_off, src, bytes, after, queue_of(layer, slot));
   ch.n_issued++;
   ch.last = seq;
   st_.copies[prio]++;
@@ -132,7 +132,8 @@ void Prefetcher::issue_pending(int layer, int slot, int64_t after_compute, Prio 
     }
     const int64_t seq = next_seq_++;
     const size_t slot_off = ((size_t)layer * C_ + slot) * expert_bytes;
-    eng_->issue(seq, cache_ + slot_off + start, host_[layer * E_ + s.expert] + start, end - start, after);
+    eng_->issue(seq, cache_ + slot_off + start, host_[layer * E_ + s.expert] + start, end - start, after,
+                queue_of(layer, slot));
     st_.copies[prio]++;
     st_.bytes[prio] += (int64_t)(end - start);
     first = false;

@@ -13,7 +13,10 @@
 //     sub-copies that were already issued;
 //   * a copy into a slot waits for the last compute that read the slot
 //     (write-after-read), and compute waits for the copy of the chunk it reads
-//     (read-after-write) -- see ready_seq().
+//     (read-after-write) -- see ready_seq();
+//   * every copy into a slot goes to the same engine queue, so copies into one
+//     slot never overtake each other and the latest copy of a slot completes
+//     after all earlier ones (the engine may run several queues at once).
 //
 // No HIP here: the physical queue is a CopyEngine (HIP streams and events in
 // the library, a simulated clock in the CPU tests).  Not thread-safe; the
@@ -31,9 +34,12 @@ namespace promoe {
 class CopyEngine {
  public:
   virtual ~CopyEngine() = default;
-  // Enqueue copy number `seq` (consecutive from 0): wait for compute token
-  // `after_compute` (-1 none), then copy `bytes` from src to dst.
-  virtual void issue(int64_t seq, void* dst, const void* src, size_t bytes, int64_t after_compute) = 0;
+  // Enqueue copy number `seq` (consecutive from 0) on ordered queue `queue`
+  // (< queues()): wait for compute token `after_compute` (-1 none), then copy
+  // `bytes` from src to dst.  Copies of one queue complete in issue order;
+  // copies of different queues may overlap.
+  virtual void issue(int64_t seq, void* dst, const void* src, size_t bytes, int64_t after_compute, int queue) = 0;
+  virtual int queues() const { return 1; }
   virtual bool done(int64_t seq) = 0;  // non-blocking completion test
   virtual void wait(int64_t seq) = 0;  // block until copy `seq` completed
   // Most copies that may be in flight at once (bounded by the engine's event ring).
@@ -96,12 +102,14 @@ class Prefetcher {
   int window() const { return window_; }
 
   // Copy sequence number that a reader of chunks [0, upto] of the slot must
-  // wait for, -1 if they are all known complete, or -2 if some sub-copy has
-  // not been issued yet.
+  // wait for (on the slot's queue), -1 if they are all known complete, or -2 if
+  // some sub-copy has not been issued yet.
   int64_t ready_seq(int layer, int slot, int upto_chunk) const;
   // Record that compute token `tok` reads the slot.
   void set_last_read(int layer, int slot, int64_t tok);
   int expert_in(int layer, int slot) const { return slot_(layer, slot).expert; }
+  // Engine queue of every copy into the slot.
+  int queue_of(int layer, int slot) const { return (layer * C_ + slot) % eng_->queues(); }
 
   const PhysStats& stats() const { return st_; }
   void reset_stats() { st_ = PhysStats(); }

@@ -37,7 +37,11 @@ struct FakeEngine : CopyEngine {
   };
   std::vector<Copy> log;
   std::map<int64_t, double> compute_done;  // compute token -> completion time
-  void issue(int64_t seq, void* dst, const void*, size_t bytes, int64_t after) override {
+  int nq = 1;                      // queues reported to the scheduler (all run as one FIFO here)
+  std::vector<int> queue_of_copy;  // queue each copy was issued on
+  int queues() const override { return nq; }
+  void issue(int64_t seq, void* dst, const void*, size_t bytes, int64_t after, int queue) override {
+    queue_of_copy.push_back(queue);
     double start = now;
     if (!log.empty()) start = std::max(start, log.back().end);
     if (after >= 0) {
@@ -146,6 +150,37 @@ void test_whole_expert_low() {
     r.worker_until(100.0);
     CHECK(r.pf->stats().bytes[LOW] == 300 && r.pf->stats().copies[HIGH] == 0);
   }
+}
+
+// With several engine queues, every copy into one slot uses the same queue (so
+// copies into a slot stay ordered), and different slots spread over the queues.
+void test_queue_per_slot() {
+  Rig r(2, 4, 8, 100, 50, 2, 1000);
+  r.eng.nq = 2;
+  r.eng.bw = 100.0;
+  for (int s = 0; s < 4; ++s) {
+    r.pf->assign(0, s, s);
+    r.pf->push_low(0, s);
+  }
+  r.worker_until(2.0);
+  r.pf->assign(0, 1, 6);  // reassign slot 1 while its old copies may be queued
+  r.pf->issue_high(0, 1);
+  r.pf->assign(1, 2, 5);
+  r.pf->issue_high(1, 2);
+  r.worker_until(100.0);
+  std::map<uint8_t*, int> q_of_slot;
+  bool used[2] = {false, false};
+  for (size_t i = 0; i < r.eng.log.size(); ++i) {
+    const size_t off = r.eng.log[i].dst - r.cache.data();
+    uint8_t* slot_base = r.cache.data() + off / (3 * r.chunk) * (3 * r.chunk);
+    const int q = r.eng.queue_of_copy[i];
+    CHECK(q == 0 || q == 1);
+    used[q] = true;
+    auto it = q_of_slot.find(slot_base);
+    if (it == q_of_slot.end()) q_of_slot[slot_base] = q;
+    else CHECK(it->second == q);
+  }
+  CHECK(used[0] && used[1]);
 }
 
 // A high-priority copy waits for at most `window` already-issued low-priority
@@ -298,7 +333,7 @@ void test_high_merge_exhaustive() {
     struct C { size_t off, bytes; };
     std::vector<C> log;
     uint8_t* base = nullptr;
-    void issue(int64_t, void* d, const void*, size_t b, int64_t) override {
+    void issue(int64_t, void* d, const void*, size_t b, int64_t, int) override {
       log.push_back({(size_t)(static_cast<uint8_t*>(d) - base), b});
     }
     bool done(int64_t) override { return true; }
@@ -350,6 +385,7 @@ int main(int argc, char** argv) {
   }
   test_example();
   test_whole_expert_low();
+  test_queue_per_slot();
   test_window_bound();
   test_purge_dedupe_and_priority();
   test_ready_and_war();
