@@ -304,7 +304,7 @@ void worker_main(promoe_ctx* c) {
       ingest_spec(c, c->rec_ingested);
     c->pf->pump();
     const bool head_spec = c->rec_ingested < c->rec_pub && c->rec_kind[c->rec_ingested % kRecRing] == 0;
-    if (c->pf->has_low() && c->pf->in_flight() >= c->pf->window()) {
+    if (c->pf->has_low() && c->pf->low_in_flight() >= c->pf->window()) {
       const int64_t seq = c->pf->oldest_in_flight();
       hipEvent_t e = c->eng.event(seq);
       lk.unlock();

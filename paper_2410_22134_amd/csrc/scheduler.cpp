@@ -72,6 +72,7 @@ void Prefetcher::issue_sub(int layer, int slot, int chunk, Prio prio, int64_t af
     retire();
   }
   int64_t seq = next_seq_++;
+  note_issued(prio);
   eng_->issue(seq, cache_ + slot_off, src, bytes, after, queue_of(layer, slot));
   ch.n_issued++;
   ch.last = seq;
@@ -131,6 +132,7 @@ void Prefetcher::issue_pending(int layer, int slot, int64_t after_compute, Prio 
       retire();
     }
     const int64_t seq = next_seq_++;
+    note_issued(prio);
     const size_t slot_off = ((size_t)layer * C_ + slot) * expert_bytes;
     eng_->issue(seq, cache_ + slot_off + start, host_[layer * E_ + s.expert] + start, end - start, after,
                 queue_of(layer, slot));
@@ -167,7 +169,7 @@ void Prefetcher::issue_high_after(int layer, int slot, int64_t after_compute) {
 int Prefetcher::pump() {
   int n = 0;
   retire();
-  while (!low_.empty() && in_flight() < window_) {
+  while (!low_.empty() && low_in_flight_ < window_) {
     LowTask t = low_.front();
     Slot& s = slot_(t.layer, t.slot);
     Chunk& ch = s.ch[t.chunk];
@@ -191,8 +193,17 @@ int Prefetcher::pump() {
   return n;
 }
 
+void Prefetcher::note_issued(Prio prio) {
+  prio_of_.push_back((uint8_t)prio);
+  if (prio == LOW) ++low_in_flight_;
+}
+
 void Prefetcher::retire() {
-  while (retired_ < next_seq_ && eng_->done(retired_)) ++retired_;
+  while (retired_ < next_seq_ && eng_->done(retired_)) {
+    if (prio_of_.front() == LOW) --low_in_flight_;
+    prio_of_.pop_front();
+    ++retired_;
+  }
 }
 
 int64_t Prefetcher::ready_seq(int layer, int slot, int upto_chunk) const {

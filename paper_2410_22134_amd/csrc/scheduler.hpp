@@ -9,8 +9,10 @@
 // been copied into each slot and issues copies, one FIFO queue, so that:
 //   * high-priority copies are issued at once, in the order the route returns;
 //   * low-priority copies are issued one sub-copy at a time, at most `window`
-//     sub-copies in flight, so a high-priority copy waits for at most `window`
-//     sub-copies that were already issued;
+//     low-priority sub-copies in flight, so a high-priority copy waits for at
+//     most `window` of them; high-priority copies in flight do not hold them
+//     back (a prefetch then queues right behind the misses, keeping the link
+//     busy through the compute that follows);
 //   * a copy into a slot waits for the last compute that read the slot
 //     (write-after-read), and compute waits for the copy of the chunk it reads
 //     (read-after-write) -- see ready_seq();
@@ -89,7 +91,7 @@ class Prefetcher {
   // high-priority copy may wait for a whole expert).
   void set_whole_expert_low(bool on) { whole_low_ = on; }
 
-  // Issue low-priority sub-copies while fewer than `window` copies are in
+  // Issue low-priority sub-copies while fewer than `window` of them are in
   // flight.  Returns the number of tasks started.
   int pump();
   // Note completed copies (in FIFO order).
@@ -97,6 +99,7 @@ class Prefetcher {
 
   bool has_low() const { return !low_.empty(); }
   int64_t in_flight() const { return next_seq_ - retired_; }
+  int64_t low_in_flight() const { return low_in_flight_; }
   int64_t oldest_in_flight() const { return retired_ < next_seq_ ? retired_ : -1; }
   int64_t issued() const { return next_seq_; }
   int window() const { return window_; }
@@ -133,6 +136,7 @@ class Prefetcher {
   Slot& slot_(int l, int s) { return slots_[l * C_ + s]; }
   const Slot& slot_(int l, int s) const { return slots_[l * C_ + s]; }
   void issue_sub(int layer, int slot, int chunk, Prio prio, int64_t after_compute);
+  void note_issued(Prio prio);
   // Issue every pending sub-copy of the slot (coalesced when merge_ > 0),
   // dropping its queued low-priority tasks.
   void issue_pending(int layer, int slot, int64_t after_compute, Prio prio);
@@ -149,6 +153,8 @@ class Prefetcher {
   std::deque<LowTask> low_;
   int64_t next_seq_ = 0;
   int64_t retired_ = 0;  // copies [0, retired_) are known complete
+  std::deque<uint8_t> prio_of_;  // priority of each copy in [retired_, next_seq_)
+  int64_t low_in_flight_ = 0;
   PhysStats st_;
 };
 

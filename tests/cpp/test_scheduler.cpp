@@ -183,6 +183,26 @@ void test_queue_per_slot() {
   CHECK(used[0] && used[1]);
 }
 
+// High-priority copies in flight do not count against the low-priority window:
+// a prefetch queues right behind the misses, so the link has no idle gap
+// between them, and a later miss still waits for at most `window` of them.
+void test_low_queues_behind_high() {
+  Rig r(2, 4, 8, 100, 100, 2);
+  r.eng.bw = 100.0;
+  for (int s = 0; s < 3; ++s) {
+    r.pf->assign(0, s, s);
+    r.pf->issue_high(0, s);  // 9 chunks of misses, 9 time units
+  }
+  r.pf->assign(1, 0, 5);
+  r.pf->push_low(1, 0);
+  CHECK(r.pf->pump() == 2);  // two prefetch chunks queue behind the misses at once
+  CHECK(r.eng.log.size() == 11);
+  CHECK(std::fabs(r.eng.log[9].start - r.eng.log[8].end) < 1e-9);  // no gap after the misses
+  CHECK(r.pf->low_in_flight() == 2);
+  r.worker_until(100.0);
+  CHECK(r.pf->low_in_flight() == 0 && r.eng.log.size() == 12);
+}
+
 // A high-priority copy waits for at most `window` already-issued low-priority
 // sub-copies (earlier high-priority copies are drained before each miss).
 void test_window_bound() {
@@ -385,6 +405,7 @@ int main(int argc, char** argv) {
   }
   test_example();
   test_whole_expert_low();
+  test_low_queues_behind_high();
   test_queue_per_slot();
   test_window_bound();
   test_purge_dedupe_and_priority();
