@@ -51,11 +51,12 @@ def parse():
                    help="slots a predicted plan may fill: 0 no limit, n>0 the first n, -1 none")
     p.add_argument("--copy-calib-mib", type=int, default=1024,
                    help="size of the plain device copy run after the timed region (counter calibration)")
-    p.add_argument("--legs", default="decode,prefill,mfma,ablation",
-                   help="decode is always run (it is the reported value); add prefill, mfma, ablation")
+    p.add_argument("--legs", default="decode,prefill,mfma,ablation,sweep",
+                   help="decode is always run (it is the reported value); add prefill, mfma, ablation, sweep")
     p.add_argument("--prefill-steps", type=int, default=3)
     p.add_argument("--prefill-warmup", type=int, default=1)
     p.add_argument("--ablation-steps", type=int, default=32)
+    p.add_argument("--sweep-steps", type=int, default=24)
     return p.parse_args()
 
 
@@ -259,6 +260,51 @@ def leg_ablation(torch, args):
     return out
 
 
+def leg_sweep(torch, args):
+    """Cache-rate sweep (25-90% of the experts cached, batch 1) and batch sweep
+    (1-8 tokens per step at 50%) of the DeepSeek-MoE-16B-shaped decode, for the
+    method (fill limit as configured) and reactive LRU, on one model."""
+    import numpy as np
+    from synth import configs, model as sm
+    from paper_2410_22134_amd import FLAG_NO_PREFETCH, FLAG_PROFILE
+    from paper_2410_22134_amd.model import SyntheticModel
+    from paper_2410_22134_amd.stack import Stack
+    cfg = configs.C2
+    E, warm, steps = cfg.n_experts, 4, args.sweep_steps
+    model = SyntheticModel(cfg, max_tokens=8, gen_threads=8)
+    out = {"cache_rate": [], "batch": []}
+
+    def one(T, slots, flags, lim):
+        model.open(flags=flags | FLAG_PROFILE, spec_fill_limit=lim, slots=slots)
+        st = Stack(model, T)
+        h = torch.from_numpy(np.stack([sm.stack_input(cfg, 4000 + i, T) for i in range(warm + steps)])).cuda()
+        dt, s = run_steps(torch, model, st, h, warm, steps)
+        copied = s["bytes_high"] + s["bytes_low"]
+        r = {"tok_s": round(T * steps / dt, 2), "copied_GB_per_step": round(copied / steps / 1e9, 3),
+             "hit_rate": round(s["hit"] / max(1, s["prec_access"]), 4),
+             "overlap": overlap_metrics(s, dt, 56.7), "prediction": prediction_metrics(s)}
+        return r
+    try:
+        for frac in (0.25, 0.5, 0.75, 0.9):
+            C = int(round(frac * E))
+            row = {"cached": f"{C}/{E}"}
+            for mode, flags, lim in (("method", 0, args.spec_fill_limit), ("reactive", FLAG_NO_PREFETCH, 0)):
+                row[mode] = one(1, C, flags, lim)
+            print(f"[bench] sweep cache {C}/{E}: {row['method']['tok_s']} / {row['reactive']['tok_s']} tok/s",
+                  file=sys.stderr, flush=True)
+            out["cache_rate"].append(row)
+        for T in (1, 2, 4, 8):
+            row = {"batch": T}
+            for mode, flags, lim in (("method", 0, args.spec_fill_limit), ("reactive", FLAG_NO_PREFETCH, 0)):
+                row[mode] = one(T, E // 2, flags, lim)
+            print(f"[bench] sweep batch {T}: {row['method']['tok_s']} / {row['reactive']['tok_s']} tok/s",
+                  file=sys.stderr, flush=True)
+            out["batch"].append(row)
+    finally:
+        model.close()
+    return out
+
+
 def leg_mfma(torch, args):
     """Shared-expert GEMMs at the Qwen2-57B-A14B shape (hidden 3584, shared I = 20480),
     1024-token prefill, two layers with every expert resident (compute only)."""
@@ -378,6 +424,9 @@ def main():
     if "ablation" in args.legs:
         print("[bench] ablation leg", file=sys.stderr, flush=True)
         out["detail"]["ablation"] = leg_ablation(torch, args)
+    if "sweep" in args.legs:
+        print("[bench] sweep leg", file=sys.stderr, flush=True)
+        out["detail"]["sweep"] = leg_sweep(torch, args)
     if "mfma" in args.legs:
         print("[bench] shared-expert MFMA leg", file=sys.stderr, flush=True)
         out["roofline_prefill_gemm"] = leg_mfma(torch, args)

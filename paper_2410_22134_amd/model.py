@@ -69,12 +69,20 @@ class SyntheticModel:
         self.ctx = None
         self.open(flags, window, subchunk, spec_fill_limit, warm)
 
-    def open(self, flags=0, window=0, subchunk=0, spec_fill_limit=0, warm=True):
-        """(Re)create the context over the same weights and cache region, e.g. to
-        run another cache policy; the cache starts over from the warm set."""
-        cfg, L, E, eb = self.cfg, self.cfg.n_layers, self.cfg.n_experts, self.cfg.expert_bytes
+    def open(self, flags=0, window=0, subchunk=0, spec_fill_limit=0, warm=True, slots=None):
+        """(Re)create the context over the same weights, e.g. to run another cache
+        policy or (slots=...) another cache size; the cache starts over from the
+        warm set."""
+        import torch
         if self.ctx is not None:
             self.ctx.close()
+            self.ctx = None
+        if slots is not None and slots != self.cfg.slots:
+            self.cfg = self.cfg.with_(slots=slots)
+            self.cache = None
+            self.cache = torch.empty(self.cfg.n_layers * slots * self.cfg.expert_bytes, dtype=torch.uint8,
+                                     device=self.device)
+        cfg, L, E, eb = self.cfg, self.cfg.n_layers, self.cfg.n_experts, self.cfg.expert_bytes
         self.ctx = Context(lib_config(cfg, self.max_tokens, flags, window, subchunk, spec_fill_limit),
                            self.cache.data_ptr(), self.cache.numel())
         for l in range(L):
