@@ -57,6 +57,9 @@ def parse():
     p.add_argument("--prefill-warmup", type=int, default=1)
     p.add_argument("--ablation-steps", type=int, default=32)
     p.add_argument("--sweep-steps", type=int, default=24)
+    p.add_argument("--train-steps", type=int, default=128, help="predtrain leg: trace steps of 512 tokens")
+    p.add_argument("--train-epochs", type=int, default=16)
+    p.add_argument("--train-lr", type=float, default=3e-4)
     return p.parse_args()
 
 
@@ -305,6 +308,67 @@ def leg_sweep(torch, args):
     return out
 
 
+def leg_predtrain(torch, args):
+    """Offline predictor training on synthetic traces (DeepSeek-MoE-16B shape):
+    traces from the library's forward pass with every expert resident, 9:1
+    split, look-ahead 1 and 2; then the decode workload (50% cached) with the
+    trained look-ahead-1 predictors against the constructed ones."""
+    import numpy as np
+    from synth import configs, model as sm
+    from paper_2410_22134_amd import FLAG_PROFILE
+    from paper_2410_22134_amd import train_predictor as tp
+    from paper_2410_22134_amd.model import SyntheticModel
+    from paper_2410_22134_amd.stack import Stack
+    cfg = configs.C2
+    T = 512
+    model = SyntheticModel(cfg.with_(slots=cfg.n_experts), max_tokens=T, gen_threads=8)
+    out = {"trace_tokens": args.train_steps * T}
+    try:
+        t0 = time.perf_counter()
+        xs, ids = tp.collect_traces(model, args.train_steps, T)
+        out["trace_s"] = round(time.perf_counter() - t0, 1)
+        trained = {}
+        for d in (1, 2):
+            t0 = time.perf_counter()
+            res = tp.train_all(model, xs, ids, d, epochs=args.train_epochs, lr=args.train_lr)
+            a0 = [m["acc_start"] for _, _, m in res.values()]
+            a1 = [m["acc_trained"] for _, _, m in res.values()]
+            out[f"lookahead_{d}"] = {
+                "layers": len(res), "train_s": round(time.perf_counter() - t0, 1),
+                "heldout_acc_constructed": {"mean": round(float(np.mean(a0)), 4), "min": round(float(np.min(a0)), 4),
+                                            "max": round(float(np.max(a0)), 4)},
+                "heldout_acc_trained": {"mean": round(float(np.mean(a1)), 4), "min": round(float(np.min(a1)), 4),
+                                        "max": round(float(np.max(a1)), 4)},
+                "train_split_acc_trained_mean": round(float(np.mean([m["acc_train"] for _, _, m in res.values()])), 4),
+                "per_layer_trained": [round(x, 3) for x in a1]}
+            print(f"[bench] predtrain d={d}: held-out accuracy {np.mean(a0):.3f} -> {np.mean(a1):.3f} (train split "
+                  f"{out[f'lookahead_{d}']['train_split_acc_trained_mean']:.3f})",
+                  file=sys.stderr, flush=True)
+            trained[d] = res
+        del xs, ids
+        # runtime: decode at 50% cached, constructed vs trained look-ahead-1 predictors
+        st = Stack(model, 1)
+        n = 4 + args.sweep_steps * 2
+        h = torch.from_numpy(np.stack([sm.stack_input(cfg, 6000 + i, 1) for i in range(n)])).cuda()
+        runtime = {}
+        for name in ("constructed", "trained"):
+            if name == "trained":
+                tp.install(model, trained[1])
+            for lim in (args.spec_fill_limit, 0):
+                model.open(flags=FLAG_PROFILE, spec_fill_limit=lim, slots=cfg.n_experts // 2)
+                dt, s = run_steps(torch, model, st, h, 4, n - 4)
+                runtime[f"{name}_fill_limit_{lim}"] = {"tok_s": round((n - 4) / dt, 2),
+                                                       "hit_rate": round(s["hit"] / max(1, s["prec_access"]), 4),
+                                                       "prediction": prediction_metrics(s)}
+                print(f"[bench] predtrain runtime {name} limit {lim}: {runtime[f'{name}_fill_limit_{lim}']['tok_s']}"
+                      f" tok/s, accuracy {runtime[f'{name}_fill_limit_{lim}']['prediction']['accuracy']}",
+                      file=sys.stderr, flush=True)
+        out["decode_50pct"] = runtime
+    finally:
+        model.close()
+    return out
+
+
 def leg_mfma(torch, args):
     """Shared-expert GEMMs at the Qwen2-57B-A14B shape (hidden 3584, shared I = 20480),
     1024-token prefill, two layers with every expert resident (compute only)."""
@@ -427,6 +491,9 @@ def main():
     if "sweep" in args.legs:
         print("[bench] sweep leg", file=sys.stderr, flush=True)
         out["detail"]["sweep"] = leg_sweep(torch, args)
+    if "predtrain" in args.legs:
+        print("[bench] predictor training leg", file=sys.stderr, flush=True)
+        out["detail"]["predictor_training"] = leg_predtrain(torch, args)
     if "mfma" in args.legs:
         print("[bench] shared-expert MFMA leg", file=sys.stderr, flush=True)
         out["roofline_prefill_gemm"] = leg_mfma(torch, args)
