@@ -55,6 +55,7 @@ typedef enum {
 } promoe_err;
 
 enum { PROMOE_F32 = 0, PROMOE_BF16 = 1 };
+enum { PROMOE_WEIGHTS_DENSE = 0, PROMOE_WEIGHTS_INT4 = 1 };
 enum { PROMOE_PRIO_LOW = 0, PROMOE_PRIO_HIGH = 1 };
 
 /* flags.  The NO_* switches turn off one technique each, for the paper's
@@ -111,6 +112,16 @@ typedef struct promoe_config {
                                 low-priority copies start before the layer's route
                                 when the host link is the bottleneck.  Lists passed to
                                 promoe_prefetch are never limited.  -1..64. */
+  int32_t weight_format;     /* Storage of the routed experts (host copies and cache
+                                slots alike).  PROMOE_WEIGHTS_DENSE: dtype elements.
+                                PROMOE_WEIGHTS_INT4: 4-bit codes for models quantised to
+                                four bits (the paper's larger models, Sec. "Evaluation"):
+                                each matrix of R rows and reduction length K is R x K/2
+                                bytes of codes, row-major, two per byte (even k in the
+                                low nibble), then R x K/128 bf16 scales, row-major; the
+                                weight at (r, k) is (code - 8) * scale[r][k / 128].
+                                Needs dtype bf16 and hidden, inter multiples of 128.
+                                Gates, predictors and shared experts stay in dtype. */
 } promoe_config;
 
 typedef struct promoe_stats {

@@ -10,6 +10,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("PROMOE_LIB", os.path.join(HERE, "libpromoe.so"))
 
 PROMOE_F32, PROMOE_BF16 = 0, 1
+WEIGHTS_DENSE, WEIGHTS_INT4 = 0, 1
 PRIO_LOW, PRIO_HIGH = 0, 1
 FLAG_PROFILE, FLAG_NO_PREFETCH, FLAG_NO_CHUNK, FLAG_NO_PREEMPT, FLAG_NO_REORDER, FLAG_STATIC = 1, 2, 4, 8, 16, 32
 
@@ -21,7 +22,7 @@ class Config(ctypes.Structure):
                 ("shared_inter", _i32), ("shared_gate", _i32), ("renorm", _i32), ("router_bias", _i32),
                 ("slots_per_layer", _i32), ("lookahead", _i32), ("pred_hidden", _i32), ("max_tokens", _i32),
                 ("dtype", _i32), ("copy_subchunk_bytes", _i64), ("copy_window", _i32), ("flags", _i32),
-                ("spec_fill_limit", _i32)]
+                ("spec_fill_limit", _i32), ("weight_format", _i32)]
 
 
 STAT_COUNTERS = ("prec_access", "hit", "miss", "spec_issued", "spec_resident", "spec_used", "spec_wasted", "evict",

@@ -24,6 +24,7 @@ struct RowsArgs {
 // Expert FFN launch: a list of jobs (route positions, or the shared expert),
 // each job split into row tiles; block b runs tile b - job_tile0[j] of the job
 // j with job_tile0[j] <= b < job_tile0[j + 1].
+constexpr int kInt4Group = 128;  // 4-bit expert storage: codes per bf16 scale
 constexpr int kMaxJobs = 80;  // 64 route positions + pieces of the shared expert
 // Launch clock slot: word 0 = max of ~start over the first blocks (so ~word0 is
 // the earliest start), then kTclkLines 128-byte lines whose first words hold
@@ -61,6 +62,7 @@ struct FfnArgs {
   float* Ysh;                 // [T x H]
   int n_jobs;
   int piece_rows;             // GEMV: rows per piece; the shared expert spans several pieces
+  int q4;                     // routed experts stored as 4-bit codes (then bf16 scales)
   int ksplit;                   // split-K slices of the shared expert's down GEMM (>= 1)
   int64_t ysh_split_stride;     // elements between the slices' partial outputs in Ysh
   unsigned long long* tclock;   // optional launch clock slot (see kTclkWords), zero-initialised

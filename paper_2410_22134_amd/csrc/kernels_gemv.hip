@@ -353,6 +353,197 @@ __global__ __launch_bounds__(kThreads) void k_ffn_down(FfnArgs a) {
   tclock_end(a);
 }
 
+// ============================================================ 4-bit experts
+// Dequantising GEMVs for experts stored as 4-bit codes: a matrix of R rows and
+// reduction length K is R x K/2 bytes of codes (two per byte, even k in the low
+// nibble) followed by R x K/128 bf16 scales; weight (r, k) = (code - 8) *
+// scale[r][k / 128].  A lane takes 16-byte pieces of a row (32 weights, a
+// quarter of a scale group); per piece and token it forms sum(code * x) and
+// sum(x) and adds scale * (sum(code * x) - 8 sum(x)) to the row's accumulator.
+// Codes go to floats once per row and piece and serve every token of the group.
+
+struct Q4Row {
+  const uint8_t* codes;  // row start in the code block
+  const bf16_t* scales;  // row start in the scale block
+};
+
+__device__ __forceinline__ Q4Row q4_row(const uint8_t* mat, int rows, int K, int r) {
+  Q4Row q;
+  q.codes = mat + (size_t)r * (K / 2);
+  q.scales = reinterpret_cast<const bf16_t*>(mat + (size_t)rows * (K / 2)) + (size_t)r * (K / kInt4Group);
+  return q;
+}
+
+// acc[r][m] += <row r, xs[m]> over K for R rows of one matrix.
+template <int R, int MT>
+__device__ __forceinline__ void wave_rows_dot_q4(const Q4Row (&rows)[R], const bool (&rv)[R],
+                                                 const bf16_t* const (&xs)[MT], int mt, int K, int lane,
+                                                 float (&acc)[R][MT]) {
+  const int np = K / 32;  // 16-byte pieces per row
+  for (int c = lane; c < np; c += kWave) {
+    uint4 w[R];
+    float sc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      w[r] = rv[r] ? ld16_stream(rows[r].codes + (size_t)c * 16) : make_uint4(0x88888888u, 0x88888888u, 0x88888888u,
+                                                                             0x88888888u);
+      sc[r] = rv[r] ? bf16_to_f32(rows[r].scales[c / 4]) : 0.0f;
+    }
+    // token pieces: 32 bf16 = 16 words; word j holds elements 2j (low half) and 2j+1
+    uint32_t xw[MT][16];
+    float sx[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      const uint4* xp = reinterpret_cast<const uint4*>(xs[m] + (size_t)c * 32);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const uint4 u = (m < mt) ? xp[v] : make_uint4(0, 0, 0, 0);
+        xw[m][4 * v] = u.x; xw[m][4 * v + 1] = u.y; xw[m][4 * v + 2] = u.z; xw[m][4 * v + 3] = u.w;
+      }
+      float s = 0.0f;
+#pragma unroll
+      for (int j = 0; j < 16; ++j) s += __uint_as_float(xw[m][j] << 16) + __uint_as_float(xw[m][j] & 0xFFFF0000u);
+      sx[m] = s;
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const uint32_t ww[4] = {w[r].x, w[r].y, w[r].z, w[r].w};
+      float cf[32];  // codes of elements 0..31 of the piece
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const uint32_t lo = ww[i] & 0x0F0F0F0Fu, hi = (ww[i] >> 4) & 0x0F0F0F0Fu;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          cf[8 * i + 2 * b] = (float)((lo >> (8 * b)) & 0xFFu);
+          cf[8 * i + 2 * b + 1] = (float)((hi >> (8 * b)) & 0xFFu);
+        }
+      }
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        float t = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          t = fmaf(cf[2 * j], __uint_as_float(xw[m][j] << 16), t);
+          t = fmaf(cf[2 * j + 1], __uint_as_float(xw[m][j] & 0xFFFF0000u), t);
+        }
+        acc[r][m] = fmaf(sc[r], t - 8.0f * sx[m], acc[r][m]);
+      }
+    }
+  }
+}
+
+// pass 1, 4-bit experts: act[q][i] for the wave's RW rows i (gate rows, up rows)
+template <int MT, int RW>
+__global__ __launch_bounds__(kThreads) void k_ffn_gateup_q4(FfnArgs a) {
+  constexpr int R = 2 * RW;
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const Job<bf16_t> jb = job_of<bf16_t>(a, -1);
+  const int H = a.hidden, I = jb.I, T = a.T, top_k = a.top_k;
+  const int32_t* perm = a.perm;
+  bf16_t* act = reinterpret_cast<bf16_t*>(a.act);
+  const bf16_t* xb = reinterpret_cast<const bf16_t*>(a.x);
+  // materialise every argument here, so all of their loads issue together
+  asm volatile("" ::"s"(H), "s"(T), "s"(top_k), "s"(perm), "s"(act), "s"(xb), "s"(jb.W), "s"(jb.I), "s"(jb.q0),
+               "s"(jb.q1), "s"(jb.r1));
+  tclock_start(a);
+  const int i0 = jb.r0 + (blockIdx.x * kBlockWaves + wave) * RW;
+  if (i0 >= jb.r1) return;
+  const uint8_t* base = reinterpret_cast<const uint8_t*>(jb.W);
+  const size_t mat = (size_t)I * H / 2 + (size_t)I * (H / kInt4Group) * 2;
+  Q4Row rows[R];
+  bool rv[R];
+#pragma unroll
+  for (int r = 0; r < RW; ++r) {
+    const bool v = i0 + r < jb.r1;
+    rv[2 * r] = rv[2 * r + 1] = v;
+    rows[2 * r] = q4_row(base, I, H, v ? i0 + r : 0);            // gate row
+    rows[2 * r + 1] = q4_row(base + mat, I, H, v ? i0 + r : 0);  // up row
+  }
+  for (int g = jb.q0; g < jb.q1; g += MT) {
+    const int mt = min(MT, jb.q1 - g);
+    const bf16_t* xs[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) {
+      const int q = g + min(m, mt - 1);
+      const int t = T == 1 ? 0 : perm[q] / top_k;
+      xs[m] = xb + (size_t)t * H;
+    }
+    float acc[R][MT];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int m = 0; m < MT; ++m) acc[r][m] = 0.0f;
+    wave_rows_dot_q4<R, MT>(rows, rv, xs, mt, H, lane, acc);
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int m = 0; m < MT; ++m) acc[r][m] = wave_sum(acc[r][m]);
+    if (lane < RW * MT) {
+      const int r = lane % RW, m = lane / RW;
+      float ga = 0.0f, ub = 0.0f;
+#pragma unroll
+      for (int rr = 0; rr < RW; ++rr)
+#pragma unroll
+        for (int mm = 0; mm < MT; ++mm)
+          if (rr == r && mm == m) { ga = acc[2 * rr][mm]; ub = acc[2 * rr + 1][mm]; }
+      if (m < mt && i0 + r < jb.r1) Elem<bf16_t>::store(act, (g + m) * I + i0 + r, silu(ga) * ub);
+    }
+  }
+  tclock_end(a);
+}
+
+// pass 2, 4-bit experts: Y[pair][n] = Wd[n] . act[q] for the wave's RW rows n
+template <int MT, int RW>
+__global__ __launch_bounds__(kThreads) void k_ffn_down_q4(FfnArgs a) {
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const Job<bf16_t> jb = job_of<bf16_t>(a, a.hidden);
+  const int H = a.hidden, I = jb.I;
+  const bf16_t* actb = reinterpret_cast<const bf16_t*>(a.act);
+  float* Y = a.Y;
+  const int32_t* perm = a.perm;
+  // materialise every argument here, so all of their loads issue together
+  asm volatile("" ::"s"(H), "s"(actb), "s"(Y), "s"(perm), "s"(jb.W), "s"(jb.I), "s"(jb.q0), "s"(jb.q1), "s"(jb.r1));
+  tclock_start(a);
+  const int n0 = jb.r0 + (blockIdx.x * kBlockWaves + wave) * RW;
+  if (n0 >= jb.r1) return;
+  const uint8_t* base = reinterpret_cast<const uint8_t*>(jb.W);
+  const size_t mat = (size_t)I * H / 2 + (size_t)I * (H / kInt4Group) * 2;
+  Q4Row rows[RW];
+  bool rv[RW];
+#pragma unroll
+  for (int r = 0; r < RW; ++r) {
+    rv[r] = n0 + r < jb.r1;
+    rows[r] = q4_row(base + 2 * mat, H, I, rv[r] ? n0 + r : 0);
+  }
+  for (int g = jb.q0; g < jb.q1; g += MT) {
+    const int mt = min(MT, jb.q1 - g);
+    const bf16_t* xs[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m) xs[m] = actb + (size_t)(g + min(m, mt - 1)) * I;
+    float acc[RW][MT];
+#pragma unroll
+    for (int r = 0; r < RW; ++r)
+#pragma unroll
+      for (int m = 0; m < MT; ++m) acc[r][m] = 0.0f;
+    wave_rows_dot_q4<RW, MT>(rows, rv, xs, mt, I, lane, acc);
+#pragma unroll
+    for (int r = 0; r < RW; ++r)
+#pragma unroll
+      for (int m = 0; m < MT; ++m) acc[r][m] = wave_sum(acc[r][m]);
+    if (lane < RW * MT) {
+      const int r = lane % RW, m = lane / RW;
+      float v = 0.0f;
+#pragma unroll
+      for (int rr = 0; rr < RW; ++rr)
+#pragma unroll
+        for (int mm = 0; mm < MT; ++mm)
+          if (rr == r && mm == m) v = acc[rr][mm];
+      if (m < mt && rv[r]) Y[(size_t)perm[g + m] * H + n0 + r] = v;
+    }
+  }
+  tclock_end(a);
+}
+
 // ============================================================ combine
 template <typename TY>
 __global__ __launch_bounds__(kThreads) void k_combine(CombineArgs a) {
@@ -446,6 +637,19 @@ static int gemv_jobs(const FfnArgs& in, int pass, FfnArgs& a) {
   return n;
 }
 
+// 4-bit experts (routed jobs only): rows per wave shrink as the token group grows,
+// keeping registers bounded (token pieces MT x 16 words, accumulators R x MT).
+template <int MT>
+static void ffn_dispatch_q4(const FfnArgs& in, int pass, hipStream_t s) {
+  constexpr int RWG = MT <= 2 ? 8 : (MT == 4 ? 4 : 2), RWD = 2 * RWG;
+  const int rows_per_block = kBlockWaves * (pass == 0 ? RWG : RWD);
+  FfnArgs a;
+  if (gemv_jobs(in, pass, a) == 0 || a.piece_rows <= 0) return;
+  const dim3 grid((a.piece_rows + rows_per_block - 1) / rows_per_block, a.n_jobs);
+  if (pass == 0) k_ffn_gateup_q4<MT, RWG><<<grid, kThreads, 0, s>>>(a);
+  else k_ffn_down_q4<MT, RWD><<<grid, kThreads, 0, s>>>(a);
+}
+
 template <typename TW, int MT>
 static void ffn_dispatch(const FfnArgs& in, int pass, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   constexpr int NCH = MT <= 2 ? 4 : (MT == 4 ? 2 : 1);
@@ -466,6 +670,13 @@ static void ffn_dispatch(const FfnArgs& in, int pass, hipStream_t s, hipEvent_t 
 
 void launch_ffn(const FfnArgs& a, int pass, int max_tokens, int dtype, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   const int mt = max_tokens >= 8 ? 8 : (max_tokens >= 4 ? 4 : (max_tokens >= 2 ? 2 : 1));
+  if (a.q4) {
+    if (mt == 8) ffn_dispatch_q4<8>(a, pass, s);
+    else if (mt == 4) ffn_dispatch_q4<4>(a, pass, s);
+    else if (mt == 2) ffn_dispatch_q4<2>(a, pass, s);
+    else ffn_dispatch_q4<1>(a, pass, s);
+    return;
+  }
   if (dtype == 1) {
     if (mt == 8) ffn_dispatch<bf16_t, 8>(a, pass, s, ev0, ev1);
     else if (mt == 4) ffn_dispatch<bf16_t, 4>(a, pass, s, ev0, ev1);

@@ -108,6 +108,7 @@ struct promoe_ctx {
   promoe_config cfg{};
   int dev = 0;
   int L, H, E, K, I, Ish, C, D, Ph, maxT, dt, eb;
+  bool q4 = false;  // routed experts stored as 4-bit codes
   size_t chunk_bytes, expert_bytes;
   uint8_t* cache = nullptr;
 
@@ -467,10 +468,16 @@ const char* promoe_strerror(int err) {
 
 const char* promoe_last_error_string(void) { return g_last_error.c_str(); }
 
+// Bytes of one stored expert matrix (I x H elements).
+static size_t matrix_bytes(const promoe_config* cfg) {
+  const size_t n = (size_t)cfg->inter * (size_t)cfg->hidden;
+  if (cfg->weight_format == PROMOE_WEIGHTS_INT4) return n / 2 + (n / kInt4Group) * 2;
+  return n * (cfg->dtype == PROMOE_BF16 ? 2 : 4);
+}
+
 size_t promoe_expert_bytes(const promoe_config* cfg) {
   if (!cfg) return 0;
-  const size_t eb = cfg->dtype == PROMOE_BF16 ? 2 : 4;
-  return 3 * (size_t)cfg->inter * (size_t)cfg->hidden * eb;
+  return 3 * matrix_bytes(cfg);
 }
 
 int promoe_host_alloc(size_t bytes, void** out) {
@@ -494,12 +501,15 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   if (g.n_layers < 1 || g.hidden < 8 || g.inter < 8 || g.n_experts < 1 || g.top_k < 1 ||
       g.slots_per_layer < 1 || g.max_tokens < 1 || g.lookahead < 0 || g.pred_hidden < 0 || g.shared_inter < 0 ||
       (g.dtype != PROMOE_F32 && g.dtype != PROMOE_BF16) || g.top_k > g.n_experts || g.spec_fill_limit < -1 ||
-      g.spec_fill_limit > 64 || ((g.flags & PROMOE_FLAG_STATIC) && g.slots_per_layer < 3)) {
+      g.spec_fill_limit > 64 || ((g.flags & PROMOE_FLAG_STATIC) && g.slots_per_layer < 3) ||
+      (g.weight_format != PROMOE_WEIGHTS_DENSE && g.weight_format != PROMOE_WEIGHTS_INT4)) {
     g_last_error = "invalid config";
     return PROMOE_EINVAL;
   }
   if (g.n_experts > kMaxE || g.slots_per_layer > 64 || g.top_k > kMaxK || g.hidden % 8 || g.inter % 8 ||
-      g.shared_inter % 8 || (int64_t)g.max_tokens * g.top_k > 8192) {
+      g.shared_inter % 8 || (int64_t)g.max_tokens * g.top_k > 8192 ||
+      (g.weight_format == PROMOE_WEIGHTS_INT4 &&
+       (g.dtype != PROMOE_BF16 || g.hidden % kInt4Group || g.inter % kInt4Group))) {
     g_last_error = "unsupported shape";
     return PROMOE_EUNSUP;
   }
@@ -514,7 +524,8 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   c->L = g.n_layers; c->H = g.hidden; c->E = g.n_experts; c->K = g.top_k; c->I = g.inter;
   c->Ish = g.shared_inter; c->C = g.slots_per_layer; c->D = g.lookahead; c->Ph = g.pred_hidden;
   c->maxT = g.max_tokens; c->dt = g.dtype; c->eb = g.dtype == PROMOE_BF16 ? 2 : 4;
-  c->chunk_bytes = (size_t)c->I * c->H * c->eb;
+  c->q4 = g.weight_format == PROMOE_WEIGHTS_INT4;
+  c->chunk_bytes = matrix_bytes(&g);
   c->expert_bytes = 3 * c->chunk_bytes;
   c->cache = static_cast<uint8_t*>(d_cache);
   c->profile = (g.flags & PROMOE_FLAG_PROFILE) != 0;
@@ -968,7 +979,7 @@ int ffn_launch_one(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipSt
     const int cnt = sh ? a.T : rec.count[jobs[i]];
     const double melems = (double)(sh ? c->Ish : c->I) * c->H;
     maxc = std::max(maxc, cnt);
-    wbytes += melems * c->eb;
+    wbytes += a.q4 ? (double)c->chunk_bytes : melems * c->eb;  // stored bytes of a matrix
     flops += 2.0 * cnt * melems;
   }
   for (int pass = 0; pass < 2; ++pass) {
@@ -1003,11 +1014,13 @@ int ffn_launch(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipStream
                const CopyWait& wait2) {
   // split by kernel family; the shared expert (M = T) gets its own GEMM launch
   // so the routed groups can use the small-M tile
-  std::vector<int> gv, gm, sh;
+  // 4-bit routed experts all go to the dequantising GEMV (the shared expert stays dense)
+  std::vector<int> gv, gm, sh, gq;
   for (int p : jobs) {
     const bool is_sh = p == kSharedJob;
     const int cnt = is_sh ? a.T : c->route_rec.count[p];
-    if (!use_gemm(c, cnt, is_sh)) gv.push_back(p);
+    if (c->q4 && !is_sh) gq.push_back(p);
+    else if (!use_gemm(c, cnt, is_sh)) gv.push_back(p);
     else if (is_sh) sh.push_back(p);
     else gm.push_back(p);
   }
@@ -1015,6 +1028,10 @@ int ffn_launch(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipStream
   if (!sh.empty() && (rc = ffn_launch_one(c, a, sh, s, wait01, wait2, true))) return rc;
   if (!gm.empty() && (rc = ffn_launch_one(c, a, gm, s, wait01, wait2, true))) return rc;
   if (!gv.empty() && (rc = ffn_launch_one(c, a, gv, s, wait01, wait2, false))) return rc;
+  if (!gq.empty()) {
+    a.q4 = 1;
+    if ((rc = ffn_launch_one(c, a, gq, s, wait01, wait2, false))) return rc;
+  }
   return PROMOE_OK;
 }
 

@@ -11,7 +11,7 @@ import numpy as np
 from synth import model as sm
 from synth.configs import MoEConfig
 
-from ._abi import PROMOE_BF16, PROMOE_F32, Config, Context, HostBuffer
+from ._abi import PROMOE_BF16, PROMOE_F32, WEIGHTS_DENSE, WEIGHTS_INT4, Config, Context, HostBuffer
 
 
 def lib_config(cfg: MoEConfig, max_tokens: int, flags: int = 0, window: int = 0, subchunk: int = 0,
@@ -25,6 +25,7 @@ def lib_config(cfg: MoEConfig, max_tokens: int, flags: int = 0, window: int = 0,
     c.dtype = PROMOE_BF16 if cfg.dtype == "bf16" else PROMOE_F32
     c.copy_subchunk_bytes, c.copy_window, c.flags = subchunk, window, flags
     c.spec_fill_limit = spec_fill_limit
+    c.weight_format = WEIGHTS_INT4 if cfg.weight_format == "int4" else WEIGHTS_DENSE
     return c
 
 
@@ -98,6 +99,8 @@ class SyntheticModel:
     # host views for the oracle (data, not code)
     def expert_host(self, layer: int, e: int) -> np.ndarray:
         cfg = self.cfg
+        if cfg.weight_format == "int4":
+            return self.host[layer].numpy(np.uint8, count=cfg.expert_bytes, offset=e * cfg.expert_bytes)
         n = 3 * cfg.inter * cfg.hidden
         dt = np.uint16 if cfg.dtype == "bf16" else np.float32
         return self.host[layer].numpy(dt, count=n, offset=e * cfg.expert_bytes)

@@ -25,6 +25,9 @@ class Workload:
     steps: int         # number of steps
 
 
+INT4_GROUP = 128
+
+
 @dataclass(frozen=True)
 class MoEConfig:
     name: str
@@ -47,6 +50,9 @@ class MoEConfig:
     pred_noise_std: float = 0.005
     attn_surrogate: int = 1    # stack has a hidden x hidden linear mix per layer
     workloads: tuple = field(default_factory=tuple)
+    # routed-expert storage: "dense" (dtype) or "int4" (4-bit codes in groups of
+    # INT4_GROUP along the reduction dimension, one bf16 scale per group)
+    weight_format: str = "dense"
 
     @property
     def shared_total(self) -> int:
@@ -62,6 +68,9 @@ class MoEConfig:
 
     @property
     def chunk_bytes(self) -> int:
+        """Bytes of one expert matrix as stored (codes then scales for int4)."""
+        if self.weight_format == "int4":
+            return self.matrix_elems // 2 + (self.matrix_elems // INT4_GROUP) * 2
         return self.matrix_elems * self.elem_bytes
 
     @property

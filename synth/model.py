@@ -20,7 +20,7 @@ from __future__ import annotations
 import numpy as np
 
 from . import normal
-from .configs import MoEConfig
+from .configs import INT4_GROUP, MoEConfig
 
 K_GATE, K_BIAS, K_EG, K_EU, K_ED, K_SG, K_SU, K_SD, K_SGATE, K_PN1, K_PN2, K_ATTN, K_H0, K_X = range(1, 15)
 
@@ -55,18 +55,46 @@ def expert(cfg: MoEConfig, layer: int, e: int):
 
 
 def write_expert(cfg: MoEConfig, layer: int, e: int, addr: int) -> None:
-    """Write [Wg | Wu | Wd] of one routed expert to raw memory at addr."""
+    """Write [Wg | Wu | Wd] of one routed expert to raw memory at addr (each
+    matrix as codes then scales for the int4 format)."""
     n = cfg.inter * cfg.hidden
+    if cfg.weight_format == "int4":
+        import ctypes
+        mats = expert(cfg, layer, e)
+        for i, m in enumerate(mats):
+            codes, scales = quantize_int4(bf16_to_f32(m))
+            raw = np.concatenate([codes.reshape(-1), scales.reshape(-1).view(np.uint8)])
+            ctypes.memmove(addr + i * cfg.chunk_bytes, raw.ctypes.data, raw.nbytes)
+        return
     eb = cfg.elem_bytes
     _w(cfg, K_EG, layer, e, n, out=addr)
     _w(cfg, K_EU, layer, e, n, out=addr + n * eb)
     _w(cfg, K_ED, layer, e, n, out=addr + 2 * n * eb)
 
 
+def quantize_int4(w: np.ndarray, group: int = INT4_GROUP):
+    """Round-to-nearest symmetric 4-bit quantisation of fp32 rows w [R, K] in
+    groups of `group` along K (data preparation only): scale s = bf16(absmax / 7),
+    code = clamp(rint(w / s), -8, 7) + 8, two codes per byte (even k in the low
+    nibble).  Returns (codes uint8 [R, K/2], scales bf16 bits uint16 [R, K/group])."""
+    R, K = w.shape
+    g = w.reshape(R, K // group, group)
+    s_bits = _bf16_bits((np.abs(g).max(axis=2) / 7.0).astype(np.float32))
+    s = bf16_to_f32(s_bits)[:, :, None]
+    q = np.where(s > 0, np.rint(g / np.where(s > 0, s, 1.0)), 0.0)
+    codes = (np.clip(q, -8, 7) + 8).astype(np.uint8).reshape(R, K)
+    packed = (codes[:, 0::2] | (codes[:, 1::2] << 4)).astype(np.uint8)
+    return packed, s_bits
+
+
 def expert_from_bytes(cfg: MoEConfig, buf: np.ndarray):
-    """Split a flat [Wg|Wu|Wd] element array into its three matrices."""
+    """Split a flat [Wg|Wu|Wd] element array into its three matrices (for int4,
+    `buf` is the raw bytes and each matrix is returned as its stored byte block)."""
     I, H = cfg.inter, cfg.hidden
     n = I * H
+    if cfg.weight_format == "int4":
+        cb = cfg.chunk_bytes
+        return buf[:cb], buf[cb:2 * cb], buf[2 * cb:3 * cb]
     return buf[:n].reshape(I, H), buf[n:2 * n].reshape(I, H), buf[2 * n:3 * n].reshape(H, I)
 
 

@@ -21,6 +21,7 @@ from oracle import bf16 as obf16
 from oracle import cache as ocache
 from oracle import ffn as offn
 from oracle import predictor as opred
+from oracle import quant as oquant
 from oracle import router as orouter
 from oracle import stack as ostack
 from synth import model as sm
@@ -147,6 +148,8 @@ def check_ffn(cfg, model, l, x64, g_ids, w_ref, s_ref, y_gpu, tokens=None):
         s_ref = None if s_ref is None else s_ref[tokens]
         y_gpu = y_gpu[tokens]
     def expert_fn(e):  # called once per distinct expert
+        if cfg.weight_format == "int4":
+            return oquant.decode_expert(model.expert_host(l, e), cfg.inter, cfg.hidden)
         wg, wu, wd = sm.expert_from_bytes(cfg, model.expert_host(l, e))
         return f64(wg, cfg.dtype), f64(wu, cfg.dtype), f64(wd, cfg.dtype)
 

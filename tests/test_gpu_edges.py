@@ -133,6 +133,24 @@ def test_ablation_modes(mode, T):
         m.close()
 
 
+@pytest.mark.parametrize("T", [1, 5, 13, 77])
+def test_int4_experts(T):
+    # 4-bit routed experts through the dequantising GEMVs (token groups of 1, 2, 4, 8)
+    cfg = SMALL.with_(weight_format="int4")
+    _log("int4 T", T)
+    m = SyntheticModel(cfg, max_tokens=T)
+    try:
+        st = Stack(m, T)
+        lcs = {l: ocache.LayerCache(cfg.n_experts, cfg.slots) for l in range(cfg.n_layers)}
+        for step in range(2):
+            for l in range(cfg.n_layers):
+                pu.moe_layer_check(cfg, m, st, l, lcs, sm.layer_input(cfg, l, T, tag=600 + step))
+        pu.check_counters(m, lcs)
+        assert m.ctx.stats()["bytes_high"] % cfg.chunk_bytes == 0
+    finally:
+        m.close()
+
+
 def test_external_pushes_low_and_high():
     cfg = SMALL.with_(n_layers=1, lookahead=0)
     m = SyntheticModel(cfg, max_tokens=2)
@@ -196,3 +214,6 @@ def test_error_returns():
     assert _abi.lib().promoe_create(ctypes.byref(c), buf.data_ptr(), buf.numel(), ctypes.byref(h)) == -1
     c.spec_fill_limit, c.flags, c.slots_per_layer = 0, FLAG_STATIC, 2   # static needs C >= 3
     assert _abi.lib().promoe_create(ctypes.byref(c), buf.data_ptr(), buf.numel(), ctypes.byref(h)) == -1
+    c.flags, c.slots_per_layer, c.weight_format = 0, 4, _abi.WEIGHTS_INT4
+    c.inter = 520                                                      # int4 needs multiples of 128
+    assert _abi.lib().promoe_create(ctypes.byref(c), buf.data_ptr(), buf.numel(), ctypes.byref(h)) == -5
