@@ -51,8 +51,9 @@ def parse():
                    help="slots a predicted plan may fill: 0 no limit, n>0 the first n, -1 none")
     p.add_argument("--copy-calib-mib", type=int, default=1024,
                    help="size of the plain device copy run after the timed region (counter calibration)")
-    p.add_argument("--legs", default="decode,prefill,mfma,ablation,sweep",
-                   help="decode is always run (it is the reported value); add prefill, mfma, ablation, sweep")
+    p.add_argument("--legs", default="decode,prefill,mfma,ablation,sweep,int4",
+                   help="decode is always run (it is the reported value); add prefill, mfma, ablation, sweep, "
+                        "int4, predtrain")
     p.add_argument("--prefill-steps", type=int, default=3)
     p.add_argument("--prefill-warmup", type=int, default=1)
     p.add_argument("--ablation-steps", type=int, default=32)
@@ -369,6 +370,44 @@ def leg_predtrain(torch, args):
     return out
 
 
+def leg_int4(torch, args):
+    """4-bit routed experts (the paper's bits-per-weight study): decode of the
+    DeepSeek-MoE-16B shape (50% cached) and 512-token prefill of the
+    Qwen1.5-MoE shape, under the LRU baseline, the method (unlimited fills and
+    fill limit 1) and reactive; plus the dequantising GEMV's rate."""
+    import numpy as np
+    from synth import configs, model as sm
+    from paper_2410_22134_amd import ABLATION, FLAG_NO_PREFETCH, FLAG_PROFILE
+    from paper_2410_22134_amd.model import SyntheticModel
+    from paper_2410_22134_amd.stack import Stack
+    modes = (("lru", ABLATION["lru"], 0), ("+pcer", 0, 0), ("+pcer fill limit 1", 0, 1),
+             ("+cer (no prefetch)", FLAG_NO_PREFETCH, 0))
+    out = {}
+    for name, base, T, warm, steps in (("decode", configs.C2, 1, 4, args.ablation_steps * 2),
+                                       ("prefill", configs.C3, 512, 1, 2)):
+        cfg = base.with_(weight_format="int4")
+        model = SyntheticModel(cfg, max_tokens=T, gen_threads=8)
+        try:
+            st = Stack(model, T)
+            h = torch.from_numpy(np.stack([sm.stack_input(cfg, 7000 + i, T) for i in range(warm + steps)])).cuda()
+            res = {"expert_MB": round(cfg.expert_bytes / 1e6, 3)}
+            for mode, flags, lim in modes:
+                model.open(flags=flags | FLAG_PROFILE, spec_fill_limit=lim)
+                dt, s = run_steps(torch, model, st, h, warm, steps)
+                r = {"tok_s": round(T * steps / dt, 2),
+                     "copied_GB": round((s["bytes_high"] + s["bytes_low"]) / 1e9, 3),
+                     "hit": s["hit"], "miss": s["miss"], "overlap": overlap_metrics(s, dt, 56.7)}
+                if name == "decode":
+                    r["kernels"] = _classes(s)
+                res[mode] = r
+                print(f"[bench] int4 {name} {mode}: {r['tok_s']} tok/s, {r['copied_GB']} GB", file=sys.stderr,
+                      flush=True)
+            out[name] = res
+        finally:
+            model.close()
+    return out
+
+
 def leg_mfma(torch, args):
     """Shared-expert GEMMs at the Qwen2-57B-A14B shape (hidden 3584, shared I = 20480),
     1024-token prefill, two layers with every expert resident (compute only)."""
@@ -494,6 +533,9 @@ def main():
     if "predtrain" in args.legs:
         print("[bench] predictor training leg", file=sys.stderr, flush=True)
         out["detail"]["predictor_training"] = leg_predtrain(torch, args)
+    if "int4" in args.legs:
+        print("[bench] 4-bit experts leg", file=sys.stderr, flush=True)
+        out["detail"]["int4"] = leg_int4(torch, args)
     if "mfma" in args.legs:
         print("[bench] shared-expert MFMA leg", file=sys.stderr, flush=True)
         out["roofline_prefill_gemm"] = leg_mfma(torch, args)
