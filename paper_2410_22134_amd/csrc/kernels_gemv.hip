@@ -641,7 +641,7 @@ static int gemv_jobs(const FfnArgs& in, int pass, FfnArgs& a) {
 // keeping registers bounded (token pieces MT x 16 words, accumulators R x MT).
 template <int MT>
 static void ffn_dispatch_q4(const FfnArgs& in, int pass, hipStream_t s) {
-  constexpr int RWG = MT <= 2 ? 8 : (MT == 4 ? 4 : 2), RWD = 2 * RWG;
+  constexpr int RWG = MT <= 2 ? 2 : (MT == 4 ? 2 : 1), RWD = 2 * RWG;
   const int rows_per_block = kBlockWaves * (pass == 0 ? RWG : RWD);
   FfnArgs a;
   if (gemv_jobs(in, pass, a) == 0 || a.piece_rows <= 0) return;
