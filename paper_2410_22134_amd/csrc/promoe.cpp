@@ -65,7 +65,12 @@ class HipEngine : public CopyEngine {
   void issue(int64_t seq, void* dst, const void* src, size_t bytes, int64_t after, int queue) override {
     hipStream_t s = stream[queue];
     hipError_t e = hipSuccess;
-    if (after >= 0) e = hipStreamWaitEvent(s, (*compute_ev)[after % kComputeRing], 0);
+    // A wait on a compute event costs the copy queue a barrier and a poll even
+    // when the event has long completed; wait only on compute still running.
+    if (after >= 0) {
+      hipEvent_t ce = (*compute_ev)[after % kComputeRing];
+      if (hipEventQuery(ce) != hipSuccess) e = hipStreamWaitEvent(s, ce, 0);
+    }
     if (e == hipSuccess) e = hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, s);
     if (e == hipSuccess) e = hipEventRecord(ev[seq % kCopyRing], s);
     if (e != hipSuccess && err == hipSuccess) err = e;
