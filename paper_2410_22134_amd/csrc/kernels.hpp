@@ -152,6 +152,16 @@ __device__ __forceinline__ void tclock_end(const FfnArgs& a) {
   }
 }
 
+// Expand 4-bit experts into dense bf16 [Wg | Wu | Wd] copies (the MFMA GEMM's
+// operand type: each weight (code - 8) * scale is rounded to bf16).
+struct DequantArgs {
+  const uint8_t* src[8];  // stored experts (cache slots)
+  bf16_t* dst;            // n consecutive dense experts
+  int n, inter, hidden;
+};
+constexpr int kStageExperts = 8;
+void launch_dequant_q4(const DequantArgs& a, hipStream_t s);
+
 void launch_rows_gemv(const RowsArgs& a, int wdtype, int xdtype, hipStream_t s);
 // Launches one pass of the GEMV kernels over the jobs (a copy of `a` is
 // adjusted per pass; `a` is unchanged).  max_tokens = most pairs of any job.

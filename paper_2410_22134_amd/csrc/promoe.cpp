@@ -114,6 +114,7 @@ struct promoe_ctx {
   int dev = 0;
   int L, H, E, K, I, Ish, C, D, Ph, maxT, dt, eb;
   bool q4 = false;  // routed experts stored as 4-bit codes
+  bf16_t* d_stage = nullptr;  // 4-bit experts expanded for the MFMA GEMM (kStageExperts)
   size_t chunk_bytes, expert_bytes;
   uint8_t* cache = nullptr;
 
@@ -587,6 +588,14 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   c->d_act_sh = b + o_actsh;
   c->d_Ysh = reinterpret_cast<float*>(b + o_Ysh);
   c->d_u = b + o_u;
+  if (c->q4 && gemm_supported(c->I, c->H) && gemm_supported(c->H, c->I)) {
+    e = hipMalloc(&c->d_stage, (size_t)kStageExperts * 3 * c->I * c->H * sizeof(bf16_t));
+    if (e != hipSuccess) {
+      hipFree(c->dmem);
+      delete c;
+      return fail_hip(e, "hipMalloc(stage)");
+    }
+  }
 
   launch_state_init(c->st, L, C, E, nullptr);
   e = hipGetLastError();
@@ -697,6 +706,7 @@ int promoe_destroy(promoe_ctx* c) {
   hipHostFree(c->rec_h);
   if (c->d_tclock) hipFree(c->d_tclock);
   hipFree(c->dmem);
+  if (c->d_stage) hipFree(c->d_stage);
   delete c->pf;
   delete c;
   return PROMOE_OK;
@@ -959,7 +969,7 @@ namespace {
 constexpr int kGemmMinTokens = 16;
 
 int ffn_launch_one(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipStream_t s, const CopyWait& wait01,
-                   const CopyWait& wait2, bool gemm) {
+                   const CopyWait& wait2, bool gemm, const bf16_t* stage = nullptr) {
   const PlanRecord& rec = c->route_rec;
   int maxc = 1;
   double wbytes = 0, flops = 0;
@@ -976,7 +986,8 @@ int ffn_launch_one(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipSt
       jb.q1 = a.T;
       jb.I = c->Ish;
     } else {
-      jb.w = c->cache + ((size_t)a.layer * c->C + rec.slot[jobs[i]]) * c->expert_bytes;
+      jb.w = stage ? static_cast<const void*>(stage + i * 3 * (size_t)c->I * c->H)
+                   : static_cast<const void*>(c->cache + ((size_t)a.layer * c->C + rec.slot[jobs[i]]) * c->expert_bytes);
       jb.q0 = rec.offset[jobs[i]];
       jb.q1 = rec.offset[jobs[i] + 1];
       jb.I = c->I;
@@ -984,7 +995,7 @@ int ffn_launch_one(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipSt
     const int cnt = sh ? a.T : rec.count[jobs[i]];
     const double melems = (double)(sh ? c->Ish : c->I) * c->H;
     maxc = std::max(maxc, cnt);
-    wbytes += a.q4 ? (double)c->chunk_bytes : melems * c->eb;  // stored bytes of a matrix
+    wbytes += (a.q4 && !stage) ? (double)c->chunk_bytes : melems * c->eb;  // bytes the kernel reads
     flops += 2.0 * cnt * melems;
   }
   for (int pass = 0; pass < 2; ++pass) {
@@ -1019,12 +1030,13 @@ int ffn_launch(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipStream
                const CopyWait& wait2) {
   // split by kernel family; the shared expert (M = T) gets its own GEMM launch
   // so the routed groups can use the small-M tile
-  // 4-bit routed experts all go to the dequantising GEMV (the shared expert stays dense)
-  std::vector<int> gv, gm, sh, gq;
+  // 4-bit routed experts go to the dequantising GEMV, or -- with enough tokens --
+  // are expanded to bf16 and run on the MFMA GEMM (the shared expert stays dense)
+  std::vector<int> gv, gm, sh, gq, gqm;
   for (int p : jobs) {
     const bool is_sh = p == kSharedJob;
     const int cnt = is_sh ? a.T : c->route_rec.count[p];
-    if (c->q4 && !is_sh) gq.push_back(p);
+    if (c->q4 && !is_sh) (c->d_stage && use_gemm(c, cnt, false) ? gqm : gq).push_back(p);
     else if (!use_gemm(c, cnt, is_sh)) gv.push_back(p);
     else if (is_sh) sh.push_back(p);
     else gm.push_back(p);
@@ -1034,8 +1046,27 @@ int ffn_launch(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipStream
   if (!gm.empty() && (rc = ffn_launch_one(c, a, gm, s, wait01, wait2, true))) return rc;
   if (!gv.empty() && (rc = ffn_launch_one(c, a, gv, s, wait01, wait2, false))) return rc;
   if (!gq.empty()) {
-    a.q4 = 1;
-    if ((rc = ffn_launch_one(c, a, gq, s, wait01, wait2, false))) return rc;
+    FfnArgs q = a;
+    q.q4 = 1;
+    if ((rc = ffn_launch_one(c, q, gq, s, wait01, wait2, false))) return rc;
+  }
+  // staged: every copy of the batch before the expansion, then two GEMM passes
+  for (size_t b0 = 0; b0 < gqm.size(); b0 += kStageExperts) {
+    const std::vector<int> batch(gqm.begin() + b0, gqm.begin() + std::min(gqm.size(), b0 + kStageExperts));
+    CopyWait w;
+    for (int q = 0; q < kCopyStreams; ++q) w.seq[q] = std::max(wait01.seq[q], wait2.seq[q]);
+    for (int64_t q : w.seq)
+      if (q >= 0) HIPCHK(hipStreamWaitEvent(s, c->eng.event(q), 0));
+    DequantArgs d{};
+    d.dst = c->d_stage;
+    d.n = (int)batch.size();
+    d.inter = c->I;
+    d.hidden = c->H;
+    for (size_t i = 0; i < batch.size(); ++i)
+      d.src[i] = c->cache + ((size_t)a.layer * c->C + c->route_rec.slot[batch[i]]) * c->expert_bytes;
+    launch_dequant_q4(d, s);
+    LAUNCHCHK("dequant");
+    if ((rc = ffn_launch_one(c, a, batch, s, CopyWait(), CopyWait(), true, c->d_stage))) return rc;
   }
   return PROMOE_OK;
 }
