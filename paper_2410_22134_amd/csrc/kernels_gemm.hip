@@ -12,14 +12,17 @@
 // m-tiles that share an n-tile (the same weight rows) run on the same XCD and
 // meet in its L2.
 //
-// Block = 4 or 8 waves, tile BM x 128 x 64 (k).  A and B tiles go global -> LDS
-// directly (global_load_lds_dwordx4: each wave instruction fills 8 rows of
-// 128 bytes, no staging registers) through a 3-stage ring, so the loads of two
-// later k-tiles are in flight while one feeds v_mfma_f32_16x16x32_bf16; one
-// barrier per k-tile.  LDS rows are unpadded and their 16-byte chunks are
-// XOR-swizzled by (row >> 1) & 7, so the 16 rows read by one ds_read_b128 phase
-// fall in distinct banks.  Lane l of an MFMA supplies A[l % 16][8*(l/16)..+8]
-// and B[l % 16][8*(l/16)..+8] and receives C[4*(l/16) + i][l % 16], i < 4.
+// Block = 4 or 8 waves (two per SIMD for 8), tile BM x 128 x 64 (k).  A and B
+// tiles go global -> LDS directly (global_load_lds_dwordx4: each wave
+// instruction fills 8 rows of 128 bytes, no staging registers) through a 2- or
+// 3-stage ring.  Each wave double-buffers its MFMA fragments in registers: the
+// MFMAs of one 32-wide k step run while the fragments of the next are read
+// from LDS, and the DMA of a later k-tile is spread over the same MFMA stream
+// (one load per row block) instead of being issued in a burst.  LDS rows are
+// unpadded and their 16-byte chunks are XOR-swizzled by (row >> 1) & 7, so the
+// 16 rows read by one ds_read_b128 phase fall in distinct banks.  Lane l of an
+// MFMA supplies A[l % 16][8*(l/16)..+8] and B[l % 16][8*(l/16)..+8] and
+// receives C[4*(l/16) + i][l % 16], i < 4.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -80,6 +83,89 @@ struct GemmTile {
   static_assert(ROWS % (8 * NW) == 0 && BM % 16 == 0 && TM >= 1 && TN >= 1, "tile shape");
   static_assert(STAGES == 2 || STAGES == 3, "stages");
 
+  // Fragments of one 32-wide k step: lane l holds A[l % 16][8*(l/16)..+8] of
+  // each 16-row A block and B[l % 16][..] of each 16-row B block.
+  struct Frag {
+    bf16x8_t a[TM];
+    bf16x8_t b[NB][TN];
+  };
+
+  __device__ static bf16x8_t lds_frag(const bf16_t* L, int r, int c) {
+    return as_bf16x8(*reinterpret_cast<const uint4*>(&L[r * kBK + (c ^ swz(r)) * 8]));
+  }
+
+  // One k step's MFMAs on f, row block by row block, while the next k step's
+  // fragments are read into g: its B blocks after f's first row block, and A
+  // block i right after the MFMAs of f's A block i (so g.a[i] can take
+  // f.a[i]'s registers).  L is the stage that holds g's k-tile, s2 its k step.
+  // With DMA, the loads of a later k-tile (source offset k0, LDS stage dst) are
+  // spread over the row blocks too, so no wave stalls on a burst of them
+  // before its MFMAs.
+  template <bool DMA>
+  __device__ static void step(const Frag& f, Frag& g, const bf16_t* L, int s2, f32x4_t (&acc)[NB][TM][TN],
+                              int wm, int wn, int lr, int lg, const bf16_t* const (&src)[NLD], int k0,
+                              bf16_t* dst, int wave) {
+    const int c = s2 * 4 + lg;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int h = 0; h < NB; ++h)
+#pragma unroll
+        for (int jn = 0; jn < TN; ++jn)
+          acc[h][i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.a[i], f.b[h][jn], acc[h][i][jn], 0, 0, 0);
+      if (i == 0) {
+#pragma unroll
+        for (int h = 0; h < NB; ++h)
+#pragma unroll
+          for (int jn = 0; jn < TN; ++jn) g.b[h][jn] = lds_frag(L, BM + h * kBN + wn * WTN + jn * 16 + lr, c);
+      }
+      g.a[i] = lds_frag(L, wm * WTM + i * 16 + lr, c);
+      if (DMA) {
+#pragma unroll
+        for (int d = i * NLD / TM; d < (i + 1) * NLD / TM; ++d)
+          __builtin_amdgcn_global_load_lds((gbl_ptr_t)(src[d] + k0), (lds_ptr_t)(dst + 8 * (NW * d + wave) * kBK),
+                                           16, 0, 0);
+      }
+    }
+    sched_rows<0, DMA>();
+  }
+
+  template <int I, bool DMA>
+  __device__ static void sched_rows() {
+    if constexpr (I < TM) {
+      __builtin_amdgcn_sched_group_barrier(0x008, NB * TN, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, I == 0 ? NB * TN + 1 : 1, 0);
+      constexpr int nd = DMA ? (I + 1) * NLD / TM - I * NLD / TM : 0;
+      if constexpr (nd > 0) __builtin_amdgcn_sched_group_barrier(0x010, nd, 0);
+      sched_rows<I + 1, DMA>();
+    }
+  }
+
+  __device__ static void first(Frag& g, const bf16_t* L, int wm, int wn, int lr, int lg) {
+#pragma unroll
+    for (int h = 0; h < NB; ++h)
+#pragma unroll
+      for (int jn = 0; jn < TN; ++jn) g.b[h][jn] = lds_frag(L, BM + h * kBN + wn * WTN + jn * 16 + lr, lg);
+#pragma unroll
+    for (int i = 0; i < TM; ++i) g.a[i] = lds_frag(L, wm * WTM + i * 16 + lr, lg);
+  }
+
+  __device__ static void last(const Frag& f, f32x4_t (&acc)[NB][TM][TN]) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int h = 0; h < NB; ++h)
+#pragma unroll
+        for (int jn = 0; jn < TN; ++jn)
+          acc[h][i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(f.a[i], f.b[h][jn], acc[h][i][jn], 0, 0, 0);
+  }
+
+  __device__ static void barrier() {
+    __asm__ volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    __asm__ volatile("" ::: "memory");
+  }
+
   __device__ static void run(const bf16_t* const (&src)[NLD], int kt0, int kt1, bf16_t* lds,
                              f32x4_t (&acc)[NB][TM][TN], int wave, int lane) {
     const int wm = wave / WN, wn = wave % WN;
@@ -90,62 +176,41 @@ struct GemmTile {
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int jn = 0; jn < TN; ++jn) acc[h][i][jn] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    auto issue = [&](int stage, int k0) {
-      bf16_t* dst = lds + stage * STAGE;
+    // k-tile kt lives in stage (kt - kt0) % STAGES.  A tile's stage is
+    // refilled as soon as every wave has read both of its k steps into
+    // registers: the barrier between the two k steps of tile t follows each
+    // wave's wait for its own reads of tile t and its own DMA of tile t + 1,
+    // so after it tile t + 1 is visible to all waves and tile t + STAGES may
+    // overwrite tile t's stage; its DMA is spread over the next k step.  Every
+    // iteration issues one tile (past the last tile, the last tile again, into
+    // a stage that is not read any more), so exactly STAGES - 2 later tiles
+    // may be in flight when tile t + 1 must have landed.
+    const int nk = kt1 - kt0;
+    if (nk <= 0) return;
+#pragma unroll
+    for (int st = 0; st < STAGES; ++st) {
+      bf16_t* dst = lds + st * STAGE;
+      const int k0 = (kt0 + min(st, nk - 1)) * kBK;
 #pragma unroll
       for (int i = 0; i < NLD; ++i)
         __builtin_amdgcn_global_load_lds((gbl_ptr_t)(src[i] + k0), (lds_ptr_t)(dst + 8 * (NW * i + wave) * kBK),
                                          16, 0, 0);
-    };
-    // All fragment reads of a k-tile (both 32-wide k steps) are issued before
-    // the first MFMA so LDS latency overlaps the first step's MFMAs.
-    auto compute = [&](int stage) {
-      const bf16_t* L = lds + stage * STAGE;
-      bf16x8_t fa[2][TM], fb[2][NB][TN];
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
-        const int c = s2 * 4 + lg;  // logical 16-byte chunk of this lane
-#pragma unroll
-        for (int i = 0; i < TM; ++i) {
-          const int r = wm * WTM + i * 16 + lr;
-          fa[s2][i] = as_bf16x8(*reinterpret_cast<const uint4*>(&L[r * kBK + (c ^ swz(r)) * 8]));
-        }
-#pragma unroll
-        for (int h = 0; h < NB; ++h)
-#pragma unroll
-          for (int jn = 0; jn < TN; ++jn) {
-            const int r = BM + h * kBN + wn * WTN + jn * 16 + lr;
-            fb[s2][h][jn] = as_bf16x8(*reinterpret_cast<const uint4*>(&L[r * kBK + (c ^ swz(r)) * 8]));
-          }
-      }
-#pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2)
-#pragma unroll
-        for (int h = 0; h < NB; ++h)
-#pragma unroll
-          for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int jn = 0; jn < TN; ++jn)
-              acc[h][i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[s2][i], fb[s2][h][jn], acc[h][i][jn], 0, 0, 0);
-    };
-    // k-tile kt lives in stage (kt - kt0) % STAGES; the next STAGES-1 tiles are in
-    // flight while kt is computed.  Before computing kt a wave waits until only
-    // the loads of later tiles remain outstanding, then a bare s_barrier makes
-    // every wave's tile visible (__syncthreads() would also drain the later
-    // tiles' DMA) and guarantees the stage overwritten next has been read.
-    const int nk = kt1 - kt0;
-#pragma unroll
-    for (int st = 0; st < STAGES - 1; ++st)
-      if (st < nk) issue(st, (kt0 + st) * kBK);
-    for (int t = 0; t < nk; ++t) {
-      if (STAGES == 3 && t + 1 < nk) wait_vmcnt<NLD>();
-      else wait_vmcnt<0>();
-      __asm__ volatile("" ::: "memory");
-      __builtin_amdgcn_s_barrier();
-      __asm__ volatile("" ::: "memory");
-      if (t + STAGES - 1 < nk) issue((t + STAGES - 1) % STAGES, (kt0 + t + STAGES - 1) * kBK);
-      compute(t % STAGES);
     }
+    wait_vmcnt<(STAGES - 1) * NLD < 64 ? (STAGES - 1) * NLD : 63>();
+    barrier();
+    Frag f0, f1;
+    first(f0, lds, wm, wn, lr, lg);
+    for (int t = 0; t + 1 < nk; ++t) {
+      step<false>(f0, f1, lds + (t % STAGES) * STAGE, 1, acc, wm, wn, lr, lg, src, 0, lds, wave);
+      __builtin_amdgcn_s_waitcnt(0xc07f);  // lgkmcnt(0): this wave's reads of tile t are done
+      wait_vmcnt<(STAGES - 2) * NLD>();
+      barrier();
+      step<true>(f1, f0, lds + ((t + 1) % STAGES) * STAGE, 0, acc, wm, wn, lr, lg, src,
+                 (kt0 + min(t + STAGES, nk - 1)) * kBK, lds + (t % STAGES) * STAGE, wave);
+    }
+    step<false>(f0, f1, lds + ((nk - 1) % STAGES) * STAGE, 1, acc, wm, wn, lr, lg, src, 0, lds, wave);
+    last(f1, acc);
+    wait_vmcnt<0>();  // no DMA may land in LDS after the block has left it
   }
 };
 
