@@ -129,6 +129,38 @@ def h2d_probe(torch, mib=256, reps=5):
     return best
 
 
+def measure_peaks(torch, hbm_gib=4, reps=5):
+    """Achievable peaks of this GPU, measured with the library's probes: one
+    streaming read of a buffer far larger than the 256 MB Infinity Cache (best of
+    `reps`), and a register-only bf16 MFMA loop (two waves per SIMD)."""
+    from paper_2410_22134_amd import _abi
+    n = hbm_gib << 30
+    buf = torch.zeros(n, dtype=torch.uint8, device="cuda")
+    blocks = 256 * 16
+    sink = torch.empty(1024 * 512, dtype=torch.float32, device="cuda")
+
+    def timed(fn):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        b.synchronize()
+        return a.elapsed_time(b) * 1e-3
+
+    _abi.peak_hbm_read(buf, n, sink, blocks)
+    t_hbm = min(timed(lambda: _abi.peak_hbm_read(buf, n, sink, blocks)) for _ in range(reps))
+    del buf
+    mblocks, iters = 1024, 2000
+    flops = mblocks * 8 * iters * 32 * 16384.0
+    _abi.peak_mfma_bf16(sink, mblocks, 100)
+    t_mfma = min(timed(lambda: _abi.peak_mfma_bf16(sink, mblocks, iters)) for _ in range(3))
+    torch.cuda.synchronize()
+    return {"hbm_read_GBps": round(n / t_hbm / 1e9, 1), "hbm_read_bytes": n,
+            "mfma_bf16_TFLOPs": round(flops / t_mfma / 1e12, 1),
+            "how": "promoe_peak_hbm_read (16-byte non-temporal grid-stride read, best of 5) and "
+                   "promoe_peak_mfma_bf16 (32 independent 16x16x32 bf16 MFMAs per wave, 8 waves per block)"}
+
+
 def cpu_baseline(cfg, model, budget_s):
     """Time the oracle on consecutive layers of one decode step until the budget is spent."""
     import numpy as np
@@ -471,6 +503,7 @@ def main():
     achieved = (by / launches) / (avg_us * 1e-6) / 1e9 if launches else 0.0
     copy_bytes = s["bytes_high"] + s["bytes_low"]
     h2d_gbs = h2d_probe(torch)
+    peaks = measure_peaks(torch)
     load_s = s["bytes_high"] / (h2d_gbs * 1e9) if h2d_gbs else 0.0
     traffic = read_traffic("k_ffn_gateup")
     out = {
@@ -493,12 +526,15 @@ def main():
                    "prefetch": not args.no_prefetch, "spec_fill_limit": args.spec_fill_limit},
         "roofline": {"bound": "hbm", "kernel": "k_ffn_gateup<bf16,1>", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": traffic, "avg_launch_us": round(avg_us, 3),
+                     "traffic": traffic, "peak_measured": peaks["hbm_read_GBps"],
+                     "frac_of_measured": round(achieved / peaks["hbm_read_GBps"], 4) if peaks["hbm_read_GBps"] else None,
+                     "avg_launch_us": round(avg_us, 3),
                      "bytes_per_launch": round(by / launches) if launches else 0, "launches": launches,
                      "timing": "device clock, first block start to last wave end"},
         "detail": {
             "decode_kernels": _classes(s),
             "h2d_copy_GBps_measured_256MiB": round(h2d_gbs, 2),
+            "measured_peaks": peaks,
             "copied_GB": round(copy_bytes / 1e9, 3),
             "copy_GBps_over_timed_region": round(copy_bytes / elapsed / 1e9, 2),
             "hit": s["hit"], "miss": s["miss"], "prec_access": s["prec_access"],
@@ -538,7 +574,10 @@ def main():
         out["detail"]["int4"] = leg_int4(torch, args)
     if "mfma" in args.legs:
         print("[bench] shared-expert MFMA leg", file=sys.stderr, flush=True)
-        out["roofline_prefill_gemm"] = leg_mfma(torch, args)
+        g = leg_mfma(torch, args)
+        g["peak_measured"] = peaks["mfma_bf16_TFLOPs"]
+        g["frac_of_measured"] = round(g["achieved"] / peaks["mfma_bf16_TFLOPs"], 4) if peaks["mfma_bf16_TFLOPs"] else None
+        out["roofline_prefill_gemm"] = g
     print(json.dumps(out), flush=True)
 
 

@@ -273,6 +273,21 @@ int promoe_attn_surrogate(promoe_ctx* ctx, int layer, float* d_h, int T, void* d
 /* d_h [T x H] fp32 += d_y [T x H] (config dtype). */
 int promoe_residual_add(promoe_ctx* ctx, float* d_h, const void* d_y, int T, void* stream);
 
+/* ---- measurement (not part of the method) --------------------------------
+ * Achievable peaks of this GPU; the kernels' rooflines are reported against
+ * the nominal peaks and against these.  Both launch asynchronously on `stream`
+ * (a hipStream_t; NULL = the null stream) and return PROMOE_EINVAL for a null
+ * pointer or a size out of range, PROMOE_EHIP if the launch fails.  The caller
+ * owns every buffer. */
+/* Reads `bytes` (> 0, a multiple of 16) at d_buf once with 16-byte
+ * non-temporal loads, `blocks` blocks of 256 threads in a grid-stride loop;
+ * writes one float per block to d_sink (>= blocks floats). */
+int promoe_peak_hbm_read(const void* d_buf, size_t bytes, float* d_sink, int blocks, void* stream);
+/* `blocks` blocks of 512 threads; each wave runs `iters` rounds of 32
+ * independent v_mfma_f32_16x16x32_bf16 on register operands, i.e.
+ * blocks * 8 * iters * 32 * 16384 flops.  Writes blocks * 512 floats to d_sink. */
+int promoe_peak_mfma_bf16(float* d_sink, int blocks, int iters, void* stream);
+
 /* ---- utilities ----------------------------------------------------------- */
 
 /* Pinned host memory for expert weights (hipHostMalloc); free with promoe_host_free. */

@@ -95,6 +95,8 @@ def lib() -> ctypes.CDLL:
         "promoe_expert_bytes": ([P(Config)], _sz),
         "promoe_strerror": ([ctypes.c_int], ctypes.c_char_p),
         "promoe_last_error_string": ([], ctypes.c_char_p),
+        "promoe_peak_hbm_read": ([_vp, _sz, _vp, ctypes.c_int, _vp], ctypes.c_int),
+        "promoe_peak_mfma_bf16": ([_vp, ctypes.c_int, ctypes.c_int, _vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(l, name)
@@ -110,7 +112,18 @@ def exported_symbols():
                         "promoe_prefetch", "promoe_expert_ffn", "promoe_cache_stats", "promoe_reset_stats",
                         "promoe_slot_table", "promoe_last_plan", "promoe_sync", "promoe_attn_surrogate",
                         "promoe_residual_add", "promoe_host_alloc", "promoe_host_free", "promoe_expert_bytes",
-                        "promoe_strerror", "promoe_last_error_string")]
+                        "promoe_strerror", "promoe_last_error_string", "promoe_peak_hbm_read",
+                        "promoe_peak_mfma_bf16")]
+
+
+def peak_hbm_read(buf, nbytes: int, sink, blocks: int, stream=None) -> None:
+    """One streaming read of `nbytes` of `buf` (see promoe_peak_hbm_read)."""
+    check(lib().promoe_peak_hbm_read(_p(buf), nbytes, _p(sink), blocks, _stream(stream)), "peak_hbm_read")
+
+
+def peak_mfma_bf16(sink, blocks: int, iters: int, stream=None) -> None:
+    """Register-only MFMA loop (see promoe_peak_mfma_bf16)."""
+    check(lib().promoe_peak_mfma_bf16(_p(sink), blocks, iters, _stream(stream)), "peak_mfma_bf16")
 
 
 def check(rc: int, where: str) -> None:

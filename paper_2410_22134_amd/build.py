@@ -17,7 +17,8 @@ ROOT = os.path.dirname(HERE)
 LIB = os.environ.get("PROMOE_BUILD_OUT", os.path.join(HERE, "libpromoe.so"))
 BUILD_DIR = os.environ.get("PROMOE_BUILD_DIR", os.path.join(ROOT, "_build"))
 
-SOURCES = ["promoe.cpp", "scheduler.cpp", "kernels_gemv.hip", "kernels_route.hip", "kernels_gemm.hip"]
+SOURCES = ["promoe.cpp", "scheduler.cpp", "kernels_gemv.hip", "kernels_route.hip", "kernels_gemm.hip",
+           "peaks.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
