@@ -66,6 +66,8 @@ struct FfnArgs {
   int ksplit;                   // split-K slices of the shared expert's down GEMM (>= 1)
   int64_t ysh_split_stride;     // elements between the slices' partial outputs in Ysh
   unsigned long long* tclock;   // optional launch clock slot (see kTclkWords), zero-initialised
+  int tail_block0;              // GEMM gate/up of one job: first block of the half-height tail tiles
+  int tail_n0;                  // first n-tile (of 128 columns) the tail covers
   int32_t job_tile0[kMaxJobs + 1];  // GEMM: first block of each job in the 1-D grid
   FfnJob jobs[kMaxJobs];
 };

@@ -219,38 +219,21 @@ __device__ __forceinline__ int xcd_grouped(int b, int nblk) {
   return (nblk & 7) == 0 ? (b & 7) * (nblk >> 3) + (b >> 3) : b;
 }
 
-// PASS 0: gate/up (dual B), PASS 1: down.  WM x WN waves per block.
+// One output tile of job jd: rows m0 .. m0+BM-1 of its token range, columns
+// n0 .. n0+127 (per B), k-tiles [kt0, kt1), split-K slice ks (down pass of
+// the shared expert).  PASS 0: gate/up (dual B), PASS 1: down.
 template <int BM, int WM, int WN, int PASS, int STAGES>
-__global__ __launch_bounds__(64 * WM * WN) void k_gemm_ffn(FfnArgs a) {
+__device__ __forceinline__ void ffn_tile(const FfnArgs& a, bf16_t* lds, const FfnJob& jd, int m0, int n0, int ks,
+                                         int kt0, int kt1, int wave, int lane) {
   constexpr bool DUAL = PASS == 0;
   constexpr int NB = DUAL ? 2 : 1;
   using G = GemmTile<BM, WM, WN, NB, STAGES>;
-  __shared__ __attribute__((aligned(1024))) bf16_t lds[STAGES * G::STAGE];
-
-  const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
   const int wm = wave / WN, wn = wave % WN;
-  tclock_start(a);
-
-  const int b = xcd_grouped(blockIdx.x, gridDim.x);
-  const int j = gemm_find_job(a, b);
-  int jt = b - a.job_tile0[j];
-  const FfnJob jd = a.jobs[j];
   const bool shared = jd.pos == kSharedJob;
   const int I = jd.I;
   const int H = a.hidden;
-  const int N = PASS == 0 ? I : H;
   const int K = PASS == 0 ? H : I;
   const int q0 = jd.q0, M = jd.q1 - q0;
-  const int mtiles = (M + BM - 1) / BM;
-  const int ntiles = N / kBN;
-  // split-K (shared down pass only): slice ks of S writes its own partial output
-  const int S = (PASS == 1 && shared) ? a.ksplit : 1;
-  const int ks = jt / (mtiles * ntiles);
-  jt -= ks * mtiles * ntiles;
-  const int m0 = (jt % mtiles) * BM;
-  const int n0 = (jt / mtiles) * kBN;
-  const int nk = K / kBK;
-  const int kt0 = ks * nk / S, kt1 = (ks + 1) * nk / S;
   const bf16_t* W = reinterpret_cast<const bf16_t*>(jd.w);
 
   // DMA sources.  Load i of this wave fills LDS rows 8*(NW*i + wave) .. +8;
@@ -305,6 +288,53 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_ffn(FfnArgs a) {
       }
     }
   }
+}
+
+// Tail tiles of a one-job gate/up launch: 128 rows, 3 stages.
+using TailTile = GemmTile<128, 2, 4, 2, 3>;
+
+// Block b < tail_block0 takes tile b of the flat job x m-tile x n-tile list;
+// blocks from tail_block0 on (gate/up of one job only) take tiles of half the
+// height over the job's n-tiles from tail_n0, so the launch's last round is
+// made of half-size tiles instead of a part-filled round of full ones.
+template <int BM, int WM, int WN, int PASS, int STAGES>
+__global__ __launch_bounds__(64 * WM * WN) void k_gemm_ffn(FfnArgs a) {
+  constexpr int NB = PASS == 0 ? 2 : 1;
+  using G = GemmTile<BM, WM, WN, NB, STAGES>;
+  constexpr bool TAIL = PASS == 0 && BM == 256 && WM * WN == 8;
+  constexpr int LDS = TAIL && 3 * TailTile::STAGE > STAGES * G::STAGE ? 3 * TailTile::STAGE : STAGES * G::STAGE;
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[LDS];
+
+  const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+  tclock_start(a);
+  if constexpr (TAIL) {
+    if ((int)blockIdx.x >= a.tail_block0) {
+      const int bt = xcd_grouped(blockIdx.x - a.tail_block0, gridDim.x - a.tail_block0);
+      const FfnJob jd = a.jobs[0];
+      const int mt = (jd.q1 - jd.q0 + 127) / 128;
+      ffn_tile<128, 2, 4, PASS, 3>(a, lds, jd, (bt % mt) * 128, (a.tail_n0 + bt / mt) * kBN, 0, 0,
+                                   a.hidden / kBK, wave, lane);
+      tclock_end(a);
+      return;
+    }
+  }
+  const int b = xcd_grouped(blockIdx.x, min((int)gridDim.x, a.tail_block0));
+  const int j = gemm_find_job(a, b);
+  int jt = b - a.job_tile0[j];
+  const FfnJob jd = a.jobs[j];
+  const bool shared = jd.pos == kSharedJob;
+  const int N = PASS == 0 ? jd.I : a.hidden;
+  const int K = PASS == 0 ? a.hidden : jd.I;
+  const int M = jd.q1 - jd.q0;
+  const int mtiles = (M + BM - 1) / BM;
+  const int ntiles = N / kBN;
+  // split-K (shared down pass only): slice ks of S writes its own partial output
+  const int S = (PASS == 1 && shared) ? a.ksplit : 1;
+  const int ks = jt / (mtiles * ntiles);
+  jt -= ks * mtiles * ntiles;
+  const int nk = K / kBK;
+  ffn_tile<BM, WM, WN, PASS, STAGES>(a, lds, jd, (jt % mtiles) * BM, (jt / mtiles) * kBN, ks, ks * nk / S,
+                                     (ks + 1) * nk / S, wave, lane);
   tclock_end(a);
 }
 
@@ -362,8 +392,23 @@ static void gemm_dispatch(FfnArgs& a, int pass, hipStream_t s) {
   }
   a.job_tile0[a.n_jobs] = tiles;
   if (tiles == 0) return;
-  if (pass == 0) k_gemm_ffn<BM, WM, WN, 0, S><<<tiles, 64 * WM * WN, 0, s>>>(a);
-  else k_gemm_ffn<BM, WM, WN, 1, S><<<tiles, 64 * WM * WN, 0, s>>>(a);
+  int grid = tiles;
+  a.tail_block0 = tiles;
+  a.tail_n0 = 0;
+  if (pass == 0 && BM == 256 && WM * WN == 8 && a.n_jobs == 1 && tiles % 256 != 0 && tiles > 256) {
+    // whole rounds of full tiles over the 256 CUs, then half-height tiles
+    const int M = a.jobs[0].q1 - a.jobs[0].q0;
+    const int mtiles = (M + BM - 1) / BM, ntiles = a.jobs[0].I / kBN;
+    const int full = tiles / 256 * 256;
+    if (full % mtiles == 0) {
+      a.tail_n0 = full / mtiles;
+      a.tail_block0 = full;
+      a.job_tile0[1] = full;
+      grid = full + (ntiles - a.tail_n0) * ((M + 127) / 128);
+    }
+  }
+  if (pass == 0) k_gemm_ffn<BM, WM, WN, 0, S><<<grid, 64 * WM * WN, 0, s>>>(a);
+  else k_gemm_ffn<BM, WM, WN, 1, S><<<grid, 64 * WM * WN, 0, s>>>(a);
 }
 
 bool gemm_supported(int N, int K) { return N % kBN == 0 && K % kBK == 0; }
