@@ -48,6 +48,23 @@ def test_ragged_token_counts(T):
         m.close()
 
 
+def test_shared_gateup_half_height_tail_tiles():
+    # A one-job gate/up launch whose 256-row tiles overrun whole rounds of the
+    # 256 CUs: 2000 tokens x 40 n-tiles of the shared expert = 8 x 40 = 320
+    # tiles, so 256 full tiles run and the last 8 n-tiles go in 128-row tiles,
+    # the last of which holds 80 tokens.  Sampled tokens include the ragged end.
+    cfg = SMALL.with_(name="tail_tiles", shared_inter=5120, n_layers=1,
+                      workloads=(Workload("prefill", 2000, 1),))
+    T = 2000
+    m = SyntheticModel(cfg, max_tokens=T)
+    try:
+        st = Stack(m, T)
+        sample = np.array([0, 1, 255, 256, 1023, 1500, 1919, 1920, 1950, 1998, 1999])
+        pu.moe_layer_check(cfg, m, st, 0, None, sm.layer_input(cfg, 0, T, tag=7), sample=sample, predict=False)
+    finally:
+        m.close()
+
+
 @pytest.mark.parametrize("T", [1, 40])
 def test_every_expert_through_one_slot(T):
     # k = E: every expert is routed; with one slot each fill must wait for the
