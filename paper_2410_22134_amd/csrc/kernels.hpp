@@ -172,7 +172,7 @@ void launch_ffn(const FfnArgs& a, int pass, int max_tokens, int dtype, hipStream
                 hipEvent_t ev1 = nullptr);
 // Grouped MFMA GEMM (bf16) for the same passes; needs N % 128 == 0 and K % 64 == 0.
 bool gemm_supported(int N, int K);
-int gemm_tiles_shared_down(int T, int H);
+int gemm_shared_down_split(int T, int H);  // split-K slices of the shared down GEMM
 // MFMA rows product: out[t][o_off + n] (=|+=) sum_k W[n][k] x[t][k], bf16 in, fp32 out; K % 64 == 0.
 struct RowsGemmArgs {
   const void* w;

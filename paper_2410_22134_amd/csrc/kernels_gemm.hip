@@ -5,8 +5,9 @@
 //   gate/up: A = token rows of x (gathered through the pair permutation),
 //            B = Wg rows and Wu rows of the expert (dual B), epilogue
 //            act = bf16(silu(A.Wg^T) * (A.Wu^T));
-//   down:    A = activation rows, B = Wd rows, epilogue writes fp32 rows of Y
-//            scattered back to (token, rank).
+//   down:    A = activation rows, B = Wd rows (two adjacent 128-row ranges
+//            when H % 256 == 0), epilogue writes fp32 rows of Y scattered
+//            back to (token, rank).
 // One launch covers a list of jobs (route positions or the shared expert);
 // block b takes tile b of the flat job x m-tile x n-tile list, remapped so the
 // m-tiles that share an n-tile (the same weight rows) run on the same XCD and
@@ -23,6 +24,8 @@
 // 16 rows read by one ds_read_b128 phase fall in distinct banks.  Lane l of an
 // MFMA supplies A[l % 16][8*(l/16)..+8] and B[l % 16][8*(l/16)..+8] and
 // receives C[4*(l/16) + i][l % 16], i < 4.
+#include <algorithm>
+
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -221,12 +224,13 @@ __device__ __forceinline__ int xcd_grouped(int b, int nblk) {
 
 // One output tile of job jd: rows m0 .. m0+BM-1 of its token range, columns
 // n0 .. n0+127 (per B), k-tiles [kt0, kt1), split-K slice ks (down pass of
-// the shared expert).  PASS 0: gate/up (dual B), PASS 1: down.
+// the shared expert).  PASS 0: gate/up (dual B: Wg and Wu rows of one column
+// range), PASS 1: down over columns n0 .. n0+127, PASS 2: down over columns
+// n0 .. n0+255 (two B blocks).
 template <int BM, int WM, int WN, int PASS, int STAGES>
 __device__ __forceinline__ void ffn_tile(const FfnArgs& a, bf16_t* lds, const FfnJob& jd, int m0, int n0, int ks,
                                          int kt0, int kt1, int wave, int lane) {
-  constexpr bool DUAL = PASS == 0;
-  constexpr int NB = DUAL ? 2 : 1;
+  constexpr int NB = PASS == 1 ? 1 : 2;  // PASS 2: down over two adjacent 128-column ranges
   using G = GemmTile<BM, WM, WN, NB, STAGES>;
   const int wm = wave / WN, wn = wave % WN;
   const bool shared = jd.pos == kSharedJob;
@@ -257,7 +261,7 @@ __device__ __forceinline__ void ffn_tile(const FfnArgs& a, bf16_t* lds, const Ff
       src[i] = row + c * 8;
     } else {
       const int rb = r - BM;
-      const int which = rb / kBN, n = n0 + rb % kBN;
+      const int which = rb / kBN, n = n0 + (PASS == 2 ? which * kBN : 0) + rb % kBN;
       const bf16_t* base = PASS == 0 ? W + (size_t)which * I * H : W + (size_t)2 * I * H;  // Wg | Wu, or Wd
       src[i] = base + (size_t)n * K + c * 8;
     }
@@ -279,12 +283,14 @@ __device__ __forceinline__ void ffn_tile(const FfnArgs& a, bf16_t* lds, const Ff
 #pragma unroll
         for (int jn = 0; jn < G::TN; ++jn) {
           const int n = n0 + wn * G::WTN + jn * 16 + lr;
-          act[(size_t)q * I + n] = f32_to_bf16(silu(acc[0][i][jn][r]) * acc[DUAL ? 1 : 0][i][jn][r]);
+          act[(size_t)q * I + n] = f32_to_bf16(silu(acc[0][i][jn][r]) * acc[1][i][jn][r]);
         }
       } else {
         float* Y = shared ? a.Ysh + (size_t)ks * a.ysh_split_stride + (size_t)q * H : a.Y + (size_t)a.perm[q] * H;
 #pragma unroll
-        for (int jn = 0; jn < G::TN; ++jn) Y[n0 + wn * G::WTN + jn * 16 + lr] = acc[0][i][jn][r];
+        for (int h = 0; h < NB; ++h)
+#pragma unroll
+          for (int jn = 0; jn < G::TN; ++jn) Y[n0 + h * kBN + wn * G::WTN + jn * 16 + lr] = acc[h][i][jn][r];
       }
     }
   }
@@ -299,7 +305,7 @@ using TailTile = GemmTile<128, 2, 4, 2, 3>;
 // made of half-size tiles instead of a part-filled round of full ones.
 template <int BM, int WM, int WN, int PASS, int STAGES>
 __global__ __launch_bounds__(64 * WM * WN) void k_gemm_ffn(FfnArgs a) {
-  constexpr int NB = PASS == 0 ? 2 : 1;
+  constexpr int NB = PASS == 1 ? 1 : 2;
   using G = GemmTile<BM, WM, WN, NB, STAGES>;
   constexpr bool TAIL = PASS == 0 && BM == 256 && WM * WN == 8;
   constexpr int LDS = TAIL && 3 * TailTile::STAGE > STAGES * G::STAGE ? 3 * TailTile::STAGE : STAGES * G::STAGE;
@@ -327,13 +333,13 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_ffn(FfnArgs a) {
   const int K = PASS == 0 ? a.hidden : jd.I;
   const int M = jd.q1 - jd.q0;
   const int mtiles = (M + BM - 1) / BM;
-  const int ntiles = N / kBN;
+  const int ntiles = N / (PASS == 2 ? 2 * kBN : kBN);
   // split-K (shared down pass only): slice ks of S writes its own partial output
-  const int S = (PASS == 1 && shared) ? a.ksplit : 1;
+  const int S = (PASS != 0 && shared) ? a.ksplit : 1;
   const int ks = jt / (mtiles * ntiles);
   jt -= ks * mtiles * ntiles;
   const int nk = K / kBK;
-  ffn_tile<BM, WM, WN, PASS, STAGES>(a, lds, jd, (jt % mtiles) * BM, (jt / mtiles) * kBN, ks, ks * nk / S,
+  ffn_tile<BM, WM, WN, PASS, STAGES>(a, lds, jd, (jt % mtiles) * BM, (jt / mtiles) * kBN * (PASS == 2 ? 2 : 1), ks, ks * nk / S,
                                      (ks + 1) * nk / S, wave, lane);
   tclock_end(a);
 }
@@ -379,8 +385,13 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_rows(RowsGemmArgs a) {
     }
 }
 
+// Down pass over pairs of adjacent 128-column ranges (PASS 2): a 256 x 256
+// output tile, the same reuse of each loaded row as the dual-B gate/up tile.
+static bool down_pair(int H) { return H % (2 * kBN) == 0; }
+
 template <int BM, int WM, int WN, int S>
 static void gemm_dispatch(FfnArgs& a, int pass, hipStream_t s) {
+  const bool down2 = pass == 1 && down_pair(a.hidden);
   int tiles = 0;
   for (int j = 0; j < a.n_jobs; ++j) {
     a.job_tile0[j] = tiles;
@@ -388,7 +399,7 @@ static void gemm_dispatch(FfnArgs& a, int pass, hipStream_t s) {
     const int N = pass == 0 ? a.jobs[j].I : a.hidden;
     const int M = a.jobs[j].q1 - a.jobs[j].q0;
     const int split = (pass == 1 && sh) ? a.ksplit : 1;
-    tiles += ((M + BM - 1) / BM) * (N / kBN) * split;
+    tiles += ((M + BM - 1) / BM) * (N / (pass == 1 && down2 ? 2 * kBN : kBN)) * split;
   }
   a.job_tile0[a.n_jobs] = tiles;
   if (tiles == 0) return;
@@ -408,13 +419,16 @@ static void gemm_dispatch(FfnArgs& a, int pass, hipStream_t s) {
     }
   }
   if (pass == 0) k_gemm_ffn<BM, WM, WN, 0, S><<<grid, 64 * WM * WN, 0, s>>>(a);
+  else if (down2) k_gemm_ffn<BM, WM, WN, 2, S><<<grid, 64 * WM * WN, 0, s>>>(a);
   else k_gemm_ffn<BM, WM, WN, 1, S><<<grid, 64 * WM * WN, 0, s>>>(a);
 }
 
 bool gemm_supported(int N, int K) { return N % kBN == 0 && K % kBK == 0; }
 
-// Tile height: the tallest of 256 / 128 / 64 rows whose tile count still covers
-// the 256 CUs (most reuse of each weight tile while filling the machine).
+// Tile height: the tallest of 256 / 128 / 64 rows whose count of 128-column
+// tiles still covers the 256 CUs (most reuse of each weight tile while filling
+// the machine; a down pass over column pairs then runs half as many blocks of
+// twice the work, which measured faster than the next smaller height).
 static int pick_bm(const FfnArgs& a, int pass, int max_tokens) {
   const int cands[3] = {256, 128, 64};
   for (int ci = 0; ci < 3; ++ci) {
@@ -433,9 +447,18 @@ static int pick_bm(const FfnArgs& a, int pass, int max_tokens) {
   return 64;
 }
 
-int gemm_tiles_shared_down(int T, int H) {
+// Split-K slices of the shared expert's down GEMM, which has only (T / BM) x
+// (H / 256) output tiles.  Over column pairs: as many slices as fit in one
+// round of blocks over the 256 CUs (Qwen2-57B shape, 56 tiles: split 4 at
+// 140 us against 150 / 162 / 150 us for splits 2 / 7 / 8).  Over single
+// columns: the smallest split giving at least 1.5 rounds (112 tiles: split 4
+// at 195 us against 242 / 250 / 238 / 209 us for splits 2 / 3 / 5 / 6).
+int gemm_shared_down_split(int T, int H) {
   const int bm = T >= 512 ? 256 : (T > 64 ? 128 : 64);
-  return ((T + bm - 1) / bm) * (H / kBN);
+  const int mt = (T + bm - 1) / bm;
+  if (down_pair(H)) return std::max(1, 256 / (mt * (H / (2 * kBN))));
+  const int tiles = mt * (H / kBN);
+  return (384 + tiles - 1) / tiles;
 }
 
 void launch_gemm_rows(const RowsGemmArgs& a, hipStream_t s) {

@@ -1103,20 +1103,13 @@ int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const in
   a.shared_w = c->lw[layer].shared;
   a.act_sh = c->d_act_sh;
   a.Ysh = c->d_Ysh;
-  // The shared expert's down GEMM has only (T / BM) x (H / 128) output tiles;
-  // split its reduction so the launch covers the CUs.  Slices write separate
-  // partial outputs that the combine adds in slice order (deterministic).  The
-  // smallest split giving at least 1.5 rounds of blocks over the 256 CUs was
-  // the fastest measured (Qwen2-57B shape, 112 tiles: split 4 at 195 us against
-  // 242 / 250 / 238 / 209 us for splits 2 / 3 / 5 / 6).
+  // The shared expert's down GEMM has few output tiles; split its reduction so
+  // the launch covers the CUs (gemm_shared_down_split).  Slices write separate
+  // partial outputs that the combine adds in slice order (deterministic).
   a.ksplit = 1;
   a.ysh_split_stride = (int64_t)T * c->H;
-  if (c->Ish > 0 && use_gemm(c, T, true)) {
-    const int tiles = gemm_tiles_shared_down(T, c->H);
-    int sp = (384 + tiles - 1) / tiles;
-    sp = std::max(1, std::min(std::min(sp, kMaxSplit), c->Ish / 64 / 4));
-    a.ksplit = sp;
-  }
+  if (c->Ish > 0 && use_gemm(c, T, true))
+    a.ksplit = std::max(1, std::min(std::min(gemm_shared_down_split(T, c->H), kMaxSplit), c->Ish / 64 / 4));
 
   std::unique_lock<std::mutex> lk(c->mu);
   const int n = rec.n;
