@@ -544,43 +544,35 @@ __global__ __launch_bounds__(kThreads) void k_ffn_down_q4(FfnArgs a) {
   tclock_end(a);
 }
 
-// Dequantise whole experts for the MFMA GEMM: one thread per 16-byte piece of
-// codes (32 weights of one row), writing 64 bytes of bf16.
+// Dequantise whole experts for the MFMA GEMM: block (r, e) expands weight row r
+// of expert e (gate rows, then up rows, then down rows); each thread turns 8
+// weights (4 code bytes, low nibble first) into one 16-byte store of bf16, so
+// a wave writes 1 KB contiguously.
 __global__ __launch_bounds__(kThreads) void k_dequant_q4(DequantArgs a) {
   const int I = a.inter, H = a.hidden;
-  const int64_t per_mat = (int64_t)I * H / 32;  // pieces per matrix
-  const int64_t p = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (p >= 3 * per_mat) return;
-  const int mtx = (int)(p / per_mat);
-  const int64_t pm = p - mtx * per_mat;
+  int r = blockIdx.x, mtx = 0;
+  if (r >= I) { r -= I; mtx = 1; }
+  if (mtx == 1 && r >= I) { r -= I; mtx = 2; }
   const int K = mtx < 2 ? H : I, R = mtx < 2 ? I : H;
-  const int row = (int)(pm / (K / 32)), c = (int)(pm % (K / 32));
   const uint8_t* mat = a.src[blockIdx.y] + (size_t)mtx * ((size_t)I * H / 2 + (size_t)I * (H / kInt4Group) * 2);
-  const Q4Row q = q4_row(mat, R, K, row);
-  const uint4 w = ld16_stream(q.codes + (size_t)c * 16);
-  const float sc = bf16_to_f32(q.scales[c / 4]);
-  const uint32_t ww[4] = {w.x, w.y, w.z, w.w};
-  uint32_t out[16];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const uint32_t lo = ww[i] & 0x0F0F0F0Fu, hi = (ww[i] >> 4) & 0x0F0F0F0Fu;
+  const Q4Row q = q4_row(mat, R, K, r);
+  uint4* dst = reinterpret_cast<uint4*>(a.dst + (size_t)blockIdx.y * 3 * I * H + (size_t)mtx * I * H + (size_t)r * K);
+  for (int c = threadIdx.x; c < K / 8; c += kThreads) {  // 8-weight chunks of the row
+    const uint32_t w = __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(q.codes) + c);
+    const float sc = bf16_to_f32(q.scales[c / (kInt4Group / 8)]);
+    uint32_t out[4];
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
-      const float e0 = ((float)((lo >> (8 * b)) & 0xFFu) - 8.0f) * sc;
-      const float e1 = ((float)((hi >> (8 * b)) & 0xFFu) - 8.0f) * sc;
-      out[4 * i + b] = (uint32_t)f32_to_bf16(e0) | ((uint32_t)f32_to_bf16(e1) << 16);
+      const float e0 = ((float)((w >> (8 * b)) & 0xFu) - 8.0f) * sc;
+      const float e1 = ((float)((w >> (8 * b + 4)) & 0xFu) - 8.0f) * sc;
+      out[b] = (uint32_t)f32_to_bf16(e0) | ((uint32_t)f32_to_bf16(e1) << 16);
     }
+    dst[c] = make_uint4(out[0], out[1], out[2], out[3]);
   }
-  uint4* dst = reinterpret_cast<uint4*>(a.dst + (size_t)blockIdx.y * 3 * I * H + (size_t)mtx * I * H +
-                                        (size_t)row * K + (size_t)c * 32);
-#pragma unroll
-  for (int v = 0; v < 4; ++v) dst[v] = make_uint4(out[4 * v], out[4 * v + 1], out[4 * v + 2], out[4 * v + 3]);
 }
 
 void launch_dequant_q4(const DequantArgs& a, hipStream_t s) {
-  const int64_t pieces = 3 * (int64_t)a.inter * a.hidden / 32;
-  const dim3 grid((unsigned)((pieces + kThreads - 1) / kThreads), a.n);
-  k_dequant_q4<<<grid, kThreads, 0, s>>>(a);
+  k_dequant_q4<<<dim3(2 * a.inter + a.hidden, a.n), kThreads, 0, s>>>(a);  // one block per weight row
 }
 
 // ============================================================ combine
