@@ -168,6 +168,41 @@ def test_int4_experts(T):
         m.close()
 
 
+@pytest.mark.parametrize("T", [77, 300])
+def test_down_over_single_column_ranges(T):
+    # hidden 384 is not a multiple of 256, so the down GEMM runs 128-column tiles
+    # (the column-pair tiles need H % 256 == 0); 300 tokens use 256-row tiles
+    cfg = SMALL.with_(name="h384", hidden=384, n_layers=2)
+    _log("h384 T", T)
+    m = SyntheticModel(cfg, max_tokens=T)
+    try:
+        st = Stack(m, T)
+        lcs = {l: ocache.LayerCache(cfg.n_experts, cfg.slots) for l in range(cfg.n_layers)}
+        for l in range(cfg.n_layers):
+            pu.moe_layer_check(cfg, m, st, l, lcs, sm.layer_input(cfg, l, T, tag=900 + T))
+        pu.check_counters(m, lcs)
+    finally:
+        m.close()
+
+
+def test_int4_prefill_long_rows():
+    # 4-bit experts whose rows exceed 256 chunks of 8 weights (hidden 2304, inter
+    # 2176), so the dequantising expansion loops over each row
+    cfg = SMALL.with_(name="int4_long", hidden=2304, inter=2176, shared_inter=512, n_layers=2,
+                      weight_format="int4")
+    T = 77
+    m = SyntheticModel(cfg, max_tokens=T)
+    try:
+        st = Stack(m, T)
+        lcs = {l: ocache.LayerCache(cfg.n_experts, cfg.slots) for l in range(cfg.n_layers)}
+        sample = np.array([0, 1, 38, 75, 76])
+        for l in range(cfg.n_layers):
+            pu.moe_layer_check(cfg, m, st, l, lcs, sm.layer_input(cfg, l, T, tag=950), sample=sample)
+        pu.check_counters(m, lcs)
+    finally:
+        m.close()
+
+
 def test_external_pushes_low_and_high():
     cfg = SMALL.with_(n_layers=1, lookahead=0)
     m = SyntheticModel(cfg, max_tokens=2)
