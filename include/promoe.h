@@ -3,17 +3,20 @@
  * Mixture-of-Experts inference, after ProMoE (arXiv 2410.22134, "ProMoE: Fast
  * MoE-based LLM Serving using Proactive Caching").
  *
- * One MoE layer step is   promoe_predict (optional)
- *                      -> promoe_route
+ * One MoE layer step is   promoe_route
+ *                      -> promoe_predict (optional)
  *                      -> promoe_expert_ffn
- * on one stream.  The predictor of layer l scores the experts of layer
- * l+lookahead and queues their missing chunks as low-priority copies (the
- * paper's PushPredictedExperts, Alg. 2); the route call gates layer l, drops
- * the layer's remaining low-priority work, queues its missing experts at high
- * priority and returns the reordered expert list (PushPreciseExperts, Alg. 2,
- * "Early Preemption", "Reordered Inference"); the FFN call computes the experts
- * in that order, each waiting only for its own chunks (the dependency
- * mechanism of Sec. "System Integration").
+ * on one stream (with lookahead 0 promoe_predict comes first: it plans the
+ * layer the route then uses).  promoe_predict may also precede the route at
+ * any lookahead; after it, the low-priority copies it queues for layer
+ * l+lookahead go behind layer l's high-priority ones.  The predictor of layer
+ * l scores the experts of layer l+lookahead and queues their missing chunks as
+ * low-priority copies (the paper's PushPredictedExperts, Alg. 2); the route
+ * call gates layer l, drops the layer's remaining low-priority work, queues
+ * its missing experts at high priority and returns the reordered expert list
+ * (PushPreciseExperts, Alg. 2, "Early Preemption", "Reordered Inference"); the
+ * FFN call computes the experts in that order, each waiting only for its own
+ * chunks (the dependency mechanism of Sec. "System Integration").
  *
  * Conventions
  *  - Every call returns an int: 0 (PROMOE_OK) or a negative promoe_err.
@@ -209,7 +212,8 @@ int promoe_set_initial_cache(promoe_ctx* ctx, int layer, const int32_t* h_expert
 /* Look-ahead prediction (Sec. "Learning-based Predictor", "Stride Prefetching";
  * Alg. 2 PushPredictedExperts).  One fused pass over d_x [T x H] computes the
  * gate logits of `layer` (reused by the next promoe_route of that layer on the
- * same d_x) and the predictor of layer+lookahead; per-token top-k of the
+ * same d_x; skipped when that route already ran on the same d_x and T) and the
+ * predictor of layer+lookahead; per-token top-k of the
  * predictor output; an integer vote merges the tokens' picks into a list Q of
  * at most slots_per_layer experts (votes desc, best rank asc, id asc); the
  * target layer's cache is planned on the device: resident members are

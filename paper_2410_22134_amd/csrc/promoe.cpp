@@ -156,6 +156,7 @@ struct promoe_ctx {
   // route -> ffn hand-over
   int route_layer = -1;
   int route_T = 0;
+  const void* route_x = nullptr;  // input of the pending route (its gate logits are in d_logits)
   PlanRecord route_rec{};
   std::vector<int64_t> need01, need2;  // copy seq each position waits for (-1 none)
   std::vector<int> need_q;             // engine queue of those copies
@@ -405,13 +406,18 @@ int check_tokens(promoe_ctx* c, int T) {
 
 // Gate (+ shared-gate row) (+ predictor first layer) rows over x, one launch:
 // columns [0, E) gate logits, E shared-gate logit (if any), then predictor rows.
-int launch_gate_rows(promoe_ctx* c, int layer, const void* d_x, int T, bool with_pred, hipStream_t s) {
+// Gate rows (and the shared-gate row) of `layer` into d_logits columns
+// [0, pred_col), and with `with_pred` the predictor's first rows from column
+// pred_col; `gate` = false computes the predictor rows only (the gate columns
+// already hold this input's logits).
+int launch_gate_rows(promoe_ctx* c, int layer, const void* d_x, int T, bool with_pred, hipStream_t s,
+                     bool gate = true) {
   const LayerW& w = c->lw[layer];
   RowsArgs a{};
-  a.w[0] = w.wg;
-  a.nrows[0] = c->E;
-  a.w[1] = w.sgate;
-  a.nrows[1] = w.sgate ? 1 : 0;
+  a.w[0] = gate ? w.wg : nullptr;
+  a.nrows[0] = gate ? c->E : 0;
+  a.w[1] = gate ? w.sgate : nullptr;
+  a.nrows[1] = gate && w.sgate ? 1 : 0;
   a.w[2] = with_pred ? w.pw1 : nullptr;
   a.nrows[2] = with_pred ? (c->Ph > 0 ? c->Ph : c->E) : 0;
   a.K = c->H;
@@ -421,7 +427,8 @@ int launch_gate_rows(promoe_ctx* c, int layer, const void* d_x, int T, bool with
   a.T = T;
   a.out = c->d_logits;
   a.ldo = c->ld_logits;
-  a.o_off = 0;
+  a.o_off = gate ? 0 : c->pred_col;  // the row groups land in consecutive columns
+  if (a.nrows[0] + a.nrows[1] + a.nrows[2] == 0) return PROMOE_OK;
   if (c->dt == PROMOE_BF16 && T >= 64 && c->H % 64 == 0) {
     // prefill-sized: gate and predictor rows on MFMA, the single shared-gate row as a GEMV
     RowsGemmArgs g{};
@@ -433,7 +440,7 @@ int launch_gate_rows(promoe_ctx* c, int layer, const void* d_x, int T, bool with
     g.T = T;
     g.out = c->d_logits;
     g.ldo = c->ld_logits;
-    launch_gemm_rows(g, s);
+    if (gate) launch_gemm_rows(g, s);
     if (a.nrows[1]) {
       RowsArgs r = a;
       r.w[0] = w.sgate;
@@ -782,11 +789,16 @@ int promoe_predict(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_
     g_last_error = "prediction for a layer whose route is not consumed";
     return PROMOE_ESTATE;
   }
-  rc = launch_gate_rows(c, layer, d_x, T, has_pred, s);
+  // After route(layer) on the same input the gate logits are already in
+  // d_logits: only the predictor rows are computed.
+  const bool routed = c->route_layer == layer && c->route_x == d_x && c->route_T == T;
+  rc = launch_gate_rows(c, layer, d_x, T, has_pred, s, !routed);
   if (rc) return rc;
-  c->gate_layer = layer;
-  c->gate_x = d_x;
-  c->gate_T = T;
+  if (!routed) {
+    c->gate_layer = layer;
+    c->gate_x = d_x;
+    c->gate_T = T;
+  }
   if (n_q) *n_q = 0;
   if (!has_pred) return PROMOE_OK;
   int32_t* pids = d_pred_ids ? d_pred_ids : c->d_pred_ids;
@@ -953,6 +965,7 @@ int promoe_route(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_id
   c->cv.notify_all();
   c->route_layer = layer;
   c->route_T = T;
+  c->route_x = d_x;
   c->route_rec = rec;
   if (h_order)
     for (int i = 0; i < rec.n; ++i) h_order[i] = rec.expert[i];
