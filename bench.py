@@ -190,6 +190,7 @@ def cpu_baseline(cfg, model, budget_s):
 def _oracle_token(cfg, model, lcs, h, t0, budget_s):
     """One decode token through the oracle's layers (stops early past the budget);
     returns the layers done."""
+    import numpy as np
     from oracle import bf16 as obf
     from oracle import ffn as offn
     from oracle import predictor as opred
