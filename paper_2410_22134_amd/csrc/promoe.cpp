@@ -18,6 +18,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <condition_variable>
 #include <cstdio>
 #include <cstring>
@@ -366,6 +367,26 @@ void publish(promoe_ctx* c, int64_t r) {
     if (c->rec_pub < r + 1) c->rec_pub = r + 1;
   }
   c->cv.notify_all();
+}
+
+// Wait until plan record r is readable on the host.  The plan kernel writes
+// the record's `done` word last, after a system-scope fence, before the kernel
+// ends; polling that word sees the plan sooner than the kernel's completion
+// event.  Every 256 polls the event is queried: it ends the wait if the kernel
+// has completed, and reports a failed stream instead of spinning on.
+hipError_t wait_record(promoe_ctx* c, int64_t r) {
+  const volatile int32_t* done = &c->rec_h[r % kRecRing].done;
+  for (uint32_t i = 1;; ++i) {
+    if (*done) break;
+    if ((i & 255) == 0) {
+      const hipError_t q = hipEventQuery(c->rec_ev[r % kRecRing]);
+      if (q == hipSuccess) break;
+      if (q != hipErrorNotReady) return q;
+    }
+    __builtin_ia32_pause();
+  }
+  std::atomic_thread_fence(std::memory_order_acquire);
+  return hipSuccess;
 }
 
 int64_t record_compute(promoe_ctx* c, hipStream_t s) {
@@ -917,14 +938,14 @@ int promoe_route(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_id
   launch_plan_precise(plan_args(c, layer, d_ids, T, r), s);
   hipError_t le = hipGetLastError();
   if (le == hipSuccess) le = hipEventRecord(c->rec_ev[r % kRecRing], s);
-  if (le == hipSuccess) le = hipEventSynchronize(c->rec_ev[r % kRecRing]);
+  if (le == hipSuccess) le = wait_record(c, r);
   publish(c, r);
   if (le != hipSuccess) return fail_hip(le, "plan_precise");
   c->lw[layer].planned = true;
 
   std::unique_lock<std::mutex> lk(c->mu);
   while (c->rec_ingested < r) {  // earlier plans on the same stream: complete
-    HIPCHK(hipEventSynchronize(c->rec_ev[c->rec_ingested % kRecRing]));
+    HIPCHK(wait_record(c, c->rec_ingested));
     ingest_spec(c, c->rec_ingested);
   }
   const PlanRecord rec = c->rec_h[r % kRecRing];
