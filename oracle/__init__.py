@@ -15,6 +15,9 @@ using Proactive Caching, arXiv 2410.22134):
                    "Cache Implementation");
 * ``stack``     -- harness ops around the MoE block (RMSNorm, a linear
                    attention surrogate, residual adds);
+* ``quant``     -- decoding of group-quantised 4-bit expert weights (the
+                   paper's bits-per-weight study): (code - 8) x scale per
+                   group of 128 weights of a row;
 * ``brute``     -- brute-force checkers used only to pin the oracle itself.
 
 Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
@@ -28,4 +31,4 @@ Parity unpinned: predictor *accuracy* against the paper's trained-predictor
 figures, and all physical timing (bytes copied before a purge, stall time) --
 those are reported, not parity-checked.
 """
-from . import bf16, router, predictor, ffn, cache, stack, brute  # noqa: F401
+from . import bf16, router, predictor, ffn, cache, stack, brute, quant  # noqa: F401
