@@ -22,8 +22,23 @@ void Prefetcher::assign(int layer, int slot, int expert) {
     if (it->layer == layer && it->slot == slot) it = low_.erase(it);
     else ++it;
   }
+  bool busy = false;  // an earlier copy into the slot may still be in flight
+  for (const auto& c : s.ch) busy = busy || c.last >= retired_;
+  if (!busy) s.queue = pick_queue();
   s.expert = expert;
   for (auto& c : s.ch) c = Chunk();
+}
+
+int Prefetcher::pick_queue() {
+  const int nq = eng_->queues();
+  if ((int)q_bytes_.size() < nq) q_bytes_.resize(nq, 0);
+  int best = q_next_ % nq;
+  for (int i = 1; i < nq; ++i) {
+    const int q = (q_next_ + i) % nq;
+    if (q_bytes_[q] < q_bytes_[best]) best = q;
+  }
+  q_next_ = best + 1;
+  return best;
 }
 
 void Prefetcher::mark_resident(int layer, int slot, int expert) {
@@ -72,8 +87,9 @@ void Prefetcher::issue_sub(int layer, int slot, int chunk, Prio prio, int64_t af
     retire();
   }
   int64_t seq = next_seq_++;
-  note_issued(prio);
-  eng_->issue(seq, cache_ + slot_off, src, bytes, after, queue_of(layer, slot));
+  const int q = queue_of(layer, slot);
+  note_issued(prio, q, (int64_t)bytes);
+  eng_->issue(seq, cache_ + slot_off, src, bytes, after, q);
   ch.n_issued++;
   ch.last = seq;
   st_.copies[prio]++;
@@ -132,10 +148,10 @@ void Prefetcher::issue_pending(int layer, int slot, int64_t after_compute, Prio 
       retire();
     }
     const int64_t seq = next_seq_++;
-    note_issued(prio);
+    const int q = queue_of(layer, slot);
+    note_issued(prio, q, (int64_t)(end - start));
     const size_t slot_off = ((size_t)layer * C_ + slot) * expert_bytes;
-    eng_->issue(seq, cache_ + slot_off + start, host_[layer * E_ + s.expert] + start, end - start, after,
-                queue_of(layer, slot));
+    eng_->issue(seq, cache_ + slot_off + start, host_[layer * E_ + s.expert] + start, end - start, after, q);
     st_.copies[prio]++;
     st_.bytes[prio] += (int64_t)(end - start);
     first = false;
@@ -193,15 +209,19 @@ int Prefetcher::pump() {
   return n;
 }
 
-void Prefetcher::note_issued(Prio prio) {
-  prio_of_.push_back((uint8_t)prio);
+void Prefetcher::note_issued(Prio prio, int queue, int64_t bytes) {
+  inflight_.push_back(InFlight{(uint8_t)prio, (uint8_t)queue, bytes});
+  if ((int)q_bytes_.size() <= queue) q_bytes_.resize(queue + 1, 0);
+  q_bytes_[queue] += bytes;
   if (prio == LOW) ++low_in_flight_;
 }
 
 void Prefetcher::retire() {
   while (retired_ < next_seq_ && eng_->done(retired_)) {
-    if (prio_of_.front() == LOW) --low_in_flight_;
-    prio_of_.pop_front();
+    const InFlight& f = inflight_.front();
+    if (f.prio == LOW) --low_in_flight_;
+    q_bytes_[f.queue] -= f.bytes;
+    inflight_.pop_front();
     ++retired_;
   }
 }

@@ -111,8 +111,15 @@ class Prefetcher {
   // Record that compute token `tok` reads the slot.
   void set_last_read(int layer, int slot, int64_t tok);
   int expert_in(int layer, int slot) const { return slot_(layer, slot).expert; }
-  // Engine queue of every copy into the slot.
-  int queue_of(int layer, int slot) const { return (layer * C_ + slot) % eng_->queues(); }
+  // Engine queue of the copies into the slot.  A slot keeps its queue while any
+  // copy into it may be in flight (so copies into one slot stay ordered); when
+  // it is given a new expert with nothing in flight it moves to the queue with
+  // the fewest bytes outstanding, so fills spread over the queues and the link
+  // never waits on one queue's per-copy gap while another has work.
+  int queue_of(int layer, int slot) const {
+    const int q = slot_(layer, slot).queue;
+    return q >= 0 ? q : (layer * C_ + slot) % eng_->queues();
+  }
 
   const PhysStats& stats() const { return st_; }
   void reset_stats() { st_ = PhysStats(); }
@@ -126,8 +133,13 @@ class Prefetcher {
   };
   struct Slot {
     int expert = -1;
+    int queue = -1;  // engine queue (-1: not chosen yet)
     int64_t last_read = -1;
     Chunk ch[kChunks];
+  };
+  struct InFlight {
+    uint8_t prio, queue;
+    int64_t bytes;
   };
   struct LowTask {
     int layer, slot, chunk, expert;
@@ -136,7 +148,8 @@ class Prefetcher {
   Slot& slot_(int l, int s) { return slots_[l * C_ + s]; }
   const Slot& slot_(int l, int s) const { return slots_[l * C_ + s]; }
   void issue_sub(int layer, int slot, int chunk, Prio prio, int64_t after_compute);
-  void note_issued(Prio prio);
+  void note_issued(Prio prio, int queue, int64_t bytes);
+  int pick_queue();
   // Issue every pending sub-copy of the slot (coalesced when merge_ > 0),
   // dropping its queued low-priority tasks.
   void issue_pending(int layer, int slot, int64_t after_compute, Prio prio);
@@ -153,7 +166,9 @@ class Prefetcher {
   std::deque<LowTask> low_;
   int64_t next_seq_ = 0;
   int64_t retired_ = 0;  // copies [0, retired_) are known complete
-  std::deque<uint8_t> prio_of_;  // priority of each copy in [retired_, next_seq_)
+  std::deque<InFlight> inflight_;  // each copy in [retired_, next_seq_)
+  std::vector<int64_t> q_bytes_;   // bytes in flight per engine queue
+  int q_next_ = 0;                 // tie-break rotation for pick_queue
   int64_t low_in_flight_ = 0;
   PhysStats st_;
 };

@@ -34,6 +34,7 @@ struct FakeEngine : CopyEngine {
     uint8_t* dst;
     size_t bytes;
     int64_t after;
+    double issued;  // host time of the issue call
   };
   std::vector<Copy> log;
   std::map<int64_t, double> compute_done;  // compute token -> completion time
@@ -49,7 +50,7 @@ struct FakeEngine : CopyEngine {
       start = std::max(start, it == compute_done.end() ? 1e30 : it->second);
     }
     if ((int64_t)log.size() != seq) std::abort();
-    log.push_back({start, start + (double)bytes / bw, static_cast<uint8_t*>(dst), bytes, after});
+    log.push_back({start, start + (double)bytes / bw, static_cast<uint8_t*>(dst), bytes, after, now});
   }
   bool done(int64_t seq) override { return log[seq].end <= now + 1e-12; }
   void wait(int64_t seq) override { now = std::max(now, log[seq].end); }
@@ -152,8 +153,9 @@ void test_whole_expert_low() {
   }
 }
 
-// With several engine queues, every copy into one slot uses the same queue (so
-// copies into a slot stay ordered), and different slots spread over the queues.
+// With several engine queues, copies into one slot stay ordered: a copy goes to
+// another queue than the slot's previous copy only once that copy completed.
+// Slots given new experts spread over the queues.
 void test_queue_per_slot() {
   Rig r(2, 4, 8, 100, 50, 2, 1000);
   r.eng.nq = 2;
@@ -168,7 +170,10 @@ void test_queue_per_slot() {
   r.pf->assign(1, 2, 5);
   r.pf->issue_high(1, 2);
   r.worker_until(100.0);
-  std::map<uint8_t*, int> q_of_slot;
+  r.pf->assign(0, 1, 7);  // everything completed: the slot may move
+  r.pf->issue_high(0, 1);
+  r.worker_until(200.0);
+  std::map<uint8_t*, size_t> last_into;  // slot base -> index of its latest copy
   bool used[2] = {false, false};
   for (size_t i = 0; i < r.eng.log.size(); ++i) {
     const size_t off = r.eng.log[i].dst - r.cache.data();
@@ -176,11 +181,27 @@ void test_queue_per_slot() {
     const int q = r.eng.queue_of_copy[i];
     CHECK(q == 0 || q == 1);
     used[q] = true;
-    auto it = q_of_slot.find(slot_base);
-    if (it == q_of_slot.end()) q_of_slot[slot_base] = q;
-    else CHECK(it->second == q);
+    auto it = last_into.find(slot_base);
+    if (it != last_into.end() && r.eng.queue_of_copy[it->second] != q)
+      CHECK(r.eng.log[it->second].end <= r.eng.log[i].issued + 1e-12);
+    last_into[slot_base] = i;
   }
   CHECK(used[0] && used[1]);
+}
+
+// Fills issued one after another alternate between two queues: each goes to
+// the queue with fewer bytes in flight.
+void test_fills_balance_queues() {
+  Rig r(1, 6, 8, 100, 100, 2, 1000);
+  r.eng.nq = 2;
+  r.eng.bw = 100.0;
+  for (int s = 0; s < 6; ++s) {
+    r.pf->assign(0, s, s);
+    r.pf->issue_high(0, s);
+  }
+  CHECK(r.eng.log.size() == 6u);
+  for (int s = 0; s < 6; ++s) CHECK(r.pf->queue_of(0, s) == s % 2);
+  for (size_t i = 0; i < r.eng.log.size(); ++i) CHECK(r.eng.queue_of_copy[i] == (int)(i % 2));
 }
 
 // High-priority copies in flight do not count against the low-priority window:
@@ -407,6 +428,7 @@ int main(int argc, char** argv) {
   test_whole_expert_low();
   test_low_queues_behind_high();
   test_queue_per_slot();
+  test_fills_balance_queues();
   test_window_bound();
   test_purge_dedupe_and_priority();
   test_ready_and_war();
