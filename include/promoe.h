@@ -9,7 +9,9 @@
  * on one stream (with lookahead 0 promoe_predict comes first: it plans the
  * layer the route then uses).  promoe_predict may also precede the route at
  * any lookahead; after it, the low-priority copies it queues for layer
- * l+lookahead go behind layer l's high-priority ones.  The predictor of layer
+ * l+lookahead go behind layer l's high-priority ones.  With lookahead >= 1 it
+ * may also follow promoe_expert_ffn (while d_x still holds layer l's input).
+ * The predictor of layer
  * l scores the experts of layer l+lookahead and queues their missing chunks as
  * low-priority copies (the paper's PushPredictedExperts, Alg. 2); the route
  * call gates layer l, drops the layer's remaining low-priority work, queues
@@ -212,7 +214,8 @@ int promoe_set_initial_cache(promoe_ctx* ctx, int layer, const int32_t* h_expert
 /* Look-ahead prediction (Sec. "Learning-based Predictor", "Stride Prefetching";
  * Alg. 2 PushPredictedExperts).  One fused pass over d_x [T x H] computes the
  * gate logits of `layer` (reused by the next promoe_route of that layer on the
- * same d_x; skipped when that route already ran on the same d_x and T) and the
+ * same d_x; skipped when the latest route was of this layer on the same d_x
+ * and T, before or after its promoe_expert_ffn) and the
  * predictor of layer+lookahead; per-token top-k of the
  * predictor output; an integer vote merges the tokens' picks into a list Q of
  * at most slots_per_layer experts (votes desc, best rank asc, id asc); the
@@ -232,8 +235,14 @@ int promoe_predict(promoe_ctx* ctx, int layer, const void* d_x, int T, int32_t* 
  * shared expert d_shared_scale [T] = sigmoid(w_sg . x) (else may be NULL).
  * Then the precise plan: pending low-priority copies of the layer are dropped,
  * order = resident experts by fill order then missing experts by id; missing
- * experts get slots and are copied at high priority.  Synchronises with the
- * stream once.  h_order [>= E] receives the order, *n_order its length. */
+ * experts get slots and are copied at high priority.  A missing expert whose
+ * slot a resident one of the same step must read first is copied after that
+ * read; for steps of more than 64 routed tokens (T * k) the route itself
+ * enqueues the FFN of the readers of the first two such slots, right behind
+ * the plan, so those copies start while the caller goes on (the FFN call
+ * computes the rest; d_x must keep its contents until then, as for the FFN
+ * call).  Synchronises with the stream once.  h_order [>= E] receives the
+ * order, *n_order its length. */
 int promoe_route(promoe_ctx* ctx, int layer, const void* d_x, int T, int32_t* d_ids, float* d_w,
                  float* d_shared_scale, int32_t* h_order, int32_t* n_order, void* stream);
 

@@ -175,7 +175,10 @@ struct promoe_ctx {
   // route -> ffn hand-over
   int route_layer = -1;
   int route_T = 0;
-  const void* route_x = nullptr;  // input of the pending route (its gate logits are in d_logits)
+  const void* route_x = nullptr;  // input of the latest route (its gate logits are in d_logits)
+  int last_route_layer = -1;      // layer of the latest route, kept after its FFN call
+  std::vector<char> ffn_started;  // per route position: launched by the route itself
+  int64_t route_head_tok = -1;    // compute token of that launch (-1 none)
   PlanRecord route_rec{};
   std::vector<int64_t> need01, need2;  // copy seq each position waits for (-1 none)
   std::vector<int> need_q;             // engine queue of those copies
@@ -832,9 +835,10 @@ int promoe_predict(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_
     g_last_error = "prediction for a layer whose route is not consumed";
     return PROMOE_ESTATE;
   }
-  // After route(layer) on the same input the gate logits are already in
-  // d_logits: only the predictor rows are computed.
-  const bool routed = c->route_layer == layer && c->route_x == d_x && c->route_T == T;
+  // After route(layer) on the same input (its FFN call done or not) no route
+  // needs this layer's gate logits any more: only the predictor rows are
+  // computed.
+  const bool routed = c->last_route_layer == layer && c->route_x == d_x && c->route_T == T;
   rc = launch_gate_rows(c, layer, d_x, T, has_pred, s, !routed);
   if (rc) return rc;
   if (!routed) {
@@ -921,6 +925,8 @@ int promoe_prefetch(promoe_ctx* c, int target_layer, const int32_t* h_ids, int n
   return PROMOE_OK;
 }
 
+static int launch_route_head(promoe_ctx* c, int layer, const void* d_x, int T, hipStream_t s);
+
 int promoe_route(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_ids, float* d_w,
                  float* d_shared_scale, int32_t* h_order, int32_t* n_order, void* stream) {
   if (!c || layer < 0 || layer >= c->L || !d_x || !d_ids || !d_w || !c->lw[layer].wg) return PROMOE_EINVAL;
@@ -1003,10 +1009,15 @@ int promoe_route(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_id
     c->need_q[pos] = c->pf->queue_of(layer, slot);
     if (((predicted >> rec.expert[pos]) & 1ull) && c->need01[pos] == -1 && c->need2[pos] == -1) c->pred_in_time++;
   }
+  c->route_rec = rec;
+  c->ffn_started.assign(rec.n, 0);
+  rc = launch_route_head(c, layer, d_x, T, s);
+  if (rc) return rc;
   if (c->eng.err != hipSuccess) return fail_hip(c->eng.err, "copy engine");
   lk.unlock();
   c->cv.notify_all();
   c->route_layer = layer;
+  c->last_route_layer = layer;
   c->route_T = T;
   c->route_x = d_x;
   c->route_rec = rec;
@@ -1129,17 +1140,9 @@ int ffn_launch(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipStream
 
 }  // namespace
 
-int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const int32_t* d_ids, const float* d_w,
-                      const float* d_shared_scale, void* d_y, void* stream) {
-  if (!c || layer < 0 || layer >= c->L || !d_x || !d_ids || !d_w || !d_y) return PROMOE_EINVAL;
-  if (c->route_layer != layer || c->route_T != T) {
-    g_last_error = "expert_ffn without a matching route";
-    return PROMOE_ESTATE;
-  }
-  if (c->cfg.shared_gate && c->Ish > 0 && !d_shared_scale) return PROMOE_EINVAL;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  c->last_stream = s;
-  const PlanRecord& rec = c->route_rec;
+namespace {
+
+FfnArgs ffn_args(promoe_ctx* c, int layer, const void* d_x, int T) {
   FfnArgs a{};
   a.cache = c->cache;
   a.expert_bytes = (int64_t)c->expert_bytes;
@@ -1166,29 +1169,90 @@ int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const in
   a.ysh_split_stride = (int64_t)T * c->H;
   if (c->Ish > 0 && use_gemm(c, T, true))
     a.ksplit = std::max(1, std::min(std::min(gemm_shared_down_split(T, c->H), kMaxSplit), c->Ish / 64 / 4));
+  return a;
+}
+
+// A launch reading route positions `jobs` was enqueued on s: it becomes the
+// last read of their slots, and the fills that waited for it are issued.
+// Caller holds c->mu.  Returns the launch's compute token.
+int64_t release_after_launch(promoe_ctx* c, int layer, const std::vector<int>& jobs, hipStream_t s) {
+  const PlanRecord& rec = c->route_rec;
+  const int64_t tok = record_compute(c, s);
+  for (int p : jobs)
+    if (p != kSharedJob) c->pf->set_last_read(layer, rec.slot[p], tok);
+  for (auto it = c->deferred.begin(); it != c->deferred.end();) {
+    const Deferred d = *it;
+    if (std::find(jobs.begin(), jobs.end(), d.after) == jobs.end()) {
+      ++it;
+      continue;
+    }
+    if (d.fill) c->pf->assign(layer, d.slot, d.expert);
+    c->pf->issue_high_after(layer, d.slot, tok);
+    c->need01[d.pos] = c->pf->ready_seq(layer, d.slot, 1);
+    c->need2[d.pos] = c->pf->ready_seq(layer, d.slot, 2);
+    c->need_q[d.pos] = c->pf->queue_of(layer, d.slot);
+    it = c->deferred.erase(it);
+  }
+  return tok;
+}
+
+}  // namespace
+
+// Steps larger than decode: a fill whose victim slot is read by a resident
+// expert of the same step waits for that read.  The route launches the readers
+// of the first fills' victims itself, right behind its plan, so the link
+// starts on those fills while the caller runs the predictor and the FFN call
+// computes the rest.  Caller holds c->mu; c->route_rec is this route's plan.
+static int launch_route_head(promoe_ctx* c, int layer, const void* d_x, int T, hipStream_t s) {
+  c->route_head_tok = -1;
+  const bool in_order = (c->cfg.flags & (PROMOE_FLAG_NO_REORDER | PROMOE_FLAG_NO_PREEMPT)) != 0;
+  if ((int64_t)T * c->K <= 64 || in_order) return PROMOE_OK;
+  std::vector<int> head;
+  for (const auto& d : c->deferred) {
+    if ((int)head.size() == kHeadFills) break;
+    if (d.after < 0 || !d.fill) continue;
+    const int p = d.after;
+    bool waits = c->need01[p] != -1 || c->need2[p] != -1;  // its own chunks still arriving
+    for (const auto& e : c->deferred) waits = waits || e.pos == p;
+    if (waits || std::find(head.begin(), head.end(), p) != head.end()) continue;
+    head.push_back(p);
+  }
+  if (head.empty()) return PROMOE_OK;
+  const int rc = ffn_launch(c, ffn_args(c, layer, d_x, T), head, s, CopyWait(), CopyWait());
+  if (rc) return rc;
+  c->route_head_tok = release_after_launch(c, layer, head, s);
+  for (int p : head) c->ffn_started[p] = 1;
+  return PROMOE_OK;
+}
+
+int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const int32_t* d_ids, const float* d_w,
+                      const float* d_shared_scale, void* d_y, void* stream) {
+  if (!c || layer < 0 || layer >= c->L || !d_x || !d_ids || !d_w || !d_y) return PROMOE_EINVAL;
+  if (c->route_layer != layer || c->route_T != T) {
+    g_last_error = "expert_ffn without a matching route";
+    return PROMOE_ESTATE;
+  }
+  if (c->cfg.shared_gate && c->Ish > 0 && !d_shared_scale) return PROMOE_EINVAL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  c->last_stream = s;
+  const PlanRecord& rec = c->route_rec;
+  const FfnArgs a = ffn_args(c, layer, d_x, T);
 
   std::unique_lock<std::mutex> lk(c->mu);
   const int n = rec.n;
-  std::vector<char> done(n, 0), is_def(n, 0);
+  // The route may have started the readers of the first fills' victim slots
+  // (on its stream: order this stream after them).
+  if (c->route_head_tok >= 0 && c->cstream[c->route_head_tok % kComputeRing] != s)
+    HIPCHK(hipStreamWaitEvent(s, c->cev[c->route_head_tok % kComputeRing], 0));
+  std::vector<char> done(c->ffn_started), is_def(n, 0);
   for (const auto& d : c->deferred) is_def[d.pos] = 1;
 
   auto after_launch = [&](const std::vector<int>& jobs) {
-    const int64_t tok = record_compute(c, s);
-    for (int p : jobs) {
-      if (p == kSharedJob) continue;
-      c->pf->set_last_read(layer, rec.slot[p], tok);
-      done[p] = 1;
-    }
-    // release fills that waited for these positions' reads
-    for (const auto& d : c->deferred) {
-      if (std::find(jobs.begin(), jobs.end(), d.after) == jobs.end()) continue;
-      if (d.fill) c->pf->assign(layer, d.slot, d.expert);
-      c->pf->issue_high_after(layer, d.slot, tok);
-      c->need01[d.pos] = c->pf->ready_seq(layer, d.slot, 1);
-      c->need2[d.pos] = c->pf->ready_seq(layer, d.slot, 2);
-      c->need_q[d.pos] = c->pf->queue_of(layer, d.slot);
-      is_def[d.pos] = 0;
-    }
+    release_after_launch(c, layer, jobs, s);
+    for (int p : jobs)
+      if (p != kSharedJob) done[p] = 1;
+    for (int p = 0; p < n; ++p) is_def[p] = 0;
+    for (const auto& d : c->deferred) is_def[d.pos] = 1;
   };
 
   // Reordered inference runs every ready expert first; without it (or without
@@ -1199,32 +1263,12 @@ int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const in
   std::vector<int> jobs;
   if (c->Ish > 0) jobs.push_back(kSharedJob);
   for (int p = 0; p < n; ++p) {
+    if (done[p]) continue;
     if (!is_def[p] && c->need01[p] < 0 && c->need2[p] < 0) jobs.push_back(p);
     else if (in_order) break;
   }
   int rc = PROMOE_OK;
   const bool batch = (int64_t)T * c->K <= 64;
-  // Larger steps: a fill whose victim slot is read by a resident expert of this
-  // step waits for that read.  The victims of the first fills are run first, in
-  // a launch of their own, so the link starts on those fills while the rest of
-  // the resident experts (and the shared expert) compute.
-  if (!batch && !in_order && !jobs.empty()) {
-    std::vector<int> head;
-    for (const auto& d : c->deferred) {
-      if ((int)head.size() == kHeadFills) break;
-      if (d.after < 0 || !d.fill) continue;
-      if (std::find(jobs.begin(), jobs.end(), d.after) == jobs.end()) continue;
-      if (std::find(head.begin(), head.end(), d.after) == head.end()) head.push_back(d.after);
-    }
-    if (!head.empty() && head.size() < jobs.size()) {
-      rc = ffn_launch(c, a, head, s, CopyWait(), CopyWait());
-      if (rc) return rc;
-      after_launch(head);
-      jobs.erase(std::remove_if(jobs.begin(), jobs.end(),
-                                [&](int p) { return std::find(head.begin(), head.end(), p) != head.end(); }),
-                 jobs.end());
-    }
-  }
   if (!jobs.empty()) {
     rc = ffn_launch(c, a, jobs, s, CopyWait(), CopyWait());
     if (rc) return rc;

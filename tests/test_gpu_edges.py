@@ -205,36 +205,40 @@ def test_int4_prefill_long_rows():
 
 @pytest.mark.parametrize("T", [1, 77])
 def test_predict_before_or_after_route(T):
-    # The layer loop predicts after the route (look-ahead >= 1); predicting first
-    # fuses the gate rows into the predictor pass instead.  Both orders must give
-    # the same ids, weights, predictions, outputs and cache plans, bit for bit
-    # (the route-first order is the one the oracle checks elsewhere).
+    # The layer loop predicts after the route (look-ahead >= 1), and for large
+    # steps after the FFN call; predicting first fuses the gate rows into the
+    # predictor pass instead.  Every order must give the same ids, weights,
+    # predictions, outputs and cache plans, bit for bit (the route-first order
+    # is the one the oracle checks elsewhere).
     cfg = SMALL
     m = SyntheticModel(cfg, max_tokens=T)
     try:
         st = Stack(m, T)
         runs = []
-        for first in (True, False):
+        for when in ("first", "after_route", "after_ffn"):
             m.open()
             got = []
             for step in range(2):
                 for l in range(cfg.n_layers):
                     st.x.copy_(torch.from_numpy(sm.layer_input(cfg, l, T, tag=980 + step).view(np.int16)).cuda())
                     ctx = m.ctx
-                    if first:
+                    if when == "first":
                         ctx.predict(l, st.x, T, st.pred_ids)
                     order = ctx.route(l, st.x, T, st.ids, st.w, st.s)
-                    if not first:
+                    if when == "after_route":
                         ctx.predict(l, st.x, T, st.pred_ids)
                     ctx.expert_ffn(l, st.x, T, st.ids, st.w, st.s, st.y)
+                    if when == "after_ffn":
+                        ctx.predict(l, st.x, T, st.pred_ids)
                     torch.cuda.synchronize()
                     got.append((order, *(t.cpu().numpy().copy() for t in (st.ids, st.w, st.s, st.pred_ids, st.y)),
                                 m.ctx.last_plan(l, 1)["slot"]))
             runs.append(got)
-        for a, b in zip(*runs):
-            assert a[0] == b[0] and a[6] == b[6]
-            for u, v in zip(a[1:6], b[1:6]):
-                assert np.array_equal(u, v)
+        for other in runs[1:]:
+            for a, b in zip(runs[0], other):
+                assert a[0] == b[0] and a[6] == b[6]
+                for u, v in zip(a[1:6], b[1:6]):
+                    assert np.array_equal(u, v)
     finally:
         m.close()
 

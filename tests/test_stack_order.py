@@ -33,9 +33,9 @@ class _Ctx:
         self.calls.append(("res", None))
 
 
-def _stack(cfg):
+def _stack(cfg, T=1):
     m = types.SimpleNamespace(cfg=cfg, ctx=_Ctx(), device="cpu")
-    return Stack(m, 1), m.ctx
+    return Stack(m, T), m.ctx
 
 
 @pytest.mark.parametrize("base", [configs.C2, configs.C3])
@@ -45,6 +45,15 @@ def test_route_before_predict_with_lookahead(base):
     st.step(torch.zeros(1, cfg.hidden))
     per_layer = [c for c in ctx.calls if c[0] in ("route", "predict", "ffn")]
     assert per_layer == [(n, l) for l in range(3) for n in ("route", "predict", "ffn")]
+
+
+@pytest.mark.parametrize("T", [1, 512])
+def test_route_predict_ffn_at_any_step_size(T):
+    cfg = configs.C3.with_(n_layers=2)
+    st, ctx = _stack(cfg, T)
+    st.step(torch.zeros(T, cfg.hidden))
+    per_layer = [c for c in ctx.calls if c[0] in ("route", "predict", "ffn")]
+    assert per_layer == [(n, l) for l in range(2) for n in ("route", "predict", "ffn")]
 
 
 def test_predict_first_at_lookahead_zero():
