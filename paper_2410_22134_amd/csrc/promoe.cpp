@@ -58,6 +58,11 @@ constexpr int kCopyStreams = 2;
 // Fills whose victims' readers run ahead of the other resident experts (one per
 // copy queue keeps every queue busy from the start).
 constexpr int kHeadFills = kCopyStreams;
+// Experts per FFN launch while copies arrive, for steps larger than decode.
+constexpr int kArrivalGroup = kCopyStreams;
+// Resident experts per FFN launch, for steps larger than decode (as many as
+// one 4-bit staging batch).
+constexpr int kResidentGroup = 8;
 
 class HipEngine : public CopyEngine {
  public:
@@ -1259,26 +1264,49 @@ int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const in
   // early preemption, where a later position's copy starts only when it is
   // reached) positions run strictly in the route order.
   const bool in_order = (c->cfg.flags & (PROMOE_FLAG_NO_REORDER | PROMOE_FLAG_NO_PREEMPT)) != 0;
-  // 1. the shared expert and every routed expert whose chunks are already in HBM
-  std::vector<int> jobs;
-  if (c->Ish > 0) jobs.push_back(kSharedJob);
+  // 1. the shared expert and every routed expert whose chunks are already in HBM.
+  // Decode-sized steps run them in one launch.  Larger steps run the resident
+  // experts kResidentGroup at a time in the route order, so the fills that
+  // wait for their reads (victims in the same order) are released group by
+  // group instead of behind all of them, and the shared expert last.
+  std::vector<int> ready;
   for (int p = 0; p < n; ++p) {
     if (done[p]) continue;
-    if (!is_def[p] && c->need01[p] < 0 && c->need2[p] < 0) jobs.push_back(p);
+    if (!is_def[p] && c->need01[p] < 0 && c->need2[p] < 0) ready.push_back(p);
     else if (in_order) break;
   }
   int rc = PROMOE_OK;
   const bool batch = (int64_t)T * c->K <= 64;
-  if (!jobs.empty()) {
-    rc = ffn_launch(c, a, jobs, s, CopyWait(), CopyWait());
-    if (rc) return rc;
-    after_launch(jobs);
+  std::vector<int> jobs;
+  if (batch) {
+    if (c->Ish > 0) jobs.push_back(kSharedJob);
+    jobs.insert(jobs.end(), ready.begin(), ready.end());
+    if (!jobs.empty()) {
+      rc = ffn_launch(c, a, jobs, s, CopyWait(), CopyWait());
+      if (rc) return rc;
+      after_launch(jobs);
+    }
+  } else {
+    for (size_t g0 = 0; g0 < ready.size(); g0 += kResidentGroup) {
+      jobs.assign(ready.begin() + g0, ready.begin() + std::min(ready.size(), g0 + kResidentGroup));
+      rc = ffn_launch(c, a, jobs, s, CopyWait(), CopyWait());
+      if (rc) return rc;
+      after_launch(jobs);
+    }
+    if (c->Ish > 0) {
+      jobs.assign(1, kSharedJob);
+      rc = ffn_launch(c, a, jobs, s, CopyWait(), CopyWait());
+      if (rc) return rc;
+      after_launch(jobs);
+    }
   }
   // 2. experts still arriving.  Decode-sized steps batch them into one launch
   // behind the last copy (a GEMV is ~1% of a copy, so per-expert launches buy no
-  // overlap); larger steps launch per expert in the route order so compute
-  // follows the copies expert by expert.  Fills deferred behind an earlier
-  // expert's read are released as that expert is launched.
+  // overlap); larger steps launch in the route order, kArrivalGroup experts at
+  // a time, so compute follows the copies: consecutive fills run on different
+  // copy queues and arrive together, and a launch of one expert's few tokens
+  // leaves most CUs idle, so two experts cost about what one does.  Fills
+  // deferred behind an earlier expert's read are released as it is launched.
   for (;;) {
     jobs.clear();
     CopyWait w01, w2;
@@ -1291,7 +1319,7 @@ int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const in
       jobs.push_back(p);
       w01.add(c->need_q[p], c->need01[p]);
       w2.add(c->need_q[p], c->need2[p]);
-      if (!batch) break;
+      if (!batch && (int)jobs.size() == kArrivalGroup) break;
     }
     if (jobs.empty()) break;
     rc = ffn_launch(c, a, jobs, s, w01, w2);
