@@ -1266,9 +1266,10 @@ int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const in
   const bool in_order = (c->cfg.flags & (PROMOE_FLAG_NO_REORDER | PROMOE_FLAG_NO_PREEMPT)) != 0;
   // 1. the shared expert and every routed expert whose chunks are already in HBM.
   // Decode-sized steps run them in one launch.  Larger steps run the resident
-  // experts kResidentGroup at a time in the route order, so the fills that
-  // wait for their reads (victims in the same order) are released group by
-  // group instead of behind all of them, and the shared expert last.
+  // experts that fills wait for kResidentGroup at a time in the route order,
+  // so those fills (victims in the same order) are released group by group
+  // instead of behind all of them; then the other resident experts in one
+  // launch, and the shared expert last.
   std::vector<int> ready;
   for (int p = 0; p < n; ++p) {
     if (done[p]) continue;
@@ -1287,11 +1288,19 @@ int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const in
       after_launch(jobs);
     }
   } else {
-    for (size_t g0 = 0; g0 < ready.size(); g0 += kResidentGroup) {
-      jobs.assign(ready.begin() + g0, ready.begin() + std::min(ready.size(), g0 + kResidentGroup));
+    // groups only up to the last resident expert that a fill waits for; the
+    // rest release nothing and run in one launch (fewer, fuller GEMMs)
+    size_t last = 0;
+    for (const auto& d : c->deferred)
+      for (size_t i = 0; i < ready.size(); ++i)
+        if (ready[i] == d.after) last = std::max(last, i + 1);
+    for (size_t g0 = 0; g0 < ready.size();) {
+      const size_t g1 = g0 < last ? std::min(ready.size(), g0 + kResidentGroup) : ready.size();
+      jobs.assign(ready.begin() + g0, ready.begin() + g1);
       rc = ffn_launch(c, a, jobs, s, CopyWait(), CopyWait());
       if (rc) return rc;
       after_launch(jobs);
+      g0 = g1;
     }
     if (c->Ish > 0) {
       jobs.assign(1, kSharedJob);
