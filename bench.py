@@ -53,7 +53,7 @@ def parse():
                    help="size of the plain device copy run after the timed region (counter calibration)")
     p.add_argument("--legs", default="decode,prefill,mfma,ablation,sweep,int4",
                    help="decode is always run (it is the reported value); add prefill, mfma, ablation, sweep, "
-                        "int4, predtrain")
+                        "int4, predtrain, configs")
     p.add_argument("--prefill-steps", type=int, default=3)
     p.add_argument("--prefill-warmup", type=int, default=1)
     p.add_argument("--ablation-steps", type=int, default=32)
@@ -416,6 +416,61 @@ def leg_predtrain(torch, args):
     return out
 
 
+def leg_configs(torch, args, h2d_gbs):
+    """The other workloads at their real per-layer sizes (detail only, opt-in):
+    Qwen1.5-MoE-A2.7B decode at batch 1 (all 24 layers), Mixtral-8x7B prefill of
+    256 tokens then decode, Qwen2-57B-A14B prefill of 1024 tokens then decode at
+    batch 1 and 8.  A process may pin at most 64 GiB of host memory on the GPU
+    machines used here, less than the 90 / 99 GB that the Mixtral and Qwen2-57B
+    stacks keep there, so those two run 16 of their layers and report tok/s
+    both as measured and scaled to the full depth (every layer does the same
+    work).  One context per shape: decode follows the prefill on the cache it
+    left, as in serving.  Per run: tok/s, host-to-device GB per step, hit rate,
+    overlap, and the link bound (tokens per step over bytes per step at the
+    measured single-copy rate)."""
+    import numpy as np
+    from synth import configs, model as sm
+    from paper_2410_22134_amd import FLAG_PROFILE
+    from paper_2410_22134_amd.model import SyntheticModel
+    from paper_2410_22134_amd.stack import Stack
+    plan = (("Qwen1.5-MoE-A2.7B", configs.C3, 24, (("decode", 1, 4, 32),)),
+            ("Mixtral-8x7B", configs.C4, 16, (("prefill", 256, 1, 2), ("decode", 1, 2, 8))),
+            ("Qwen2-57B-A14B", configs.C5, 16, (("prefill", 1024, 1, 2), ("decode", 1, 2, 8), ("decode", 8, 2, 8))))
+    out = {}
+    for name, full, n_layers, runs in plan:
+        cfg = full.with_(n_layers=n_layers)
+        depth = full.n_layers / n_layers
+        t0 = time.perf_counter()
+        model = SyntheticModel(cfg, max_tokens=max(T for _, T, _, _ in runs), gen_threads=8,
+                               flags=FLAG_PROFILE, spec_fill_limit=args.spec_fill_limit)
+        setup = time.perf_counter() - t0
+        print(f"[bench] configs {name}: weights generated in {setup:.1f} s", file=sys.stderr, flush=True)
+        rows = []
+        try:
+            for kind, T, warm, steps in runs:
+                st = Stack(model, T)
+                h = torch.from_numpy(np.stack([sm.stack_input(cfg, 6000 + i, T) for i in range(warm + steps)])).cuda()
+                dt, s = run_steps(torch, model, st, h, warm, steps)
+                copied = (s["bytes_high"] + s["bytes_low"]) / steps
+                rows.append({"workload": kind, "tokens_per_step": T, "steps": steps, "tok_s": round(T * steps / dt, 2),
+                             "tok_s_full_depth": round(T * steps / dt / depth, 2),
+                             "ms_per_step": round(dt / steps * 1e3, 2), "copied_GB_per_step": round(copied / 1e9, 3),
+                             "copy_GBps": round(copied * steps / dt / 1e9, 2),
+                             "link_bound_tok_s": round(T / (copied / (h2d_gbs * 1e9)), 2) if copied else None,
+                             "hit_rate": round(s["hit"] / max(1, s["prec_access"]), 4),
+                             "overlap": overlap_metrics(s, dt, h2d_gbs), "kernels": _classes(s)})
+                print(f"[bench] configs {name} {kind} T={T}: {rows[-1]['tok_s']} tok/s over {cfg.n_layers} layers "
+                      f"(link bound {rows[-1]['link_bound_tok_s']})", file=sys.stderr, flush=True)
+                del st, h
+        finally:
+            model.close()
+        out[name] = {"layers_run": cfg.n_layers, "layers_full": full.n_layers, "experts": cfg.n_experts,
+                     "top_k": cfg.top_k,
+                     "cached_per_layer": cfg.slots, "expert_MB": round(cfg.expert_bytes / 1e6, 2),
+                     "setup_s": round(setup, 1), "runs": rows}
+    return out
+
+
 def leg_int4(torch, args):
     """4-bit routed experts (the paper's bits-per-weight study): decode of the
     DeepSeek-MoE-16B shape (50% cached) and 512-token prefill of the
@@ -586,6 +641,9 @@ def main():
     if "int4" in args.legs:
         print("[bench] 4-bit experts leg", file=sys.stderr, flush=True)
         out["detail"]["int4"] = leg_int4(torch, args)
+    if "configs" in args.legs:
+        print("[bench] other shapes leg", file=sys.stderr, flush=True)
+        out["detail"]["configs"] = leg_configs(torch, args, h2d_gbs)
     if "mfma" in args.legs:
         print("[bench] shared-expert MFMA leg", file=sys.stderr, flush=True)
         g = leg_mfma(torch, args)
