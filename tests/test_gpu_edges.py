@@ -243,6 +243,47 @@ def test_predict_before_or_after_route(T):
         m.close()
 
 
+def test_route_and_ffn_on_different_streams():
+    # With 77 tokens over 8 experts and 4 slots every expert is routed, so each
+    # fill overwrites a slot that a resident expert of the same step reads; the
+    # route launches the first of those readers on its own stream, and an FFN
+    # call on another stream must order itself after them.  Outputs, ids,
+    # weights and plans must equal the one-stream run bit for bit.
+    cfg, T = SMALL, 77
+    m = SyntheticModel(cfg, max_tokens=T)
+    try:
+        st = Stack(m, T)
+        s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+        runs = []
+        for split in (False, True):
+            m.open()
+            got = []
+            for step in range(2):
+                for l in range(cfg.n_layers):
+                    st.x.copy_(torch.from_numpy(sm.layer_input(cfg, l, T, tag=990 + step).view(np.int16)).cuda())
+                    ctx = m.ctx
+                    cur = torch.cuda.current_stream()
+                    rs, fs = (s1, s2) if split else (cur, cur)
+                    rs.wait_stream(cur)
+                    fs.wait_stream(cur)
+                    order = ctx.route(l, st.x, T, st.ids, st.w, st.s, stream=rs)
+                    ctx.predict(l, st.x, T, st.pred_ids, stream=rs)
+                    ctx.expert_ffn(l, st.x, T, st.ids, st.w, st.s, st.y, stream=fs)
+                    cur.wait_stream(rs)
+                    cur.wait_stream(fs)
+                    torch.cuda.synchronize()
+                    got.append((order, *(t.cpu().numpy().copy() for t in (st.ids, st.w, st.s, st.y)),
+                                m.ctx.last_plan(l, 1)["slot"]))
+            runs.append(got)
+        assert len(runs[0][0][0]) == cfg.n_experts  # every expert routed: fills wait for resident reads
+        for a, b in zip(*runs):
+            assert a[0] == b[0] and a[5] == b[5]
+            for u, v in zip(a[1:5], b[1:5]):
+                assert np.array_equal(u, v)
+    finally:
+        m.close()
+
+
 def test_external_pushes_low_and_high():
     cfg = SMALL.with_(n_layers=1, lookahead=0)
     m = SyntheticModel(cfg, max_tokens=2)
