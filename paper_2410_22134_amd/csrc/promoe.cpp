@@ -73,8 +73,11 @@ class HipEngine : public CopyEngine {
   hipError_t err = hipSuccess;
   // Latest compute token each queue is known to follow (it waited for it, or
   // the token had completed when a copy was queued), and that token's stream.
-  int64_t followed[kCopyStreams] = {-1, -1};
+  int64_t followed[kCopyStreams];
   hipStream_t followed_on[kCopyStreams] = {};
+  HipEngine() {
+    for (auto& f : followed) f = -1;
+  }
 
   void issue(int64_t seq, void* dst, const void* src, size_t bytes, int64_t after, int queue) override {
     hipStream_t s = stream[queue];
