@@ -1204,6 +1204,13 @@ int64_t release_after_launch(promoe_ctx* c, int layer, const std::vector<int>& j
   return tok;
 }
 
+std::vector<FillWait> fill_waits(const promoe_ctx* c) {
+  std::vector<FillWait> w;
+  w.reserve(c->deferred.size());
+  for (const auto& d : c->deferred) w.push_back(FillWait{d.pos, d.after, d.fill});
+  return w;
+}
+
 }  // namespace
 
 // Steps larger than decode: a fill whose victim slot is read by a resident
@@ -1215,16 +1222,9 @@ static int launch_route_head(promoe_ctx* c, int layer, const void* d_x, int T, h
   c->route_head_tok = -1;
   const bool in_order = (c->cfg.flags & (PROMOE_FLAG_NO_REORDER | PROMOE_FLAG_NO_PREEMPT)) != 0;
   if ((int64_t)T * c->K <= 64 || in_order) return PROMOE_OK;
-  std::vector<int> head;
-  for (const auto& d : c->deferred) {
-    if ((int)head.size() == kHeadFills) break;
-    if (d.after < 0 || !d.fill) continue;
-    const int p = d.after;
-    bool waits = c->need01[p] != -1 || c->need2[p] != -1;  // its own chunks still arriving
-    for (const auto& e : c->deferred) waits = waits || e.pos == p;
-    if (waits || std::find(head.begin(), head.end(), p) != head.end()) continue;
-    head.push_back(p);
-  }
+  std::vector<char> arriving(c->route_rec.n);
+  for (int p = 0; p < c->route_rec.n; ++p) arriving[p] = c->need01[p] != -1 || c->need2[p] != -1;
+  const std::vector<int> head = head_readers(fill_waits(c), arriving, kHeadFills);
   if (head.empty()) return PROMOE_OK;
   const int rc = ffn_launch(c, ffn_args(c, layer, d_x, T), head, s, CopyWait(), CopyWait());
   if (rc) return rc;
@@ -1293,17 +1293,10 @@ int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const in
   } else {
     // groups only up to the last resident expert that a fill waits for; the
     // rest release nothing and run in one launch (fewer, fuller GEMMs)
-    size_t last = 0;
-    for (const auto& d : c->deferred)
-      for (size_t i = 0; i < ready.size(); ++i)
-        if (ready[i] == d.after) last = std::max(last, i + 1);
-    for (size_t g0 = 0; g0 < ready.size();) {
-      const size_t g1 = g0 < last ? std::min(ready.size(), g0 + kResidentGroup) : ready.size();
-      jobs.assign(ready.begin() + g0, ready.begin() + g1);
-      rc = ffn_launch(c, a, jobs, s, CopyWait(), CopyWait());
+    for (const auto& g : resident_groups(ready, fill_waits(c), kResidentGroup)) {
+      rc = ffn_launch(c, a, g, s, CopyWait(), CopyWait());
       if (rc) return rc;
-      after_launch(jobs);
-      g0 = g1;
+      after_launch(g);
     }
     if (c->Ish > 0) {
       jobs.assign(1, kSharedJob);

@@ -242,4 +242,34 @@ void Prefetcher::set_last_read(int layer, int slot, int64_t tok) {
   s.last_read = std::max(s.last_read, tok);
 }
 
+std::vector<int> head_readers(const std::vector<FillWait>& waits, const std::vector<char>& arriving, int max_head) {
+  std::vector<int> head;
+  for (const auto& w : waits) {
+    if ((int)head.size() >= max_head) break;
+    if (w.after < 0 || !w.fill) continue;
+    const int p = w.after;
+    bool busy = p < (int)arriving.size() && arriving[p];
+    for (const auto& o : waits) busy = busy || o.pos == p;
+    if (busy || std::find(head.begin(), head.end(), p) != head.end()) continue;
+    head.push_back(p);
+  }
+  return head;
+}
+
+std::vector<std::vector<int>> resident_groups(const std::vector<int>& ready, const std::vector<FillWait>& waits,
+                                              int group) {
+  size_t last = 0;  // one past the last ready position a fill waits for
+  for (const auto& w : waits)
+    for (size_t i = 0; i < ready.size(); ++i)
+      if (ready[i] == w.after) last = std::max(last, i + 1);
+  std::vector<std::vector<int>> out;
+  const size_t g = group < 1 ? 1 : (size_t)group;
+  for (size_t g0 = 0; g0 < ready.size();) {
+    const size_t g1 = g0 < last ? std::min(ready.size(), g0 + g) : ready.size();
+    out.emplace_back(ready.begin() + g0, ready.begin() + g1);
+    g0 = g1;
+  }
+  return out;
+}
+
 }  // namespace promoe

@@ -16,9 +16,11 @@
 //   * a copy into a slot waits for the last compute that read the slot
 //     (write-after-read), and compute waits for the copy of the chunk it reads
 //     (read-after-write) -- see ready_seq();
-//   * every copy into a slot goes to the same engine queue, so copies into one
-//     slot never overtake each other and the latest copy of a slot completes
-//     after all earlier ones (the engine may run several queues at once).
+//   * copies into a slot go to one engine queue while any of them may be in
+//     flight (a slot refilled with nothing in flight moves to the queue with
+//     the fewest bytes outstanding), so copies into one slot never overtake
+//     each other and the latest copy of a slot completes after all earlier
+//     ones (the engine may run several queues at once).
 //
 // No HIP here: the physical queue is a CopyEngine (HIP streams and events in
 // the library, a simulated clock in the CPU tests).  Not thread-safe; the
@@ -172,5 +174,27 @@ class Prefetcher {
   int64_t low_in_flight_ = 0;
   PhysStats st_;
 };
+
+// ---- launch order of one FFN call (host logic, no HIP) ----
+
+// A route position whose copies wait for an earlier position's compute.
+struct FillWait {
+  int pos;    // the waiting position
+  int after;  // position whose launch must precede its copies (-1: none)
+  bool fill;  // the position's slot changes expert (a write after read)
+};
+
+// The resident readers of the victim slots of the first `max_head` fills, in
+// fill order, each once: positions that a fill waits for, skipping positions
+// that wait themselves (listed in `waits`, or arriving[p]: chunks still being
+// copied).  Launching them first starts the link on those fills.
+std::vector<int> head_readers(const std::vector<FillWait>& waits, const std::vector<char>& arriving, int max_head);
+
+// Launch groups for the resident positions `ready` (route order) of a step
+// larger than decode: groups of `group` positions up to the last one a fill
+// waits for, so those fills are released group by group; then every later
+// position in one group (they release nothing).
+std::vector<std::vector<int>> resident_groups(const std::vector<int>& ready, const std::vector<FillWait>& waits,
+                                              int group);
 
 }  // namespace promoe

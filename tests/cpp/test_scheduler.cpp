@@ -204,6 +204,51 @@ void test_fills_balance_queues() {
   for (size_t i = 0; i < r.eng.log.size(); ++i) CHECK(r.eng.queue_of_copy[i] == (int)(i % 2));
 }
 
+// Launch order of a large step.  Fills wait for the resident experts whose
+// slots they take (position p's fill after position p - 30 in a 60-expert step
+// over 30 slots); the head is the first two such readers.
+void test_head_readers() {
+  std::vector<FillWait> w;
+  for (int j = 0; j < 30; ++j) w.push_back(FillWait{30 + j, j, true});
+  std::vector<char> arriving(60, 0);
+  CHECK((head_readers(w, arriving, 2) == std::vector<int>{0, 1}));
+  // a reader whose own chunks are still arriving, and fills that wait on nothing
+  // or are not fills, are skipped; each reader appears once
+  arriving[0] = 1;
+  std::vector<FillWait> w2 = {{40, -1, true}, {41, 0, true}, {42, 2, false}, {43, 1, true}, {44, 1, true}, {45, 3, true}};
+  CHECK((head_readers(w2, arriving, 2) == std::vector<int>{1, 3}));
+  // a reader that itself waits (listed as a waiting position) is skipped
+  std::vector<FillWait> w3 = {{5, 4, true}, {4, 2, true}, {6, 1, true}};
+  CHECK((head_readers(w3, std::vector<char>(8, 0), 3) == std::vector<int>{2, 1}));
+  CHECK(head_readers(w, std::vector<char>(60, 0), 0).empty());
+}
+
+void test_resident_groups() {
+  std::vector<int> ready;
+  for (int p = 2; p < 30; ++p) ready.push_back(p);  // 0 and 1 ran with the route
+  std::vector<FillWait> w;
+  for (int j = 0; j < 30; ++j) w.push_back(FillWait{30 + j, j, true});
+  auto g = resident_groups(ready, w, 8);
+  CHECK(g.size() == 4u);
+  CHECK(g.size() == 4u && g[0].front() == 2 && g[0].back() == 9 && g[1].front() == 10 && g[3].back() == 29 &&
+        g[3].size() == 4u);
+  // nothing waits: one launch
+  g = resident_groups(ready, {}, 8);
+  CHECK(g.size() == 1u && g[0] == ready);
+  // only position 3 is waited for: one group of eight through it, the rest together
+  g = resident_groups(ready, {{40, 3, true}}, 8);
+  CHECK(g.size() == 2u && g[0].size() == 8u && g[1].size() == ready.size() - 8);
+  // waited position in the third group: groups of eight through it, then the rest
+  g = resident_groups(ready, {{40, 20, true}}, 8);
+  CHECK(g.size() == 4u && g[0].size() == 8u && g[1].size() == 8u && g[2].front() == 18 && g[2].back() == 25 &&
+        g[3].front() == 26 && g[3].back() == 29);
+  // every position appears exactly once, in order
+  std::vector<int> flat;
+  for (const auto& x : resident_groups(ready, w, 3)) flat.insert(flat.end(), x.begin(), x.end());
+  CHECK(flat == ready);
+  CHECK(resident_groups({}, w, 8).empty());
+}
+
 // High-priority copies in flight do not count against the low-priority window:
 // a prefetch queues right behind the misses, so the link has no idle gap
 // between them, and a later miss still waits for at most `window` of them.
@@ -429,6 +474,8 @@ int main(int argc, char** argv) {
   test_low_queues_behind_high();
   test_queue_per_slot();
   test_fills_balance_queues();
+  test_head_readers();
+  test_resident_groups();
   test_window_bound();
   test_purge_dedupe_and_priority();
   test_ready_and_war();
