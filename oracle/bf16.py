@@ -10,9 +10,11 @@ import numpy as np
 
 
 def decode(bits) -> np.ndarray:
-    """raw bf16 bits (uint16) -> float64, exactly."""
+    """raw bf16 bits (uint16) -> float64, exactly (a signalling-NaN pattern
+    becomes a quiet NaN, as any widening conversion makes it)."""
     b = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
-    return b.view(np.float32).astype(np.float64)
+    with np.errstate(invalid="ignore"):
+        return b.view(np.float32).astype(np.float64)
 
 
 def encode_rne(x) -> np.ndarray:
