@@ -158,6 +158,11 @@ class Context:
         self._h = _vp()
         check(lib().promoe_create(ctypes.byref(cfg), cache_ptr, cache_bytes, ctypes.byref(self._h)), "promoe_create")
         self._keep = []
+        # out-arrays of the per-layer calls, allocated once
+        self._order = (ctypes.c_int32 * 64)()
+        self._q = (ctypes.c_int32 * 64)()
+        self._n = ctypes.c_int32(0)
+        self._n_ref = ctypes.byref(self._n)
 
     def close(self):
         if self._h:
@@ -189,18 +194,14 @@ class Context:
 
     # hot path
     def predict(self, layer, x, T, pred_ids=None, want_q=False, stream=None):
-        q = (ctypes.c_int32 * 64)()
-        n = ctypes.c_int32(0)
-        check(lib().promoe_predict(self._h, layer, _p(x), T, _p(pred_ids), q if want_q else None,
-                                   ctypes.byref(n) if want_q else None, _stream(stream)), "promoe_predict")
-        return list(q)[:n.value] if want_q else None
+        check(lib().promoe_predict(self._h, layer, _p(x), T, _p(pred_ids), self._q if want_q else None,
+                                   self._n_ref if want_q else None, _stream(stream)), "promoe_predict")
+        return self._q[:self._n.value] if want_q else None
 
     def route(self, layer, x, T, ids, w, shared_scale=None, stream=None):
-        order = (ctypes.c_int32 * 64)()
-        n = ctypes.c_int32(0)
-        check(lib().promoe_route(self._h, layer, _p(x), T, _p(ids), _p(w), _p(shared_scale), order,
-                                 ctypes.byref(n), _stream(stream)), "promoe_route")
-        return list(order)[:n.value]
+        check(lib().promoe_route(self._h, layer, _p(x), T, _p(ids), _p(w), _p(shared_scale), self._order,
+                                 self._n_ref, _stream(stream)), "promoe_route")
+        return self._order[:self._n.value]
 
     def prefetch(self, layer, ids, prio=PRIO_LOW, stream=None):
         arr = (ctypes.c_int32 * max(1, len(ids)))(*ids)

@@ -22,6 +22,11 @@ class Stack:
         self.w = torch.zeros(T, k, dtype=torch.float32, device=dev)
         self.s = torch.zeros(T, dtype=torch.float32, device=dev)
         self.pred_ids = torch.zeros(T, k, dtype=torch.int32, device=dev)
+        # device addresses of the buffers above, passed to every per-layer call
+        self._h, self._x, self._y = self.h.data_ptr(), self.x.data_ptr(), self.y.data_ptr()
+        self._ids, self._w, self._s = self.ids.data_ptr(), self.w.data_ptr(), self.s.data_ptr()
+        self._pred = self.pred_ids.data_ptr()
+        self._cuda = str(dev).startswith("cuda")
 
     def moe_layer(self, l: int, predict: bool = True, want_q: bool = False, stream=None):
         """route -> predict -> ffn on self.x (predict first at look-ahead 0); returns (order, q).
@@ -31,28 +36,39 @@ class Stack:
         of layer l and fill the link while layer l computes (measured 35.8 ->
         37.1 tok/s on the DeepSeek-16B decode)."""
         ctx, T = self.m.ctx, self.T
+        s = _handle(stream) if self._cuda else stream
         first = self.m.cfg.lookahead == 0
         q = None
         if predict and first:
-            q = ctx.predict(l, self.x, T, self.pred_ids, want_q=want_q, stream=stream)
-        order = ctx.route(l, self.x, T, self.ids, self.w, self.s, stream=stream)
+            q = ctx.predict(l, self._x, T, self._pred, want_q=want_q, stream=s)
+        order = ctx.route(l, self._x, T, self._ids, self._w, self._s, stream=s)
         if predict and not first:
-            q = ctx.predict(l, self.x, T, self.pred_ids, want_q=want_q, stream=stream)
-        ctx.expert_ffn(l, self.x, T, self.ids, self.w, self.s, self.y, stream=stream)
+            q = ctx.predict(l, self._x, T, self._pred, want_q=want_q, stream=s)
+        ctx.expert_ffn(l, self._x, T, self._ids, self._w, self._s, self._y, stream=s)
         return order, q
 
     def step(self, h0, predict: bool = True, record=None, stream=None):
-        """One step over all layers from residual input h0 [T, H] (fp32, device)."""
+        """One step over all layers from residual input h0 [T, H] (fp32, device),
+        on `stream` (default: the current stream, looked up once per step)."""
         ctx, T = self.m.ctx, self.T
+        s = _handle(stream) if self._cuda else stream
         self.h.copy_(h0)
         for l in range(self.m.cfg.n_layers):
             if record is not None:
                 record("h", l, self)
-            ctx.attn_surrogate(l, self.h, T, self.x, stream=stream)
+            ctx.attn_surrogate(l, self._h, T, self._x, stream=s)
             if record is not None:
                 record("x", l, self)
-            order, q = self.moe_layer(l, predict, want_q=record is not None, stream=stream)
+            order, q = self.moe_layer(l, predict, want_q=record is not None, stream=s)
             if record is not None:
                 record("moe", l, self, order=order, q=q)
-            ctx.residual_add(self.h, self.y, T, stream=stream)
+            ctx.residual_add(self._h, self._y, T, stream=s)
         return self.h
+
+
+def _handle(stream) -> int:
+    """A hipStream_t as an int: the given stream's, or the current stream's."""
+    if isinstance(stream, int):
+        return stream
+    import torch
+    return (stream if stream is not None else torch.cuda.current_stream()).cuda_stream
