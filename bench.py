@@ -65,21 +65,23 @@ def parse():
 
 
 def read_traffic(kernel):
-    """HBM bytes per launch of `kernel` from the committed counter summary, or None when the
-    summary is missing or was taken on a different kernel source."""
+    """(HBM bytes per launch of `kernel`, those bytes over the algorithmic bytes of the same
+    counter runs) from the committed counter summary, or (None, None) when the summary is
+    missing or was taken on a different kernel source."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "traffic_counters.txt")
     src = os.path.join(ROOT, "paper_2410_22134_amd", "csrc", "kernels_gemv.hip")
     if not os.path.exists(path):
-        return None
+        return None, None
     digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
     for line in open(path):
         f = line.split()
         if len(f) >= 4 and f[0] == "traffic" and f[1] == kernel:
             if f[2] != digest:
-                return None
-            return int(float(f[3]))
-    return None
+                return None, None
+            ratio = round(float(f[3]) / float(f[4]), 4) if len(f) >= 5 else None
+            return int(float(f[3])), ratio
+    return None, None
 
 
 def prediction_metrics(s):
@@ -574,7 +576,7 @@ def main():
     h2d_gbs = h2d_probe(torch)
     peaks = measure_peaks(torch)
     load_s = s["bytes_high"] / (h2d_gbs * 1e9) if h2d_gbs else 0.0
-    traffic = read_traffic("k_ffn_gateup")
+    traffic, traffic_ratio = read_traffic("k_ffn_gateup")
     out = {
         "metric": METRIC,
         "value": round(tok_s, 3),
@@ -595,7 +597,8 @@ def main():
                    "prefetch": not args.no_prefetch, "spec_fill_limit": args.spec_fill_limit},
         "roofline": {"bound": "hbm", "kernel": "k_ffn_gateup<bf16,1>", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": traffic, "peak_measured": peaks["hbm_read_GBps"],
+                     "traffic": traffic, "traffic_over_algorithmic": traffic_ratio,
+                     "peak_measured": peaks["hbm_read_GBps"],
                      "frac_of_measured": round(achieved / peaks["hbm_read_GBps"], 4) if peaks["hbm_read_GBps"] else None,
                      "avg_launch_us": round(avg_us, 3),
                      "bytes_per_launch": round(by / launches) if launches else 0, "launches": launches,
