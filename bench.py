@@ -101,9 +101,12 @@ def prediction_metrics(s):
 
 def overlap_metrics(s, elapsed, h2d_gbs):
     """Share of copy time hidden behind compute: H_time = 1 - stall / load, where stall is
-    the compute stream's measured wait on copies and load = copied bytes at the measured
-    single-copy rate; H_max = min(1, (elapsed - stall) / load) bounds it."""
-    load = (s["bytes_high"] + s["bytes_low"]) / (h2d_gbs * 1e9) if h2d_gbs else 0.0
+    the compute stream's measured wait on copies and load = copied bytes at the link rate
+    (the measured probe rate, or the rate this run itself achieved if that is higher);
+    H_max = min(1, (elapsed - stall) / load) bounds it."""
+    copied = s["bytes_high"] + s["bytes_low"]
+    rate = max(h2d_gbs or 0.0, copied / elapsed / 1e9 if elapsed > 0 else 0.0)
+    load = copied / (rate * 1e9) if rate else 0.0
     stall = s["stall_ms"] * 1e-3
     if load <= 0:
         return None
@@ -113,21 +116,29 @@ def overlap_metrics(s, elapsed, h2d_gbs):
             "H_max": round(h_max, 4), "H_time_over_H_max": round(h_time / h_max, 4) if h_max > 0 else None}
 
 
-def h2d_probe(torch, mib=256, reps=5):
-    """Pinned host -> device copy bandwidth (GB/s) of one large async copy."""
+def h2d_probe(torch, mib=256, reps=5, pieces=8):
+    """Pinned host -> device copy bandwidth (GB/s): `mib` MiB in `pieces` copies
+    alternating over two streams, as the library's copy engine issues them
+    (best of `reps`)."""
     n = mib << 20
+    piece = n // pieces
     src = torch.empty(n, dtype=torch.uint8, pin_memory=True)
     dst = torch.empty(n, dtype=torch.uint8, device="cuda")
-    s = torch.cuda.Stream()
+    ss = (torch.cuda.Stream(), torch.cuda.Stream())
     best = 0.0
     for _ in range(reps):
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        with torch.cuda.stream(s):
-            a.record()
-            dst.copy_(src, non_blocking=True)
-            b.record()
+        torch.cuda.synchronize()
+        a, b, j = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        a.record(ss[0])
+        ss[1].wait_event(a)
+        for i in range(pieces):
+            with torch.cuda.stream(ss[i % 2]):
+                dst[i * piece:(i + 1) * piece].copy_(src[i * piece:(i + 1) * piece], non_blocking=True)
+        j.record(ss[1])
+        ss[0].wait_event(j)
+        b.record(ss[0])
         b.synchronize()
-        best = max(best, n / (a.elapsed_time(b) * 1e-3) / 1e9)
+        best = max(best, pieces * piece / (a.elapsed_time(b) * 1e-3) / 1e9)
     return best
 
 
@@ -574,8 +585,10 @@ def main():
     achieved = (by / launches) / (avg_us * 1e-6) / 1e9 if launches else 0.0
     copy_bytes = s["bytes_high"] + s["bytes_low"]
     h2d_gbs = h2d_probe(torch)
+    # the link moved at least what this run moved: never price the load below it
+    h2d_eff = max(h2d_gbs, copy_bytes / elapsed / 1e9)
     peaks = measure_peaks(torch)
-    load_s = s["bytes_high"] / (h2d_gbs * 1e9) if h2d_gbs else 0.0
+    load_s = s["bytes_high"] / (h2d_eff * 1e9) if h2d_eff else 0.0
     traffic, traffic_ratio = read_traffic("k_ffn_gateup")
     out = {
         "metric": METRIC,
@@ -606,6 +619,7 @@ def main():
         "detail": {
             "decode_kernels": _classes(s),
             "h2d_copy_GBps_measured_256MiB": round(h2d_gbs, 2),
+            "h2d_GBps_for_overlap": round(h2d_eff, 2),
             "measured_peaks": peaks,
             "copied_GB": round(copy_bytes / 1e9, 3),
             "copy_GBps_over_timed_region": round(copy_bytes / elapsed / 1e9, 2),
@@ -613,7 +627,7 @@ def main():
             "spec_issued": s["spec_issued"], "spec_used": s["spec_used"], "spec_wasted": s["spec_wasted"],
             "low_purged_subcopies": s["low_purged"],
             "prediction": prediction_metrics(s),
-            "overlap": overlap_metrics(s, elapsed, h2d_gbs),
+            "overlap": overlap_metrics(s, elapsed, h2d_eff),
             "stall_s": round(s["stall_ms"] * 1e-3, 4), "miss_load_s_at_measured_h2d": round(load_s, 4),
             "setup_s": round(setup_s, 1),
         },
