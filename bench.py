@@ -47,6 +47,10 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="bound on the oracle sample")
     p.add_argument("--no-prefetch", action="store_true", help="reactive LRU (predictions ignored)")
+    p.add_argument("--trained-predictor", action="store_true",
+                   help="decode with look-ahead predictors trained offline on the model's own traces (other "
+                        "inputs than the timed ones), as the paper trains its predictors; default: the "
+                        "constructed skip predictor")
     p.add_argument("--spec-fill-limit", type=int, default=1,
                    help="slots a predicted plan may fill: 0 no limit, n>0 the first n, -1 none")
     p.add_argument("--copy-calib-mib", type=int, default=1024,
@@ -368,6 +372,32 @@ def leg_sweep(torch, args):
     return out
 
 
+def train_decode_predictors(torch, model, args, steps=64, T=512):
+    """Train the decode model's look-ahead predictors offline (before the timed
+    region): routing traces of `steps` x `T` tokens from the model's own forward
+    pass with every expert resident (inputs from other seeds than the timed
+    ones), then each layer's MLP fitted as in the predtrain leg."""
+    import numpy as np
+    from paper_2410_22134_amd import train_predictor as tp
+    cfg = model.cfg
+    t0 = time.perf_counter()
+    keep = model.max_tokens
+    model.max_tokens = T
+    model.open(slots=cfg.n_experts)
+    xs, ids = tp.collect_traces(model, steps, T)
+    model.max_tokens = keep
+    res = tp.train_all(model, xs, ids, cfg.lookahead, epochs=args.train_epochs, lr=args.train_lr)
+    del xs, ids
+    tp.install(model, res)
+    a0 = float(np.mean([m["acc_start"] for _, _, m in res.values()]))
+    a1 = float(np.mean([m["acc_trained"] for _, _, m in res.values()]))
+    took = time.perf_counter() - t0
+    print(f"[bench] decode predictors trained in {took:.1f} s: held-out accuracy {a0:.3f} -> {a1:.3f}",
+          file=sys.stderr, flush=True)
+    return {"trace_tokens": steps * T, "seconds": round(took, 1), "heldout_acc_constructed": round(a0, 4),
+            "heldout_acc_trained": round(a1, 4)}
+
+
 def leg_predtrain(torch, args):
     """Offline predictor training on synthetic traces (DeepSeek-MoE-16B shape):
     traces from the library's forward pass with every expert resident, 9:1
@@ -570,6 +600,10 @@ def main():
     flags = FLAG_PROFILE | (FLAG_NO_PREFETCH if args.no_prefetch else 0)
     t_setup = time.perf_counter()
     model = SyntheticModel(cfg, max_tokens=1, flags=flags, gen_threads=8, spec_fill_limit=args.spec_fill_limit)
+    train_info = None
+    if args.trained_predictor:
+        train_info = train_decode_predictors(torch, model, args)
+        model.open(flags=flags, spec_fill_limit=args.spec_fill_limit, slots=configs.C2.slots)
     st = Stack(model, 1)
     n_in = args.warmup + args.steps
     h_in = torch.from_numpy(np.stack([sm.stack_input(cfg, i, 1) for i in range(n_in)])).cuda()
@@ -607,7 +641,9 @@ def main():
                                "experts (I=1408) top-6 + 2 shared, 32 of 64 experts per layer cached in HBM, "
                                "the rest in pinned host memory, look-ahead 1, 2-layer MLP predictor",
                    "global_batch": 1, "seq_len": 1, "parallelism": "none (1 GPU)",
-                   "prefetch": not args.no_prefetch, "spec_fill_limit": args.spec_fill_limit},
+                   "prefetch": not args.no_prefetch, "spec_fill_limit": args.spec_fill_limit,
+                   "predictor": "trained offline on the model's traces" if args.trained_predictor else
+                                "constructed skip predictor"},
         "roofline": {"bound": "hbm", "kernel": "k_ffn_gateup<bf16,1>", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": traffic, "traffic_over_algorithmic": traffic_ratio,
@@ -632,6 +668,8 @@ def main():
             "setup_s": round(setup_s, 1),
         },
     }
+    if train_info is not None:
+        out["detail"]["predictor_training"] = train_info
     if not args.no_cpu_baseline:
         print("[bench] cpu baseline (oracle)", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(cfg, model, args.cpu_seconds)
