@@ -97,6 +97,7 @@ CASES = [
     ("c4_prefill", configs.C4, 256, 1),
     ("c4_decode", configs.C4, 1, 2),
     ("c5_prefill", configs.C5, 1024, 1),
+    ("c5_decode", configs.C5, 1, 2),
     ("c5_decode_b8", configs.C5, 8, 2),
     ("c2_decode_int4", configs.C2.with_(weight_format="int4"), 1, 3),
     ("c3_prefill_int4", configs.C3.with_(weight_format="int4"), 512, 1),
