@@ -101,6 +101,9 @@ CASES = [
     ("c5_decode_b8", configs.C5, 8, 2),
     ("c2_decode_int4", configs.C2.with_(weight_format="int4"), 1, 3),
     ("c3_prefill_int4", configs.C3.with_(weight_format="int4"), 512, 1),
+    ("c4_decode_int4", configs.C4.with_(weight_format="int4"), 1, 2),
+    ("c5_prefill_int4", configs.C5.with_(weight_format="int4"), 1024, 1),
+    ("c2_decode_b4", configs.C2, 4, 2),
 ]
 
 
