@@ -25,6 +25,8 @@
  *    No C++ exception crosses this boundary.
  *  - d_* arguments are device pointers, h_* host pointers; a `stream`
  *    argument is a hipStream_t passed as void* (NULL = the null stream).
+ *  - A token count T must be 1..max_tokens; otherwise (an empty step
+ *    included) the call returns PROMOE_EINVAL before any device work.
  *  - Matrices are row-major with the reduction dimension contiguous.
  *    Element type is the config dtype: fp32, or bf16 (raw 16-bit words).
  *  - A routed expert is stored as [Wg (I x H) | Wu (I x H) | Wd (H x I)],
@@ -32,7 +34,7 @@
  *    matrices are the expert's three copy chunks (Sec. "Chunked Prefetching").
  *  - Ownership: the caller owns every d_* / h_* buffer, the cache region and
  *    the streams; buffers given to set_* calls must outlive the context.  The
- *    library owns its copy stream, events, worker thread, slot tables,
+ *    library owns its copy streams, events, worker thread, slot tables,
  *    counters and scratch buffers (allocated in promoe_create).
  *  - One context per GPU; calls on a context come from one host thread.
  *    Asynchronous kernel faults surface as PROMOE_EHIP at the next call that

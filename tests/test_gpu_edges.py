@@ -309,6 +309,13 @@ def test_error_returns():
         with pytest.raises(PromoeError) as e:
             ctx.route(0, st.x, 5, st.ids, st.w, st.s)          # T > max_tokens
         assert e.value.code == -1
+        for call in (lambda: ctx.route(0, st.x, 0, st.ids, st.w, st.s),      # empty step
+                     lambda: ctx.predict(0, st.x, 0, st.pred_ids),
+                     lambda: ctx.attn_surrogate(0, st.h, 0, st.x),
+                     lambda: ctx.residual_add(st.h, st.y, 0)):
+            with pytest.raises(PromoeError) as e:
+                call()
+            assert e.value.code == -1
         with pytest.raises(PromoeError) as e:
             ctx.route(1, st.x, 1, st.ids, st.w, st.s)          # layer out of range
         assert e.value.code == -1
