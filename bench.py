@@ -199,9 +199,24 @@ def cpu_baseline(cfg, model, budget_s):
         tok += 1
     dt = time.perf_counter() - t0
     per_token = dt / layers * cfg.n_layers
-    return {"value": round(1.0 / per_token, 4), "unit": "tok/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{layers} layers ({layers / cfg.n_layers:.2f} decode tokens of {cfg.n_layers} layers, batch 1), "
-                      f"float64 NumPy, {dt:.1f} s, scaled to a whole token"}
+    out = {"value": round(1.0 / per_token, 4), "unit": "tok/s", "cores": int(threads), "kind": "oracle",
+           "sample": f"{layers} layers ({layers / cfg.n_layers:.2f} decode tokens of {cfg.n_layers} layers, batch 1), "
+                     f"float64 NumPy, {dt:.1f} s, scaled to a whole token"}
+    # the same oracle on one thread (a shorter sample), for per-core comparisons
+    try:
+        from threadpoolctl import threadpool_limits
+        lcs1 = [ocache.LayerCache(cfg.n_experts, cfg.slots) for _ in range(cfg.n_layers)]
+        with threadpool_limits(limits=1):
+            t1 = time.perf_counter()
+            n1 = _oracle_token(cfg, model, lcs1, sm.stack_input(cfg, 20_000, 1).astype(np.float64), t1,
+                               budget_s / 3)
+            d1 = time.perf_counter() - t1
+        out["single_thread_value"] = round(n1 / d1 / cfg.n_layers, 4)
+        out["single_thread_sample"] = f"{n1} layers of one decode token, {d1:.1f} s, one BLAS thread"
+    except Exception as e:  # threadpoolctl missing or unable to limit: report the main figure only
+        out["single_thread_value"] = None
+        out["single_thread_sample"] = f"not measured ({type(e).__name__})"
+    return out
 
 
 def _oracle_token(cfg, model, lcs, h, t0, budget_s):
