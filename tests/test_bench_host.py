@@ -1,0 +1,67 @@
+"""Host-side logic of bench.py (CPU): the overlap and prediction metrics, the
+committed traffic summary it reads, and the one-GPU guard."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(HERE)
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+
+
+def _stats(high, low=0, stall_ms=0.0, **kw):
+    s = {"bytes_high": high, "bytes_low": low, "stall_ms": stall_ms}
+    s.update(kw)
+    return s
+
+
+def test_overlap_closed_form():
+    # 10 GB at 50 GB/s = 0.2 s of load; 0.05 s stalled over a 1 s run
+    m = bench.overlap_metrics(_stats(10e9, stall_ms=50.0), 1.0, 50.0)
+    assert m["load_s"] == pytest.approx(0.2)
+    assert m["H_time"] == pytest.approx(0.75)
+    assert m["H_max"] == pytest.approx(1.0)  # (1 - 0.05) / 0.2 > 1: capped
+
+
+def test_overlap_never_prices_the_link_below_the_run():
+    # the run moved 54 GB/s while the probe read 52: the load uses 54, so the
+    # load cannot exceed the elapsed time and H_time cannot exceed H_max
+    s = _stats(54e9, stall_ms=800.0)
+    m = bench.overlap_metrics(s, 1.0, 52.0)
+    assert m["load_s"] == pytest.approx(1.0)
+    assert m["H_max"] <= 1.0
+    assert m["H_time"] <= m["H_max"] + 1e-12
+
+
+def test_overlap_without_copies():
+    assert bench.overlap_metrics(_stats(0), 1.0, 50.0) is None
+
+
+def test_prediction_metrics():
+    s = {"pred_n": 100, "pred_correct": 70, "pred_in_time": 35, "spec_used": 20, "miss": 30}
+    m = bench.prediction_metrics(s)
+    assert m["accuracy"] == pytest.approx(0.7)
+    assert m["fetch_rate"] == pytest.approx(0.5)
+    assert m["goodpred"] == pytest.approx(0.35)
+    assert m["proactive_coverage"] == pytest.approx(0.4)
+    assert bench.prediction_metrics({"pred_n": 0, "pred_correct": 0, "pred_in_time": 0, "spec_used": 0,
+                                     "miss": 0})["accuracy"] is None
+
+
+def test_traffic_summary_matches_the_kernel_source():
+    # the committed counter summary was taken on the current GEMV source
+    traffic, ratio = bench.read_traffic("k_ffn_gateup")
+    assert traffic is not None and traffic > 0
+    assert ratio == pytest.approx(1.008, abs=1e-3)
+    assert bench.read_traffic("no_such_kernel") == (None, None)
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=300, cwd=ROOT)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
