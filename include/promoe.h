@@ -102,7 +102,8 @@ typedef struct promoe_config {
   int32_t slots_per_layer;   /* C cache slots per layer, 1..64 */
   int32_t lookahead;         /* d: the predictor of layer l targets layer l+d (d >= 0) */
   int32_t pred_hidden;       /* 0: predictor is one GEMV Wp [E x H];
-                                else a 2-layer MLP: W1 [pred_hidden x H], W2 [E x pred_hidden] */
+                                else a 2-layer MLP: W1 [pred_hidden x H], W2 [E x pred_hidden];
+                                a multiple of 8 */
   int32_t max_tokens;        /* T limit of every call (1..8192 / top_k) */
   int32_t dtype;             /* PROMOE_F32 or PROMOE_BF16 */
   int64_t copy_subchunk_bytes; /* copy issue unit; 0 = 16 MiB */
@@ -179,11 +180,13 @@ typedef struct promoe_plan {
 
 /* ---- lifetime ------------------------------------------------------------ */
 
-/* Create a context on the current HIP device.  d_cache is the caller's cache
- * region of at least n_layers*slots_per_layer*expert_bytes bytes (slot s of
- * layer l at offset (l*C+s)*expert_bytes).  All slots start free.
- * Errors: EINVAL (null/size), EUNSUP (E > 64, C > 64, k > 8, H or I not a
- * multiple of 8), ENOMEM, EHIP. */
+/* Create a context on the current HIP device (Sec. "Cache Implementation": a
+ * per-layer LRU cache of experts whose storage is one contiguous region
+ * allocated up front).  d_cache is the caller's cache region of at least
+ * n_layers*slots_per_layer*expert_bytes bytes (slot s of layer l at offset
+ * (l*C+s)*expert_bytes).  All slots start free.
+ * Errors: EINVAL (null/size), EUNSUP (E > 64, C > 64, k > 8, H, I,
+ * shared_inter or pred_hidden not a multiple of 8), ENOMEM, EHIP. */
 int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, promoe_ctx** out);
 
 /* Drain all copies, stop the worker and free library resources. */
@@ -266,8 +269,13 @@ int promoe_expert_ffn(promoe_ctx* ctx, int layer, const void* d_x, int T, const 
 
 /* ---- state and statistics ------------------------------------------------ */
 
-/* Logical counters of one layer, or of all layers summed (layer = -1); the
- * physical counters and timings always cover all layers.  Synchronises. */
+/* Counters behind the paper's metrics (Sec. "A New Prediction Metric: GoodPred":
+ * Accuracy = pred_correct / pred_n, FetchRate = pred_in_time / pred_correct,
+ * GoodPred = Accuracy x FetchRate; Sec. "Evaluation": hit and miss counts, bytes
+ * copied per priority, the stall of compute on copies).  Logical counters of
+ * one layer, or of all layers summed (layer = -1); the physical counters and
+ * timings always cover all layers.  Synchronises.  Errors: EINVAL (null out,
+ * layer out of range), EHIP (a copy or kernel failed). */
 int promoe_cache_stats(promoe_ctx* ctx, int layer, promoe_stats* out);
 int promoe_reset_stats(promoe_ctx* ctx);
 /* h_slot_of [E]: slot of each expert of the layer, -1 if not resident.  Synchronises. */

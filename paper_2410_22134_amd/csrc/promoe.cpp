@@ -186,7 +186,8 @@ struct promoe_ctx {
   const void* route_x = nullptr;  // input of the latest route (its gate logits are in d_logits)
   int last_route_layer = -1;      // layer of the latest route, kept after its FFN call
   std::vector<char> ffn_started;  // per route position: launched by the route itself
-  int64_t route_head_tok = -1;    // compute token of that launch (-1 none)
+  hipStream_t route_stream = nullptr;  // stream of the latest route
+  hipEvent_t route_done = nullptr;     // recorded on it after the route's last launch
   PlanRecord route_rec{};
   std::vector<int64_t> need01, need2;  // copy seq each position waits for (-1 none)
   std::vector<int> need_q;             // engine queue of those copies
@@ -572,7 +573,7 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
     return PROMOE_EINVAL;
   }
   if (g.n_experts > kMaxE || g.slots_per_layer > 64 || g.top_k > kMaxK || g.hidden % 8 || g.inter % 8 ||
-      g.shared_inter % 8 || (int64_t)g.max_tokens * g.top_k > 8192 ||
+      g.shared_inter % 8 || g.pred_hidden % 8 || (int64_t)g.max_tokens * g.top_k > 8192 ||
       (g.weight_format == PROMOE_WEIGHTS_INT4 &&
        (g.dtype != PROMOE_BF16 || g.hidden % kInt4Group || g.inter % kInt4Group))) {
     g_last_error = "unsupported shape";
@@ -685,6 +686,7 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   c->rec_h = static_cast<PlanRecord*>(rh);
   c->rec_d = static_cast<PlanRecord*>(rd);
   for (int i = 0; i < kRecRing; ++i) hipEventCreateWithFlags(&c->rec_ev[i], hipEventDisableTiming);
+  hipEventCreateWithFlags(&c->route_done, hipEventDisableTiming);
 
   // ---- copy engine + scheduler
   for (auto& cs : c->eng.stream) hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
@@ -763,6 +765,7 @@ int promoe_destroy(promoe_ctx* c) {
   for (auto& e : c->eng.ev) hipEventDestroy(e);
   for (auto& e : c->cev) hipEventDestroy(e);
   for (int i = 0; i < kRecRing; ++i) hipEventDestroy(c->rec_ev[i]);
+  hipEventDestroy(c->route_done);
   for (auto& cs : c->eng.stream) hipStreamDestroy(cs);
   hipHostFree(c->rec_h);
   if (c->d_tclock) hipFree(c->d_tclock);
@@ -1022,6 +1025,10 @@ int promoe_route(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_id
   rc = launch_route_head(c, layer, d_x, T, s);
   if (rc) return rc;
   if (c->eng.err != hipSuccess) return fail_hip(c->eng.err, "copy engine");
+  // the FFN call reads what the route's kernels wrote (ids, weights, the plan's
+  // slots and permutation): one on another stream waits for this event
+  HIPCHK(hipEventRecord(c->route_done, s));
+  c->route_stream = s;
   lk.unlock();
   c->cv.notify_all();
   c->route_layer = layer;
@@ -1219,7 +1226,6 @@ std::vector<FillWait> fill_waits(const promoe_ctx* c) {
 // starts on those fills while the caller runs the predictor and the FFN call
 // computes the rest.  Caller holds c->mu; c->route_rec is this route's plan.
 static int launch_route_head(promoe_ctx* c, int layer, const void* d_x, int T, hipStream_t s) {
-  c->route_head_tok = -1;
   const bool in_order = (c->cfg.flags & (PROMOE_FLAG_NO_REORDER | PROMOE_FLAG_NO_PREEMPT)) != 0;
   if ((int64_t)T * c->K <= 64 || in_order) return PROMOE_OK;
   std::vector<char> arriving(c->route_rec.n);
@@ -1228,7 +1234,7 @@ static int launch_route_head(promoe_ctx* c, int layer, const void* d_x, int T, h
   if (head.empty()) return PROMOE_OK;
   const int rc = ffn_launch(c, ffn_args(c, layer, d_x, T), head, s, CopyWait(), CopyWait());
   if (rc) return rc;
-  c->route_head_tok = release_after_launch(c, layer, head, s);
+  release_after_launch(c, layer, head, s);
   for (int p : head) c->ffn_started[p] = 1;
   return PROMOE_OK;
 }
@@ -1248,10 +1254,10 @@ int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const in
 
   std::unique_lock<std::mutex> lk(c->mu);
   const int n = rec.n;
-  // The route may have started the readers of the first fills' victim slots
-  // (on its stream: order this stream after them).
-  if (c->route_head_tok >= 0 && c->cstream[c->route_head_tok % kComputeRing] != s)
-    HIPCHK(hipStreamWaitEvent(s, c->cev[c->route_head_tok % kComputeRing], 0));
+  // On another stream than the route's, order this call after everything the
+  // route enqueued: its top-k and plan (ids, weights, slots, permutation) and
+  // the readers of the first fills' victim slots it may have started.
+  if (c->route_stream != s) HIPCHK(hipStreamWaitEvent(s, c->route_done, 0));
   std::vector<char> done(c->ffn_started), is_def(n, 0);
   for (const auto& d : c->deferred) is_def[d.pos] = 1;
 

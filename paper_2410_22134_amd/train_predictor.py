@@ -136,7 +136,14 @@ def to_model_dtype(w, dtype: str):
 
 
 def install(model, trained):
-    """Use trained predictors in the model's context (the cache starts over)."""
+    """Use trained predictors in the model: the device weights the next
+    model.open() hands to the library, and the host copy of the same stored
+    values (bf16 bits or fp32) that model.np_pred exposes as data."""
     cfg = model.cfg
     for l, (w1, w2, _) in trained.items():
-        model.d_pred[l] = (to_model_dtype(w1, cfg.dtype), to_model_dtype(w2, cfg.dtype))
+        d1, d2 = to_model_dtype(w1, cfg.dtype), to_model_dtype(w2, cfg.dtype)
+        model.d_pred[l] = (d1, d2)
+        host = [t.cpu().numpy() for t in (d1, d2)]
+        if cfg.dtype == "bf16":
+            host = [h.view(np.uint16) for h in host]
+        model.np_pred[l] = (host[0], host[1])

@@ -25,6 +25,12 @@ from oracle import quant as oquant
 from oracle import router as orouter
 from oracle import stack as ostack
 from synth import model as sm
+from synth.configs import MoEConfig, Workload
+
+# a small bf16 shape whose dimensions meet the MFMA tiling (hidden % 64, inter % 128)
+SMALL = MoEConfig(name="small_bf16", seed=11, n_layers=3, hidden=256, n_experts=8, top_k=2, inter=512,
+                  slots=4, lookahead=1, pred_hidden=64, dtype="bf16", n_shared=1, shared_inter=256,
+                  shared_gate=1, workloads=(Workload("prefill", 77, 1),))
 
 MARGIN = 1e-3
 TOL_BF16_MAXABS, TOL_BF16_RELL2, TOL_F32 = 2e-2, 1e-2, 1e-4
@@ -130,15 +136,36 @@ def half_ulp_bf16(v):
     return 0.5 * 2.0 ** (np.floor(np.log2(a)) - 7)
 
 
-def check_bf16_output(yg, y_exact, where):
-    """bf16 bar: max-abs error beyond the output's own final rounding <= 2e-2, rel-L2 < 1e-2.
+# Below this magnitude half a bf16 step is at most 2^-8 (0.0078), so the raw
+# max-abs bound is asserted as is; at and above it the final rounding alone may
+# move y by 0.0156 (|y| in [4, 8)) or 0.031 (|y| in [8, 16)), and the bound
+# applies to the error beyond that rounding.
+RAW_BOUND_BELOW = 4.0
 
-    The final rounding of y to bf16 may move it by half a bf16 step, which is
-    already 0.03 for |y| in [8, 16); the 2e-2 bound applies to everything else."""
-    excess = np.abs(yg - y_exact) - half_ulp_bf16(y_exact)
-    rel = np.linalg.norm(yg - y_exact) / max(np.linalg.norm(y_exact), 1e-30)
-    assert excess.max() <= TOL_BF16_MAXABS and rel < TOL_BF16_RELL2, (where, excess.max(), rel)
-    return float(np.abs(yg - y_exact).max()), float(rel)
+# (test, where, worst raw error, worst raw error where |y| < 4, worst excess
+# beyond half a step where |y| >= 4, rel-L2) of every bf16 output check, for
+# the end-of-session summary
+BF16_REPORT = []
+
+
+def check_bf16_output(yg, y_exact, where):
+    """bf16 bar: max-abs <= 2e-2 and rel-L2 < 1e-2.
+
+    Where |y| < 4 the raw error |y_gpu - y_exact| is held to 2e-2.  Where
+    |y| >= 4 the bound applies to the error beyond the output's own final
+    rounding (half a bf16 step, which is already 0.031 for |y| in [8, 16))."""
+    import os
+    diff = np.abs(yg - y_exact)
+    small = np.abs(y_exact) < RAW_BOUND_BELOW
+    raw_small = float(diff[small].max()) if small.any() else 0.0
+    excess = float((diff - half_ulp_bf16(y_exact))[~small].max()) if (~small).any() else float("-inf")
+    rel = float(np.linalg.norm(yg - y_exact) / max(np.linalg.norm(y_exact), 1e-30))
+    raw = float(diff.max()) if diff.size else 0.0
+    test = os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0]
+    BF16_REPORT.append((test, str(where), raw, raw_small, excess, rel))
+    assert raw_small <= TOL_BF16_MAXABS and excess <= TOL_BF16_MAXABS and rel < TOL_BF16_RELL2, \
+        (where, raw_small, excess, rel)
+    return raw, rel
 
 
 def check_ffn(cfg, model, l, x64, g_ids, w_ref, s_ref, y_gpu, tokens=None):

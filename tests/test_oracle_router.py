@@ -73,3 +73,36 @@ def test_shared_scale_is_sigmoid():
     assert np.allclose(s, scipy.special.expit([0.0, 0.0]))
     s = router.shared_scale(x, np.array([1.0, 0.0]))
     assert np.allclose(s, scipy.special.expit([1.0, 0.0]))
+
+
+def test_weights_for_on_route_ids_equals_route_weights():
+    # evaluated on the oracle's own selection, the helper reproduces route()
+    rng = np.random.default_rng(4)
+    z = rng.standard_normal((40, 12)) * 2
+    for k in (1, 3, 12):
+        for renorm in (True, False):
+            ids, w, p = router.route(z, k, renorm)
+            assert np.array_equal(router.weights_for(p, ids, renorm), w)
+
+
+def test_weights_for_arbitrary_ids_closed_form():
+    # on any distinct ids (not the top-k, any order) the renormalised weights are
+    # the softmax over exactly those logits, in the given order; without
+    # renormalisation they are the full softmax's values at those ids
+    rng = np.random.default_rng(5)
+    T, E, k = 30, 9, 3
+    z = rng.standard_normal((T, E)) * 3
+    p = scipy.special.softmax(z, axis=1)
+    ids = np.stack([rng.permutation(E)[:k] for _ in range(T)])
+    w = router.weights_for(p, ids, renorm=True)
+    for t in range(T):
+        sel = z[t, ids[t]]
+        expect = np.exp(sel - sel.max()) / np.exp(sel - sel.max()).sum()
+        assert np.allclose(w[t], expect, rtol=1e-12, atol=1e-15)
+    w_nr = router.weights_for(p, ids, renorm=False)
+    for t in range(T):
+        for r in range(k):
+            assert w_nr[t, r] == p[t, ids[t, r]]
+    # a permutation of the ids permutes the weights the same way (no axis mix-up)
+    perm = ids[:, ::-1]
+    assert np.allclose(router.weights_for(p, perm, True), w[:, ::-1], rtol=1e-14, atol=0)
