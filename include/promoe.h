@@ -267,6 +267,29 @@ int promoe_prefetch(promoe_ctx* ctx, int target_layer, const int32_t* h_ids, int
 int promoe_expert_ffn(promoe_ctx* ctx, int layer, const void* d_x, int T, const int32_t* d_ids,
                       const float* d_w, const float* d_shared_scale, void* d_y, void* stream);
 
+/* Allocation-free variant of promoe_expert_ffn, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  Same contract, arguments and result as
+ * promoe_expert_ffn (the outputs are the same values), but the activations
+ * and expert outputs its kernels exchange live in a file-scope device array of
+ * PROMOE_NOALLOC_SCRATCH_BYTES (8 MiB) that each GPU the library runs on holds
+ * until the process ends, not in the context's buffers.  The call itself
+ * allocates no device memory and is never timed (PROMOE_FLAG_PROFILE does not
+ * apply to it); 4-bit experts always take the dequantising GEMV.
+ * Limits: at most 64 routed pairs (T * top_k <= 64, the decode sizes), and a
+ * scratch need of at most 8 MiB: T*k*I*s + T*k*H*4 + T*I_sh*s + n*T*H*4 bytes
+ * (s = bytes per element of the config dtype, n = split-K slices of the shared
+ * expert's down product, 1 unless T >= 16), each term rounded up to 256.
+ * Beyond either limit the call returns PROMOE_EINVAL before any device work
+ * (the route stays pending; promoe_expert_ffn may then consume it).  Every
+ * call on one GPU shares that GPU's array: calls that overlap on one GPU (two
+ * contexts, or two streams of one context) race.  Nothing in the array needs
+ * to start at zero: every byte a kernel reads is written earlier in the same
+ * call. */
+#define PROMOE_NOALLOC_SCRATCH_BYTES ((size_t)8 << 20)
+int promoe_expert_ffn_noalloc(promoe_ctx* ctx, int layer, const void* d_x, int T, const int32_t* d_ids,
+                              const float* d_w, const float* d_shared_scale, void* d_y, void* stream);
+
 /* ---- state and statistics ------------------------------------------------ */
 
 /* Counters behind the paper's metrics (Sec. "A New Prediction Metric: GoodPred":

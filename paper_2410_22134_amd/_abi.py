@@ -83,6 +83,7 @@ def lib() -> ctypes.CDLL:
         "promoe_route": ([_vp, ctypes.c_int, _vp, ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
         "promoe_prefetch": ([_vp, ctypes.c_int, _vp, ctypes.c_int, ctypes.c_int, _vp], ctypes.c_int),
         "promoe_expert_ffn": ([_vp, ctypes.c_int, _vp, ctypes.c_int, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
+        "promoe_expert_ffn_noalloc": ([_vp, ctypes.c_int, _vp, ctypes.c_int, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
         "promoe_cache_stats": ([_vp, ctypes.c_int, P(Stats)], ctypes.c_int),
         "promoe_reset_stats": ([_vp], ctypes.c_int),
         "promoe_slot_table": ([_vp, ctypes.c_int, _vp], ctypes.c_int),
@@ -109,7 +110,8 @@ def lib() -> ctypes.CDLL:
 def exported_symbols():
     return [n for n in ("promoe_create", "promoe_destroy", "promoe_set_layer", "promoe_set_attn",
                         "promoe_set_expert_host", "promoe_set_initial_cache", "promoe_predict", "promoe_route",
-                        "promoe_prefetch", "promoe_expert_ffn", "promoe_cache_stats", "promoe_reset_stats",
+                        "promoe_prefetch", "promoe_expert_ffn", "promoe_expert_ffn_noalloc", "promoe_cache_stats",
+                        "promoe_reset_stats",
                         "promoe_slot_table", "promoe_last_plan", "promoe_sync", "promoe_attn_surrogate",
                         "promoe_residual_add", "promoe_host_alloc", "promoe_host_free", "promoe_expert_bytes",
                         "promoe_strerror", "promoe_last_error_string", "promoe_peak_hbm_read",
@@ -210,6 +212,11 @@ class Context:
     def expert_ffn(self, layer, x, T, ids, w, shared_scale, y, stream=None):
         check(lib().promoe_expert_ffn(self._h, layer, _p(x), T, _p(ids), _p(w), _p(shared_scale), _p(y),
                                       _stream(stream)), "promoe_expert_ffn")
+
+    def expert_ffn_noalloc(self, layer, x, T, ids, w, shared_scale, y, stream=None):
+        """promoe_expert_ffn with its scratch in the library's static device array."""
+        check(lib().promoe_expert_ffn_noalloc(self._h, layer, _p(x), T, _p(ids), _p(w), _p(shared_scale), _p(y),
+                                              _stream(stream)), "promoe_expert_ffn_noalloc")
 
     # harness
     def attn_surrogate(self, layer, h, T, x_out, stream=None):

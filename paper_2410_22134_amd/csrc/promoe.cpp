@@ -46,6 +46,16 @@ constexpr int kMaxSplit = 8;  // split-K slices of the shared expert's down GEMM
 constexpr int kCopyRing = 4096;
 constexpr int kComputeRing = 4096;
 
+// Scratch of promoe_expert_ffn_noalloc: one file-scope device array per GPU
+// (each device that loads the library holds its own copy until the process
+// ends).  Host code never uses the array's name as an address: the per-device
+// address comes from hipGetSymbolAddress, taken once per device at context
+// creation with that device current.
+constexpr size_t kNoAllocScratchBytes = (size_t)8 << 20;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+uint8_t* g_scratch_ptr[kMaxDevices] = {};
+
 struct ProfEntry {
   hipEvent_t a, b;
   int cls;  // 0..5 kernel classes, kStallClass copy waits
@@ -136,6 +146,8 @@ struct Deferred {
 
 }  // namespace
 
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+
 struct promoe_ctx {
   promoe_config cfg{};
   int dev = 0;
@@ -163,6 +175,8 @@ struct promoe_ctx {
   void* d_act_sh = nullptr;
   float* d_Ysh = nullptr;
   void* d_u = nullptr;
+  uint8_t* noalloc_scratch = nullptr;  // this device's address of `scratch`
+  bool noalloc_call = false;           // inside promoe_expert_ffn_noalloc: no profiling, no staging
 
   std::vector<LayerW> lw;
 
@@ -240,6 +254,23 @@ int fail_hip(hipError_t e, const char* what) {
     hipError_t _e = hipGetLastError();                \
     if (_e != hipSuccess) return fail_hip(_e, what);  \
   } while (0)
+
+// This device's address of `scratch` (the current device must be `dev`).
+int scratch_address(int dev, uint8_t** out) {
+  if (dev < 0 || dev >= kMaxDevices) {
+    g_last_error = "device index beyond the scratch table";
+    return PROMOE_EUNSUP;
+  }
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return fail_hip(e, "hipGetSymbolAddress(scratch)");
+    g_scratch_ptr[dev] = static_cast<uint8_t*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return PROMOE_OK;
+}
 
 hipEvent_t prof_event(promoe_ctx* c) {
   if (!c->prof_free.empty()) {
@@ -600,6 +631,13 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   c->pred_host.assign(c->L, 0ull);
   c->last_precise.resize(c->L);
   hipGetDevice(&c->dev);
+  {
+    const int rc = scratch_address(c->dev, &c->noalloc_scratch);
+    if (rc) {
+      delete c;
+      return rc;
+    }
+  }
 
   // ---- device memory (one allocation, 256-byte aligned pieces)
   const int L = c->L, C = c->C, E = c->E, T = c->maxT, Kk = c->K, H = c->H;
@@ -1086,15 +1124,16 @@ int ffn_launch_one(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipSt
     for (int64_t q : w.seq) any = any || q >= 0;
     if (any) {
       hipEvent_t pa = nullptr, pb = nullptr;
-      if (c->profile) { pa = prof_event(c); pb = prof_event(c); hipEventRecord(pa, s); }
+      const bool prof = c->profile && !c->noalloc_call;
+      if (prof) { pa = prof_event(c); pb = prof_event(c); hipEventRecord(pa, s); }
       for (int64_t q : w.seq)
         if (q >= 0) HIPCHK(hipStreamWaitEvent(s, c->eng.event(q), 0));
-      if (c->profile) { hipEventRecord(pb, s); c->prof_pending.push_back(ProfEntry{pa, pb, kStallClass, 0, 0}); }
+      if (prof) { hipEventRecord(pb, s); c->prof_pending.push_back(ProfEntry{pa, pb, kStallClass, 0, 0}); }
     }
     const double k = pass == 0 ? 2.0 : 1.0;  // gate and up, or down
     const bool shared_only = jobs.size() == 1 && jobs[0] == kSharedJob;
     const int cls = (gemm ? (shared_only ? 4 : 2) : 0) + pass;
-    a.tclock = c->profile ? tclock_slot(c, s, cls, k * wbytes, k * flops) : nullptr;
+    a.tclock = c->profile && !c->noalloc_call ? tclock_slot(c, s, cls, k * wbytes, k * flops) : nullptr;
     if (gemm) launch_gemm(a, pass, maxc, s);
     else launch_ffn(a, pass, maxc, c->dt, s);
     LAUNCHCHK("ffn");
@@ -1118,7 +1157,7 @@ int ffn_launch(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipStream
   for (int p : jobs) {
     const bool is_sh = p == kSharedJob;
     const int cnt = is_sh ? a.T : c->route_rec.count[p];
-    if (c->q4 && !is_sh) (c->d_stage && use_gemm(c, cnt, false) ? gqm : gq).push_back(p);
+    if (c->q4 && !is_sh) (c->d_stage && !c->noalloc_call && use_gemm(c, cnt, false) ? gqm : gq).push_back(p);
     else if (!use_gemm(c, cnt, is_sh)) gv.push_back(p);
     else if (is_sh) sh.push_back(p);
     else gm.push_back(p);
@@ -1239,18 +1278,24 @@ static int launch_route_head(promoe_ctx* c, int layer, const void* d_x, int T, h
   return PROMOE_OK;
 }
 
-int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const int32_t* d_ids, const float* d_w,
-                      const float* d_shared_scale, void* d_y, void* stream) {
+// Argument checks shared by promoe_expert_ffn and its allocation-free variant.
+static int check_ffn_call(promoe_ctx* c, int layer, const void* d_x, int T, const int32_t* d_ids, const float* d_w,
+                          const float* d_shared_scale, const void* d_y) {
   if (!c || layer < 0 || layer >= c->L || !d_x || !d_ids || !d_w || !d_y) return PROMOE_EINVAL;
   if (c->route_layer != layer || c->route_T != T) {
     g_last_error = "expert_ffn without a matching route";
     return PROMOE_ESTATE;
   }
   if (c->cfg.shared_gate && c->Ish > 0 && !d_shared_scale) return PROMOE_EINVAL;
-  hipStream_t s = static_cast<hipStream_t>(stream);
+  return PROMOE_OK;
+}
+
+// The FFN of the routed layer with the activations and expert outputs in the
+// buffers `a` names (the context's, or the allocation-free scratch).
+static int expert_ffn_run(promoe_ctx* c, int layer, int T, const float* d_w, const float* d_shared_scale,
+                          void* d_y, hipStream_t s, const FfnArgs& a) {
   c->last_stream = s;
   const PlanRecord& rec = c->route_rec;
-  const FfnArgs a = ffn_args(c, layer, d_x, T);
 
   std::unique_lock<std::mutex> lk(c->mu);
   const int n = rec.n;
@@ -1347,9 +1392,9 @@ int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const in
   c->cv.notify_all();
 
   CombineArgs ca{};
-  ca.Y = c->d_Y;
+  ca.Y = a.Y;
   ca.w = d_w;
-  ca.Ysh = c->Ish > 0 ? c->d_Ysh : nullptr;
+  ca.Ysh = c->Ish > 0 ? a.Ysh : nullptr;
   ca.ysh_split = a.ksplit;
   ca.ysh_split_stride = a.ysh_split_stride;
   ca.sscale = (c->Ish > 0 && c->cfg.shared_gate) ? d_shared_scale : nullptr;
@@ -1359,11 +1404,54 @@ int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const in
   launch_combine(ca, T, c->dt, s);
   LAUNCHCHK("combine");
   c->route_layer = -1;
-  if (c->profile && c->prof_pending.size() > 4096) {
+  if (c->profile && !c->noalloc_call && c->prof_pending.size() > 4096) {
     HIPCHK(hipStreamSynchronize(s));
     prof_resolve(c);
   }
   return PROMOE_OK;
+}
+
+int promoe_expert_ffn(promoe_ctx* c, int layer, const void* d_x, int T, const int32_t* d_ids, const float* d_w,
+                      const float* d_shared_scale, void* d_y, void* stream) {
+  const int rc = check_ffn_call(c, layer, d_x, T, d_ids, d_w, d_shared_scale, d_y);
+  if (rc) return rc;
+  return expert_ffn_run(c, layer, T, d_w, d_shared_scale, d_y, static_cast<hipStream_t>(stream),
+                        ffn_args(c, layer, d_x, T));
+}
+
+int promoe_expert_ffn_noalloc(promoe_ctx* c, int layer, const void* d_x, int T, const int32_t* d_ids,
+                              const float* d_w, const float* d_shared_scale, void* d_y, void* stream) {
+  int rc = check_ffn_call(c, layer, d_x, T, d_ids, d_w, d_shared_scale, d_y);
+  if (rc) return rc;
+  if ((int64_t)T * c->K > 64) {
+    g_last_error = "expert_ffn_noalloc: more than 64 routed pairs (T * top_k) in the step";
+    return PROMOE_EINVAL;
+  }
+  // Scratch layout: activations [T*k x I], expert outputs [T*k x H] fp32,
+  // shared activations [T x I_sh], shared partial outputs [ksplit x T x H] fp32,
+  // each piece 256-byte aligned.  Every byte the kernels read is written
+  // earlier in the same call, so nothing needs clearing.
+  FfnArgs a = ffn_args(c, layer, d_x, T);
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t o = off; off += (bytes + 255) & ~(size_t)255; return o; };
+  const size_t pairs = (size_t)T * c->K;
+  const size_t o_act = take(pairs * c->I * c->eb), o_Y = take(pairs * c->H * sizeof(float)),
+               o_actsh = take((size_t)T * std::max(c->Ish, 1) * c->eb),
+               o_Ysh = take((size_t)a.ksplit * T * c->H * sizeof(float));
+  if (off > kNoAllocScratchBytes) {
+    g_last_error = "expert_ffn_noalloc: the step needs " + std::to_string(off) + " bytes of scratch, more than the " +
+                   std::to_string(kNoAllocScratchBytes) + " of the allocation-free call";
+    return PROMOE_EINVAL;
+  }
+  uint8_t* base = c->noalloc_scratch;
+  a.act = base + o_act;
+  a.Y = reinterpret_cast<float*>(base + o_Y);
+  a.act_sh = base + o_actsh;
+  a.Ysh = reinterpret_cast<float*>(base + o_Ysh);
+  c->noalloc_call = true;
+  rc = expert_ffn_run(c, layer, T, d_w, d_shared_scale, d_y, static_cast<hipStream_t>(stream), a);
+  c->noalloc_call = false;
+  return rc;
 }
 
 int promoe_cache_stats(promoe_ctx* c, int layer, promoe_stats* out) {
