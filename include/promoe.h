@@ -326,8 +326,9 @@ int promoe_residual_add(promoe_ctx* ctx, float* d_h, const void* d_y, int T, voi
  * pointer or a size out of range, PROMOE_EHIP if the launch fails.  The caller
  * owns every buffer. */
 /* Reads `bytes` (> 0, a multiple of 16) at d_buf once with 16-byte
- * non-temporal loads, `blocks` blocks of 256 threads in a grid-stride loop;
- * writes one float per block to d_sink (>= blocks floats). */
+ * non-temporal loads, `blocks` blocks of 256 threads, each streaming one
+ * contiguous piece of ceil(bytes / blocks) bytes (16-128 KiB pieces read
+ * fastest); writes one float per block to d_sink (>= blocks floats). */
 int promoe_peak_hbm_read(const void* d_buf, size_t bytes, float* d_sink, int blocks, void* stream);
 /* `blocks` blocks of 512 threads; each wave runs `iters` rounds of 32
  * independent v_mfma_f32_16x16x32_bf16 on register operands, i.e.

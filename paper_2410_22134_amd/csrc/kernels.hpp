@@ -26,17 +26,13 @@ struct RowsArgs {
 // j with job_tile0[j] <= b < job_tile0[j + 1].
 constexpr int kInt4Group = 128;  // 4-bit expert storage: codes per bf16 scale
 constexpr int kMaxJobs = 80;  // 64 route positions + pieces of the shared expert
-// Launch clock slot: word 0 = max of ~start over the first blocks (so ~word0 is
-// the earliest start), then kTclkLines 128-byte lines whose first words hold
-// the latest wave end seen by the waves hashed to that line.
-constexpr int kTclkLines = 32;
-constexpr int kTclkWords = 16 * (kTclkLines + 1);
 constexpr uint8_t kSharedJob = 255;
 // One expert job of an FFN launch (a route position, the shared expert, or a
 // piece of the shared expert's rows), 32 bytes: a block reads it with one
 // scalar load.
 struct alignas(16) FfnJob {
-  const void* w;   // expert weights [Wg | Wu | Wd] (slot or resident shared expert)
+  const void* w;   // expert weights [Wg | Wu | Wd] (slot or resident shared expert); null: a route
+                   // position resolved on the device (GEMV kernels; see FfnArgs::npos)
   int32_t q0, q1;  // pair range [q0, q1) (token range for the shared expert)
   int32_t I;       // intermediate size of the expert
   int32_t r0;      // GEMV: first row of the job's piece
@@ -65,7 +61,12 @@ struct FfnArgs {
   int q4;                     // routed experts stored as 4-bit codes (then bf16 scales)
   int ksplit;                   // split-K slices of the shared expert's down GEMM (>= 1)
   int64_t ysh_split_stride;     // elements between the slices' partial outputs in Ysh
-  unsigned long long* tclock;   // optional launch clock slot (see kTclkWords), zero-initialised
+  // Jobs with w == null are route positions `pos` resolved on the device from the
+  // plan: computed only when pos < npos[0] (the resident positions, which the
+  // reordered plan puts first) and the position's slot is not in busy_mask;
+  // weights from the slot order_slot[pos], pairs offsets[pos] .. offsets[pos + 1].
+  const int32_t* npos;
+  uint64_t busy_mask;
   int tail_block0;              // GEMM gate/up of one job: first block of the half-height tail tiles
   int tail_n0;                  // first n-tile (of 128 columns) the tail covers
   int32_t job_tile0[kMaxJobs + 1];  // GEMM: first block of each job in the 1-D grid
@@ -139,20 +140,8 @@ struct PlanArgs {
   int32_t* d_offsets;    // [65]
   int32_t* d_perm;       // [T*k]
   int32_t* d_pos_of;     // [64] scratch
+  int32_t* d_npos;       // [1] precise plan: resident positions (reordered: they come first)
 };
-
-// Launch timing on the device's constant-rate clock (profiling only): the
-// first blocks carry the launch start (blocks start in index order), and wave
-// ends are spread over kTclkLines cache lines so the atomics do not serialise.
-__device__ __forceinline__ void tclock_start(const FfnArgs& a) {
-  if (a.tclock && threadIdx.x == 0 && blockIdx.x < 8 && blockIdx.y == 0) atomicMax(a.tclock, ~(unsigned long long)wall_clock64());
-}
-__device__ __forceinline__ void tclock_end(const FfnArgs& a) {
-  if (a.tclock && (threadIdx.x & 63) == 0) {
-    const int line = 1 + (blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6)) % kTclkLines;
-    atomicMax(a.tclock + 16 * line, (unsigned long long)wall_clock64());
-  }
-}
 
 // Expand 4-bit experts into dense bf16 [Wg | Wu | Wd] copies (the MFMA GEMM's
 // operand type: each weight (code - 8) * scale is rounded to bf16).
@@ -167,7 +156,8 @@ void launch_dequant_q4(const DequantArgs& a, hipStream_t s);
 void launch_rows_gemv(const RowsArgs& a, int wdtype, int xdtype, hipStream_t s);
 // Launches one pass of the GEMV kernels over the jobs (a copy of `a` is
 // adjusted per pass; `a` is unchanged).  max_tokens = most pairs of any job.
-// With ev0/ev1 set, the launch records them itself (kernel execution time).
+// With ev0/ev1 set, the launch records them itself at the kernel's start and
+// end (hipExtLaunchKernelGGL: kernel execution time, as a profiler sees it).
 void launch_ffn(const FfnArgs& a, int pass, int max_tokens, int dtype, hipStream_t s, hipEvent_t ev0 = nullptr,
                 hipEvent_t ev1 = nullptr);
 // Grouped MFMA GEMM (bf16) for the same passes; needs N % 128 == 0 and K % 64 == 0.
@@ -183,7 +173,8 @@ struct RowsGemmArgs {
   int ldo, o_off, add;
 };
 void launch_gemm_rows(const RowsGemmArgs& a, hipStream_t s);
-void launch_gemm(FfnArgs& a, int pass, int max_tokens, hipStream_t s);
+void launch_gemm(FfnArgs& a, int pass, int max_tokens, hipStream_t s, hipEvent_t ev0 = nullptr,
+                 hipEvent_t ev1 = nullptr);
 void launch_combine(const CombineArgs& a, int T, int dtype, hipStream_t s);
 void launch_rmsnorm_quant(const float* h, void* out, int T, int H, int dtype, hipStream_t s);
 void launch_residual_add(float* h, const void* y, int n, int dtype, hipStream_t s);

@@ -24,6 +24,8 @@
 // 16 rows read by one ds_read_b128 phase fall in distinct banks.  Lane l of an
 // MFMA supplies A[l % 16][8*(l/16)..+8] and B[l % 16][8*(l/16)..+8] and
 // receives C[4*(l/16) + i][l % 16], i < 4.
+#include <hip/hip_ext.h>
+
 #include <algorithm>
 
 #include "common.hpp"
@@ -312,7 +314,6 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_ffn(FfnArgs a) {
   __shared__ __attribute__((aligned(1024))) bf16_t lds[LDS];
 
   const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
-  tclock_start(a);
   if constexpr (TAIL) {
     if ((int)blockIdx.x >= a.tail_block0) {
       const int bt = xcd_grouped(blockIdx.x - a.tail_block0, gridDim.x - a.tail_block0);
@@ -320,7 +321,6 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_ffn(FfnArgs a) {
       const int mt = (jd.q1 - jd.q0 + 127) / 128;
       ffn_tile<128, 2, 4, PASS, 3>(a, lds, jd, (bt % mt) * 128, (a.tail_n0 + bt / mt) * kBN, 0, 0,
                                    a.hidden / kBK, wave, lane);
-      tclock_end(a);
       return;
     }
   }
@@ -341,7 +341,6 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_ffn(FfnArgs a) {
   const int nk = K / kBK;
   ffn_tile<BM, WM, WN, PASS, STAGES>(a, lds, jd, (jt % mtiles) * BM, (jt / mtiles) * kBN * (PASS == 2 ? 2 : 1), ks, ks * nk / S,
                                      (ks + 1) * nk / S, wave, lane);
-  tclock_end(a);
 }
 
 // out[t][o_off + n] (=|+=) sum_k W[n][k] x[t][k] for n < N (rows past N load the
@@ -390,7 +389,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm_rows(RowsGemmArgs a) {
 static bool down_pair(int H) { return H % (2 * kBN) == 0; }
 
 template <int BM, int WM, int WN, int S>
-static void gemm_dispatch(FfnArgs& a, int pass, hipStream_t s) {
+static void gemm_dispatch(FfnArgs& a, int pass, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   const bool down2 = pass == 1 && down_pair(a.hidden);
   int tiles = 0;
   for (int j = 0; j < a.n_jobs; ++j) {
@@ -418,9 +417,10 @@ static void gemm_dispatch(FfnArgs& a, int pass, hipStream_t s) {
       grid = full + (ntiles - a.tail_n0) * ((M + 127) / 128);
     }
   }
-  if (pass == 0) k_gemm_ffn<BM, WM, WN, 0, S><<<grid, 64 * WM * WN, 0, s>>>(a);
-  else if (down2) k_gemm_ffn<BM, WM, WN, 2, S><<<grid, 64 * WM * WN, 0, s>>>(a);
-  else k_gemm_ffn<BM, WM, WN, 1, S><<<grid, 64 * WM * WN, 0, s>>>(a);
+  const dim3 g(grid), b(64 * WM * WN);
+  if (pass == 0) hipExtLaunchKernelGGL((k_gemm_ffn<BM, WM, WN, 0, S>), g, b, 0, s, ev0, ev1, 0, a);
+  else if (down2) hipExtLaunchKernelGGL((k_gemm_ffn<BM, WM, WN, 2, S>), g, b, 0, s, ev0, ev1, 0, a);
+  else hipExtLaunchKernelGGL((k_gemm_ffn<BM, WM, WN, 1, S>), g, b, 0, s, ev0, ev1, 0, a);
 }
 
 bool gemm_supported(int N, int K) { return N % kBN == 0 && K % kBK == 0; }
@@ -470,11 +470,11 @@ void launch_gemm_rows(const RowsGemmArgs& a, hipStream_t s) {
   }
 }
 
-void launch_gemm(FfnArgs& a, int pass, int max_tokens, hipStream_t s) {
+void launch_gemm(FfnArgs& a, int pass, int max_tokens, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   const int bm = pick_bm(a, pass, max_tokens);
-  if (bm == 256) gemm_dispatch<256, 2, 4, 2>(a, pass, s);
-  else if (bm == 128) gemm_dispatch<128, 2, 4, 3>(a, pass, s);
-  else gemm_dispatch<64, 1, 4, 3>(a, pass, s);
+  if (bm == 256) gemm_dispatch<256, 2, 4, 2>(a, pass, s, ev0, ev1);
+  else if (bm == 128) gemm_dispatch<128, 2, 4, 3>(a, pass, s, ev0, ev1);
+  else gemm_dispatch<64, 1, 4, 3>(a, pass, s, ev0, ev1);
 }
 
 }  // namespace promoe

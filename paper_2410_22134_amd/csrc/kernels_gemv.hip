@@ -177,6 +177,19 @@ __device__ __forceinline__ Job<TW> job_of(const FfnArgs& a, int nrows) {
   jb.q1 = jd.q1;
   jb.r0 = jd.r0;
   jb.r1 = min(jd.r0 + a.piece_rows, nrows < 0 ? jd.I : nrows);
+  if (jd.w == nullptr) {
+    // a route position resolved from the plan on the device (one round trip of
+    // independent loads); positions that are not resident, or whose slot may
+    // still be receiving copies, run no rows
+    const int nh = a.npos[0];
+    const int slot = a.order_slot[jd.pos];
+    const int q0 = a.offsets[jd.pos], q1 = a.offsets[jd.pos + 1];
+    const bool run = jd.pos < nh && slot >= 0 && slot < a.slots && !((a.busy_mask >> slot) & 1ull);
+    jb.W = reinterpret_cast<const TW*>(a.cache + ((size_t)a.layer * a.slots + (run ? slot : 0)) * a.expert_bytes);
+    jb.q0 = q0;
+    jb.q1 = run ? q1 : q0;
+    if (!run) jb.r1 = jb.r0;
+  }
   return jb;
 }
 
@@ -247,7 +260,6 @@ __global__ __launch_bounds__(kThreads) void k_ffn_gateup(FfnArgs a) {
                "s"(jb.q0), "s"(jb.q1), "s"(jb.r1), "s"(jb.pos));
   const bool shared = jb.pos == kSharedJob;
   TW* act = reinterpret_cast<TW*>(shared ? act_s : act_r);
-  tclock_start(a);
   const int i0 = jb.r0 + (blockIdx.x * kBlockWaves + wave) * RW;
   if (i0 >= jb.r1) return;
   const TW* rows[R];
@@ -289,7 +301,6 @@ __global__ __launch_bounds__(kThreads) void k_ffn_gateup(FfnArgs a) {
       if (m < mt && i0 + r < jb.r1) Elem<TW>::store(act, (g + m) * I + i0 + r, silu(ga) * ub);
     }
   }
-  tclock_end(a);
 }
 
 // pass 2: Y[pair][n] = Wd[n] . act[q] for the wave's RW rows n
@@ -309,7 +320,6 @@ __global__ __launch_bounds__(kThreads) void k_ffn_down(FfnArgs a) {
   const bool shared = jb.pos == kSharedJob;
   const TW* actb = reinterpret_cast<const TW*>(shared ? act_s : act_r);
   float* Yb = shared ? y_s : y_r;
-  tclock_start(a);
   const int n0 = jb.r0 + (blockIdx.x * kBlockWaves + wave) * RW;
   if (n0 >= jb.r1) return;
   const TW* Wd = jb.W + (size_t)2 * I * H;
@@ -350,7 +360,6 @@ __global__ __launch_bounds__(kThreads) void k_ffn_down(FfnArgs a) {
       }
     }
   }
-  tclock_end(a);
 }
 
 // ============================================================ 4-bit experts
@@ -445,7 +454,6 @@ __global__ __launch_bounds__(kThreads) void k_ffn_gateup_q4(FfnArgs a) {
   // materialise every argument here, so all of their loads issue together
   asm volatile("" ::"s"(H), "s"(T), "s"(top_k), "s"(perm), "s"(act), "s"(xb), "s"(jb.W), "s"(jb.I), "s"(jb.q0),
                "s"(jb.q1), "s"(jb.r1));
-  tclock_start(a);
   const int i0 = jb.r0 + (blockIdx.x * kBlockWaves + wave) * RW;
   if (i0 >= jb.r1) return;
   const uint8_t* base = reinterpret_cast<const uint8_t*>(jb.W);
@@ -489,7 +497,6 @@ __global__ __launch_bounds__(kThreads) void k_ffn_gateup_q4(FfnArgs a) {
       if (m < mt && i0 + r < jb.r1) Elem<bf16_t>::store(act, (g + m) * I + i0 + r, silu(ga) * ub);
     }
   }
-  tclock_end(a);
 }
 
 // pass 2, 4-bit experts: Y[pair][n] = Wd[n] . act[q] for the wave's RW rows n
@@ -503,7 +510,6 @@ __global__ __launch_bounds__(kThreads) void k_ffn_down_q4(FfnArgs a) {
   const int32_t* perm = a.perm;
   // materialise every argument here, so all of their loads issue together
   asm volatile("" ::"s"(H), "s"(actb), "s"(Y), "s"(perm), "s"(jb.W), "s"(jb.I), "s"(jb.q0), "s"(jb.q1), "s"(jb.r1));
-  tclock_start(a);
   const int n0 = jb.r0 + (blockIdx.x * kBlockWaves + wave) * RW;
   if (n0 >= jb.r1) return;
   const uint8_t* base = reinterpret_cast<const uint8_t*>(jb.W);
@@ -541,7 +547,6 @@ __global__ __launch_bounds__(kThreads) void k_ffn_down_q4(FfnArgs a) {
       if (m < mt && rv[r]) Y[(size_t)perm[g + m] * H + n0 + r] = v;
     }
   }
-  tclock_end(a);
 }
 
 // Dequantise whole experts for the MFMA GEMM: block (r, e) expands weight row r
@@ -671,24 +676,21 @@ static int gemv_jobs(const FfnArgs& in, int pass, FfnArgs& a) {
 // 4-bit experts (routed jobs only): rows per wave shrink as the token group grows,
 // keeping registers bounded (token pieces MT x 16 words, accumulators R x MT).
 template <int MT>
-static void ffn_dispatch_q4(const FfnArgs& in, int pass, hipStream_t s) {
+static void ffn_dispatch_q4(const FfnArgs& in, int pass, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   constexpr int RWG = MT <= 2 ? 2 : (MT == 4 ? 2 : 1), RWD = 2 * RWG;
   const int rows_per_block = kBlockWaves * (pass == 0 ? RWG : RWD);
   FfnArgs a;
   if (gemv_jobs(in, pass, a) == 0 || a.piece_rows <= 0) return;
   const dim3 grid((a.piece_rows + rows_per_block - 1) / rows_per_block, a.n_jobs);
-  if (pass == 0) k_ffn_gateup_q4<MT, RWG><<<grid, kThreads, 0, s>>>(a);
-  else k_ffn_down_q4<MT, RWD><<<grid, kThreads, 0, s>>>(a);
+  if (pass == 0) hipExtLaunchKernelGGL(k_ffn_gateup_q4<MT, RWG>, grid, dim3(kThreads), 0, s, ev0, ev1, 0, a);
+  else hipExtLaunchKernelGGL(k_ffn_down_q4<MT, RWD>, grid, dim3(kThreads), 0, s, ev0, ev1, 0, a);
 }
 
-template <typename TW, int MT>
-static void ffn_dispatch(const FfnArgs& in, int pass, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
-  constexpr int NCH = MT <= 2 ? 4 : (MT == 4 ? 2 : 1);
+// One launch of pass `pass` with NCH 16-byte chunks per lane and row in flight.
+template <typename TW, int MT, int NCH>
+static void ffn_launch_nch(const FfnArgs& a, int pass, const dim3& grid, hipStream_t s, hipEvent_t ev0,
+                           hipEvent_t ev1) {
   constexpr int RWG = 1, RWD = 2;
-  const int rows_per_block = kBlockWaves * (pass == 0 ? RWG : RWD);
-  FfnArgs a;
-  if (gemv_jobs(in, pass, a) == 0 || a.piece_rows <= 0) return;
-  const dim3 grid((a.piece_rows + rows_per_block - 1) / rows_per_block, a.n_jobs);
   if (ev0) {
     if (pass == 0) hipExtLaunchKernelGGL(k_ffn_gateup<TW, MT, NCH, RWG>, grid, dim3(kThreads), 0, s, ev0, ev1, 0, a);
     else hipExtLaunchKernelGGL(k_ffn_down<TW, MT, NCH, RWD>, grid, dim3(kThreads), 0, s, ev0, ev1, 0, a);
@@ -699,13 +701,38 @@ static void ffn_dispatch(const FfnArgs& in, int pass, hipStream_t s, hipEvent_t 
   }
 }
 
+template <typename TW, int MT>
+static void ffn_dispatch(const FfnArgs& in, int pass, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
+  constexpr int RWG = 1, RWD = 2;
+  const int rows_per_block = kBlockWaves * (pass == 0 ? RWG : RWD);
+  FfnArgs a;
+  if (gemv_jobs(in, pass, a) == 0 || a.piece_rows <= 0) return;
+  const dim3 grid((a.piece_rows + rows_per_block - 1) / rows_per_block, a.n_jobs);
+  if constexpr (MT == 1) {
+    // Single-token rows: as many chunks per lane as cover the row in one round
+    // when that is at most 4 (a 1408-wide down row is 176 chunks: 3 per lane
+    // leaves 16 lanes idle where 4 leave 80, measured 10.9 -> 9.5 us for 46 MB).
+    // The lane -> chunk map of one round does not depend on NCH, so the sums
+    // are the same bit for bit.
+    const int K = pass == 0 ? a.hidden : a.inter;
+    const int per_lane = (K / Elem<TW>::kPer16B + kWave - 1) / kWave;
+    if (per_lane <= 1) ffn_launch_nch<TW, MT, 1>(a, pass, grid, s, ev0, ev1);
+    else if (per_lane == 2) ffn_launch_nch<TW, MT, 2>(a, pass, grid, s, ev0, ev1);
+    else if (per_lane == 3) ffn_launch_nch<TW, MT, 3>(a, pass, grid, s, ev0, ev1);
+    else ffn_launch_nch<TW, MT, 4>(a, pass, grid, s, ev0, ev1);
+  } else {
+    constexpr int NCH = MT == 2 ? 4 : (MT == 4 ? 2 : 1);
+    ffn_launch_nch<TW, MT, NCH>(a, pass, grid, s, ev0, ev1);
+  }
+}
+
 void launch_ffn(const FfnArgs& a, int pass, int max_tokens, int dtype, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   const int mt = max_tokens >= 8 ? 8 : (max_tokens >= 4 ? 4 : (max_tokens >= 2 ? 2 : 1));
   if (a.q4) {
-    if (mt == 8) ffn_dispatch_q4<8>(a, pass, s);
-    else if (mt == 4) ffn_dispatch_q4<4>(a, pass, s);
-    else if (mt == 2) ffn_dispatch_q4<2>(a, pass, s);
-    else ffn_dispatch_q4<1>(a, pass, s);
+    if (mt == 8) ffn_dispatch_q4<8>(a, pass, s, ev0, ev1);
+    else if (mt == 4) ffn_dispatch_q4<4>(a, pass, s, ev0, ev1);
+    else if (mt == 2) ffn_dispatch_q4<2>(a, pass, s, ev0, ev1);
+    else ffn_dispatch_q4<1>(a, pass, s, ev0, ev1);
     return;
   }
   if (dtype == 1) {

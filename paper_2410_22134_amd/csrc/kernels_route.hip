@@ -302,6 +302,7 @@ __global__ __launch_bounds__(256) void k_plan_precise(PlanArgs a) {
       rec->layer = a.layer;
       rec->n = np;
       rec->n_hit = n_hit;
+      a.d_npos[0] = n_hit;
       n_pos = np;
     }
   }

@@ -170,6 +170,7 @@ struct promoe_ctx {
   int32_t* d_perm = nullptr;
   int32_t* d_pos_of = nullptr;
   int32_t* d_warm = nullptr;
+  int32_t* d_npos = nullptr;  // resident positions of the latest precise plan (device)
   void* d_act = nullptr;
   float* d_Y = nullptr;
   void* d_act_sh = nullptr;
@@ -200,6 +201,9 @@ struct promoe_ctx {
   const void* route_x = nullptr;  // input of the latest route (its gate logits are in d_logits)
   int last_route_layer = -1;      // layer of the latest route, kept after its FFN call
   std::vector<char> ffn_started;  // per route position: launched by the route itself
+  bool shared_started = false;    // the shared expert too
+  uint64_t early_busy = 0;        // slots the route's early launch skipped
+  size_t early_prof0 = 0, early_nprof = 0;  // its profiling entries (bytes filled in by the route)
   hipStream_t route_stream = nullptr;  // stream of the latest route
   hipEvent_t route_done = nullptr;     // recorded on it after the route's last launch
   PlanRecord route_rec{};
@@ -222,14 +226,10 @@ struct promoe_ctx {
   int64_t cnext = 0;
   hipStream_t last_stream = nullptr;
 
-  // profiling: FFN launches timed on the device clock (d_tclock ring of
-  // [start, end] pairs), copy-wait stalls with HIP events
+  // profiling: FFN launches timed by the start and end events the launch
+  // itself records (kernel execution time), copy-wait stalls by event pairs
+  // around the waits
   bool profile = false;
-  unsigned long long* d_tclock = nullptr;
-  int64_t tclk_next = 0, tclk_resolved = 0;
-  struct TclkMeta { int cls; double bytes, flops; };
-  std::vector<TclkMeta> tclk_meta;
-  double wall_khz = 100000.0;
   std::vector<ProfEntry> prof_pending;
   std::vector<hipEvent_t> prof_free;
   static constexpr int kClasses = 6;
@@ -285,46 +285,7 @@ hipEvent_t prof_event(promoe_ctx* c) {
   return e;
 }
 
-constexpr int kTclkRing = 8192;
-
-// Read back finished launch clocks (caller has synchronised the launch stream)
-// and clear the slots.
-void tclock_resolve(promoe_ctx* c) {
-  const int64_t from = c->tclk_resolved, to = c->tclk_next;
-  if (to == from) return;
-  std::vector<unsigned long long> v((size_t)kTclkWords * kTclkRing);
-  hipMemcpy(v.data(), c->d_tclock, sizeof(unsigned long long) * v.size(), hipMemcpyDeviceToHost);
-  for (int64_t i = from; i < to; ++i) {
-    const int64_t slot = i % kTclkRing;
-    const unsigned long long* w = v.data() + (size_t)kTclkWords * slot;
-    const unsigned long long t0 = ~w[0];
-    unsigned long long t1 = 0;
-    for (int l = 1; l <= kTclkLines; ++l) t1 = std::max(t1, w[16 * l]);
-    const promoe_ctx::TclkMeta& m = c->tclk_meta[slot];
-    if (w[0] == 0 || t1 < t0) continue;  // launch without blocks
-    c->k_launches[m.cls]++;
-    c->k_ms[m.cls] += (double)(t1 - t0) / c->wall_khz;
-    c->k_bytes[m.cls] += m.bytes;
-    c->k_flops[m.cls] += m.flops;
-  }
-  hipMemset(c->d_tclock, 0, sizeof(unsigned long long) * v.size());
-  c->tclk_resolved = to;
-}
-
-// Slot of the next timed launch; resolves (synchronising) when the ring is full.
-unsigned long long* tclock_slot(promoe_ctx* c, hipStream_t s, int cls, double bytes, double flops) {
-  if (!c->d_tclock) return nullptr;
-  if (c->tclk_next - c->tclk_resolved >= kTclkRing) {
-    hipStreamSynchronize(s);
-    tclock_resolve(c);
-  }
-  const int64_t slot = c->tclk_next++ % kTclkRing;
-  c->tclk_meta[slot] = promoe_ctx::TclkMeta{cls, bytes, flops};
-  return c->d_tclock + (size_t)kTclkWords * slot;
-}
-
 void prof_resolve(promoe_ctx* c) {
-  tclock_resolve(c);
   for (auto& p : c->prof_pending) {
     hipEventSynchronize(p.b);
     float ms = 0.0f;
@@ -477,6 +438,7 @@ PlanArgs plan_args(promoe_ctx* c, int layer, const int32_t* ids, int T, int64_t 
   a.d_offsets = c->d_offsets;
   a.d_perm = c->d_perm;
   a.d_pos_of = c->d_pos_of;
+  a.d_npos = c->d_npos;
   return a;
 }
 
@@ -654,6 +616,7 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
                o_pids = take(sizeof(int32_t) * (size_t)T * Kk), o_oslot = take(sizeof(int32_t) * 64),
                o_offs = take(sizeof(int32_t) * 65), o_perm = take(sizeof(int32_t) * (size_t)T * Kk),
                o_posof = take(sizeof(int32_t) * 64), o_warm = take(sizeof(int32_t) * 64),
+               o_npos = take(sizeof(int32_t) * 4),
                o_act = take((size_t)c->eb * T * Kk * c->I), o_Y = take(sizeof(float) * (size_t)T * Kk * H),
                o_actsh = take((size_t)c->eb * T * std::max(c->Ish, 1)),
                o_Ysh = take(sizeof(float) * (size_t)kMaxSplit * T * H),
@@ -681,6 +644,7 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   c->d_perm = reinterpret_cast<int32_t*>(b + o_perm);
   c->d_pos_of = reinterpret_cast<int32_t*>(b + o_posof);
   c->d_warm = reinterpret_cast<int32_t*>(b + o_warm);
+  c->d_npos = reinterpret_cast<int32_t*>(b + o_npos);
   c->d_act = b + o_act;
   c->d_Y = reinterpret_cast<float*>(b + o_Y);
   c->d_act_sh = b + o_actsh;
@@ -740,14 +704,10 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   c->pf = new Prefetcher(L, C, E, c->chunk_bytes, sub, window, c->cache, &c->eng, std::max(sub, kHighMergeBytes));
   c->pf->set_whole_expert_low((g.flags & PROMOE_FLAG_NO_CHUNK) != 0);
   if (c->profile) {
-    int khz = 0;
-    if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, c->dev) == hipSuccess && khz > 0)
-      c->wall_khz = khz;
-    const size_t tb = sizeof(unsigned long long) * kTclkWords * kTclkRing;
-    if (hipMalloc(&c->d_tclock, tb) == hipSuccess && hipMemset(c->d_tclock, 0, tb) == hipSuccess) {
-      c->tclk_meta.resize(kTclkRing);
-    } else {
-      c->d_tclock = nullptr;
+    // timing events for the first steps, so few are created inside a timed region
+    for (int i = 0; i < 512; ++i) {
+      hipEvent_t e = nullptr;
+      if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) == hipSuccess) c->prof_free.push_back(e);
     }
   }
   c->worker = std::thread(worker_main, c);
@@ -806,7 +766,6 @@ int promoe_destroy(promoe_ctx* c) {
   hipEventDestroy(c->route_done);
   for (auto& cs : c->eng.stream) hipStreamDestroy(cs);
   hipHostFree(c->rec_h);
-  if (c->d_tclock) hipFree(c->d_tclock);
   hipFree(c->dmem);
   if (c->d_stage) hipFree(c->d_stage);
   delete c->pf;
@@ -975,6 +934,9 @@ int promoe_prefetch(promoe_ctx* c, int target_layer, const int32_t* h_ids, int n
 }
 
 static int launch_route_head(promoe_ctx* c, int layer, const void* d_x, int T, hipStream_t s);
+static int early_resident_launch(promoe_ctx* c, int layer, const void* d_x, int T, hipStream_t s, int64_t r,
+                                 bool* launched);
+static void early_resident_release(promoe_ctx* c, int layer, int T, hipStream_t s);
 
 int promoe_route(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_ids, float* d_w,
                  float* d_shared_scale, int32_t* h_order, int32_t* n_order, void* stream) {
@@ -1015,6 +977,14 @@ int promoe_route(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_id
   launch_plan_precise(plan_args(c, layer, d_ids, T, r), s);
   hipError_t le = hipGetLastError();
   if (le == hipSuccess) le = hipEventRecord(c->rec_ev[r % kRecRing], s);
+  bool early_ffn = false;
+  if (le == hipSuccess) {
+    rc = early_resident_launch(c, layer, d_x, T, s, r, &early_ffn);
+    if (rc) {
+      publish(c, r);
+      return rc;
+    }
+  }
   if (le == hipSuccess) le = wait_record(c, r);
   publish(c, r);
   if (le != hipSuccess) return fail_hip(le, "plan_precise");
@@ -1060,6 +1030,8 @@ int promoe_route(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_id
   }
   c->route_rec = rec;
   c->ffn_started.assign(rec.n, 0);
+  c->shared_started = false;
+  if (early_ffn) early_resident_release(c, layer, T, s);
   rc = launch_route_head(c, layer, d_x, T, s);
   if (rc) return rc;
   if (c->eng.err != hipSuccess) return fail_hip(c->eng.err, "copy engine");
@@ -1133,9 +1105,14 @@ int ffn_launch_one(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipSt
     const double k = pass == 0 ? 2.0 : 1.0;  // gate and up, or down
     const bool shared_only = jobs.size() == 1 && jobs[0] == kSharedJob;
     const int cls = (gemm ? (shared_only ? 4 : 2) : 0) + pass;
-    a.tclock = c->profile && !c->noalloc_call ? tclock_slot(c, s, cls, k * wbytes, k * flops) : nullptr;
-    if (gemm) launch_gemm(a, pass, maxc, s);
-    else launch_ffn(a, pass, maxc, c->dt, s);
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (c->profile && !c->noalloc_call) {
+      e0 = prof_event(c);
+      e1 = prof_event(c);
+      c->prof_pending.push_back(ProfEntry{e0, e1, cls, k * wbytes, k * flops});
+    }
+    if (gemm) launch_gemm(a, pass, maxc, s, e0, e1);
+    else launch_ffn(a, pass, maxc, c->dt, s, e0, e1);
     LAUNCHCHK("ffn");
   }
   return PROMOE_OK;
@@ -1259,6 +1236,122 @@ std::vector<FillWait> fill_waits(const promoe_ctx* c) {
 
 }  // namespace
 
+// Decode-sized steps: the FFN of the resident positions and the shared expert
+// is enqueued right behind the precise plan, before the host has seen the plan,
+// with every route position resolved on the device (FfnJob::w == null): the
+// reordered plan puts the resident experts first and writes their count, slots
+// and pair ranges to device memory.  Only slots with no copy pending can be
+// read that early, so the spec plans queued for the layer must all have been
+// ingested (their plan kernels done) and the slots whose bytes are not all
+// known to have landed are passed as busy_mask and skipped; the host replays
+// the same rule once the plan is known (early_resident_release).  The route's
+// host round trip then overlaps the experts' compute instead of preceding it.
+static int early_resident_launch(promoe_ctx* c, int layer, const void* d_x, int T, hipStream_t s, int64_t r,
+                                 bool* launched) {
+  *launched = false;
+  const bool in_order = (c->cfg.flags & (PROMOE_FLAG_NO_REORDER | PROMOE_FLAG_NO_PREEMPT)) != 0;
+  if (in_order || (int64_t)T * c->K > 64 || T >= kGemmMinTokens || c->noalloc_call) return PROMOE_OK;
+  uint64_t busy = 0;
+  {
+    std::lock_guard<std::mutex> lk(c->mu);
+    for (int64_t rr = c->rec_ingested; rr < r; ++rr)
+      if (c->rec_kind[rr % kRecRing] != 0 || rr >= c->rec_pub || !c->rec_h[rr % kRecRing].done) return PROMOE_OK;
+    std::atomic_thread_fence(std::memory_order_acquire);
+    while (c->rec_ingested < r) ingest_spec(c, c->rec_ingested);
+    c->pf->retire();
+    for (int slot = 0; slot < c->C; ++slot)
+      if (c->pf->ready_seq(layer, slot, 2) != -1) busy |= 1ull << slot;
+  }
+  FfnArgs a = ffn_args(c, layer, d_x, T);
+  a.npos = c->d_npos;
+  a.busy_mask = busy;
+  const size_t prof0 = c->prof_pending.size();
+  // dense experts: one launch of the shared expert and the positions; 4-bit
+  // experts: the dense shared expert, then the positions on the 4-bit GEMV
+  for (int part = 0; part < 2; ++part) {
+    const bool routed_q4 = part == 1;
+    if (part == 1 && !c->q4) break;
+    int n = 0;
+    if (c->Ish > 0 && part == 0) {
+      FfnJob& j = a.jobs[n++];
+      j.w = a.shared_w;
+      j.q0 = 0;
+      j.q1 = T;
+      j.I = c->Ish;
+      j.r0 = 0;
+      j.pos = kSharedJob;
+      j.pad = 0;
+    }
+    if (c->q4 == routed_q4) {
+      const int P = std::min(c->E, T * c->K);
+      for (int p = 0; p < P; ++p) {
+        FfnJob& j = a.jobs[n++];
+        j.w = nullptr;
+        j.q0 = j.q1 = 0;
+        j.I = c->I;
+        j.r0 = 0;
+        j.pos = p;
+        j.pad = 0;
+      }
+    }
+    if (n == 0) continue;
+    a.n_jobs = n;
+    a.q4 = routed_q4 ? 1 : 0;
+    for (int pass = 0; pass < 2; ++pass) {
+      hipEvent_t e0 = nullptr, e1 = nullptr;
+      if (c->profile) {
+        e0 = prof_event(c);
+        e1 = prof_event(c);
+        c->prof_pending.push_back(ProfEntry{e0, e1, pass, 0.0, 0.0});
+      }
+      launch_ffn(a, pass, T, c->dt, s, e0, e1);
+      LAUNCHCHK("early ffn");
+    }
+  }
+  c->early_busy = busy;
+  c->early_prof0 = prof0;
+  c->early_nprof = c->prof_pending.size() - prof0;
+  *launched = true;
+  return PROMOE_OK;
+}
+
+// The plan is known: the positions the early launch computed (resident, slot not
+// busy) are marked started, their slots' last reader becomes that launch (its
+// compute token is recorded now: nothing was enqueued on s since), fills that
+// wait for them are released, and the launch's profiling entries get their bytes.
+static void early_resident_release(promoe_ctx* c, int layer, int T, hipStream_t s) {
+  const PlanRecord& rec = c->route_rec;
+  std::vector<int> jobs;
+  double routed_bytes = 0.0, routed_flops = 0.0;
+  const double melems = (double)c->I * c->H;
+  for (int p = 0; p < rec.n_hit; ++p) {
+    if ((c->early_busy >> rec.slot[p]) & 1ull) continue;
+    c->ffn_started[p] = 1;
+    jobs.push_back(p);
+    routed_bytes += c->q4 ? (double)c->chunk_bytes : melems * c->eb;
+    routed_flops += 2.0 * rec.count[p] * melems;
+  }
+  if (c->Ish > 0) {
+    c->shared_started = true;
+    jobs.push_back(kSharedJob);
+  }
+  release_after_launch(c, layer, jobs, s);
+  if (c->profile && c->early_nprof) {
+    const double sh_elems = (double)c->Ish * c->H;
+    const double sh_bytes = sh_elems * c->eb, sh_flops = 2.0 * T * sh_elems;
+    for (size_t i = 0; i < c->early_nprof; ++i) {
+      ProfEntry& pe = c->prof_pending[c->early_prof0 + i];
+      const double k = pe.cls == 0 ? 2.0 : 1.0;
+      // dense: [shared + routed] x 2 passes; 4-bit: [shared] x 2, then [routed] x 2
+      const bool shared_part = c->q4 ? i < 2 && c->Ish > 0 : true;
+      const bool routed_part = c->q4 ? !(i < 2 && c->Ish > 0) : true;
+      pe.bytes = k * ((shared_part ? sh_bytes : 0.0) + (routed_part ? routed_bytes : 0.0));
+      pe.flops = k * ((shared_part ? sh_flops : 0.0) + (routed_part ? routed_flops : 0.0));
+    }
+  }
+  c->early_nprof = 0;
+}
+
 // Steps larger than decode: a fill whose victim slot is read by a resident
 // expert of the same step waits for that read.  The route launches the readers
 // of the first fills' victims itself, right behind its plan, so the link
@@ -1303,6 +1396,17 @@ static int expert_ffn_run(promoe_ctx* c, int layer, int T, const float* d_w, con
   // route enqueued: its top-k and plan (ids, weights, slots, permutation) and
   // the readers of the first fills' victim slots it may have started.
   if (c->route_stream != s) HIPCHK(hipStreamWaitEvent(s, c->route_done, 0));
+  // Outputs the route's own launches wrote into the context's buffers, when this
+  // call keeps its expert outputs elsewhere (the allocation-free variant): every
+  // pair's row is carried over, and the launches below overwrite the rest.
+  const bool any_started = c->shared_started ||
+                           std::find(c->ffn_started.begin(), c->ffn_started.end(), 1) != c->ffn_started.end();
+  if (any_started && a.Y != c->d_Y) {
+    HIPCHK(hipMemcpyAsync(a.Y, c->d_Y, sizeof(float) * (size_t)T * c->K * c->H, hipMemcpyDeviceToDevice, s));
+    if (c->shared_started)
+      HIPCHK(hipMemcpyAsync(a.Ysh, c->d_Ysh, sizeof(float) * a.ksplit * (size_t)a.ysh_split_stride,
+                            hipMemcpyDeviceToDevice, s));
+  }
   std::vector<char> done(c->ffn_started), is_def(n, 0);
   for (const auto& d : c->deferred) is_def[d.pos] = 1;
 
@@ -1334,7 +1438,7 @@ static int expert_ffn_run(promoe_ctx* c, int layer, int T, const float* d_w, con
   const bool batch = (int64_t)T * c->K <= 64;
   std::vector<int> jobs;
   if (batch) {
-    if (c->Ish > 0) jobs.push_back(kSharedJob);
+    if (c->Ish > 0 && !c->shared_started) jobs.push_back(kSharedJob);
     jobs.insert(jobs.end(), ready.begin(), ready.end());
     if (!jobs.empty()) {
       rc = ffn_launch(c, a, jobs, s, CopyWait(), CopyWait());

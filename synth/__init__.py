@@ -50,6 +50,9 @@ def lib() -> ctypes.CDLL:
                 fn.restype = None
             l.synth_philox4x32_10.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
             l.synth_philox4x32_10.restype = None
+            i64 = ctypes.c_int64
+            l.synth_quant_int4.argtypes = [ctypes.c_void_p, i64, i64, i64, ctypes.c_void_p, ctypes.c_void_p]
+            l.synth_quant_int4.restype = None
             _lib = l
     return _lib
 
@@ -90,3 +93,13 @@ def normal(seed: int, stream: int, n: int, std: float = 1.0, mean: float = 0.0,
            ctypes.c_uint64(offset), ctypes.c_size_t(n), ctypes.c_float(mean), ctypes.c_float(std),
            ctypes.c_void_p(addr))
     return arr
+
+
+def quant_int4(w_bf16, rows: int, K: int, group: int, codes_addr: int, scales_addr: int) -> None:
+    """4-bit storage of a bf16 matrix [rows, K] (raw uint16 bits, C-contiguous
+    numpy array): codes (rows x K/2 bytes) to codes_addr, bf16 scales (rows x
+    K/group) to scales_addr; see synth_quant_int4 in synth.c."""
+    w = np.ascontiguousarray(w_bf16, dtype=np.uint16)
+    assert w.size == rows * K and K % group == 0 and group % 2 == 0
+    lib().synth_quant_int4(ctypes.c_void_p(w.ctypes.data), rows, K, group, ctypes.c_void_p(codes_addr),
+                           ctypes.c_void_p(scales_addr))

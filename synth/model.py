@@ -59,12 +59,11 @@ def write_expert(cfg: MoEConfig, layer: int, e: int, addr: int) -> None:
     matrix as codes then scales for the int4 format)."""
     n = cfg.inter * cfg.hidden
     if cfg.weight_format == "int4":
-        import ctypes
-        mats = expert(cfg, layer, e)
-        for i, m in enumerate(mats):
-            codes, scales = quantize_int4(bf16_to_f32(m))
-            raw = np.concatenate([codes.reshape(-1), scales.reshape(-1).view(np.uint8)])
-            ctypes.memmove(addr + i * cfg.chunk_bytes, raw.ctypes.data, raw.nbytes)
+        from . import quant_int4
+        for i, m in enumerate(expert(cfg, layer, e)):
+            rows, K = m.shape
+            base = addr + i * cfg.chunk_bytes
+            quant_int4(m, rows, K, INT4_GROUP, base, base + rows * K // 2)
         return
     eb = cfg.elem_bytes
     _w(cfg, K_EG, layer, e, n, out=addr)
@@ -74,7 +73,9 @@ def write_expert(cfg: MoEConfig, layer: int, e: int, addr: int) -> None:
 
 def quantize_int4(w: np.ndarray, group: int = INT4_GROUP):
     """Round-to-nearest symmetric 4-bit quantisation of fp32 rows w [R, K] in
-    groups of `group` along K (data preparation only): scale s = bf16(absmax / 7),
+    groups of `group` along K (data preparation only; write_expert uses the
+    same recipe in C, synth.quant_int4, checked equal to this one on the CPU):
+    scale s = bf16(absmax / 7),
     code = clamp(rint(w / s), -8, 7) + 8, two codes per byte (even k in the low
     nibble).  Returns (codes uint8 [R, K/2], scales bf16 bits uint16 [R, K/group])."""
     R, K = w.shape

@@ -104,3 +104,46 @@ void synth_normal_bf16(uint64_t seed, uint64_t stream, uint64_t offset, size_t n
     }
   }
 }
+
+/*
+ * Symmetric round-to-nearest 4-bit storage of bf16 rows (data preparation of
+ * the 4-bit synthetic models, not part of the method): for each group of
+ * `group` consecutive values of a row, scale s = bf16(absmax / 7) and
+ * code = clamp(rint(w / s), -8, 7) + 8 (0 when s == 0), computed in fp32 with
+ * round-half-to-even; two codes per byte, even k in the low nibble.
+ * codes: R x K/2 bytes; scales: R x K/group bf16 bits.
+ */
+void synth_quant_int4(const uint16_t* w, int64_t R, int64_t K, int64_t group, uint8_t* codes, uint16_t* scales) {
+  #pragma omp parallel for schedule(static)
+  for (int64_t r = 0; r < R; ++r) {
+    const uint16_t* row = w + r * K;
+    for (int64_t g0 = 0; g0 < K; g0 += group) {
+      float amax = 0.0f;
+      for (int64_t k = g0; k < g0 + group; ++k) {
+        uint32_t u = (uint32_t)row[k] << 16;
+        float v;
+        memcpy(&v, &u, 4);
+        v = fabsf(v);
+        if (v > amax) amax = v;
+      }
+      const uint16_t sb = f32_to_bf16_rne(amax / 7.0f);
+      scales[r * (K / group) + g0 / group] = sb;
+      uint32_t su = (uint32_t)sb << 16;
+      float s;
+      memcpy(&s, &su, 4);
+      for (int64_t k = g0; k < g0 + group; k += 2) {
+        int q[2];
+        for (int j = 0; j < 2; ++j) {
+          uint32_t u = (uint32_t)row[k + j] << 16;
+          float v;
+          memcpy(&v, &u, 4);
+          float t = s > 0.0f ? rintf(v / s) : 0.0f;
+          if (t < -8.0f) t = -8.0f;
+          if (t > 7.0f) t = 7.0f;
+          q[j] = (int)t + 8;
+        }
+        codes[r * (K / 2) + k / 2] = (uint8_t)(q[0] | (q[1] << 4));
+      }
+    }
+  }
+}

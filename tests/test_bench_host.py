@@ -74,3 +74,58 @@ def test_more_than_one_gpu_is_refused():
                        text=True, timeout=300, cwd=ROOT)
     assert r.returncode == 2
     assert "one GPU" in r.stderr
+
+
+class _HostModel:
+    """The host views bench's oracle timing reads (weights as data), built from the
+    seeded recipes without a GPU."""
+
+    def __init__(self, cfg):
+        import numpy as np
+        from synth import model as sm
+        self.cfg = cfg
+        self.np_gate = [sm.gate(cfg, l) for l in range(cfg.n_layers)]
+        self.np_bias = [sm.bias(cfg, l) for l in range(cfg.n_layers)]
+        self.np_pred = [sm.predictor(cfg, l) for l in range(cfg.n_layers)]
+        self.np_sgate = [sm.shared_gate_vec(cfg, l) for l in range(cfg.n_layers)]
+        self._buf = {}
+        for l in range(cfg.n_layers):
+            for e in range(cfg.n_experts):
+                b = np.zeros(cfg.expert_bytes, np.uint8)
+                sm.write_expert(cfg, l, e, b.ctypes.data)
+                self._buf[l, e] = b
+
+    def expert_host(self, l, e):
+        import numpy as np
+        b = self._buf[l, e]
+        if self.cfg.weight_format == "int4":
+            return b
+        return b.view(np.uint16 if self.cfg.dtype == "bf16" else np.float32)
+
+
+@pytest.mark.parametrize("fmt,T", [("dense", 1), ("dense", 7), ("int4", 3)])
+def test_oracle_rate_on_a_small_model(fmt, T):
+    sys.path.insert(0, HERE)
+    import parity_util as pu
+    cfg = pu.SMALL.with_(weight_format=fmt)
+    r = bench.oracle_rate(cfg, _HostModel(cfg), T, 0.05)
+    assert r["value"] > 0 and r["kind"] == "oracle" and r["unit"] == "tok/s" and r["cores"] >= 1
+
+
+def test_summary_line_reads_every_leg():
+    k = {"gemv_gateup": {"frac_hbm": 0.7}, "gemv_down": {"frac_hbm": 0.6}}
+    out = {"value": 37.0, "roofline": {"frac": 0.6, "down": {"frac": 0.5}},
+           "detail": {"overlap": {"H_time_over_H_max": 0.8}, "prediction": {"goodpred": 0.35, "accuracy": 0.7},
+                      "allres": {"tok_s": 500.0, "of_ceiling": 0.25, "kernels": k},
+                      "prefill": {"tok_s": 2100.0},
+                      "configs": {"Mixtral-8x7B int4": {"runs": [{"workload": "prefill", "tokens_per_step": 256,
+                                                                  "tok_s": 900.0},
+                                                                 {"workload": "decode", "tokens_per_step": 1,
+                                                                  "tok_s": 14.0}]}},
+                      "predictor_training": {"lookahead_1": {"heldout_acc_trained": {"mean": 0.73}},
+                                             "lookahead_2": {"heldout_acc_trained": {"mean": 0.71}}}},
+           "roofline_prefill_gemm": {"frac": 0.44}, "cpu_baseline": {"value": 0.26}}
+    line = bench.summary_line(out)
+    for piece in ("decode 37.0 tok/s", "all-resident 500.0", "Mixtral-8x7B int4: prefill 900.0, decode b1 14.0",
+                  "shared GEMM 0.440", "GoodPred 0.350", "oracle 0.26"):
+        assert piece in line, (piece, line)

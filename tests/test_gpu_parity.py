@@ -140,11 +140,16 @@ INVARIANCE = [
     # name, config, tokens, cache sizes (slots per layer)
     ("small_T77", pu.SMALL, 77, (1, 2, 4, 8)),
     ("c3_T512", configs.C3.with_(n_layers=3), 512, (15, 30, 60)),
+    # decode-sized steps: resident experts run right behind the plan, resolved
+    # on the device, the others once their copies land
+    ("small_decode_T1", pu.SMALL, 1, (1, 2, 4, 8)),
+    ("small_decode_T4", pu.SMALL, 4, (1, 2, 4, 8)),
+    ("c2_decode_T1", configs.C2.with_(n_layers=3), 1, (16, 32, 64)),
 ]
 
 
 @pytest.mark.parametrize("name,cfg,T,slot_list", INVARIANCE, ids=[c[0] for c in INVARIANCE])
-def test_bf16_prefill_output_invariant_to_cache_size_and_prefetch(name, cfg, T, slot_list):
+def test_bf16_output_invariant_to_cache_size_and_prefetch(name, cfg, T, slot_list):
     # The layer outputs must not depend on what the cache holds or what was
     # prefetched (the combine sums the k routed outputs in rank order, and every
     # expert's product runs the same reduction order whichever launch it is in).

@@ -42,3 +42,21 @@ def test_model_tensors_shapes_and_predictor_identity():
     assert model.predictor(c, 2) is None
     sh = model.shared_concat(configs.C2.with_(n_layers=1), 0)
     assert sh.size == 3 * 2816 * 2048
+
+
+def test_int4_storage_in_c_equals_the_numpy_recipe():
+    # write_expert stores 4-bit experts through synth.quant_int4 (C); it must
+    # give the same bytes as model.quantize_int4 (numpy), rounding ties to even
+    rng = np.random.default_rng(3)
+    R, K = 24, 512
+    w = model._bf16_bits((rng.standard_normal((R, K)) * 0.02).astype(np.float32))
+    w[0, :128] = 0                                   # an all-zero group: scale 0, codes 8
+    s = 0.5 * np.arange(-16, 16, dtype=np.float32)   # exact halves of a power-of-two scale: ties
+    w[1, 128:256] = model._bf16_bits(np.resize(s, 128) * np.float32(2.0 ** -7))
+    w[1, 128] = model._bf16_bits(np.array([7.0 * 2.0 ** -7], np.float32))[0]   # absmax 7 * 2^-7: scale 2^-7
+    codes_np, scales_np = model.quantize_int4(model.bf16_to_f32(w))
+    codes = np.zeros((R, K // 2), np.uint8)
+    scales = np.zeros((R, K // 128), np.uint16)
+    synth.quant_int4(w, R, K, 128, codes.ctypes.data, scales.ctypes.data)
+    assert np.array_equal(scales, scales_np) and np.array_equal(codes, codes_np)
+    assert scales[0, 0] == 0 and np.all(codes[0, :64] == 0x88)
