@@ -42,7 +42,7 @@ MFMA_BF16_PEAK_TFLOPS = 2500.0
 METRIC = "decode & prefill tok/s at 50% expert cache; expert-FFN HBM GB/s, MFMA util"
 KERNEL_CLASSES = ("gemv_gateup", "gemv_down", "gemm_gateup_routed", "gemm_down_routed", "gemm_gateup_shared",
                   "gemm_down_shared")
-DEFAULT_LEGS = "decode,allres,prefill,configs,mfma,ablation,sweep,int4,predtrain,cpu"
+DEFAULT_LEGS = "decode,allres,prefill,configs,mfma,ablation,sweep,int4,predtrain,hbmsize,cpu"
 
 
 def parse(argv=None):
@@ -64,6 +64,8 @@ def parse(argv=None):
                    help="size of the plain device copy run after the timed region (counter calibration)")
     p.add_argument("--legs", default=DEFAULT_LEGS,
                    help="decode is always run (it is the reported value); the others: " + DEFAULT_LEGS)
+    p.add_argument("--config-filter", default="", help="configs leg: run only the workloads whose name contains "
+                                                         "this text (default: all)")
     p.add_argument("--prefill-steps", type=int, default=3)
     p.add_argument("--prefill-warmup", type=int, default=1)
     p.add_argument("--allres-steps", type=int, default=64)
@@ -551,6 +553,8 @@ def leg_configs(torch, args, h2d_gbs, cpu=False):
     from paper_2410_22134_amd.stack import Stack
     out = {}
     for name, key, n_layers, fmt, timed_oracle, runs in CONFIG_PLAN:
+        if args.config_filter and args.config_filter not in name:
+            continue
         full = getattr(configs, key)
         cfg = full.with_(n_layers=n_layers or full.n_layers, weight_format=fmt)
         t0 = time.perf_counter()
@@ -652,6 +656,47 @@ def leg_mfma(torch, args):
         model.close()
 
 
+def leg_hbm_sizes(torch, reps=20):
+    """The library's streaming-read probe (contiguous 32 KiB per block) at the byte
+    counts of single decode GEMV launches: what a kernel that only streams
+    reaches at each launch size.  Each size runs `reps` launches over fresh parts
+    of a 4 GiB buffer (no cache reuse), queued behind two full reads of the
+    buffer so that they run back to back; the batch is timed with events (per
+    launch: the kernel and the gap to the next one).  Kernel-only durations come
+    from a rocprofv3 kernel trace of the same run."""
+    from paper_2410_22134_amd import _abi
+    G = 4 << 30
+    buf = torch.empty(G, dtype=torch.uint8, device="cuda")
+    buf.fill_(1)
+    sink = torch.empty(G // (32 << 10), dtype=torch.float32, device="cuda")
+    out = []
+    off = 0
+    for mb in (11.5, 23.1, 34.6, 46.1, 69.2, 92.3, 138.4, 276.8, 1024.0):
+        n = int(mb * 1e6) // 4096 * 4096
+        blocks = max(1, n // (32 << 10))
+        offs = []
+        for _ in range(reps):
+            if off + n > G:
+                off = 0
+            offs.append(off)
+            off += n
+        _abi.peak_hbm_read(buf.data_ptr() + offs[0], n, sink, blocks)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        for _ in range(2):  # ~1.2 ms of queued work while the host enqueues the batch
+            _abi.peak_hbm_read(buf, G, sink, G // (32 << 10))
+        a.record()
+        for o in offs:
+            _abi.peak_hbm_read(buf.data_ptr() + o, n, sink, blocks)
+        b.record()
+        b.synchronize()
+        us = a.elapsed_time(b) * 1e3 / reps
+        out.append({"MB": mb, "blocks": blocks, "us_per_launch_back_to_back": round(us, 2),
+                    "GBps": round(n / (us * 1e-6) / 1e9, 1), "frac": round(n / (us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)})
+    del buf, sink
+    return out
+
+
 def summary_line(out):
     """One compact line of the secondary figures (stderr)."""
     d = out["detail"]
@@ -724,6 +769,7 @@ def main():
     peaks = measure_peaks(torch)
     load_s = s["bytes_high"] / (h2d_eff * 1e9) if h2d_eff else 0.0
     traffic, traffic_ratio = read_traffic("k_ffn_gateup")
+    traffic_d, traffic_ratio_d = read_traffic("k_ffn_down")
     hbm_meas = peaks["hbm_read_GBps"]
 
     def roof(c):
@@ -756,7 +802,8 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "k_ffn_gateup<bf16,1,4,1>", **roof(gu),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "traffic": traffic,
                      "traffic_over_algorithmic": traffic_ratio, "peak_measured": hbm_meas,
-                     "down": {"kernel": "k_ffn_down<bf16,1,3,2>", **roof(dn)},
+                     "down": {"kernel": "k_ffn_down<bf16,1,3,2>", **roof(dn), "traffic": traffic_d,
+                              "traffic_over_algorithmic": traffic_ratio_d},
                      "gateup_and_down": {"achieved": round(both, 1), "frac": round(both / HBM_PEAK_GBPS, 4)},
                      "timing": "kernel start and end events recorded by each launch (hipExtLaunchKernelGGL), "
                                "averaged over every launch of the timed region"},
@@ -827,6 +874,9 @@ def main():
         g["peak_measured"] = peaks["mfma_bf16_TFLOPs"]
         g["frac_of_measured"] = round(g["achieved"] / peaks["mfma_bf16_TFLOPs"], 4) if peaks["mfma_bf16_TFLOPs"] else None
         out["roofline_prefill_gemm"] = g
+    if "hbmsize" in legs:
+        print("[bench] streaming-read probe at GEMV launch sizes", file=sys.stderr, flush=True)
+        out["detail"]["hbm_read_by_launch_size"] = leg_hbm_sizes(torch)
     if "int4" in legs:
         print("[bench] 4-bit experts leg", file=sys.stderr, flush=True)
         out["detail"]["int4"] = leg_int4(torch, args)
