@@ -245,8 +245,8 @@ def _oracle_step(cfg, model, lcs, h, t0, budget_s):
         tgt = sm.predictor_target(cfg, l)
         if pred is not None and tgt is not None:
             q = opred.logits(x, obf.decode(pred[0]), None if pred[1] is None else obf.decode(pred[1]))
-            Q, _, _ = opred.vote(opred.per_token(q, cfg.top_k), cfg.n_experts, cfg.slots)
-            lcs[tgt].spec_plan(Q)
+            Q, votes, _ = opred.vote(opred.per_token(q, cfg.top_k), cfg.n_experts, cfg.slots)
+            lcs[tgt].spec_plan(Q, voted=np.nonzero(votes)[0].tolist())
         z = orouter.gate_logits(x, obf.decode(model.np_gate[l]), model.np_bias[l])
         ids, w, _ = orouter.route(z, cfg.top_k, bool(cfg.renorm))
         lcs[l].precise_plan(np.unique(ids).tolist())
@@ -377,10 +377,11 @@ def leg_ablation(torch, args, name, model, slots):
     technique on; the unlimited and limit-1 speculative fills) on one workload
     ("decode": DeepSeek-16B shape, batch 1; "prefill": Qwen1.5-MoE shape, 512
     tokens), one context per mode over the same weights, `slots` cached per layer."""
-    from paper_2410_22134_amd import ABLATION, FLAG_NO_PREFETCH
+    from paper_2410_22134_amd import ABLATION, FLAG_FILL_BY_DEADLINE, FLAG_NO_PREFETCH
     from paper_2410_22134_amd.stack import Stack
     modes = [(k, f, 0) for k, f in ABLATION.items()] + [("+cer (no prefetch)", FLAG_NO_PREFETCH, 0),
-                                                         ("+pcer fill limit 1", 0, 1)]
+                                                         ("+pcer fill limit 1", 0, 1),
+                                                         ("+pcer fill by deadline", FLAG_FILL_BY_DEADLINE, 0)]
     T, warm, steps = (1, 4, args.ablation_steps) if name == "decode" else (512, 1, 2)
     cfg = model.cfg
     st = Stack(model, T)
@@ -400,10 +401,12 @@ def leg_sweep(torch, args, model):
     """Cache-rate sweep (25-90% of the experts cached, batch 1) and batch sweep
     (1-8 tokens per step at 50%) of the DeepSeek-MoE-16B-shaped decode, for the
     method (fill limit as configured) and reactive LRU, on the headline model."""
-    from paper_2410_22134_amd import FLAG_NO_PREFETCH, FLAG_PROFILE
+    from paper_2410_22134_amd import FLAG_FILL_BY_DEADLINE, FLAG_NO_PREFETCH, FLAG_PROFILE
     from paper_2410_22134_amd.stack import Stack
     cfg = model.cfg
     E, warm, steps = cfg.n_experts, 4, args.sweep_steps
+    modes = (("method", 0, args.spec_fill_limit), ("deadline", FLAG_FILL_BY_DEADLINE, 0),
+             ("reactive", FLAG_NO_PREFETCH, 0))
     model.max_tokens = 8
     out = {"cache_rate": [], "batch": []}
 
@@ -420,17 +423,17 @@ def leg_sweep(torch, args, model):
         for frac in (0.25, 0.5, 0.75, 0.9):
             C = int(round(frac * E))
             row = {"cached": f"{C}/{E}"}
-            for mode, flags, lim in (("method", 0, args.spec_fill_limit), ("reactive", FLAG_NO_PREFETCH, 0)):
+            for mode, flags, lim in modes:
                 row[mode] = one(1, C, flags, lim)
-            print(f"[bench] sweep cache {C}/{E}: {row['method']['tok_s']} / {row['reactive']['tok_s']} tok/s",
-                  file=sys.stderr, flush=True)
+            print(f"[bench] sweep cache {C}/{E}: method {row['method']['tok_s']}, deadline {row['deadline']['tok_s']}, "
+                  f"reactive {row['reactive']['tok_s']} tok/s", file=sys.stderr, flush=True)
             out["cache_rate"].append(row)
         for T in (1, 2, 4, 8):
             row = {"batch": T}
-            for mode, flags, lim in (("method", 0, args.spec_fill_limit), ("reactive", FLAG_NO_PREFETCH, 0)):
+            for mode, flags, lim in modes:
                 row[mode] = one(T, E // 2, flags, lim)
-            print(f"[bench] sweep batch {T}: {row['method']['tok_s']} / {row['reactive']['tok_s']} tok/s",
-                  file=sys.stderr, flush=True)
+            print(f"[bench] sweep batch {T}: method {row['method']['tok_s']}, deadline {row['deadline']['tok_s']}, "
+                  f"reactive {row['reactive']['tok_s']} tok/s", file=sys.stderr, flush=True)
             out["batch"].append(row)
     finally:
         model.max_tokens = 1
@@ -596,11 +599,11 @@ def leg_int4(torch, args):
     Qwen1.5-MoE shape, under the LRU baseline, the method (unlimited fills and
     fill limit 1) and reactive; plus the dequantising GEMV's rate."""
     from synth import configs
-    from paper_2410_22134_amd import ABLATION, FLAG_NO_PREEMPT, FLAG_NO_PREFETCH, FLAG_PROFILE
+    from paper_2410_22134_amd import ABLATION, FLAG_FILL_BY_DEADLINE, FLAG_NO_PREEMPT, FLAG_NO_PREFETCH, FLAG_PROFILE
     from paper_2410_22134_amd.model import SyntheticModel
     from paper_2410_22134_amd.stack import Stack
     modes = (("lru", ABLATION["lru"], 0), ("+pcer", 0, 0), ("+pcer fill limit 1", 0, 1),
-             ("+cer (no prefetch)", FLAG_NO_PREFETCH, 0))
+             ("+pcer fill by deadline", FLAG_FILL_BY_DEADLINE, 0), ("+cer (no prefetch)", FLAG_NO_PREFETCH, 0))
     out = {}
     for name, base, T, warm, steps in (("decode", configs.C2, 1, 4, args.ablation_steps * 2),
                                        ("prefill", configs.C3, 512, 1, 2)):

@@ -86,6 +86,17 @@ enum { PROMOE_PRIO_LOW = 0, PROMOE_PRIO_HIGH = 1 };
 #define PROMOE_FLAG_STATIC 32      /* static cache baseline: the first C-2 slots keep their
                                       initial experts for good, misses rotate through the
                                       last 2 (LRU among them).  Needs C >= 3. */
+#define PROMOE_FLAG_FILL_BY_DEADLINE 64  /* a predictor-driven plan fills only as many slots
+                                      as the host link can copy before the target layer's
+                                      route: floor((link rate x lookahead x mean interval
+                                      between routes - bytes already queued or in flight)
+                                      / expert bytes), at most spec_fill_limit when that is
+                                      > 0.  The paper's prefetcher replaces a slot only when
+                                      the copy starts and drops what has not started when
+                                      the route comes (Alg. 1, "Early Preemption"); a fill
+                                      that cannot land in time would only move mispredicted
+                                      bytes and evict.  Plans depend on host timing; each
+                                      records the budget it used. */
 
 typedef struct promoe_config {
   int32_t n_layers;          /* L */
@@ -130,6 +141,8 @@ typedef struct promoe_config {
                                 weight at (r, k) is (code - 8) * scale[r][k / 128].
                                 Needs dtype bf16 and hidden, inter multiples of 128.
                                 Gates, predictors and shared experts stay in dtype. */
+  float link_gb_per_s;       /* host-to-device rate assumed by PROMOE_FLAG_FILL_BY_DEADLINE,
+                                GB/s; 0 = 56 (PCIe Gen5 x16 as measured on MI355X) */
 } promoe_config;
 
 typedef struct promoe_stats {
@@ -176,6 +189,7 @@ typedef struct promoe_plan {
                        compute must finish before the fill (-1 none), count[i] = tokens. */
   int32_t n;
   int32_t expert[64], slot[64], flag[64], victim[64], after[64], count[64];
+  int32_t fill_budget;  /* kind 0: most slots the plan could fill (-1: no limit) */
 } promoe_plan;
 
 /* ---- lifetime ------------------------------------------------------------ */
@@ -224,9 +238,18 @@ int promoe_set_initial_cache(promoe_ctx* ctx, int layer, const int32_t* h_expert
  * predictor of layer+lookahead; per-token top-k of the
  * predictor output; an integer vote merges the tokens' picks into a list Q of
  * at most slots_per_layer experts (votes desc, best rank asc, id asc); the
- * target layer's cache is planned on the device: resident members are
- * touched, others take the free or least-recently-used slot and their three
- * chunks are queued at low priority, copied by the library's worker thread.
+ * target layer's cache is planned on the device: first every resident member
+ * of Q is touched (Alg. 2 counts these hits as it pushes the list), then each
+ * other member, in Q order, takes the lowest free slot or the least recently
+ * used one whose expert the prediction does not vote for (the worker of
+ * Alg. 1 replaces a slot only when a copy starts, after the list is pushed;
+ * trading one predicted expert for another only adds copies), and its three
+ * chunks are queued at low priority, copied by the library's worker thread;
+ * a member with no such slot, or past cfg.spec_fill_limit, is skipped.
+ * The kernels after the predictor's first rows run on a side stream of the
+ * library, forked from `stream` once those rows are written and joined back
+ * into it before the call returns: they overlap expert work already queued
+ * on `stream`, and everything queued on `stream` later follows them.
  * Optional outputs: d_pred_ids [T x k] per-token predicted ids; h_q/n_q the
  * list Q (requesting it synchronises the stream).  When layer+lookahead is
  * past the last layer only the gate logits are computed and *n_q = 0. */
@@ -250,6 +273,24 @@ int promoe_predict(promoe_ctx* ctx, int layer, const void* d_x, int T, int32_t* 
  * order, *n_order its length. */
 int promoe_route(promoe_ctx* ctx, int layer, const void* d_x, int T, int32_t* d_ids, float* d_w,
                  float* d_shared_scale, int32_t* h_order, int32_t* n_order, void* stream);
+
+/* promoe_route of `layer` followed by promoe_predict of the same layer on the
+ * same input (d_pred_ids as there; Q is not returned), in one call: the
+ * predictor's first rows ride in the gate launch, and its other kernels are
+ * launched while the host waits for the precise plan, so the prediction adds
+ * next to no host time to the step.  The predictor runs beside the layer's
+ * experts with no device-side join: the spec plan that ends it is awaited on
+ * the host by the context's next promoe_route, promoe_route_predict,
+ * promoe_predict, promoe_prefetch or promoe_sync call, before that call queues
+ * anything (without a spec plan, e.g. with PROMOE_FLAG_NO_PREFETCH, the
+ * layer's promoe_expert_ffn call joins the side stream into `stream` after its
+ * last launch).  d_pred_ids is complete once such a call has returned.
+ * Needs cfg.lookahead >= 1 (with 0 the prediction plans the routed layer
+ * itself and must come first), else PROMOE_EINVAL.  Results are those of the
+ * two calls made in that order. */
+int promoe_route_predict(promoe_ctx* ctx, int layer, const void* d_x, int T, int32_t* d_ids, float* d_w,
+                         float* d_shared_scale, int32_t* d_pred_ids, int32_t* h_order, int32_t* n_order,
+                         void* stream);
 
 /* External push of a list of experts for `target_layer` (Alg. 2
  * PushPredictedExperts with a caller-chosen list): the same device plan as a

@@ -60,18 +60,22 @@ class NaiveLRU:
                 return i
         return -1
 
-    def _free_or_lru(self):
-        # slots below `pinned` are never given away
+    def _free_or_lru(self, keep=frozenset()):
+        # slots below `pinned` are never given away, nor experts in `keep`
         used = set(self.where.values())
         free = [s for s in range(self.pinned, self.C) if s not in used]
         if free:
             return free[0], None
-        movable = [e for e in self.where if self.where[e] >= self.pinned]
+        movable = [e for e in self.where if self.where[e] >= self.pinned and e not in keep]
+        if not movable:
+            return -1, None
         v = min(movable, key=lambda e: self._last(e, ("touch", "fill")))
         return self.where[v], v
 
-    def _bring(self, e, speculative):
-        s, v = self._free_or_lru()
+    def _bring(self, e, speculative, keep=frozenset()):
+        s, v = self._free_or_lru(keep)
+        if s < 0:
+            return -1, None
         if v is not None:
             self.c["evict"] += 1
             if v in self.spec_pending:
@@ -86,24 +90,33 @@ class NaiveLRU:
             self.spec_pending.discard(e)
         return s, v
 
-    def spec(self, Q, budget=-1, predicted=True):
+    def spec(self, Q, budget=-1, predicted=True, voted=None):
+        """Touch the list's resident members, then bring the others in list
+        order, never evicting a list member or an expert in `voted`."""
         if predicted:
             self.predicted = list(Q)
             self.c["pred_n"] += len(Q)
+        keep = frozenset(Q) | frozenset(voted or ())
+        resident_before = {e: self.where[e] for e in Q if e in self.where}
+        for e in Q:
+            if e in resident_before:
+                self.log.append(("touch", e))
+                self.c["spec_resident"] += 1
         out = []
         brought = 0
         for e in Q:
-            if e in self.where:
-                self.log.append(("touch", e))
-                self.c["spec_resident"] += 1
-                out.append((e, self.where[e], False))
-            elif budget >= 0 and brought >= budget:
+            if e in resident_before:
+                out.append((e, resident_before[e], False))
+                continue
+            s = -1
+            if not (budget >= 0 and brought >= budget):
+                s, _ = self._bring(e, True, keep)
+            if s < 0:
                 out.append((e, -1, False))
-            else:
-                brought += 1
-                s, _ = self._bring(e, True)
-                self.c["spec_issued"] += 1
-                out.append((e, s, True))
+                continue
+            brought += 1
+            self.c["spec_issued"] += 1
+            out.append((e, s, True))
         return out
 
     def _fill_time(self, e):

@@ -15,15 +15,28 @@ per-layer clock, fetch_seq[C] (order in which slots were (re)filled),
 spec_unused[C] (filled by a prediction and not yet used).
 Warm start: experts 0..C-1 in slots 0..C-1, stamp = slot index, fetch_seq 0.
 
-spec_plan(Q)      -- PushPredictedExperts: for e in Q order, touch it if
-                     resident; else take the lowest free slot or the least
-                     recently stamped one, evict, assign, mark speculative and
-                     queue its three chunks at low priority.  With a budget
-                     b >= 0 at most b experts per plan are filled (later
-                     non-resident members are skipped): the paper's worker
-                     replaces a slot only when a copy starts, and when copies
-                     are the bottleneck only the first few predicted experts of
-                     a layer start before the layer's route drops the rest.
+spec_plan(Q)      -- PushPredictedExperts: first every resident member of Q is
+                     touched, in Q order; then, in Q order, each non-resident
+                     member takes the lowest free slot or the least recently
+                     stamped one, evicts, assigns, is marked speculative and
+                     queues its three chunks at low priority.  Touches first:
+                     Alg. 2 counts the hits while it pushes the list, and the
+                     worker of Alg. 1 replaces a slot only when it starts a
+                     copy, after the whole list has been pushed; so a fill never
+                     evicts a member of its own list (|Q| <= C).
+                     A fill never evicts an expert the same prediction names
+                     (``voted``: every expert with a vote, of which Q is the
+                     first C; default Q): when every candidate victim is
+                     predicted, the rest of the list is skipped.  The paper
+                     pushes one token's list, where this never binds; for a
+                     batch whose votes cover the cache, trading one predicted
+                     expert for another only adds copies (a design reading).
+                     With a budget b >= 0 at most b experts per plan are filled
+                     (later non-resident members are skipped): the paper's
+                     worker replaces a slot only when a copy starts, and when
+                     copies are the bottleneck only the first few predicted
+                     experts of a layer start before the layer's route drops
+                     the rest.
 precise_plan(P)   -- PushPreciseExperts: P = the distinct experts the layer's
                      tokens chose, ascending.  Low-priority work of the layer is
                      dropped (physical only).  Order = resident experts by
@@ -100,12 +113,15 @@ class LayerCache:
                 self.stamp[s] = s
 
     # -- helpers
-    def _victim(self) -> int:
+    def _victim(self, spare=()) -> int:
+        """Lowest free slot, else the least recently stamped one whose expert is
+        not in `spare`; -1 when there is none."""
         cand = range(self.pinned, self.C)
         for s in cand:
             if self.slot_expert[s] < 0:
                 return s
-        return min(cand, key=lambda s: self.stamp[s])
+        cand = [s for s in cand if self.slot_expert[s] not in spare]
+        return min(cand, key=lambda s: self.stamp[s]) if cand else -1
 
     def _evict(self, s: int) -> int:
         v = self.slot_expert[s]
@@ -130,28 +146,32 @@ class LayerCache:
         self._touch(s)
 
     # -- plans
-    def spec_plan(self, Q, budget: int = -1, predicted: bool = True):
+    def spec_plan(self, Q, budget: int = -1, predicted: bool = True, voted=None):
+        Q = [int(e) for e in Q]
         if predicted:
-            self.pred_set = set(int(e) for e in Q)
+            self.pred_set = set(Q)
             self.count["pred_n"] += len(self.pred_set)
-        out = []
-        fills = 0
-        for e in Q:
-            e = int(e)
+        spare = set(Q) | set(int(e) for e in (voted if voted is not None else ()))
+        out = [None] * len(Q)
+        for i, e in enumerate(Q):          # the list's hits
             s = self.slot_of[e]
             if s >= 0:
                 self._touch(s)
                 self.count["spec_resident"] += 1
-                out.append(SpecEntry(e, s, False, -1))
-            elif 0 <= budget <= fills:
-                out.append(SpecEntry(e, -1, False, -1, True))
-            else:
-                fills += 1
-                s = self._victim()
-                v = self._evict(s)
-                self._fill(e, s, True)
-                self.count["spec_issued"] += 1
-                out.append(SpecEntry(e, s, True, v))
+                out[i] = SpecEntry(e, s, False, -1)
+        fills = 0
+        for i, e in enumerate(Q):          # then its fills
+            if out[i] is not None:
+                continue
+            s = -1 if 0 <= budget <= fills else self._victim(spare)
+            if s < 0:
+                out[i] = SpecEntry(e, -1, False, -1, True)
+                continue
+            fills += 1
+            v = self._evict(s)
+            self._fill(e, s, True)
+            self.count["spec_issued"] += 1
+            out[i] = SpecEntry(e, s, True, v)
         return out
 
     def _hit(self, e: int) -> PreciseEntry:

@@ -13,6 +13,7 @@ PROMOE_F32, PROMOE_BF16 = 0, 1
 WEIGHTS_DENSE, WEIGHTS_INT4 = 0, 1
 PRIO_LOW, PRIO_HIGH = 0, 1
 FLAG_PROFILE, FLAG_NO_PREFETCH, FLAG_NO_CHUNK, FLAG_NO_PREEMPT, FLAG_NO_REORDER, FLAG_STATIC = 1, 2, 4, 8, 16, 32
+FLAG_FILL_BY_DEADLINE = 64
 
 _i32, _i64, _vp, _sz, _dbl = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_double
 
@@ -22,7 +23,7 @@ class Config(ctypes.Structure):
                 ("shared_inter", _i32), ("shared_gate", _i32), ("renorm", _i32), ("router_bias", _i32),
                 ("slots_per_layer", _i32), ("lookahead", _i32), ("pred_hidden", _i32), ("max_tokens", _i32),
                 ("dtype", _i32), ("copy_subchunk_bytes", _i64), ("copy_window", _i32), ("flags", _i32),
-                ("spec_fill_limit", _i32), ("weight_format", _i32)]
+                ("spec_fill_limit", _i32), ("weight_format", _i32), ("link_gb_per_s", ctypes.c_float)]
 
 
 STAT_COUNTERS = ("prec_access", "hit", "miss", "spec_issued", "spec_resident", "spec_used", "spec_wasted", "evict",
@@ -47,11 +48,13 @@ class Stats(ctypes.Structure):
 
 
 class Plan(ctypes.Structure):
-    _fields_ = [("n", _i32)] + [(n, _i32 * 64) for n in ("expert", "slot", "flag", "victim", "after", "count")]
+    _fields_ = [("n", _i32)] + [(n, _i32 * 64) for n in ("expert", "slot", "flag", "victim", "after", "count")] + \
+        [("fill_budget", _i32)]
 
     def as_dict(self):
         n = self.n
-        return {"n": n, **{f: list(getattr(self, f))[:n] for f in ("expert", "slot", "flag", "victim", "after", "count")}}
+        return {"n": n, "fill_budget": int(self.fill_budget),
+                **{f: list(getattr(self, f))[:n] for f in ("expert", "slot", "flag", "victim", "after", "count")}}
 
 
 class PromoeError(RuntimeError):
@@ -81,6 +84,8 @@ def lib() -> ctypes.CDLL:
         "promoe_set_initial_cache": ([_vp, ctypes.c_int, _vp, ctypes.c_int], ctypes.c_int),
         "promoe_predict": ([_vp, ctypes.c_int, _vp, ctypes.c_int, _vp, _vp, _vp, _vp], ctypes.c_int),
         "promoe_route": ([_vp, ctypes.c_int, _vp, ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
+        "promoe_route_predict": ([_vp, ctypes.c_int, _vp, ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp],
+                                 ctypes.c_int),
         "promoe_prefetch": ([_vp, ctypes.c_int, _vp, ctypes.c_int, ctypes.c_int, _vp], ctypes.c_int),
         "promoe_expert_ffn": ([_vp, ctypes.c_int, _vp, ctypes.c_int, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
         "promoe_expert_ffn_noalloc": ([_vp, ctypes.c_int, _vp, ctypes.c_int, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
@@ -110,7 +115,7 @@ def lib() -> ctypes.CDLL:
 def exported_symbols():
     return [n for n in ("promoe_create", "promoe_destroy", "promoe_set_layer", "promoe_set_attn",
                         "promoe_set_expert_host", "promoe_set_initial_cache", "promoe_predict", "promoe_route",
-                        "promoe_prefetch", "promoe_expert_ffn", "promoe_expert_ffn_noalloc", "promoe_cache_stats",
+                        "promoe_route_predict", "promoe_prefetch", "promoe_expert_ffn", "promoe_expert_ffn_noalloc", "promoe_cache_stats",
                         "promoe_reset_stats",
                         "promoe_slot_table", "promoe_last_plan", "promoe_sync", "promoe_attn_surrogate",
                         "promoe_residual_add", "promoe_host_alloc", "promoe_host_free", "promoe_expert_bytes",
@@ -203,6 +208,13 @@ class Context:
     def route(self, layer, x, T, ids, w, shared_scale=None, stream=None):
         check(lib().promoe_route(self._h, layer, _p(x), T, _p(ids), _p(w), _p(shared_scale), self._order,
                                  self._n_ref, _stream(stream)), "promoe_route")
+        return self._order[:self._n.value]
+
+    def route_predict(self, layer, x, T, ids, w, shared_scale=None, pred_ids=None, stream=None):
+        """route then predict of one layer on one input, in one call (look-ahead >= 1)."""
+        check(lib().promoe_route_predict(self._h, layer, _p(x), T, _p(ids), _p(w), _p(shared_scale),
+                                         _p(pred_ids), self._order, self._n_ref, _stream(stream)),
+              "promoe_route_predict")
         return self._order[:self._n.value]
 
     def prefetch(self, layer, ids, prio=PRIO_LOW, stream=None):

@@ -111,6 +111,7 @@ struct PlanRecord {
   int32_t offset[65];
   int32_t q_in[64];  // host-provided list for promoe_prefetch
   int32_t n_q_in;
+  int32_t fill_budget;  // spec plan: most slots it could fill (-1: no limit)
   int32_t done;
 };
 

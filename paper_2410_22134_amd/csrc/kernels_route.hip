@@ -8,8 +8,9 @@
 //                       only, by the predictor.
 //  * k_plan_spec     -- speculative plan of a target layer (Alg. 2
 //                       PushPredictedExperts): integer vote over the tokens'
-//                       predicted ids, then the LRU plan (optionally filling
-//                       only the first few non-resident experts).
+//                       predicted ids, then the LRU plan: the list's resident
+//                       experts touched, then its others filled (optionally
+//                       only the first few), never evicting a predicted expert.
 //  * k_plan_precise  -- precise plan of the routed layer (Alg. 2
 //                       PushPreciseExperts, Sec. "Reordered Inference"):
 //                       hit/miss, order, victim slots, counters, followed by the
@@ -107,6 +108,19 @@ __device__ __forceinline__ int victim_slot(const PlanArgs& a, int lane, const Wa
   return (int)(wave_min_u64(key) & 63ull);
 }
 
+// victim_slot among the slots whose expert is not in `spare` (a bit per
+// expert); -1 when every candidate slot holds such an expert.
+__device__ __forceinline__ int spare_victim_slot(const PlanArgs& a, int lane, const WaveState& w, uint64_t spare) {
+  uint64_t key = ~0ull;
+  if (lane < a.C && lane >= a.pinned) {
+    if (w.slot_expert < 0) key = (uint64_t)lane;
+    else if (!((spare >> w.slot_expert) & 1ull)) key = (1ull << 40) | (uint64_t)w.stamp;
+  }
+  key = (key << 6) | (uint64_t)lane;
+  const uint64_t m = wave_min_u64(key);
+  return m >= (1ull << 47) ? -1 : (int)(m & 63ull);
+}
+
 // Give slot v to expert e: evict its occupant (counted), fill, stamp.
 __device__ __forceinline__ int fill_slot(const PlanArgs& a, int lane, WaveState& w, int e, int v, bool speculative,
                                          uint32_t& clock, uint32_t& fseq, int64_t (&cnt)[kCounters]) {
@@ -180,7 +194,18 @@ __global__ __launch_bounds__(256) void k_plan_spec(PlanArgs a) {
     if (lane == 0) a.st.pred_mask[a.layer] = m;
     cnt[CNT_PRED_N] += nq;
   }
-  int fills = 0;
+  // Experts no fill may evict: every expert the prediction votes for (of which
+  // Q is the first C), or the caller's whole list.
+  uint64_t spare = 0;
+  if (a.ids) {
+    if (lane < a.E && votes[lane] > 0) spare = 1ull << lane;
+    spare = __ballot(spare != 0);
+  } else {
+    for (int i = 0; i < nq; ++i) spare |= 1ull << Q[i];
+  }
+  // The list's hits first (Alg. 2 counts them as it pushes the list), then its
+  // fills (the worker of Alg. 1 replaces a slot only when a copy starts): no
+  // fill evicts a member of the list.
   for (int i = 0; i < nq; ++i) {
     const int e = Q[i];
     const int s_res = __shfl(w.slot_of, e, kWave);
@@ -189,15 +214,21 @@ __global__ __launch_bounds__(256) void k_plan_spec(PlanArgs a) {
       if (lane == s_res) w.stamp = clock;
       cnt[CNT_SPEC_RESIDENT]++;
       if (lane == 0) { rec->expert[i] = e; rec->slot[i] = s_res; rec->flag[i] = 0; rec->victim[i] = -1; rec->after[i] = -1; }
-    } else if (budget >= 0 && fills >= budget) {
-      if (lane == 0) { rec->expert[i] = e; rec->slot[i] = -1; rec->flag[i] = 0; rec->victim[i] = -1; rec->after[i] = -1; }
-    } else {
-      ++fills;
-      const int v = victim_slot(a, lane, w);
-      const int old = fill_slot(a, lane, w, e, v, true, clock, fseq, cnt);
-      cnt[CNT_SPEC_ISSUED]++;
-      if (lane == 0) { rec->expert[i] = e; rec->slot[i] = v; rec->flag[i] = 1; rec->victim[i] = old; rec->after[i] = -1; }
     }
+  }
+  int fills = 0;
+  for (int i = 0; i < nq; ++i) {
+    const int e = Q[i];
+    if (__shfl(w.slot_of, e, kWave) >= 0) continue;
+    const int v = (budget >= 0 && fills >= budget) ? -1 : spare_victim_slot(a, lane, w, spare);
+    if (v < 0) {
+      if (lane == 0) { rec->expert[i] = e; rec->slot[i] = -1; rec->flag[i] = 0; rec->victim[i] = -1; rec->after[i] = -1; }
+      continue;
+    }
+    ++fills;
+    const int old = fill_slot(a, lane, w, e, v, true, clock, fseq, cnt);
+    cnt[CNT_SPEC_ISSUED]++;
+    if (lane == 0) { rec->expert[i] = e; rec->slot[i] = v; rec->flag[i] = 1; rec->victim[i] = old; rec->after[i] = -1; }
   }
   store_state(a, lane, w, clock, fseq, cnt);
   if (lane == 0) {
@@ -206,6 +237,7 @@ __global__ __launch_bounds__(256) void k_plan_spec(PlanArgs a) {
     rec->n = nq;
     rec->n_hit = 0;
     rec->predicted = a.ids ? 1 : 0;
+    rec->fill_budget = budget;
     __threadfence_system();
     rec->done = 1;
   }

@@ -19,6 +19,8 @@
 
 #include <algorithm>
 #include <atomic>
+#include <chrono>
+#include <cmath>
 #include <condition_variable>
 #include <cstdio>
 #include <cstring>
@@ -202,10 +204,31 @@ struct promoe_ctx {
   int last_route_layer = -1;      // layer of the latest route, kept after its FFN call
   std::vector<char> ffn_started;  // per route position: launched by the route itself
   bool shared_started = false;    // the shared expert too
+  // mean interval between consecutive routes (PROMOE_FLAG_FILL_BY_DEADLINE)
+  std::chrono::steady_clock::time_point last_route_t{};
+  bool have_route_t = false;
+  double route_dt_ema = 0.0;
   uint64_t early_busy = 0;        // slots the route's early launch skipped
   size_t early_prof0 = 0, early_nprof = 0;  // its profiling entries (bytes filled in by the route)
   hipStream_t route_stream = nullptr;  // stream of the latest route
   hipEvent_t route_done = nullptr;     // recorded on it after the route's last launch
+  // The predictor's kernels after its first rows (second layer, top-k, spec
+  // plan) run on a side stream of the library, forked from the caller's stream
+  // once those rows are written and joined back into it at the end of the
+  // predict call: they overlap the layer's expert launches queued before them.
+  hipStream_t pred_stream = nullptr;
+  hipEvent_t pred_in = nullptr, pred_done = nullptr;
+  bool pred_nojoin = true;            // no prediction's side-stream work needs a device join
+  bool pred_pending = false;          // else: pred_done recorded, no stream has waited for it yet
+  hipStream_t pred_joined = nullptr;  // or the latest stream that did
+  // A prediction launched by promoe_route_predict ends with its spec plan,
+  // record pred_host_rec: the next call that could touch what it reads or
+  // writes first waits on the host for that record (no device-side join).
+  int64_t pred_host_rec = -1;
+  // first predictor rows computed by a route's gate launch (layer, input, T)
+  int pred_rows_layer = -1;
+  const void* pred_rows_x = nullptr;
+  int pred_rows_T = 0;
   PlanRecord route_rec{};
   std::vector<int64_t> need01, need2;  // copy seq each position waits for (-1 none)
   std::vector<int> need_q;             // engine queue of those copies
@@ -440,6 +463,26 @@ PlanArgs plan_args(promoe_ctx* c, int layer, const int32_t* ids, int T, int64_t 
   a.d_pos_of = c->d_pos_of;
   a.d_npos = c->d_npos;
   return a;
+}
+
+// PROMOE_FLAG_FILL_BY_DEADLINE: slots a predictor-driven plan may fill, the
+// whole experts the link can still copy before the target layer's route
+// (lookahead routes from now at the mean interval between routes) after what
+// is already queued or in flight.
+int deadline_fill_budget(promoe_ctx* c) {
+  const int lim = c->cfg.spec_fill_limit;
+  if (lim < 0 || c->D <= 0 || c->route_dt_ema <= 0.0) return 0;
+  const int cap = lim > 0 ? lim : 64;
+  int64_t pending;
+  {
+    std::lock_guard<std::mutex> lk(c->mu);
+    c->pf->retire();
+    pending = c->pf->pending_bytes();
+  }
+  const double rate = (c->cfg.link_gb_per_s > 0.0f ? c->cfg.link_gb_per_s : 56.0) * 1e9;
+  const double room = rate * c->D * c->route_dt_ema - (double)pending;
+  if (room <= 0.0) return 0;
+  return (int)std::min<double>(cap, std::floor(room / (double)c->expert_bytes));
 }
 
 int check_tokens(promoe_ctx* c, int T) {
@@ -689,6 +732,9 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   c->rec_d = static_cast<PlanRecord*>(rd);
   for (int i = 0; i < kRecRing; ++i) hipEventCreateWithFlags(&c->rec_ev[i], hipEventDisableTiming);
   hipEventCreateWithFlags(&c->route_done, hipEventDisableTiming);
+  hipEventCreateWithFlags(&c->pred_in, hipEventDisableTiming);
+  hipEventCreateWithFlags(&c->pred_done, hipEventDisableTiming);
+  hipStreamCreateWithFlags(&c->pred_stream, hipStreamNonBlocking);
 
   // ---- copy engine + scheduler
   for (auto& cs : c->eng.stream) hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
@@ -715,8 +761,12 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   return PROMOE_OK;
 }
 
+static int pred_host_join(promoe_ctx* c);
+
 int promoe_sync(promoe_ctx* c) {
   if (!c) return PROMOE_EINVAL;
+  const int jrc = pred_host_join(c);
+  if (jrc) return jrc;
   {
     std::unique_lock<std::mutex> lk(c->mu);
     // flush speculative records and low-priority work, then wait for every copy
@@ -742,6 +792,7 @@ int promoe_sync(promoe_ctx* c) {
     }
     if (c->eng.err != hipSuccess) return fail_hip(c->eng.err, "copy engine");
   }
+  HIPCHK(hipStreamSynchronize(c->pred_stream));
   if (c->last_stream) HIPCHK(hipStreamSynchronize(c->last_stream));
   HIPCHK(hipStreamSynchronize(nullptr));
   if (c->profile) prof_resolve(c);
@@ -757,6 +808,7 @@ int promoe_destroy(promoe_ctx* c) {
   c->cv.notify_all();
   if (c->worker.joinable()) c->worker.join();
   for (auto& cs : c->eng.stream) hipStreamSynchronize(cs);
+  hipStreamSynchronize(c->pred_stream);
   hipDeviceSynchronize();
   if (c->profile) prof_resolve(c);
   for (auto& e : c->prof_free) hipEventDestroy(e);
@@ -764,6 +816,9 @@ int promoe_destroy(promoe_ctx* c) {
   for (auto& e : c->cev) hipEventDestroy(e);
   for (int i = 0; i < kRecRing; ++i) hipEventDestroy(c->rec_ev[i]);
   hipEventDestroy(c->route_done);
+  hipEventDestroy(c->pred_in);
+  hipEventDestroy(c->pred_done);
+  hipStreamDestroy(c->pred_stream);
   for (auto& cs : c->eng.stream) hipStreamDestroy(cs);
   hipHostFree(c->rec_h);
   hipFree(c->dmem);
@@ -830,6 +885,85 @@ int promoe_set_initial_cache(promoe_ctx* c, int layer, const int32_t* h_experts,
   return PROMOE_OK;
 }
 
+static int predict_tail(promoe_ctx* c, int layer, int target, int T, int32_t* d_pred_ids, int32_t* h_q,
+                        int32_t* n_q, hipStream_t s, int64_t* rec_out);
+
+// The host waits for the spec plan that ends a prediction of promoe_route_predict:
+// the side stream's kernels before it are then complete too.
+static int pred_host_join(promoe_ctx* c) {
+  if (c->pred_host_rec < 0) return PROMOE_OK;
+  const int64_t r = c->pred_host_rec;
+  c->pred_host_rec = -1;
+  const hipError_t e = wait_record(c, r);
+  return e == hipSuccess ? PROMOE_OK : fail_hip(e, "prediction");
+}
+
+// Order stream s after the predictor's side-stream work (its reads of the
+// predictor rows in d_logits, its writes of the predicted ids and of the
+// target layer's cache state), unless s already waited for it.
+static hipError_t pred_join(promoe_ctx* c, hipStream_t s) {
+  if (c->pred_nojoin || (!c->pred_pending && c->pred_joined == s)) return hipSuccess;
+  const hipError_t e = hipStreamWaitEvent(s, c->pred_done, 0);
+  if (e == hipSuccess) {
+    c->pred_pending = false;
+    c->pred_joined = s;
+  }
+  return e;
+}
+
+// The prediction of `layer` on stream s (routed: no route will need this
+// layer's gate logits on this input any more, so only predictor rows are
+// computed).  join_now: s waits for the side stream before the call returns;
+// else the layer's FFN call joins it (after its last launch).
+static int predict_launch(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_pred_ids, int32_t* h_q,
+                          int32_t* n_q, hipStream_t s, bool routed, bool join_now) {
+  int rc = pred_host_join(c);
+  if (rc) return rc;
+  HIPCHK(pred_join(c, s));
+  const int target = layer + c->D;
+  const bool has_pred = target < c->L && c->lw[layer].pw1 != nullptr;
+  const bool rows_ready =
+      has_pred && c->pred_rows_layer == layer && c->pred_rows_x == d_x && c->pred_rows_T == T;
+  c->pred_rows_layer = -1;
+  if (!rows_ready) {
+    rc = launch_gate_rows(c, layer, d_x, T, has_pred, s, !routed);
+    if (rc) return rc;
+    if (!routed) {
+      c->gate_layer = layer;
+      c->gate_x = d_x;
+      c->gate_T = T;
+    }
+  }
+  if (n_q) *n_q = 0;
+  if (!has_pred) return PROMOE_OK;
+  // Fork: the rest reads the predictor rows (and the cache state of the target
+  // layer, which no launch on s touches before the join below).
+  if (!rows_ready) HIPCHK(hipEventRecord(c->pred_in, s));
+  hipStream_t ps = c->pred_stream;
+  HIPCHK(hipStreamWaitEvent(ps, c->pred_in, 0));
+  int64_t spec_rec;
+  rc = predict_tail(c, layer, target, T, d_pred_ids, h_q, n_q, ps, &spec_rec);
+  if (!rc && !join_now && spec_rec >= 0) {
+    // the spec plan's record marks the end of the side stream's work (earlier
+    // side-stream work was joined at the top of this call)
+    c->pred_host_rec = spec_rec;
+    c->pred_nojoin = true;
+    return PROMOE_OK;
+  }
+  // Join: whatever s runs after it (the caller's reads of the predicted ids, the
+  // next gate launch over d_logits, the target layer's route) follows it.
+  hipError_t je = hipEventRecord(c->pred_done, ps);
+  if (je == hipSuccess) {
+    c->pred_nojoin = false;
+    c->pred_pending = true;
+    c->pred_joined = nullptr;
+    if (join_now) je = pred_join(c, s);
+  }
+  if (rc) return rc;
+  if (je != hipSuccess) return fail_hip(je, "predictor join");
+  return PROMOE_OK;
+}
+
 int promoe_predict(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_pred_ids, int32_t* h_q,
                    int32_t* n_q, void* stream) {
   if (!c || layer < 0 || layer >= c->L || !d_x || !c->lw[layer].wg) return PROMOE_EINVAL;
@@ -838,24 +972,20 @@ int promoe_predict(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_
   hipStream_t s = static_cast<hipStream_t>(stream);
   c->last_stream = s;
   const int target = layer + c->D;
-  const bool has_pred = target < c->L && c->lw[layer].pw1 != nullptr;
-  if (has_pred && c->route_layer == target) {
+  if (target < c->L && c->lw[layer].pw1 && c->route_layer == target) {
     g_last_error = "prediction for a layer whose route is not consumed";
     return PROMOE_ESTATE;
   }
   // After route(layer) on the same input (its FFN call done or not) no route
-  // needs this layer's gate logits any more: only the predictor rows are
-  // computed.
+  // needs this layer's gate logits any more.
   const bool routed = c->last_route_layer == layer && c->route_x == d_x && c->route_T == T;
-  rc = launch_gate_rows(c, layer, d_x, T, has_pred, s, !routed);
-  if (rc) return rc;
-  if (!routed) {
-    c->gate_layer = layer;
-    c->gate_x = d_x;
-    c->gate_T = T;
-  }
-  if (n_q) *n_q = 0;
-  if (!has_pred) return PROMOE_OK;
+  return predict_launch(c, layer, d_x, T, d_pred_ids, h_q, n_q, s, routed, true);
+}
+
+static int predict_tail(promoe_ctx* c, int layer, int target, int T, int32_t* d_pred_ids, int32_t* h_q,
+                        int32_t* n_q, hipStream_t s, int64_t* rec_out) {
+  int rc;
+  *rec_out = -1;
   int32_t* pids = d_pred_ids ? d_pred_ids : c->d_pred_ids;
   TopkArgs tk{};
   if (c->Ph > 0) {
@@ -889,11 +1019,14 @@ int promoe_predict(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_
   int64_t r;
   rc = new_record(c, 0, PROMOE_PRIO_LOW, &r);
   if (rc) return rc;
-  launch_plan_spec(plan_args(c, target, pids, T, r), s);
+  PlanArgs pa = plan_args(c, target, pids, T, r);
+  if (c->cfg.flags & PROMOE_FLAG_FILL_BY_DEADLINE) pa.fill_budget = deadline_fill_budget(c);
+  launch_plan_spec(pa, s);
   hipError_t le = hipGetLastError();
   if (le == hipSuccess) le = hipEventRecord(c->rec_ev[r % kRecRing], s);
   publish(c, r);
   if (le != hipSuccess) return fail_hip(le, "plan_spec");
+  *rec_out = r;
   c->lw[target].planned = true;
   if (h_q || n_q) {
     HIPCHK(hipEventSynchronize(c->rec_ev[r % kRecRing]));
@@ -918,8 +1051,12 @@ int promoe_prefetch(promoe_ctx* c, int target_layer, const int32_t* h_ids, int n
   if (c->cfg.flags & PROMOE_FLAG_NO_PREFETCH) return PROMOE_OK;
   hipStream_t s = static_cast<hipStream_t>(stream);
   c->last_stream = s;
+  // a prediction may still be planning on the side stream
+  int rc = pred_host_join(c);
+  if (rc) return rc;
+  HIPCHK(pred_join(c, s));
   int64_t r;
-  int rc = new_record(c, 0, prio, &r);
+  rc = new_record(c, 0, prio, &r);
   if (rc) return rc;
   PlanRecord& rec = c->rec_h[r % kRecRing];
   rec.n_q_in = n;
@@ -938,8 +1075,32 @@ static int early_resident_launch(promoe_ctx* c, int layer, const void* d_x, int 
                                  bool* launched);
 static void early_resident_release(promoe_ctx* c, int layer, int T, hipStream_t s);
 
+// The route of `layer`; with_pred: also the layer's prediction, launched while
+// the host waits for the precise plan.
+static int route_impl(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_ids, float* d_w,
+                      float* d_shared_scale, int32_t* h_order, int32_t* n_order, hipStream_t s, bool with_predict,
+                      int32_t* d_pred_ids);
+
 int promoe_route(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_ids, float* d_w,
                  float* d_shared_scale, int32_t* h_order, int32_t* n_order, void* stream) {
+  return route_impl(c, layer, d_x, T, d_ids, d_w, d_shared_scale, h_order, n_order,
+                    static_cast<hipStream_t>(stream), false, nullptr);
+}
+
+int promoe_route_predict(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_ids, float* d_w,
+                         float* d_shared_scale, int32_t* d_pred_ids, int32_t* h_order, int32_t* n_order,
+                         void* stream) {
+  if (c && c->D == 0) {
+    g_last_error = "promoe_route_predict needs a look-ahead of at least 1";
+    return PROMOE_EINVAL;
+  }
+  return route_impl(c, layer, d_x, T, d_ids, d_w, d_shared_scale, h_order, n_order,
+                    static_cast<hipStream_t>(stream), true, d_pred_ids);
+}
+
+static int route_impl(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_ids, float* d_w,
+                      float* d_shared_scale, int32_t* h_order, int32_t* n_order, hipStream_t s, bool with_predict,
+                      int32_t* d_pred_ids) {
   if (!c || layer < 0 || layer >= c->L || !d_x || !d_ids || !d_w || !c->lw[layer].wg) return PROMOE_EINVAL;
   if (c->cfg.shared_gate && c->Ish > 0 && !d_shared_scale) return PROMOE_EINVAL;
   int rc = check_tokens(c, T);
@@ -948,11 +1109,34 @@ int promoe_route(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_id
     g_last_error = "previous route not consumed by promoe_expert_ffn";
     return PROMOE_ESTATE;
   }
-  hipStream_t s = static_cast<hipStream_t>(stream);
   c->last_stream = s;
+  rc = pred_host_join(c);
+  if (rc) return rc;
+  HIPCHK(pred_join(c, s));
+  {
+    const auto now = std::chrono::steady_clock::now();
+    if (c->have_route_t) {
+      const double dt = std::chrono::duration<double>(now - c->last_route_t).count();
+      if (dt < 1.0) c->route_dt_ema = c->route_dt_ema > 0.0 ? 0.8 * c->route_dt_ema + 0.2 * dt : dt;
+    }
+    c->last_route_t = now;
+    c->have_route_t = true;
+  }
   if (!(c->gate_layer == layer && c->gate_x == d_x && c->gate_T == T)) {
-    rc = launch_gate_rows(c, layer, d_x, T, false, s);
+    // With a look-ahead the layer's prediction follows its route on the same
+    // input: its first predictor rows ride in the gate launch, and the side
+    // stream of the predictor starts from this point.
+    const bool with_pred = c->D > 0 && layer + c->D < c->L && c->lw[layer].pw1 &&
+                           !(c->cfg.flags & PROMOE_FLAG_NO_PREFETCH);
+    rc = launch_gate_rows(c, layer, d_x, T, with_pred, s);
     if (rc) return rc;
+    c->pred_rows_layer = -1;
+    if (with_pred) {
+      HIPCHK(hipEventRecord(c->pred_in, s));
+      c->pred_rows_layer = layer;
+      c->pred_rows_x = d_x;
+      c->pred_rows_T = T;
+    }
   }
   c->gate_layer = -1;
   TopkArgs tk{};
@@ -980,6 +1164,8 @@ int promoe_route(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_id
   bool early_ffn = false;
   if (le == hipSuccess) {
     rc = early_resident_launch(c, layer, d_x, T, s, r, &early_ffn);
+    // the prediction's launches (on the side stream) fill the host's wait for the plan
+    if (!rc && with_predict) rc = predict_launch(c, layer, d_x, T, d_pred_ids, nullptr, nullptr, s, true, false);
     if (rc) {
       publish(c, r);
       return rc;
@@ -1253,10 +1439,20 @@ static int early_resident_launch(promoe_ctx* c, int layer, const void* d_x, int 
   if (in_order || (int64_t)T * c->K > 64 || T >= kGemmMinTokens || c->noalloc_call) return PROMOE_OK;
   uint64_t busy = 0;
   {
-    std::lock_guard<std::mutex> lk(c->mu);
-    for (int64_t rr = c->rec_ingested; rr < r; ++rr)
-      if (c->rec_kind[rr % kRecRing] != 0 || rr >= c->rec_pub || !c->rec_h[rr % kRecRing].done) return PROMOE_OK;
-    std::atomic_thread_fence(std::memory_order_acquire);
+    // Earlier plans must be on the host first (their fills decide which slots
+    // are busy): they are speculative ones (a precise one would still await its
+    // FFN call), and a spec plan published before this route was queued ahead
+    // of it, so waiting for it costs at most the wait for this route's plan.
+    std::unique_lock<std::mutex> lk(c->mu);
+    const int64_t first = c->rec_ingested;
+    for (int64_t rr = first; rr < r; ++rr)
+      if (c->rec_kind[rr % kRecRing] != 0 || rr >= c->rec_pub) return PROMOE_OK;
+    lk.unlock();
+    for (int64_t rr = first; rr < r; ++rr) {
+      const hipError_t e = wait_record(c, rr);
+      if (e != hipSuccess) return fail_hip(e, "spec plan");
+    }
+    lk.lock();
     while (c->rec_ingested < r) ingest_spec(c, c->rec_ingested);
     c->pf->retire();
     for (int slot = 0; slot < c->C; ++slot)
@@ -1507,6 +1703,8 @@ static int expert_ffn_run(promoe_ctx* c, int layer, int T, const float* d_w, con
   ca.top_k = c->K;
   launch_combine(ca, T, c->dt, s);
   LAUNCHCHK("combine");
+  // a prediction the route launched on the side stream: later work on s follows it
+  HIPCHK(pred_join(c, s));
   c->route_layer = -1;
   if (c->profile && !c->noalloc_call && c->prof_pending.size() > 4096) {
     HIPCHK(hipStreamSynchronize(s));
@@ -1619,6 +1817,7 @@ int promoe_last_plan(promoe_ctx* c, int layer, int kind, promoe_plan* out) {
   std::lock_guard<std::mutex> lk(c->mu);
   const PlanRecord& r = kind == 0 ? c->last_spec[layer] : c->last_precise[layer];
   out->n = r.n;
+  out->fill_budget = r.fill_budget;
   for (int i = 0; i < 64; ++i) {
     out->expert[i] = r.expert[i];
     out->slot[i] = r.slot[i];

@@ -15,6 +15,13 @@ Prefetcher::Prefetcher(int n_layers, int slots, int n_experts, size_t chunk_byte
 
 void Prefetcher::set_host(int layer, int expert, const uint8_t* p) { host_[layer * E_ + expert] = p; }
 
+int64_t Prefetcher::pending_bytes() const {
+  int64_t b = 0;
+  for (int64_t q : q_bytes_) b += q;
+  for (const LowTask& t : low_) b += (int64_t)chunk_bytes_ - (int64_t)slot_(t.layer, t.slot).ch[t.chunk].n_issued * (int64_t)sub_bytes_;
+  return b;
+}
+
 void Prefetcher::assign(int layer, int slot, int expert) {
   Slot& s = slot_(layer, slot);
   // cancel queued low-priority work aimed at this slot (it belongs to the old expert)

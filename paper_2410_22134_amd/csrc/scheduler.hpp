@@ -100,6 +100,9 @@ class Prefetcher {
   void retire();
 
   bool has_low() const { return !low_.empty(); }
+  // Bytes issued and not yet known complete, plus the bytes of queued
+  // low-priority tasks: what the link must still carry before anything new.
+  int64_t pending_bytes() const;
   int64_t in_flight() const { return next_seq_ - retired_; }
   int64_t low_in_flight() const { return low_in_flight_; }
   int64_t oldest_in_flight() const { return retired_ < next_seq_ ? retired_ : -1; }

@@ -78,6 +78,7 @@ class SyntheticModel:
         if self.ctx is not None:
             self.ctx.close()
             self.ctx = None
+        self.flags = flags
         if slots is not None and slots != self.cfg.slots:
             self.cfg = self.cfg.with_(slots=slots)
             self.cache = None

@@ -4,6 +4,7 @@ attention surrogate -> route -> predict -> expert_ffn -> residual add (predict
 before route when the look-ahead is 0)."""
 from __future__ import annotations
 
+from ._abi import FLAG_NO_PREFETCH
 from .model import SyntheticModel
 
 
@@ -39,6 +40,11 @@ class Stack:
         s = _handle(stream) if self._cuda else stream
         first = self.m.cfg.lookahead == 0
         q = None
+        if predict and not first and not want_q:
+            # one call: the predictor's launches fill the route's wait for its plan
+            order = ctx.route_predict(l, self._x, T, self._ids, self._w, self._s, self._pred, stream=s)
+            ctx.expert_ffn(l, self._x, T, self._ids, self._w, self._s, self._y, stream=s)
+            return order, None
         if predict and first:
             q = ctx.predict(l, self._x, T, self._pred, want_q=want_q, stream=s)
         order = ctx.route(l, self._x, T, self._ids, self._w, self._s, stream=s)
@@ -47,11 +53,15 @@ class Stack:
         ctx.expert_ffn(l, self._x, T, self._ids, self._w, self._s, self._y, stream=s)
         return order, q
 
-    def step(self, h0, predict: bool = True, record=None, stream=None):
+    def step(self, h0, predict: bool | None = None, record=None, stream=None):
         """One step over all layers from residual input h0 [T, H] (fp32, device),
-        on `stream` (default: the current stream, looked up once per step)."""
+        on `stream` (default: the current stream, looked up once per step).
+        predict=None: the predictor runs unless the context was opened without
+        prefetching (then nothing would read its output)."""
         ctx, T = self.m.ctx, self.T
         s = _handle(stream) if self._cuda else stream
+        if predict is None:
+            predict = not getattr(self.m, "flags", 0) & FLAG_NO_PREFETCH
         self.h.copy_(h0)
         for l in range(self.m.cfg.n_layers):
             if record is not None:

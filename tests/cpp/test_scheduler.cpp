@@ -269,6 +269,30 @@ void test_low_queues_behind_high() {
   CHECK(r.pf->low_in_flight() == 0 && r.eng.log.size() == 12);
 }
 
+// pending_bytes(): bytes issued and not yet retired, plus the unissued bytes of
+// queued low-priority chunks (what the link must carry before a new copy).
+void test_pending_bytes() {
+  Rig r(2, 4, 8, 300, 100, 1);  // chunks of 3 sub-copies of 100 bytes
+  r.eng.bw = 100.0;
+  CHECK(r.pf->pending_bytes() == 0);
+  r.pf->assign(0, 0, 0);
+  r.pf->issue_high(0, 0);  // 3 chunks = 900 bytes in flight
+  CHECK(r.pf->pending_bytes() == 900);
+  r.pf->assign(1, 0, 5);
+  r.pf->push_low(1, 0);    // 3 chunks queued, none issued yet
+  CHECK(r.pf->pending_bytes() == 1800);
+  CHECK(r.pf->pump() == 1);  // window 1: one 100-byte sub-copy of the first low chunk
+  CHECK(r.pf->pending_bytes() == 1800);  // moved from queued to in flight
+  r.eng.advance(9.0);        // the misses (9 units) are done, the low sub-copy (10th unit) not yet
+  r.pf->retire();
+  CHECK(r.pf->pending_bytes() == 900);
+  r.pf->purge_low(1);        // early preemption drops the unissued 800 bytes
+  CHECK(r.pf->pending_bytes() == 100);
+  r.eng.advance(20.0);
+  r.pf->retire();
+  CHECK(r.pf->pending_bytes() == 0);
+}
+
 // A high-priority copy waits for at most `window` already-issued low-priority
 // sub-copies (earlier high-priority copies are drained before each miss).
 void test_window_bound() {
@@ -472,6 +496,7 @@ int main(int argc, char** argv) {
   test_example();
   test_whole_expert_low();
   test_low_queues_behind_high();
+  test_pending_bytes();
   test_queue_per_slot();
   test_fills_balance_queues();
   test_head_readers();

@@ -125,8 +125,9 @@ def check_predictor(cfg, model, l, x64, rec):
         assert set(g[t]) == set(ids_o[t]), (l, t)
         if inner[t] > MARGIN:
             assert list(g[t]) == list(ids_o[t])
-    Q, _, _ = opred.vote(g, cfg.n_experts, cfg.slots)
+    Q, votes, _ = opred.vote(g, cfg.n_experts, cfg.slots)
     assert rec.q == Q, (l, rec.q, Q)
+    rec.voted = [e for e in range(cfg.n_experts) if votes[e] > 0]
     return Q
 
 
@@ -212,8 +213,8 @@ def fill_budget(spec_fill_limit: int) -> int:
     return -1 if spec_fill_limit == 0 else (0 if spec_fill_limit < 0 else spec_fill_limit)
 
 
-def check_plan_spec(lc: ocache.LayerCache, Q, gpu_plan, budget: int = -1, predicted: bool = True):
-    entries = lc.spec_plan(Q, budget, predicted)
+def check_plan_spec(lc: ocache.LayerCache, Q, gpu_plan, budget: int = -1, predicted: bool = True, voted=None):
+    entries = lc.spec_plan(Q, budget, predicted, voted)
     assert gpu_plan["expert"] == [e.expert for e in entries]
     assert gpu_plan["slot"] == [e.slot for e in entries]
     assert gpu_plan["flag"] == [int(e.new) for e in entries]
@@ -249,23 +250,28 @@ def check_harness(cfg, model, l, rec):
         assert err.max() <= TOL_F32, (l, err.max())
 
 
-def moe_layer_check(cfg, m, st, l, lcs, x_np, sample=None, predict=True, budget=-1, reorder=True):
+def moe_layer_check(cfg, m, st, l, lcs, x_np, sample=None, predict=True, budget=-1, reorder=True, combined=False):
     """Run predict (optional) -> route -> ffn of layer l on x through the C ABI and check
-    every output against the oracle, replaying the cache plans on lcs."""
+    every output against the oracle, replaying the cache plans on lcs.  combined: route
+    and predict in one promoe_route_predict call (Q then read from the spec plan)."""
     import torch
     from synth import model as sm
     st.x.copy_(torch.from_numpy(x_np.view(np.int16) if x_np.dtype == np.uint16 else x_np).cuda())
-    order, q = st.moe_layer(l, predict=predict, want_q=predict)
+    order, q = st.moe_layer(l, predict=predict, want_q=predict and not combined)
+    tgt = sm.predictor_target(cfg, l)
+    if combined and predict and tgt is not None and m.np_pred[l] is not None:
+        q = m.ctx.last_plan(tgt, 0)["expert"]
     rec = LayerRecord()
     rec.x = x_np
     rec.ids, rec.w, rec.s, rec.y = (to_np(t).copy() for t in (st.ids, st.w, st.s, st.y))
     rec.pred_ids = to_np(st.pred_ids).copy()
     rec.order, rec.q = order, q
     x64 = f64(x_np, cfg.dtype)
-    tgt = sm.predictor_target(cfg, l)
     if predict and tgt is not None and m.np_pred[l] is not None and lcs is not None:
         Q = check_predictor(cfg, m, l, x64, rec)
-        check_plan_spec(lcs[tgt], Q, m.ctx.last_plan(tgt, 0), budget)
+        plan = m.ctx.last_plan(tgt, 0)
+        # budget None: the budget the plan itself records (timing-dependent budgets)
+        check_plan_spec(lcs[tgt], Q, plan, plan["fill_budget"] if budget is None else budget, voted=rec.voted)
     g_ids, w_ref, s_ref, clear = check_route(cfg, m, l, x64, rec)
     if lcs is not None:
         check_plan_precise(lcs[l], g_ids, m.ctx.last_plan(l, 1), reorder)

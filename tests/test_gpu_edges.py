@@ -17,7 +17,7 @@ from oracle import cache as ocache  # noqa: E402
 from synth import configs, model as sm  # noqa: E402
 from synth.configs import Workload  # noqa: E402
 
-from paper_2410_22134_amd import ABLATION, FLAG_NO_PREFETCH, FLAG_NO_REORDER, FLAG_STATIC  # noqa: E402
+from paper_2410_22134_amd import ABLATION, FLAG_FILL_BY_DEADLINE, FLAG_NO_PREFETCH, FLAG_NO_REORDER, FLAG_STATIC  # noqa: E402,E501
 from paper_2410_22134_amd import PRIO_HIGH, PRIO_LOW, PromoeError  # noqa: E402
 from paper_2410_22134_amd import _abi  # noqa: E402
 from paper_2410_22134_amd.model import SyntheticModel  # noqa: E402
@@ -117,6 +117,32 @@ def test_spec_fill_limit(limit, T):
         pu.check_counters(m, lcs)
         if limit < 0:
             assert m.ctx.stats(1)["spec_issued"] == 0
+    finally:
+        m.close()
+
+
+@pytest.mark.parametrize("limit,T", [(0, 1), (2, 4), (1, 77)])
+def test_fill_by_deadline(limit, T):
+    # Speculative fills budgeted by the copy time left before the target route:
+    # each plan records the budget it was given (host timing), and the oracle
+    # replays every plan with that budget; outputs, plans and counters exact.
+    cfg = SMALL
+    _log("fill by deadline, limit", limit, "T", T)
+    m = SyntheticModel(cfg, max_tokens=T, flags=FLAG_FILL_BY_DEADLINE, spec_fill_limit=limit)
+    try:
+        st = Stack(m, T)
+        lcs = {l: ocache.LayerCache(cfg.n_experts, cfg.slots) for l in range(cfg.n_layers)}
+        budgets = []
+        for step in range(6):
+            for l in range(cfg.n_layers):
+                pu.moe_layer_check(cfg, m, st, l, lcs, sm.layer_input(cfg, l, T, tag=1400 + step), budget=None)
+                tgt = sm.predictor_target(cfg, l)
+                if tgt is not None:
+                    budgets.append(m.ctx.last_plan(tgt, 0)["fill_budget"])
+        pu.check_counters(m, lcs)
+        assert budgets[0] == 0                      # no route interval measured yet: no fills
+        cap = limit if limit > 0 else 64
+        assert all(0 <= b <= cap for b in budgets), budgets
     finally:
         m.close()
 
@@ -319,6 +345,9 @@ def test_error_returns():
             ctx.route(1, st.x, 1, st.ids, st.w, st.s)          # layer out of range
         assert e.value.code == -1
         with pytest.raises(PromoeError) as e:
+            ctx.route_predict(0, st.x, 1, st.ids, st.w, st.s, st.pred_ids)  # look-ahead 0
+        assert e.value.code == -1
+        with pytest.raises(PromoeError) as e:
             ctx.expert_ffn(0, st.x, 1, st.ids, st.w, st.s, st.y)  # no route before
         assert e.value.code == -4
         with pytest.raises(PromoeError) as e:
@@ -358,3 +387,22 @@ def test_error_returns():
     assert _abi.lib().promoe_create(ctypes.byref(c), buf.data_ptr(), buf.numel(), ctypes.byref(h)) == -5
     c.weight_format, c.inter, c.pred_hidden = _abi.WEIGHTS_DENSE, 512, 60   # predictor width % 8
     assert _abi.lib().promoe_create(ctypes.byref(c), buf.data_ptr(), buf.numel(), ctypes.byref(h)) == -5
+
+
+@pytest.mark.parametrize("fmt", ["dense", "int4"])
+@pytest.mark.parametrize("T", [1, 4, 77])
+def test_route_predict_in_one_call(T, fmt):
+    # promoe_route_predict is promoe_route then promoe_predict: per-token predicted
+    # ids, both plans, the counters and every output as the oracle's
+    cfg = SMALL.with_(weight_format=fmt)
+    _log("route_predict T", T, fmt)
+    m = SyntheticModel(cfg, max_tokens=T)
+    try:
+        st = Stack(m, T)
+        lcs = {l: ocache.LayerCache(cfg.n_experts, cfg.slots) for l in range(cfg.n_layers)}
+        for step in range(3):
+            for l in range(cfg.n_layers):
+                pu.moe_layer_check(cfg, m, st, l, lcs, sm.layer_input(cfg, l, T, tag=800 + step), combined=True)
+        pu.check_counters(m, lcs)
+    finally:
+        m.close()

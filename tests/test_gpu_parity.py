@@ -38,7 +38,7 @@ def _moe_layer_check(cfg, m, st, l, lcs, x_np, sample=None):
     tgt = sm.predictor_target(cfg, l)
     if tgt is not None and m.np_pred[l] is not None:
         Q = pu.check_predictor(cfg, m, l, x64, rec)
-        pu.check_plan_spec(lcs[tgt], Q, m.ctx.last_plan(tgt, 0))
+        pu.check_plan_spec(lcs[tgt], Q, m.ctx.last_plan(tgt, 0), voted=rec.voted)
     g_ids, w_ref, s_ref, clear = pu.check_route(cfg, m, l, x64, rec)
     pu.check_plan_precise(lcs[l], g_ids, m.ctx.last_plan(l, 1))
     assert rec.order == m.ctx.last_plan(l, 1)["expert"]
@@ -126,7 +126,7 @@ def test_stack_layers_full_shape(name, base, T, steps):
                 x64 = pu.f64(rec.x, cfg.dtype)
                 if rec.spec_plan is not None:
                     Q = pu.check_predictor(cfg, m, l, x64, rec)
-                    pu.check_plan_spec(lcs[sm.predictor_target(cfg, l)], Q, rec.spec_plan)
+                    pu.check_plan_spec(lcs[sm.predictor_target(cfg, l)], Q, rec.spec_plan, voted=rec.voted)
                 g_ids, w_ref, s_ref, _ = pu.check_route(cfg, m, l, x64, rec)
                 pu.check_plan_precise(lcs[l], g_ids, rec.precise_plan)
                 pu.check_ffn(cfg, m, l, x64, g_ids, w_ref, s_ref, rec.y)
@@ -220,7 +220,7 @@ def test_trained_predictor_plans_and_accuracy_counters():
                 x64 = pu.f64(rec.x, cfg.dtype)
                 if rec.spec_plan is not None:
                     Q = pu.check_predictor(cfg, m, l, x64, rec)
-                    pu.check_plan_spec(lcs[sm.predictor_target(cfg, l)], Q, rec.spec_plan)
+                    pu.check_plan_spec(lcs[sm.predictor_target(cfg, l)], Q, rec.spec_plan, voted=rec.voted)
                 g_ids, w_ref, s_ref, _ = pu.check_route(cfg, m, l, x64, rec)
                 pu.check_plan_precise(lcs[l], g_ids, rec.precise_plan)
                 pu.check_ffn(cfg, m, l, x64, g_ids, w_ref, s_ref, rec.y)

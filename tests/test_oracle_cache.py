@@ -283,3 +283,53 @@ def test_streaming_more_experts_than_slots():
     assert [x.slot for x in entries] == [0, 1, 0, 1, 0, 1, 0, 1]
     assert [x.after for x in entries] == [-1, -1, 0, 1, 2, 3, 4, 5]
     assert lc.count["miss"] == 6 and lc.count["hit"] == 2
+
+
+def test_spec_touches_its_list_before_filling():
+    # Alg. 2 counts the list's hits while pushing it; Alg. 1 replaces a slot only
+    # when the worker starts a copy.  Warm 0, 1 (0 the least recent): the list
+    # [2, 0] touches 0 first, so filling 2 evicts 1, not the listed 0.
+    lc = cache.LayerCache(4, 2)
+    e = lc.spec_plan([2, 0])
+    assert [(x.expert, x.slot, x.new, x.victim) for x in e] == [(2, 1, True, 1), (0, 0, False, -1)]
+    assert lc.resident() == {0, 2} and lc.count["evict"] == 1
+    b = brute.NaiveLRU(4, 2)
+    assert b.spec([2, 0]) == [(2, 1, True), (0, 0, False)]
+
+
+def test_spec_never_evicts_a_predicted_expert():
+    # every resident expert has a vote: the fill is skipped, nothing moves
+    lc = cache.LayerCache(6, 3)
+    e = lc.spec_plan([3], voted=[0, 1, 2, 3])
+    assert e[0].skipped and e[0].slot == -1 and lc.count["spec_issued"] == 0 and lc.resident() == {0, 1, 2}
+    # one unvoted resident (2): it is the victim, though 0 is older
+    e = lc.spec_plan([3, 4], voted=[0, 1, 3, 4])
+    assert (e[0].slot, e[0].victim, e[0].new) == (2, 2, True) and e[1].skipped
+    assert lc.resident() == {0, 1, 3}
+    # a free slot is always taken
+    f = cache.LayerCache(6, 3, warm=False)
+    assert f.spec_plan([5], voted=[5])[0].slot == 0
+
+
+def test_random_replays_with_votes():
+    rng = np.random.default_rng(21)
+    for trial in range(300):
+        E = int(rng.integers(2, 9))
+        C = int(rng.integers(1, E + 1))
+        a, b = cache.LayerCache(E, C), brute.NaiveLRU(E, C)
+        for _ in range(int(rng.integers(1, 12))):
+            if rng.random() < 0.5:
+                Q = rng.choice(E, size=int(rng.integers(1, C + 1)), replace=False).tolist()
+                voted = sorted(set(Q) | set(rng.choice(E, size=int(rng.integers(0, E + 1))).tolist()))
+                budget = int(rng.integers(-1, 3))
+                ea = a.spec_plan(Q, budget, voted=voted)
+                eb = b.spec(Q, budget, voted=voted)
+                assert [(x.expert, x.slot, x.new) for x in ea] == eb
+                # no fill evicts a voted expert or a member of the list
+                assert all(x.victim not in voted for x in ea if x.new)
+            else:
+                P = rng.choice(E, size=int(rng.integers(1, E + 1)), replace=False).tolist()
+                order, entries = a.precise_plan(P)
+                assert order == b.precise(P)[0]
+            _check_invariants(a)
+            assert a.count == b.c

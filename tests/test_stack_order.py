@@ -23,6 +23,10 @@ class _Ctx:
         self.calls.append(("route", l))
         return []
 
+    def route_predict(self, l, *a, **k):
+        self.calls += [("route", l), ("predict", l)]
+        return []
+
     def expert_ffn(self, l, *a, **k):
         self.calls.append(("ffn", l))
 
@@ -33,8 +37,8 @@ class _Ctx:
         self.calls.append(("res", None))
 
 
-def _stack(cfg, T=1):
-    m = types.SimpleNamespace(cfg=cfg, ctx=_Ctx(), device="cpu")
+def _stack(cfg, T=1, flags=0):
+    m = types.SimpleNamespace(cfg=cfg, ctx=_Ctx(), device="cpu", flags=flags)
     return Stack(m, T), m.ctx
 
 
@@ -68,3 +72,14 @@ def test_no_prediction_when_disabled():
     st, ctx = _stack(cfg)
     st.moe_layer(1, predict=False)
     assert ctx.calls == [("route", 1), ("ffn", 1)]
+
+
+def test_no_prediction_without_prefetching():
+    # a context opened without prefetching reads no prediction: the step skips it
+    from paper_2410_22134_amd import FLAG_NO_PREFETCH
+    cfg = configs.C2.with_(n_layers=2)
+    st, ctx = _stack(cfg, flags=FLAG_NO_PREFETCH)
+    st.step(torch.zeros(1, cfg.hidden))
+    assert not [c for c in ctx.calls if c[0] == "predict"]
+    st.step(torch.zeros(1, cfg.hidden), predict=True)
+    assert [c for c in ctx.calls if c[0] == "predict"] == [("predict", 0), ("predict", 1)]
