@@ -144,6 +144,21 @@ struct PlanArgs {
   int32_t* d_npos;       // [1] precise plan: resident positions (reordered: they come first)
 };
 
+// Predictor tail and spec plan in one block (steps of at most kFusedPredMaxT
+// tokens, predictor hidden width at most kFusedPredMaxHidden, a multiple of 8).
+constexpr int kFusedPredMaxT = 8;
+constexpr int kFusedPredMaxHidden = 1024;
+struct PredictPlanArgs {
+  PlanArgs plan;        // plan.ids: the predicted-ids output (marks a prediction)
+  const float* h;       // [T x ldh] first-layer outputs before relu, or the logits when Ph == 0
+  int ldh;
+  int Ph;               // hidden width (0: one-layer predictor)
+  const void* w2;       // [E x Ph], 16-byte aligned rows
+  int w2_bf16;          // 1: bf16 weights, 0: fp32
+  int32_t* pred_ids;    // [T x k] out
+};
+void launch_predict_plan(const PredictPlanArgs& p, hipStream_t s);
+
 // Expand 4-bit experts into dense bf16 [Wg | Wu | Wd] copies (the MFMA GEMM's
 // operand type: each weight (code - 8) * scale is rounded to bf16).
 struct DequantArgs {

@@ -144,16 +144,26 @@ __device__ __forceinline__ int fill_slot(const PlanArgs& a, int lane, WaveState&
 }
 
 // ============================================================ spec plan
-__global__ __launch_bounds__(256) void k_plan_spec(PlanArgs a) {
-  __shared__ int votes[kMaxE], best[kMaxE], Q[kMaxE];
-  __shared__ int nq;
+struct SpecLds {
+  int votes[kMaxE], best[kMaxE], Q[kMaxE];
+  int nq;
+};
+
+// The spec plan over the predicted ids `ids` [T x k] (global or LDS; a.ids
+// non-null marks the plan as a prediction), or over the caller's list in the
+// record when a.ids is null.  All 256 threads of the block enter.
+__device__ __forceinline__ void plan_spec_body(const PlanArgs& a, const int32_t* ids, SpecLds& sh) {
+  int* votes = sh.votes;
+  int* best = sh.best;
+  int* Q = sh.Q;
+  int& nq = sh.nq;
   const int tid = threadIdx.x, lane = tid % kWave;
   if (tid < kMaxE) { votes[tid] = 0; best[tid] = kMaxK; }
   __syncthreads();
   if (a.ids) {
     const int n = a.T * a.k;
     for (int i = tid; i < n; i += 256) {
-      const int e = a.ids[i];
+      const int e = ids[i];
       atomicAdd(&votes[e], 1);
       atomicMin(&best[e], i % a.k);
     }
@@ -241,6 +251,91 @@ __global__ __launch_bounds__(256) void k_plan_spec(PlanArgs a) {
     __threadfence_system();
     rec->done = 1;
   }
+}
+
+__global__ __launch_bounds__(256) void k_plan_spec(PlanArgs a) {
+  __shared__ SpecLds sh;
+  plan_spec_body(a, a.ids, sh);
+}
+
+// ============================================================ predictor tail + spec plan, one block
+// For a step of at most kFusedPredMaxT tokens: the predictor's second layer
+// q[t][e] = W2[e] . relu(h[t]) (fp32 accumulation; or q = h when the
+// predictor is one layer), each token's top-k by (q desc, id asc) as k_topk
+// orders them, written out and kept in LDS, then the spec plan of the vote.
+__global__ __launch_bounds__(256) void k_predict_plan(PredictPlanArgs p) {
+  __shared__ float hs[kFusedPredMaxT * kFusedPredMaxHidden];
+  __shared__ float qs[kFusedPredMaxT * kMaxE];
+  __shared__ int32_t ids_l[kFusedPredMaxT * kMaxK];
+  __shared__ SpecLds sh;
+  const PlanArgs& a = p.plan;
+  const int tid = threadIdx.x, lane = tid % kWave, wv = tid / kWave;
+  const int T = a.T, E = a.E, k = a.k, Ph = p.Ph;
+  if (Ph > 0) {
+    for (int i = tid; i < T * Ph; i += 256) {
+      const int t = i / Ph, j = i - t * Ph;
+      hs[i] = fmaxf(p.h[(size_t)t * p.ldh + j], 0.0f);
+    }
+    __syncthreads();
+    const int n8 = Ph / 8;  // Ph % 8 == 0
+    for (int e = wv; e < E; e += 4) {
+      float acc[kFusedPredMaxT];
+#pragma unroll
+      for (int t = 0; t < kFusedPredMaxT; ++t) acc[t] = 0.0f;
+      for (int j8 = lane; j8 < n8; j8 += kWave) {
+        float wj[8];
+        if (p.w2_bf16) {
+          const uint4 u = reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(p.w2) + (size_t)e * Ph)[j8];
+          const uint32_t q4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            wj[2 * i] = __uint_as_float(q4[i] << 16);
+            wj[2 * i + 1] = __uint_as_float(q4[i] & 0xFFFF0000u);
+          }
+        } else {
+          const float* w = static_cast<const float*>(p.w2) + (size_t)e * Ph + j8 * 8;
+#pragma unroll
+          for (int i = 0; i < 8; ++i) wj[i] = w[i];
+        }
+#pragma unroll
+        for (int t = 0; t < kFusedPredMaxT; ++t) {
+          if (t < T) {
+            const float* h = hs + t * Ph + j8 * 8;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) acc[t] = fmaf(wj[i], h[i], acc[t]);
+          }
+        }
+      }
+#pragma unroll
+      for (int t = 0; t < kFusedPredMaxT; ++t) {
+        if (t < T) {
+          const float v = wave_sum(acc[t]);
+          if (lane == 0) qs[t * kMaxE + e] = v;
+        }
+      }
+    }
+  } else {
+    for (int i = tid; i < T * E; i += 256) {
+      const int t = i / E, e = i - t * E;
+      qs[t * kMaxE + e] = p.h[(size_t)t * p.ldh + e];
+    }
+  }
+  __syncthreads();
+  for (int t = wv; t < T; t += 4) {
+    const bool valid = lane < E;
+    uint64_t key = valid ? (((uint64_t)f32_order_key(qs[t * kMaxE + lane]) << 32) | (uint32_t)(63 - lane)) : 0ull;
+    for (int r = 0; r < k; ++r) {
+      const uint64_t kmax = wave_max_u64(key);
+      const int e = 63 - (int)(uint32_t)(kmax & 0xFFFFFFFFu);
+      if (lane == e) key = 0ull;
+      if (lane == 0) {
+        ids_l[t * k + r] = e;
+        p.pred_ids[t * k + r] = e;
+      }
+    }
+  }
+  __syncthreads();
+  plan_spec_body(a, ids_l, sh);
 }
 
 // ============================================================ precise plan + permutation
@@ -404,6 +499,7 @@ void launch_topk(const TopkArgs& a, hipStream_t s) {
   k_topk<<<(a.T + 3) / 4, 256, 0, s>>>(a);
 }
 void launch_plan_spec(const PlanArgs& a, hipStream_t s) { k_plan_spec<<<1, 256, 0, s>>>(a); }
+void launch_predict_plan(const PredictPlanArgs& p, hipStream_t s) { k_predict_plan<<<1, 256, 0, s>>>(p); }
 void launch_plan_precise(const PlanArgs& a, hipStream_t s) { k_plan_precise<<<1, 256, 0, s>>>(a); }
 void launch_state_init(CacheState st, int L, int C, int E, hipStream_t s) {
   int n = L * (C > E ? C : E);

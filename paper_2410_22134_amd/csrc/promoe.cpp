@@ -887,6 +887,8 @@ int promoe_set_initial_cache(promoe_ctx* c, int layer, const int32_t* h_experts,
 
 static int predict_tail(promoe_ctx* c, int layer, int target, int T, int32_t* d_pred_ids, int32_t* h_q,
                         int32_t* n_q, hipStream_t s, int64_t* rec_out);
+static int finish_spec(promoe_ctx* c, int target, int64_t r, hipStream_t s, int32_t* h_q, int32_t* n_q,
+                       int64_t* rec_out);
 
 // The host waits for the spec plan that ends a prediction of promoe_route_predict:
 // the side stream's kernels before it are then complete too.
@@ -987,6 +989,27 @@ static int predict_tail(promoe_ctx* c, int layer, int target, int T, int32_t* d_
   int rc;
   *rec_out = -1;
   int32_t* pids = d_pred_ids ? d_pred_ids : c->d_pred_ids;
+  const bool plan = !(c->cfg.flags & PROMOE_FLAG_NO_PREFETCH);
+  // Decode-sized steps: the predictor's second layer, top-k and the spec plan
+  // in one launch.
+  const bool fused = plan && T <= kFusedPredMaxT && c->Ph <= kFusedPredMaxHidden &&
+                     (c->Ph == 0 || reinterpret_cast<uintptr_t>(c->lw[layer].pw2) % 16 == 0);
+  if (fused) {
+    int64_t r;
+    rc = new_record(c, 0, PROMOE_PRIO_LOW, &r);
+    if (rc) return rc;
+    PredictPlanArgs pp{};
+    pp.plan = plan_args(c, target, pids, T, r);
+    if (c->cfg.flags & PROMOE_FLAG_FILL_BY_DEADLINE) pp.plan.fill_budget = deadline_fill_budget(c);
+    pp.h = c->d_logits + c->pred_col;
+    pp.ldh = c->ld_logits;
+    pp.Ph = c->Ph;
+    pp.w2 = c->lw[layer].pw2;
+    pp.w2_bf16 = c->dt == PROMOE_BF16;
+    pp.pred_ids = pids;
+    launch_predict_plan(pp, s);
+    return finish_spec(c, target, r, s, h_q, n_q, rec_out);
+  }
   TopkArgs tk{};
   if (c->Ph > 0) {
     RowsArgs a{};
@@ -1015,13 +1038,20 @@ static int predict_tail(promoe_ctx* c, int layer, int target, int T, int32_t* d_
   tk.sgate_col = -1;
   launch_topk(tk, s);
   LAUNCHCHK("predictor");
-  if (c->cfg.flags & PROMOE_FLAG_NO_PREFETCH) return PROMOE_OK;
+  if (!plan) return PROMOE_OK;
   int64_t r;
   rc = new_record(c, 0, PROMOE_PRIO_LOW, &r);
   if (rc) return rc;
   PlanArgs pa = plan_args(c, target, pids, T, r);
   if (c->cfg.flags & PROMOE_FLAG_FILL_BY_DEADLINE) pa.fill_budget = deadline_fill_budget(c);
   launch_plan_spec(pa, s);
+  return finish_spec(c, target, r, s, h_q, n_q, rec_out);
+}
+
+// After a spec plan's launch on s: its record's event, publication, and the
+// optional host copy of the list.
+static int finish_spec(promoe_ctx* c, int target, int64_t r, hipStream_t s, int32_t* h_q, int32_t* n_q,
+                       int64_t* rec_out) {
   hipError_t le = hipGetLastError();
   if (le == hipSuccess) le = hipEventRecord(c->rec_ev[r % kRecRing], s);
   publish(c, r);
