@@ -367,9 +367,16 @@ __global__ __launch_bounds__(kThreads) void k_ffn_down(FfnArgs a) {
 // reduction length K is R x K/2 bytes of codes (two per byte, even k in the low
 // nibble) followed by R x K/128 bf16 scales; weight (r, k) = (code - 8) *
 // scale[r][k / 128].  A lane takes 16-byte pieces of a row (32 weights, a
-// quarter of a scale group); per piece and token it forms sum(code * x) and
-// sum(x) and adds scale * (sum(code * x) - 8 sum(x)) to the row's accumulator.
-// Codes go to floats once per row and piece and serve every token of the group.
+// quarter of a scale group); per piece and token it forms sum((128 + code) x)
+// and sum(x) with bf16 dot2 instructions (128 + code is exact in bf16) and adds
+// scale * (sum((128 + code) x) - 136 sum(x)) to the row's accumulator.
+
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+
+// c + a.lo * b.lo + a.hi * b.hi over two bf16 pairs packed in 32-bit words.
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), c, false);
+}
 
 struct Q4Row {
   const uint8_t* codes;  // row start in the code block
@@ -383,66 +390,85 @@ __device__ __forceinline__ Q4Row q4_row(const uint8_t* mat, int rows, int K, int
   return q;
 }
 
-// acc[r][m] += <row r, xs[m]> over K for R rows of one matrix.
-template <int R, int MT>
+// acc[r][m] += <row r, xs[m]> over K for R rows of one matrix; each lane has
+// NCH pieces of every row (and the matching token pieces) in flight at once.
+template <int R, int MT, int NCH>
 __device__ __forceinline__ void wave_rows_dot_q4(const Q4Row (&rows)[R], const bool (&rv)[R],
                                                  const bf16_t* const (&xs)[MT], int mt, int K, int lane,
                                                  float (&acc)[R][MT]) {
   const int np = K / 32;  // 16-byte pieces per row
-  for (int c = lane; c < np; c += kWave) {
-    uint4 w[R];
-    float sc[R];
+  for (int cb = 0; cb < np; cb += kWave * NCH) {
+    uint4 wq[R][NCH];
+    float scq[R][NCH];
+    uint4 xq[MT][NCH][4];
 #pragma unroll
-    for (int r = 0; r < R; ++r) {
-      w[r] = rv[r] ? ld16_stream(rows[r].codes + (size_t)c * 16) : make_uint4(0x88888888u, 0x88888888u, 0x88888888u,
-                                                                             0x88888888u);
-      sc[r] = rv[r] ? bf16_to_f32(rows[r].scales[c / 4]) : 0.0f;
-    }
-    // token pieces: 32 bf16 = 16 words; word j holds elements 2j (low half) and 2j+1
-    uint32_t xw[MT][16];
-    float sx[MT];
+    for (int u = 0; u < NCH; ++u) {
+      const int c = cb + lane + u * kWave;
+      const bool in = c < np;
 #pragma unroll
-    for (int m = 0; m < MT; ++m) {
-      const uint4* xp = reinterpret_cast<const uint4*>(xs[m] + (size_t)c * 32);
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const uint4 u = (m < mt) ? xp[v] : make_uint4(0, 0, 0, 0);
-        xw[m][4 * v] = u.x; xw[m][4 * v + 1] = u.y; xw[m][4 * v + 2] = u.z; xw[m][4 * v + 3] = u.w;
-      }
-      float s = 0.0f;
-#pragma unroll
-      for (int j = 0; j < 16; ++j) s += __uint_as_float(xw[m][j] << 16) + __uint_as_float(xw[m][j] & 0xFFFF0000u);
-      sx[m] = s;
-    }
-#pragma unroll
-    for (int r = 0; r < R; ++r) {
-      const uint32_t ww[4] = {w[r].x, w[r].y, w[r].z, w[r].w};
-      float cf[32];  // codes of elements 0..31 of the piece
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const uint32_t lo = ww[i] & 0x0F0F0F0Fu, hi = (ww[i] >> 4) & 0x0F0F0F0Fu;
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          cf[8 * i + 2 * b] = (float)((lo >> (8 * b)) & 0xFFu);
-          cf[8 * i + 2 * b + 1] = (float)((hi >> (8 * b)) & 0xFFu);
-        }
+      for (int r = 0; r < R; ++r) {
+        // a piece past the row, or of a row past the job: code 8 (weight 0), scale 0
+        wq[r][u] = (in && rv[r]) ? ld16_stream(rows[r].codes + (size_t)c * 16)
+                                 : make_uint4(0x88888888u, 0x88888888u, 0x88888888u, 0x88888888u);
+        scq[r][u] = (in && rv[r]) ? bf16_to_f32(rows[r].scales[c / 4]) : 0.0f;
       }
 #pragma unroll
       for (int m = 0; m < MT; ++m) {
-        float t = 0.0f;
+        const uint4* xp = reinterpret_cast<const uint4*>(xs[m] + (size_t)c * 32);
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          t = fmaf(cf[2 * j], __uint_as_float(xw[m][j] << 16), t);
-          t = fmaf(cf[2 * j + 1], __uint_as_float(xw[m][j] & 0xFFFF0000u), t);
+        for (int v = 0; v < 4; ++v) xq[m][u][v] = (in && m < mt) ? xp[v] : make_uint4(0, 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < NCH; ++u) {
+      // token pieces: 32 bf16 = 16 words; word j holds elements 2j (low half)
+      // and 2j+1; sum(x) by dot2 against (1, 1)
+      uint32_t xw[MT][16];
+      float sx[MT];
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const uint4 q = xq[m][u][v];
+          xw[m][4 * v] = q.x; xw[m][4 * v + 1] = q.y; xw[m][4 * v + 2] = q.z; xw[m][4 * v + 3] = q.w;
         }
-        acc[r][m] = fmaf(sc[r], t - 8.0f * sx[m], acc[r][m]);
+        float s = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 16; ++j) s = dot2_bf16(0x3F803F80u, xw[m][j], s);
+        sx[m] = s;
+      }
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const uint4 wr = wq[r][u];
+        const uint32_t ww[4] = {wr.x, wr.y, wr.z, wr.w};
+        float t[MT];
+#pragma unroll
+        for (int m = 0; m < MT; ++m) t[m] = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          // byte b of a code word holds elements 2b (low nibble) and 2b+1: the
+          // bf16 pair (128 + lo, 128 + hi), exact (0x4300 is 128, the mantissa
+          // step there is 1)
+          const uint32_t cw = ww[i];
+          const uint32_t pr[4] = {0x43004300u | (cw & 0xFu) | ((cw & 0xF0u) << 12),
+                                  0x43004300u | ((cw >> 8) & 0xFu) | ((cw & 0xF000u) << 4),
+                                  0x43004300u | ((cw >> 16) & 0xFu) | ((cw >> 4) & 0xF0000u),
+                                  0x43004300u | ((cw >> 24) & 0xFu) | ((cw >> 12) & 0xF0000u)};
+#pragma unroll
+          for (int m = 0; m < MT; ++m)
+#pragma unroll
+            for (int b = 0; b < 4; ++b) t[m] = dot2_bf16(pr[b], xw[m][4 * i + b], t[m]);
+        }
+        // sum((128 + code) x) - 136 sum(x) = sum((code - 8) x)
+#pragma unroll
+        for (int m = 0; m < MT; ++m) acc[r][m] = fmaf(scq[r][u], t[m] - 136.0f * sx[m], acc[r][m]);
       }
     }
   }
 }
 
 // pass 1, 4-bit experts: act[q][i] for the wave's RW rows i (gate rows, up rows)
-template <int MT, int RW>
+template <int MT, int RW, int NCH>
 __global__ __launch_bounds__(kThreads) void k_ffn_gateup_q4(FfnArgs a) {
   constexpr int R = 2 * RW;
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
@@ -481,7 +507,7 @@ __global__ __launch_bounds__(kThreads) void k_ffn_gateup_q4(FfnArgs a) {
     for (int r = 0; r < R; ++r)
 #pragma unroll
       for (int m = 0; m < MT; ++m) acc[r][m] = 0.0f;
-    wave_rows_dot_q4<R, MT>(rows, rv, xs, mt, H, lane, acc);
+    wave_rows_dot_q4<R, MT, NCH>(rows, rv, xs, mt, H, lane, acc);
 #pragma unroll
     for (int r = 0; r < R; ++r)
 #pragma unroll
@@ -500,7 +526,7 @@ __global__ __launch_bounds__(kThreads) void k_ffn_gateup_q4(FfnArgs a) {
 }
 
 // pass 2, 4-bit experts: Y[pair][n] = Wd[n] . act[q] for the wave's RW rows n
-template <int MT, int RW>
+template <int MT, int RW, int NCH>
 __global__ __launch_bounds__(kThreads) void k_ffn_down_q4(FfnArgs a) {
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
   const Job<bf16_t> jb = job_of<bf16_t>(a, a.hidden);
@@ -531,7 +557,7 @@ __global__ __launch_bounds__(kThreads) void k_ffn_down_q4(FfnArgs a) {
     for (int r = 0; r < RW; ++r)
 #pragma unroll
       for (int m = 0; m < MT; ++m) acc[r][m] = 0.0f;
-    wave_rows_dot_q4<RW, MT>(rows, rv, xs, mt, I, lane, acc);
+    wave_rows_dot_q4<RW, MT, NCH>(rows, rv, xs, mt, I, lane, acc);
 #pragma unroll
     for (int r = 0; r < RW; ++r)
 #pragma unroll
@@ -675,6 +701,16 @@ static int gemv_jobs(const FfnArgs& in, int pass, FfnArgs& a) {
 
 // 4-bit experts (routed jobs only): rows per wave shrink as the token group grows,
 // keeping registers bounded (token pieces MT x 16 words, accumulators R x MT).
+// Pieces in flight per lane and row: as many as cover the row in one round of
+// the wave (up to 4) for one or two tokens, one for larger token groups.
+template <int MT, int NCH>
+static void ffn_launch_q4(const FfnArgs& a, int pass, const dim3& grid, hipStream_t s, hipEvent_t ev0,
+                          hipEvent_t ev1) {
+  constexpr int RWG = MT <= 2 ? 2 : (MT == 4 ? 2 : 1), RWD = 2 * RWG;
+  if (pass == 0) hipExtLaunchKernelGGL((k_ffn_gateup_q4<MT, RWG, NCH>), grid, dim3(kThreads), 0, s, ev0, ev1, 0, a);
+  else hipExtLaunchKernelGGL((k_ffn_down_q4<MT, RWD, NCH>), grid, dim3(kThreads), 0, s, ev0, ev1, 0, a);
+}
+
 template <int MT>
 static void ffn_dispatch_q4(const FfnArgs& in, int pass, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   constexpr int RWG = MT <= 2 ? 2 : (MT == 4 ? 2 : 1), RWD = 2 * RWG;
@@ -682,8 +718,7 @@ static void ffn_dispatch_q4(const FfnArgs& in, int pass, hipStream_t s, hipEvent
   FfnArgs a;
   if (gemv_jobs(in, pass, a) == 0 || a.piece_rows <= 0) return;
   const dim3 grid((a.piece_rows + rows_per_block - 1) / rows_per_block, a.n_jobs);
-  if (pass == 0) hipExtLaunchKernelGGL(k_ffn_gateup_q4<MT, RWG>, grid, dim3(kThreads), 0, s, ev0, ev1, 0, a);
-  else hipExtLaunchKernelGGL(k_ffn_down_q4<MT, RWD>, grid, dim3(kThreads), 0, s, ev0, ev1, 0, a);
+  ffn_launch_q4<MT, 1>(a, pass, grid, s, ev0, ev1);
 }
 
 // One launch of pass `pass` with NCH 16-byte chunks per lane and row in flight.

@@ -255,11 +255,13 @@ def test_predict_before_or_after_route(T):
                     got.append((order, *(t.cpu().numpy().copy() for t in (st.ids, st.w, st.s, st.pred_ids, st.y)),
                                 m.ctx.last_plan(l, 1)["slot"]))
             runs.append(got)
-        for other in runs[1:]:
-            for a, b in zip(runs[0], other):
-                assert a[0] == b[0] and a[6] == b[6]
-                for u, v in zip(a[1:6], b[1:6]):
-                    assert np.array_equal(u, v)
+        names = ("ids", "w", "s", "pred_ids", "y")
+        for mode, other in zip(("after_route", "after_ffn"), runs[1:]):
+            for i, (a, b) in enumerate(zip(runs[0], other)):
+                where = (mode, "step", i // cfg.n_layers, "layer", i % cfg.n_layers)
+                assert a[0] == b[0] and a[6] == b[6], where
+                for name, u, v in zip(names, a[1:6], b[1:6]):
+                    assert np.array_equal(u, v), (where, name, int((u != v).sum()))
     finally:
         m.close()
 
