@@ -360,6 +360,21 @@ int promoe_attn_surrogate(promoe_ctx* ctx, int layer, float* d_h, int T, void* d
 /* d_h [T x H] fp32 += d_y [T x H] (config dtype). */
 int promoe_residual_add(promoe_ctx* ctx, float* d_h, const void* d_y, int T, void* stream);
 
+/* One step of the whole layer stack in one call, the loop a caller would
+ * otherwise drive layer by layer: for each layer l, promoe_attn_surrogate(l)
+ * into d_x, then (predict != 0) the prediction and the route as the layer loop
+ * orders them (look-ahead 0: promoe_predict then promoe_route; else
+ * promoe_route_predict), or the route alone (predict == 0), then
+ * promoe_expert_ffn into d_y and promoe_residual_add(d_h, d_y).  The buffers
+ * are the caller's and those calls' (d_x, d_y [T x H] dtype; d_ids, d_w [T x
+ * k]; d_shared_scale [T], may be NULL without a gated shared expert;
+ * d_pred_ids [T x k] or NULL); on return d_h holds the stack's output and the
+ * other buffers the last layer's values.  Results equal those of the separate
+ * calls made in that order; the first failing call's error is returned and
+ * the remaining layers are not run. */
+int promoe_stack_step(promoe_ctx* ctx, float* d_h, int T, void* d_x, void* d_y, int32_t* d_ids, float* d_w,
+                      float* d_shared_scale, int32_t* d_pred_ids, int predict, void* stream);
+
 /* ---- measurement (not part of the method) --------------------------------
  * Achievable peaks of this GPU; the kernels' rooflines are reported against
  * the nominal peaks and against these.  Both launch asynchronously on `stream`

@@ -86,6 +86,8 @@ def lib() -> ctypes.CDLL:
         "promoe_route": ([_vp, ctypes.c_int, _vp, ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
         "promoe_route_predict": ([_vp, ctypes.c_int, _vp, ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp, _vp],
                                  ctypes.c_int),
+        "promoe_stack_step": ([_vp, _vp, ctypes.c_int, _vp, _vp, _vp, _vp, _vp, _vp, ctypes.c_int, _vp],
+                              ctypes.c_int),
         "promoe_prefetch": ([_vp, ctypes.c_int, _vp, ctypes.c_int, ctypes.c_int, _vp], ctypes.c_int),
         "promoe_expert_ffn": ([_vp, ctypes.c_int, _vp, ctypes.c_int, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
         "promoe_expert_ffn_noalloc": ([_vp, ctypes.c_int, _vp, ctypes.c_int, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
@@ -118,7 +120,8 @@ def exported_symbols():
                         "promoe_route_predict", "promoe_prefetch", "promoe_expert_ffn", "promoe_expert_ffn_noalloc", "promoe_cache_stats",
                         "promoe_reset_stats",
                         "promoe_slot_table", "promoe_last_plan", "promoe_sync", "promoe_attn_surrogate",
-                        "promoe_residual_add", "promoe_host_alloc", "promoe_host_free", "promoe_expert_bytes",
+                        "promoe_residual_add", "promoe_stack_step", "promoe_host_alloc", "promoe_host_free",
+                        "promoe_expert_bytes",
                         "promoe_strerror", "promoe_last_error_string", "promoe_peak_hbm_read",
                         "promoe_peak_mfma_bf16")]
 
@@ -237,6 +240,12 @@ class Context:
 
     def residual_add(self, h, y, T, stream=None):
         check(lib().promoe_residual_add(self._h, _p(h), _p(y), T, _stream(stream)), "promoe_residual_add")
+
+    def stack_step(self, h, T, x, y, ids, w, shared_scale=None, pred_ids=None, predict=True, stream=None):
+        """Every layer of one step in one call (attention surrogate, prediction and
+        route, expert FFN, residual add); h [T, H] fp32 is updated in place."""
+        check(lib().promoe_stack_step(self._h, _p(h), T, _p(x), _p(y), _p(ids), _p(w), _p(shared_scale),
+                                      _p(pred_ids), 1 if predict else 0, _stream(stream)), "promoe_stack_step")
 
     # state
     def stats(self, layer=-1) -> dict:

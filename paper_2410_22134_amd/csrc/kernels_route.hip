@@ -277,41 +277,57 @@ __global__ __launch_bounds__(256) void k_predict_plan(PredictPlanArgs p) {
       hs[i] = fmaxf(p.h[(size_t)t * p.ldh + j], 0.0f);
     }
     __syncthreads();
+    // four threads per expert: thread q of expert e takes the 16-byte chunks
+    // q, q + 4, ... of its row, eight loads in flight at a time, then the four
+    // partial sums meet by two shuffles
     const int n8 = Ph / 8;  // Ph % 8 == 0
-    for (int e = wv; e < E; e += 4) {
-      float acc[kFusedPredMaxT];
+    const int e = tid >> 2, q = tid & 3;
+    float acc[kFusedPredMaxT];
 #pragma unroll
-      for (int t = 0; t < kFusedPredMaxT; ++t) acc[t] = 0.0f;
-      for (int j8 = lane; j8 < n8; j8 += kWave) {
-        float wj[8];
-        if (p.w2_bf16) {
-          const uint4 u = reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(p.w2) + (size_t)e * Ph)[j8];
-          const uint32_t q4[4] = {u.x, u.y, u.z, u.w};
+    for (int t = 0; t < kFusedPredMaxT; ++t) acc[t] = 0.0f;
+    if (e < E) {
+      for (int base = q; base < n8; base += 32) {
+        float wj[8][8];
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            wj[2 * i] = __uint_as_float(q4[i] << 16);
-            wj[2 * i + 1] = __uint_as_float(q4[i] & 0xFFFF0000u);
+        for (int u = 0; u < 8; ++u) {
+          const int j8 = base + 4 * u;
+          if (p.w2_bf16) {
+            const uint4 w = j8 < n8 ? reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(p.w2) + (size_t)e * Ph)[j8]
+                                    : make_uint4(0, 0, 0, 0);
+            const uint32_t q4[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              wj[u][2 * i] = __uint_as_float(q4[i] << 16);
+              wj[u][2 * i + 1] = __uint_as_float(q4[i] & 0xFFFF0000u);
+            }
+          } else {
+            const float* w = static_cast<const float*>(p.w2) + (size_t)e * Ph + j8 * 8;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) wj[u][i] = j8 < n8 ? w[i] : 0.0f;
           }
-        } else {
-          const float* w = static_cast<const float*>(p.w2) + (size_t)e * Ph + j8 * 8;
-#pragma unroll
-          for (int i = 0; i < 8; ++i) wj[i] = w[i];
         }
 #pragma unroll
-        for (int t = 0; t < kFusedPredMaxT; ++t) {
-          if (t < T) {
-            const float* h = hs + t * Ph + j8 * 8;
+        for (int u = 0; u < 8; ++u) {
+          const int j8 = base + 4 * u;
+          if (j8 >= n8) break;
 #pragma unroll
-            for (int i = 0; i < 8; ++i) acc[t] = fmaf(wj[i], h[i], acc[t]);
+          for (int t = 0; t < kFusedPredMaxT; ++t) {
+            if (t < T) {
+              const float* h = hs + t * Ph + j8 * 8;
+#pragma unroll
+              for (int i = 0; i < 8; ++i) acc[t] = fmaf(wj[u][i], h[i], acc[t]);
+            }
           }
         }
       }
+    }
 #pragma unroll
-      for (int t = 0; t < kFusedPredMaxT; ++t) {
-        if (t < T) {
-          const float v = wave_sum(acc[t]);
-          if (lane == 0) qs[t * kMaxE + e] = v;
-        }
+    for (int t = 0; t < kFusedPredMaxT; ++t) {
+      if (t < T) {
+        float v = acc[t];
+        v += __shfl_xor(v, 1, kWave);
+        v += __shfl_xor(v, 2, kWave);
+        if (q == 0 && e < E) qs[t * kMaxE + e] = v;
       }
     }
   } else {

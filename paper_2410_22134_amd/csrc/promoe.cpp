@@ -1859,6 +1859,27 @@ int promoe_last_plan(promoe_ctx* c, int layer, int kind, promoe_plan* out) {
   return PROMOE_OK;
 }
 
+int promoe_stack_step(promoe_ctx* c, float* d_h, int T, void* d_x, void* d_y, int32_t* d_ids, float* d_w,
+                      float* d_shared_scale, int32_t* d_pred_ids, int predict, void* stream) {
+  if (!c || !d_h || !d_x || !d_y || !d_ids || !d_w) return PROMOE_EINVAL;
+  int rc = check_tokens(c, T);
+  if (rc) return rc;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  for (int l = 0; l < c->L; ++l) {
+    if ((rc = promoe_attn_surrogate(c, l, d_h, T, d_x, stream))) return rc;
+    if (predict && c->D == 0) {
+      if ((rc = promoe_predict(c, l, d_x, T, d_pred_ids, nullptr, nullptr, stream))) return rc;
+      rc = route_impl(c, l, d_x, T, d_ids, d_w, d_shared_scale, nullptr, nullptr, s, false, nullptr);
+    } else {
+      rc = route_impl(c, l, d_x, T, d_ids, d_w, d_shared_scale, nullptr, nullptr, s, predict != 0, d_pred_ids);
+    }
+    if (rc) return rc;
+    if ((rc = promoe_expert_ffn(c, l, d_x, T, d_ids, d_w, d_shared_scale, d_y, stream))) return rc;
+    if ((rc = promoe_residual_add(c, d_h, d_y, T, stream))) return rc;
+  }
+  return PROMOE_OK;
+}
+
 int promoe_attn_surrogate(promoe_ctx* c, int layer, float* d_h, int T, void* d_x_out, void* stream) {
   if (!c || layer < 0 || layer >= c->L || !d_h || !d_x_out) return PROMOE_EINVAL;
   int rc = check_tokens(c, T);

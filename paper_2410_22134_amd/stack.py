@@ -53,16 +53,21 @@ class Stack:
         ctx.expert_ffn(l, self._x, T, self._ids, self._w, self._s, self._y, stream=s)
         return order, q
 
-    def step(self, h0, predict: bool | None = None, record=None, stream=None):
+    def step(self, h0, predict: bool | None = None, record=None, stream=None, native: bool = True):
         """One step over all layers from residual input h0 [T, H] (fp32, device),
         on `stream` (default: the current stream, looked up once per step).
         predict=None: the predictor runs unless the context was opened without
-        prefetching (then nothing would read its output)."""
+        prefetching (then nothing would read its output).  Without a record
+        callback the whole loop is one library call (promoe_stack_step) unless
+        native=False."""
         ctx, T = self.m.ctx, self.T
         s = _handle(stream) if self._cuda else stream
         if predict is None:
             predict = not getattr(self.m, "flags", 0) & FLAG_NO_PREFETCH
         self.h.copy_(h0)
+        if native and record is None and hasattr(ctx, "stack_step"):
+            ctx.stack_step(self._h, T, self._x, self._y, self._ids, self._w, self._s, self._pred, predict, stream=s)
+            return self.h
         for l in range(self.m.cfg.n_layers):
             if record is not None:
                 record("h", l, self)

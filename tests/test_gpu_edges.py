@@ -408,3 +408,34 @@ def test_route_predict_in_one_call(T, fmt):
         pu.check_counters(m, lcs)
     finally:
         m.close()
+
+
+@pytest.mark.parametrize("T", [1, 4, 77])
+@pytest.mark.parametrize("lookahead", [0, 1])
+def test_stack_step_in_one_call(T, lookahead):
+    # promoe_stack_step runs the layer loop of the separate calls: the residual
+    # stream after each step, the plans and every counter match them bit for bit
+    cfg = SMALL.with_(lookahead=lookahead)
+    _log("stack_step T", T, "lookahead", lookahead)
+    m = SyntheticModel(cfg, max_tokens=T)
+    try:
+        st = Stack(m, T)
+        runs = []
+        for native in (False, True):
+            m.open()
+            hs, plans = [], []
+            for step in range(3):
+                h0 = torch.from_numpy(sm.stack_input(cfg, 990 + step, T)).cuda()
+                hs.append(pu.to_np(st.step(h0, native=native)).copy())
+                plans.append([(m.ctx.last_plan(l, 0)["slot"], m.ctx.last_plan(l, 1)["slot"])
+                              for l in range(cfg.n_layers)])
+            runs.append((hs, plans, [m.ctx.stats(l) for l in range(cfg.n_layers)]))
+        (h_a, p_a, s_a), (h_b, p_b, s_b) = runs
+        for i, (a, b) in enumerate(zip(h_a, h_b)):
+            assert np.array_equal(a, b), ("step", i)
+        assert p_a == p_b
+        for l, (a, b) in enumerate(zip(s_a, s_b)):
+            for c in ocache.COUNTERS:
+                assert a[c] == b[c], (l, c)
+    finally:
+        m.close()
