@@ -97,6 +97,15 @@ def read_traffic(kernel):
     return None, None
 
 
+def traffic_here(ratio, cls):
+    """HBM bytes per launch of this run: the counter runs' measured bytes over
+    algorithmic bytes, applied to this run's algorithmic bytes per launch (the
+    average launch differs between runs with the cache's hit pattern)."""
+    if ratio is None or not cls.get("bytes_per_launch"):
+        return None
+    return int(round(ratio * cls["bytes_per_launch"]))
+
+
 def prediction_metrics(s):
     """GoodPred = Accuracy x FetchRate (Sec. "A New Prediction Metric: GoodPred").
     Accuracy: predicted experts that the target layer routes (exact, device counters);
@@ -803,10 +812,12 @@ def main():
                    "predictor": "trained offline on the model's traces" if args.trained_predictor else
                                 "constructed skip predictor"},
         "roofline": {"bound": "hbm", "kernel": "k_ffn_gateup<bf16,1,4,1>", **roof(gu),
-                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "traffic": traffic,
-                     "traffic_over_algorithmic": traffic_ratio, "peak_measured": hbm_meas,
-                     "down": {"kernel": "k_ffn_down<bf16,1,3,2>", **roof(dn), "traffic": traffic_d,
-                              "traffic_over_algorithmic": traffic_ratio_d},
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "traffic": traffic_here(traffic_ratio, gu),
+                     "traffic_over_algorithmic": traffic_ratio, "traffic_in_counter_runs": traffic,
+                     "peak_measured": hbm_meas,
+                     "down": {"kernel": "k_ffn_down<bf16,1,3,2>", **roof(dn),
+                              "traffic": traffic_here(traffic_ratio_d, dn),
+                              "traffic_over_algorithmic": traffic_ratio_d, "traffic_in_counter_runs": traffic_d},
                      "gateup_and_down": {"achieved": round(both, 1), "frac": round(both / HBM_PEAK_GBPS, 4)},
                      "timing": "kernel start and end events recorded by each launch (hipExtLaunchKernelGGL), "
                                "averaged over every launch of the timed region"},

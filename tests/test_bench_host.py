@@ -129,3 +129,10 @@ def test_summary_line_reads_every_leg():
     for piece in ("decode 37.0 tok/s", "all-resident 500.0", "Mixtral-8x7B int4: prefill 900.0, decode b1 14.0",
                   "shared GEMM 0.440", "GoodPred 0.350", "oracle 0.26"):
         assert piece in line, (piece, line)
+
+
+def test_traffic_is_scaled_to_the_run():
+    # the counter runs' bytes-over-algorithmic ratio, applied to this run's launches
+    assert bench.traffic_here(1.01, {"bytes_per_launch": 1000}) == 1010
+    assert bench.traffic_here(None, {"bytes_per_launch": 1000}) is None
+    assert bench.traffic_here(1.01, {}) is None
