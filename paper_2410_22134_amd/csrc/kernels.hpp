@@ -192,6 +192,8 @@ void launch_gemm_rows(const RowsGemmArgs& a, hipStream_t s);
 void launch_gemm(FfnArgs& a, int pass, int max_tokens, hipStream_t s, hipEvent_t ev0 = nullptr,
                  hipEvent_t ev1 = nullptr);
 void launch_combine(const CombineArgs& a, int T, int dtype, hipStream_t s);
+// combine, then h += y, in one launch
+void launch_combine_residual(const CombineArgs& a, float* h, int T, int dtype, hipStream_t s);
 void launch_rmsnorm_quant(const float* h, void* out, int T, int H, int dtype, hipStream_t s);
 void launch_residual_add(float* h, const void* y, int n, int dtype, hipStream_t s);
 void launch_topk(const TopkArgs& a, hipStream_t s);

@@ -623,6 +623,25 @@ __global__ __launch_bounds__(kThreads) void k_combine(CombineArgs a) {
   Elem<TY>::store(reinterpret_cast<TY*>(a.y), t * a.hidden + n, y);
 }
 
+// Combine and residual add in one launch (the layer loop's combine -> h += y):
+// y as k_combine rounds it, h += y as k_residual_add adds it.
+template <typename TY>
+__global__ __launch_bounds__(kThreads) void k_combine_residual(CombineArgs a, float* h) {
+  const int t = blockIdx.y;
+  const int n = blockIdx.x * kThreads + threadIdx.x;
+  if (n >= a.hidden) return;
+  float y = 0.0f;
+  for (int r = 0; r < a.top_k; ++r) y += a.w[t * a.top_k + r] * a.Y[((size_t)t * a.top_k + r) * a.hidden + n];
+  if (a.Ysh) {
+    float ysh = 0.0f;
+    for (int k = 0; k < a.ysh_split; ++k) ysh += a.Ysh[(size_t)k * a.ysh_split_stride + (size_t)t * a.hidden + n];
+    const float s = a.sscale ? a.sscale[t] : 1.0f;
+    y += s * ysh;
+  }
+  Elem<TY>::store(reinterpret_cast<TY*>(a.y), t * a.hidden + n, y);
+  h[(size_t)t * a.hidden + n] += Elem<TY>::quant(y);
+}
+
 // ============================================================ harness ops
 template <typename TQ>
 __global__ __launch_bounds__(kThreads) void k_rmsnorm_quant(const float* h, void* out, int H, float eps) {
@@ -788,6 +807,12 @@ void launch_combine(const CombineArgs& a, int T, int dtype, hipStream_t s) {
   dim3 grid((a.hidden + kThreads - 1) / kThreads, T);
   if (dtype == 1) k_combine<bf16_t><<<grid, kThreads, 0, s>>>(a);
   else k_combine<float><<<grid, kThreads, 0, s>>>(a);
+}
+
+void launch_combine_residual(const CombineArgs& a, float* h, int T, int dtype, hipStream_t s) {
+  dim3 grid((a.hidden + kThreads - 1) / kThreads, T);
+  if (dtype == 1) k_combine_residual<bf16_t><<<grid, kThreads, 0, s>>>(a, h);
+  else k_combine_residual<float><<<grid, kThreads, 0, s>>>(a, h);
 }
 
 void launch_rmsnorm_quant(const float* h, void* out, int T, int H, int dtype, hipStream_t s) {

@@ -225,6 +225,8 @@ struct promoe_ctx {
   // record pred_host_rec: the next call that could touch what it reads or
   // writes first waits on the host for that record (no device-side join).
   int64_t pred_host_rec = -1;
+  // promoe_stack_step: the FFN call's combine also adds y into fuse_h
+  float* fuse_h = nullptr;
   // first predictor rows computed by a route's gate launch (layer, input, T)
   int pred_rows_layer = -1;
   const void* pred_rows_x = nullptr;
@@ -1731,7 +1733,8 @@ static int expert_ffn_run(promoe_ctx* c, int layer, int T, const float* d_w, con
   ca.y = d_y;
   ca.hidden = c->H;
   ca.top_k = c->K;
-  launch_combine(ca, T, c->dt, s);
+  if (c->fuse_h) launch_combine_residual(ca, c->fuse_h, T, c->dt, s);
+  else launch_combine(ca, T, c->dt, s);
   LAUNCHCHK("combine");
   // a prediction the route launched on the side stream: later work on s follows it
   HIPCHK(pred_join(c, s));
@@ -1874,8 +1877,11 @@ int promoe_stack_step(promoe_ctx* c, float* d_h, int T, void* d_x, void* d_y, in
       rc = route_impl(c, l, d_x, T, d_ids, d_w, d_shared_scale, nullptr, nullptr, s, predict != 0, d_pred_ids);
     }
     if (rc) return rc;
-    if ((rc = promoe_expert_ffn(c, l, d_x, T, d_ids, d_w, d_shared_scale, d_y, stream))) return rc;
-    if ((rc = promoe_residual_add(c, d_h, d_y, T, stream))) return rc;
+    // the combine also does the residual add
+    c->fuse_h = d_h;
+    rc = promoe_expert_ffn(c, l, d_x, T, d_ids, d_w, d_shared_scale, d_y, stream);
+    c->fuse_h = nullptr;
+    if (rc) return rc;
   }
   return PROMOE_OK;
 }
