@@ -29,9 +29,9 @@ void Prefetcher::assign(int layer, int slot, int expert) {
     if (it->layer == layer && it->slot == slot) it = low_.erase(it);
     else ++it;
   }
-  bool busy = false;  // an earlier copy into the slot may still be in flight
-  for (const auto& c : s.ch) busy = busy || c.last >= retired_;
-  if (!busy) s.queue = pick_queue();
+  // an earlier copy into the slot may still be in flight (also one of an owner
+  // before the current one, whose chunk records were reset when it was evicted)
+  if (s.last_copy < retired_) s.queue = pick_queue();
   s.expert = expert;
   for (auto& c : s.ch) c = Chunk();
 }
@@ -99,6 +99,7 @@ void Prefetcher::issue_sub(int layer, int slot, int chunk, Prio prio, int64_t af
   eng_->issue(seq, cache_ + slot_off, src, bytes, after, q);
   ch.n_issued++;
   ch.last = seq;
+  s.last_copy = seq;
   st_.copies[prio]++;
   st_.bytes[prio] += (int64_t)bytes;
 }
@@ -159,6 +160,7 @@ void Prefetcher::issue_pending(int layer, int slot, int64_t after_compute, Prio 
     note_issued(prio, q, (int64_t)(end - start));
     const size_t slot_off = ((size_t)layer * C_ + slot) * expert_bytes;
     eng_->issue(seq, cache_ + slot_off + start, host_[layer * E_ + s.expert] + start, end - start, after, q);
+    s.last_copy = seq;
     st_.copies[prio]++;
     st_.bytes[prio] += (int64_t)(end - start);
     first = false;

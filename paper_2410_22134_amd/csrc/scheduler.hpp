@@ -140,6 +140,7 @@ class Prefetcher {
     int expert = -1;
     int queue = -1;  // engine queue (-1: not chosen yet)
     int64_t last_read = -1;
+    int64_t last_copy = -1;  // seq of the latest copy into the slot, whichever expert it carried
     Chunk ch[kChunks];
   };
   struct InFlight {

@@ -189,6 +189,27 @@ void test_queue_per_slot() {
   CHECK(used[0] && used[1]);
 }
 
+// A slot given a second new expert before anything was copied for the first
+// keeps the queue of the copies still in flight from before: the latest expert's
+// copies must not overtake them (they would land under the old bytes).
+void test_queue_kept_over_uncopied_owner() {
+  Rig r(1, 2, 8, 100, 50, 4, 1000);
+  r.eng.nq = 2;
+  r.eng.bw = 1.0;  // copies stay in flight
+  r.pf->assign(0, 0, 1);
+  r.pf->push_low(0, 0);
+  r.pf->pump();  // expert 1's first sub-copies go out
+  CHECK(r.pf->in_flight() > 0);
+  const int q_old = r.eng.queue_of_copy.back();
+  const size_t n_old = r.eng.log.size();
+  r.pf->assign(0, 0, 2);  // queued only, never copied
+  r.pf->purge_low(0);
+  r.pf->assign(0, 0, 3);
+  r.pf->issue_high(0, 0);
+  CHECK(r.eng.log.size() > n_old);
+  for (size_t i = n_old; i < r.eng.log.size(); ++i) CHECK(r.eng.queue_of_copy[i] == q_old);
+}
+
 // Fills issued one after another alternate between two queues: each goes to
 // the queue with fewer bytes in flight.
 void test_fills_balance_queues() {
@@ -499,6 +520,7 @@ int main(int argc, char** argv) {
   test_pending_bytes();
   test_queue_per_slot();
   test_fills_balance_queues();
+  test_queue_kept_over_uncopied_owner();
   test_head_readers();
   test_resident_groups();
   test_window_bound();
