@@ -44,6 +44,7 @@ thread_local std::string g_last_error;
 constexpr int kRecRing = 64;
 constexpr int kStallClass = 99;
 constexpr size_t kHighMergeBytes = (size_t)64 << 20;  // high-priority copies coalesce up to this size
+constexpr size_t kOneQueueChunkBytes = (size_t)24 << 20;  // chunks this large use one copy queue
 constexpr int kMaxSplit = 8;  // split-K slices of the shared expert's down GEMM
 constexpr int kCopyRing = 4096;
 constexpr int kComputeRing = 4096;
@@ -114,7 +115,8 @@ class HipEngine : public CopyEngine {
     if (e == hipSuccess) e = hipEventRecord(ev[seq % kCopyRing], s);
     if (e != hipSuccess && err == hipSuccess) err = e;
   }
-  int queues() const override { return kCopyStreams; }
+  int nq = kCopyStreams;  // queues in use (1 for large chunks)
+  int queues() const override { return nq; }
   bool done(int64_t seq) override { return hipEventQuery(ev[seq % kCopyRing]) == hipSuccess; }
   void wait(int64_t seq) override {
     hipError_t e = hipEventSynchronize(ev[seq % kCopyRing]);
@@ -749,6 +751,10 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   c->eng.compute_stream = &c->cstream;
   const size_t sub = g.copy_subchunk_bytes > 0 ? (size_t)g.copy_subchunk_bytes : ((size_t)16 << 20);
   const int window = g.copy_window > 0 ? g.copy_window : 2;
+  // A second queue only hides the per-copy setup gap, which copies of this size
+  // amortise; on one queue copies land in issue order, so the first fill of a
+  // step lands first instead of sharing the link until all land together.
+  if (c->chunk_bytes >= kOneQueueChunkBytes) c->eng.nq = 1;
   c->pf = new Prefetcher(L, C, E, c->chunk_bytes, sub, window, c->cache, &c->eng, std::max(sub, kHighMergeBytes));
   c->pf->set_whole_expert_low((g.flags & PROMOE_FLAG_NO_CHUNK) != 0);
   if (c->profile) {
@@ -1694,7 +1700,15 @@ static int expert_ffn_run(promoe_ctx* c, int layer, int T, const float* d_w, con
   // a time, so compute follows the copies: consecutive fills run on different
   // copy queues and arrive together, and a launch of one expert's few tokens
   // leaves most CUs idle, so two experts cost about what one does.  Fills
-  // deferred behind an earlier expert's read are released as it is launched.
+  // deferred behind an earlier expert's read are released as it is launched,
+  // so an expert that such a fill waits for is launched as soon as it has
+  // arrived, without waiting for a second one (with few slots per layer every
+  // fill waits for the previous occupant of its slot).
+  auto releases_fill = [&](int p) {
+    for (const auto& d : c->deferred)
+      if (d.after == p) return true;
+    return false;
+  };
   for (;;) {
     jobs.clear();
     CopyWait w01, w2;
@@ -1707,7 +1721,7 @@ static int expert_ffn_run(promoe_ctx* c, int layer, int T, const float* d_w, con
       jobs.push_back(p);
       w01.add(c->need_q[p], c->need01[p]);
       w2.add(c->need_q[p], c->need2[p]);
-      if (!batch && (int)jobs.size() == kArrivalGroup) break;
+      if (!batch && ((int)jobs.size() == kArrivalGroup || releases_fill(p))) break;
     }
     if (jobs.empty()) break;
     rc = ffn_launch(c, a, jobs, s, w01, w2);
