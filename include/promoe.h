@@ -169,8 +169,8 @@ typedef struct promoe_stats {
   int64_t pred_in_time;             /* correctly predicted experts whose bytes had all
                                        landed in HBM when the route ran: FetchRate =
                                        pred_in_time / pred_correct */
-  /* Timing, PROMOE_FLAG_PROFILE only.  Expert launches are timed on the
-     device clock (earliest block start to latest wave end); classes:
+  /* Timing, PROMOE_FLAG_PROFILE only.  Expert launches are timed by start and
+     end events that the launch itself records (kernel execution time); classes:
      [0] GEMV gate/up, [1] GEMV down, [2] GEMM gate/up (routed experts),
      [3] GEMM down (routed), [4] GEMM gate/up (shared expert), [5] GEMM down (shared). */
   int64_t k_launches[6];
@@ -179,6 +179,11 @@ typedef struct promoe_stats {
   double k_flops[6];      /* summed algorithmic flops */
   double stall_ms;        /* compute stream time spent waiting on copies (HIP events) */
   double copy_ms;         /* reserved (0) */
+  int64_t lazy_routes;    /* decode routes that returned without waiting for their plan
+                             on the host: every expert of every layer resident (slots ==
+                             experts, each layer's initial cache full), the resident launch
+                             covering the step, and no order asked for; their plans are
+                             taken in once complete (stats, sync and later routes) */
 } promoe_stats;
 
 typedef struct promoe_plan {

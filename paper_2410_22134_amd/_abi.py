@@ -35,7 +35,7 @@ class Stats(ctypes.Structure):
         ("copies_high", _i64), ("copies_low", _i64), ("bytes_high", _i64), ("bytes_low", _i64),
         ("low_purged", _i64), ("deferred", _i64), ("pred_in_time", _i64),
         ("k_launches", _i64 * 6), ("k_ms", _dbl * 6), ("k_bytes", _dbl * 6), ("k_flops", _dbl * 6),
-        ("stall_ms", _dbl), ("copy_ms", _dbl)]
+        ("stall_ms", _dbl), ("copy_ms", _dbl), ("lazy_routes", _i64)]
 
     def as_dict(self):
         d = {n: int(getattr(self, n)) for n in STAT_COUNTERS}
@@ -44,6 +44,7 @@ class Stats(ctypes.Structure):
         for n in ("k_launches", "k_ms", "k_bytes", "k_flops"):
             d[n] = list(getattr(self, n))
         d["stall_ms"] = float(self.stall_ms)
+        d["lazy_routes"] = int(self.lazy_routes)
         return d
 
 

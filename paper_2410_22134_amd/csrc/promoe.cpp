@@ -227,6 +227,19 @@ struct promoe_ctx {
   // record pred_host_rec: the next call that could touch what it reads or
   // writes first waits on the host for that record (no device-side join).
   int64_t pred_host_rec = -1;
+  // Every expert of every layer resident (as many slots as experts, and each
+  // layer's initial cache holds all of them): no plan can fill a slot, so a
+  // decode-sized route whose resident launch covers the whole step need not
+  // wait for its plan on the host ("lazy" route); its record is taken in
+  // later, once complete.
+  std::vector<char> layer_full;
+  int n_full_layers = 0;
+  bool all_resident() const { return C == E && n_full_layers == L; }
+  bool rec_lazy[kRecRing] = {};            // record of a lazy route, not yet taken in
+  int lazy_T[kRecRing] = {};                // its step's tokens
+  size_t lazy_prof0[kRecRing] = {}, lazy_nprof[kRecRing] = {};  // its launch's profiling entries
+  bool route_lazy = false;                  // the latest route is lazy
+  int64_t n_lazy_routes = 0;
   // promoe_stack_step: the FFN call's combine also adds y into fuse_h
   float* fuse_h = nullptr;
   // first predictor rows computed by a route's gate launch (layer, input, T)
@@ -354,6 +367,59 @@ void ingest_spec(promoe_ctx* c, int64_t r) {
   c->rec_ingested = r + 1;
 }
 
+// Bytes and flops of a resident launch's profiling entries, from its plan: the
+// positions it ran (resident, slot not in busy) and the shared expert.
+void early_prof_bytes(promoe_ctx* c, const PlanRecord& rec, int T, uint64_t busy, size_t prof0, size_t nprof) {
+  double routed_bytes = 0.0, routed_flops = 0.0;
+  const double melems = (double)c->I * c->H;
+  for (int p = 0; p < rec.n_hit; ++p) {
+    if ((busy >> rec.slot[p]) & 1ull) continue;
+    routed_bytes += c->q4 ? (double)c->chunk_bytes : melems * c->eb;
+    routed_flops += 2.0 * rec.count[p] * melems;
+  }
+  const double sh_elems = (double)c->Ish * c->H;
+  const double sh_bytes = sh_elems * c->eb, sh_flops = 2.0 * T * sh_elems;
+  for (size_t i = 0; i < nprof; ++i) {
+    ProfEntry& pe = c->prof_pending[prof0 + i];
+    const double k = pe.cls == 0 ? 2.0 : 1.0;
+    // dense: [shared + routed] x 2 passes; 4-bit: [shared] x 2, then [routed] x 2
+    const bool shared_part = c->q4 ? i < 2 && c->Ish > 0 : true;
+    const bool routed_part = c->q4 ? !(i < 2 && c->Ish > 0) : true;
+    pe.bytes = k * ((shared_part ? sh_bytes : 0.0) + (routed_part ? routed_bytes : 0.0));
+    pe.flops = k * ((shared_part ? sh_flops : 0.0) + (routed_part ? routed_flops : 0.0));
+  }
+}
+
+// Take in the (complete) record r of a lazy route: what the route does with its
+// plan once on the host, less the copies (there are none).  Caller holds mu.
+void consume_lazy_route(promoe_ctx* c, int64_t r) {
+  const int i = (int)(r % kRecRing);
+  const PlanRecord& rec = c->rec_h[i];
+  const int layer = rec.layer;
+  c->last_precise[layer] = rec;
+  if (!(c->cfg.flags & PROMOE_FLAG_NO_PREEMPT)) c->pf->purge_low(layer);
+  // every predicted expert that was routed was resident in time
+  const uint64_t predicted = c->pred_host[layer];
+  c->pred_host[layer] = 0ull;
+  for (int p = 0; p < rec.n; ++p)
+    if ((predicted >> rec.expert[p]) & 1ull) c->pred_in_time++;
+  if (c->profile) early_prof_bytes(c, rec, c->lazy_T[i], 0ull, c->lazy_prof0[i], c->lazy_nprof[i]);
+  c->rec_lazy[i] = false;
+  c->rec_ingested = r + 1;
+}
+
+// Records the host takes in without a route waiting on them: spec plans and
+// the plans of lazy routes.
+bool ingestable(const promoe_ctx* c, int64_t r) {
+  return c->rec_kind[r % kRecRing] == 0 || c->rec_lazy[r % kRecRing];
+}
+
+// Take in record r (complete, ingestable).  Caller holds mu.
+void ingest_rec(promoe_ctx* c, int64_t r) {
+  if (c->rec_lazy[r % kRecRing]) consume_lazy_route(c, r);
+  else ingest_spec(c, r);
+}
+
 void worker_main(promoe_ctx* c) {
   hipSetDevice(c->dev);
   std::unique_lock<std::mutex> lk(c->mu);
@@ -387,7 +453,7 @@ int new_record(promoe_ctx* c, int kind, int prio, int64_t* out) {
   std::unique_lock<std::mutex> lk(c->mu);
   while (c->rec_next - c->rec_ingested >= kRecRing) {
     const int64_t r = c->rec_ingested;
-    if (c->rec_kind[r % kRecRing] != 0) {
+    if (!ingestable(c, r)) {
       g_last_error = "plan record ring blocked by an unconsumed route";
       return PROMOE_ESTATE;
     }
@@ -399,11 +465,12 @@ int new_record(promoe_ctx* c, int kind, int prio, int64_t* out) {
     lk.unlock();
     HIPCHK(hipEventSynchronize(e));
     lk.lock();
-    if (c->rec_ingested == r) ingest_spec(c, r);
+    if (c->rec_ingested == r) ingest_rec(c, r);
   }
   const int64_t r = c->rec_next++;
   c->rec_kind[r % kRecRing] = kind;
   c->rec_prio[r % kRecRing] = prio;
+  c->rec_lazy[r % kRecRing] = false;
   std::memset(&c->rec_h[r % kRecRing], 0, sizeof(PlanRecord));
   *out = r;
   return PROMOE_OK;
@@ -436,6 +503,26 @@ hipError_t wait_record(promoe_ctx* c, int64_t r) {
     __builtin_ia32_pause();
   }
   std::atomic_thread_fence(std::memory_order_acquire);
+  return hipSuccess;
+}
+
+// Take in the ingestable records at the head of the ring whose plans have
+// completed (block: waiting for each in turn instead of stopping).
+hipError_t drain_records(promoe_ctx* c, bool block) {
+  std::unique_lock<std::mutex> lk(c->mu);
+  while (c->rec_ingested < c->rec_pub && ingestable(c, c->rec_ingested)) {
+    const int64_t r = c->rec_ingested;
+    const volatile int32_t* done = &c->rec_h[r % kRecRing].done;
+    if (!*done) {
+      if (!block && hipEventQuery(c->rec_ev[r % kRecRing]) != hipSuccess) break;
+      lk.unlock();
+      const hipError_t e = wait_record(c, r);
+      lk.lock();
+      if (e != hipSuccess) return e;
+    }
+    std::atomic_thread_fence(std::memory_order_acquire);
+    if (c->rec_ingested == r) ingest_rec(c, r);
+  }
   return hipSuccess;
 }
 
@@ -638,6 +725,7 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   c->lw.resize(c->L);
   c->last_spec.resize(c->L);
   c->pred_host.assign(c->L, 0ull);
+  c->layer_full.assign(c->L, 0);
   c->last_precise.resize(c->L);
   hipGetDevice(&c->dev);
   {
@@ -779,13 +867,13 @@ int promoe_sync(promoe_ctx* c) {
     std::unique_lock<std::mutex> lk(c->mu);
     // flush speculative records and low-priority work, then wait for every copy
     for (;;) {
-      while (c->rec_ingested < c->rec_pub && c->rec_kind[c->rec_ingested % kRecRing] == 0) {
+      while (c->rec_ingested < c->rec_pub && ingestable(c, c->rec_ingested)) {
         hipEvent_t e = c->rec_ev[c->rec_ingested % kRecRing];
         const int64_t r = c->rec_ingested;
         lk.unlock();
         hipEventSynchronize(e);
         lk.lock();
-        if (c->rec_ingested == r) ingest_spec(c, r);
+        if (c->rec_ingested == r) ingest_rec(c, r);
       }
       c->pf->pump();
       if (!c->pf->has_low() && c->pf->in_flight() == 0) break;
@@ -888,6 +976,11 @@ int promoe_set_initial_cache(promoe_ctx* c, int layer, const int32_t* h_experts,
   launch_warm(c->st, layer, c->C, c->E, c->d_warm, n, nullptr);
   LAUNCHCHK("warm");
   HIPCHK(hipDeviceSynchronize());
+  const bool full = c->C == c->E && n == c->E;
+  if (full != (c->layer_full[layer] != 0)) {
+    c->layer_full[layer] = full;
+    c->n_full_layers += full ? 1 : -1;
+  }
   std::lock_guard<std::mutex> lk(c->mu);
   for (int i = 0; i < n; ++i) c->pf->mark_resident(layer, i, h_experts[i]);
   return PROMOE_OK;
@@ -924,9 +1017,11 @@ static hipError_t pred_join(promoe_ctx* c, hipStream_t s) {
 // The prediction of `layer` on stream s (routed: no route will need this
 // layer's gate logits on this input any more, so only predictor rows are
 // computed).  join_now: s waits for the side stream before the call returns;
-// else the layer's FFN call joins it (after its last launch).
+// else, with host_join, the next call that needs it waits on the host for the
+// spec plan's record, and without, the layer's FFN call joins it on the device
+// (after its last launch).
 static int predict_launch(promoe_ctx* c, int layer, const void* d_x, int T, int32_t* d_pred_ids, int32_t* h_q,
-                          int32_t* n_q, hipStream_t s, bool routed, bool join_now) {
+                          int32_t* n_q, hipStream_t s, bool routed, bool join_now, bool host_join = true) {
   int rc = pred_host_join(c);
   if (rc) return rc;
   HIPCHK(pred_join(c, s));
@@ -953,7 +1048,7 @@ static int predict_launch(promoe_ctx* c, int layer, const void* d_x, int T, int3
   HIPCHK(hipStreamWaitEvent(ps, c->pred_in, 0));
   int64_t spec_rec;
   rc = predict_tail(c, layer, target, T, d_pred_ids, h_q, n_q, ps, &spec_rec);
-  if (!rc && !join_now && spec_rec >= 0) {
+  if (!rc && !join_now && host_join && spec_rec >= 0) {
     // the spec plan's record marks the end of the side stream's work (earlier
     // side-stream work was joined at the top of this call)
     c->pred_host_rec = spec_rec;
@@ -1151,6 +1246,8 @@ static int route_impl(promoe_ctx* c, int layer, const void* d_x, int T, int32_t*
   rc = pred_host_join(c);
   if (rc) return rc;
   HIPCHK(pred_join(c, s));
+  // plans of earlier lazy routes that have completed
+  if (c->all_resident()) HIPCHK(drain_records(c, false));
   {
     const auto now = std::chrono::steady_clock::now();
     if (c->have_route_t) {
@@ -1199,15 +1296,49 @@ static int route_impl(promoe_ctx* c, int layer, const void* d_x, int T, int32_t*
   launch_plan_precise(plan_args(c, layer, d_ids, T, r), s);
   hipError_t le = hipGetLastError();
   if (le == hipSuccess) le = hipEventRecord(c->rec_ev[r % kRecRing], s);
-  bool early_ffn = false;
+  bool early_ffn = false, lazy = false;
   if (le == hipSuccess) {
     rc = early_resident_launch(c, layer, d_x, T, s, r, &early_ffn);
+    // every expert resident: the resident launch covers the step, and the
+    // caller does not ask for the order, so the plan is taken in later
+    lazy = !rc && early_ffn && c->all_resident() && !h_order && !n_order;
     // the prediction's launches (on the side stream) fill the host's wait for the plan
-    if (!rc && with_predict) rc = predict_launch(c, layer, d_x, T, d_pred_ids, nullptr, nullptr, s, true, false);
+    if (!rc && with_predict)
+      rc = predict_launch(c, layer, d_x, T, d_pred_ids, nullptr, nullptr, s, true, false, !lazy);
     if (rc) {
       publish(c, r);
       return rc;
     }
+  }
+  if (lazy) {
+    {
+      std::lock_guard<std::mutex> lk(c->mu);
+      const int i = (int)(r % kRecRing);
+      c->rec_lazy[i] = true;
+      c->lazy_T[i] = T;
+      c->lazy_prof0[i] = c->early_prof0;
+      c->lazy_nprof[i] = c->early_nprof;
+      c->early_nprof = 0;
+      // its resident launch ran every position and the shared expert: the FFN
+      // call has no position to launch
+      c->ffn_started.clear();
+      c->deferred.clear();
+      c->need01.clear();
+      c->need2.clear();
+      c->need_q.clear();
+      c->shared_started = c->Ish > 0;
+    }
+    publish(c, r);
+    c->lw[layer].planned = true;
+    HIPCHK(hipEventRecord(c->route_done, s));
+    c->route_stream = s;
+    c->route_lazy = true;
+    c->n_lazy_routes++;
+    c->route_layer = layer;
+    c->last_route_layer = layer;
+    c->route_T = T;
+    c->route_x = d_x;
+    return PROMOE_OK;
   }
   if (le == hipSuccess) le = wait_record(c, r);
   publish(c, r);
@@ -1217,7 +1348,7 @@ static int route_impl(promoe_ctx* c, int layer, const void* d_x, int T, int32_t*
   std::unique_lock<std::mutex> lk(c->mu);
   while (c->rec_ingested < r) {  // earlier plans on the same stream: complete
     HIPCHK(wait_record(c, c->rec_ingested));
-    ingest_spec(c, c->rec_ingested);
+    ingest_rec(c, c->rec_ingested);
   }
   const PlanRecord rec = c->rec_h[r % kRecRing];
   c->rec_ingested = r + 1;
@@ -1476,22 +1607,23 @@ static int early_resident_launch(promoe_ctx* c, int layer, const void* d_x, int 
   const bool in_order = (c->cfg.flags & (PROMOE_FLAG_NO_REORDER | PROMOE_FLAG_NO_PREEMPT)) != 0;
   if (in_order || (int64_t)T * c->K > 64 || T >= kGemmMinTokens || c->noalloc_call) return PROMOE_OK;
   uint64_t busy = 0;
-  {
+  if (!c->all_resident()) {
     // Earlier plans must be on the host first (their fills decide which slots
     // are busy): they are speculative ones (a precise one would still await its
     // FFN call), and a spec plan published before this route was queued ahead
     // of it, so waiting for it costs at most the wait for this route's plan.
+    // (With every expert resident no plan fills a slot and none is busy.)
     std::unique_lock<std::mutex> lk(c->mu);
     const int64_t first = c->rec_ingested;
     for (int64_t rr = first; rr < r; ++rr)
-      if (c->rec_kind[rr % kRecRing] != 0 || rr >= c->rec_pub) return PROMOE_OK;
+      if (!ingestable(c, rr) || rr >= c->rec_pub) return PROMOE_OK;
     lk.unlock();
     for (int64_t rr = first; rr < r; ++rr) {
       const hipError_t e = wait_record(c, rr);
       if (e != hipSuccess) return fail_hip(e, "spec plan");
     }
     lk.lock();
-    while (c->rec_ingested < r) ingest_spec(c, c->rec_ingested);
+    while (c->rec_ingested < r) ingest_rec(c, c->rec_ingested);
     c->pf->retire();
     for (int slot = 0; slot < c->C; ++slot)
       if (c->pf->ready_seq(layer, slot, 2) != -1) busy |= 1ull << slot;
@@ -1556,33 +1688,17 @@ static int early_resident_launch(promoe_ctx* c, int layer, const void* d_x, int 
 static void early_resident_release(promoe_ctx* c, int layer, int T, hipStream_t s) {
   const PlanRecord& rec = c->route_rec;
   std::vector<int> jobs;
-  double routed_bytes = 0.0, routed_flops = 0.0;
-  const double melems = (double)c->I * c->H;
   for (int p = 0; p < rec.n_hit; ++p) {
     if ((c->early_busy >> rec.slot[p]) & 1ull) continue;
     c->ffn_started[p] = 1;
     jobs.push_back(p);
-    routed_bytes += c->q4 ? (double)c->chunk_bytes : melems * c->eb;
-    routed_flops += 2.0 * rec.count[p] * melems;
   }
   if (c->Ish > 0) {
     c->shared_started = true;
     jobs.push_back(kSharedJob);
   }
   release_after_launch(c, layer, jobs, s);
-  if (c->profile && c->early_nprof) {
-    const double sh_elems = (double)c->Ish * c->H;
-    const double sh_bytes = sh_elems * c->eb, sh_flops = 2.0 * T * sh_elems;
-    for (size_t i = 0; i < c->early_nprof; ++i) {
-      ProfEntry& pe = c->prof_pending[c->early_prof0 + i];
-      const double k = pe.cls == 0 ? 2.0 : 1.0;
-      // dense: [shared + routed] x 2 passes; 4-bit: [shared] x 2, then [routed] x 2
-      const bool shared_part = c->q4 ? i < 2 && c->Ish > 0 : true;
-      const bool routed_part = c->q4 ? !(i < 2 && c->Ish > 0) : true;
-      pe.bytes = k * ((shared_part ? sh_bytes : 0.0) + (routed_part ? routed_bytes : 0.0));
-      pe.flops = k * ((shared_part ? sh_flops : 0.0) + (routed_part ? routed_flops : 0.0));
-    }
-  }
+  if (c->profile && c->early_nprof) early_prof_bytes(c, rec, T, c->early_busy, c->early_prof0, c->early_nprof);
   c->early_nprof = 0;
 }
 
@@ -1625,7 +1741,9 @@ static int expert_ffn_run(promoe_ctx* c, int layer, int T, const float* d_w, con
   const PlanRecord& rec = c->route_rec;
 
   std::unique_lock<std::mutex> lk(c->mu);
-  const int n = rec.n;
+  const bool lazy = c->route_lazy;
+  c->route_lazy = false;
+  const int n = lazy ? 0 : rec.n;
   // On another stream than the route's, order this call after everything the
   // route enqueued: its top-k and plan (ids, weights, slots, permutation) and
   // the readers of the first fills' victim slots it may have started.
@@ -1633,7 +1751,7 @@ static int expert_ffn_run(promoe_ctx* c, int layer, int T, const float* d_w, con
   // Outputs the route's own launches wrote into the context's buffers, when this
   // call keeps its expert outputs elsewhere (the allocation-free variant): every
   // pair's row is carried over, and the launches below overwrite the rest.
-  const bool any_started = c->shared_started ||
+  const bool any_started = lazy || c->shared_started ||
                            std::find(c->ffn_started.begin(), c->ffn_started.end(), 1) != c->ffn_started.end();
   if (any_started && a.Y != c->d_Y) {
     HIPCHK(hipMemcpyAsync(a.Y, c->d_Y, sizeof(float) * (size_t)T * c->K * c->H, hipMemcpyDeviceToDevice, s));
@@ -1755,6 +1873,7 @@ static int expert_ffn_run(promoe_ctx* c, int layer, int T, const float* d_w, con
   c->route_layer = -1;
   if (c->profile && !c->noalloc_call && c->prof_pending.size() > 4096) {
     HIPCHK(hipStreamSynchronize(s));
+    HIPCHK(drain_records(c, true));  // lazy routes' plans give their launches' bytes
     prof_resolve(c);
   }
   return PROMOE_OK;
@@ -1824,6 +1943,7 @@ int promoe_cache_stats(promoe_ctx* c, int layer, promoe_stats* out) {
   out->low_purged = ps.low_purged;
   out->deferred = ps.deferred;
   out->pred_in_time = c->pred_in_time;
+  out->lazy_routes = c->n_lazy_routes;
   for (int i = 0; i < promoe_ctx::kClasses; ++i) {
     out->k_launches[i] = c->k_launches[i];
     out->k_ms[i] = c->k_ms[i];
@@ -1844,6 +1964,7 @@ int promoe_reset_stats(promoe_ctx* c) {
   std::lock_guard<std::mutex> lk(c->mu);
   c->pf->reset_stats();
   c->pred_in_time = 0;
+  c->n_lazy_routes = 0;
   for (int i = 0; i < promoe_ctx::kClasses; ++i) c->k_launches[i] = 0, c->k_ms[i] = c->k_bytes[i] = c->k_flops[i] = 0.0;
   c->stall_ms = 0.0;
   return PROMOE_OK;

@@ -439,3 +439,44 @@ def test_stack_step_in_one_call(T, lookahead):
                 assert a[c] == b[c], (l, c)
     finally:
         m.close()
+
+
+@pytest.mark.parametrize("T", [1, 4])
+def test_stack_step_all_resident_lazy_routes(T):
+    # With every expert of every layer resident, the layer loop's routes return
+    # without waiting for their plans on the host and the plans are taken in
+    # later.  The residual stream, the plans, the device counters, the in-time
+    # predictions and the launches' profiled bytes must equal those of the
+    # separate calls (whose routes wait, since they ask for the order) bit for
+    # bit; a run of steps with no host read in between lets the plans queue up.
+    cfg = SMALL.with_(lookahead=1, slots=SMALL.n_experts)
+    _log("stack_step all resident T", T)
+    m = SyntheticModel(cfg, max_tokens=T, flags=_abi.FLAG_PROFILE)
+    try:
+        st = Stack(m, T)
+        runs = []
+        for native in (False, True):
+            m.open(flags=_abi.FLAG_PROFILE)
+            hs, plans = [], []
+            for step in range(14):
+                h0 = torch.from_numpy(sm.stack_input(cfg, 995 + step, T)).cuda()
+                hs.append(pu.to_np(st.step(h0, native=native)).copy())
+                if step < 2 or step == 13:
+                    plans.append([(m.ctx.last_plan(l, 0)["slot"], m.ctx.last_plan(l, 1)["slot"])
+                                  for l in range(cfg.n_layers)])
+            runs.append((hs, plans, [m.ctx.stats(l) for l in range(cfg.n_layers)], m.ctx.stats(-1)))
+        (h_a, p_a, s_a, t_a), (h_b, p_b, s_b, t_b) = runs
+        assert t_a["lazy_routes"] == 0 and t_b["lazy_routes"] == 14 * cfg.n_layers, (t_a["lazy_routes"],
+                                                                                     t_b["lazy_routes"])
+        for i, (a, b) in enumerate(zip(h_a, h_b)):
+            assert np.array_equal(a, b), ("step", i)
+        assert p_a == p_b
+        for l, (a, b) in enumerate(zip(s_a, s_b)):
+            for c in ocache.COUNTERS:
+                assert a[c] == b[c], (l, c)
+        assert t_a["miss"] == 0 and t_a["pred_in_time"] == t_a["pred_correct"] > 0
+        assert t_b["pred_in_time"] == t_a["pred_in_time"]
+        assert t_b["k_launches"][:2] == t_a["k_launches"][:2]
+        assert t_b["k_bytes"][:2] == t_a["k_bytes"][:2]
+    finally:
+        m.close()
