@@ -1,19 +1,24 @@
 // Skinny matrix-vector kernels for gfx950 (wave64):
 //  * k_rows_gemv   -- gate logits + predictor rows in one pass over x, the
-//                     predictor's second layer, the attention surrogate;
+//                     predictor's second layer, the attention surrogate
+//                     (k_rows_gemv_reg for groups of up to four tokens);
 //  * k_ffn_gateup  -- expert pass 1: gate and up rows of the experts of a
 //                     launch segment read together, act = q(silu(a) * b);
 //  * k_ffn_down    -- expert pass 2: Y = Wd act, scattered to (token, rank);
-//  * k_combine     -- y = sum_r w Y + s Ysh, fixed r order, one rounding;
-//  * k_rmsnorm_quant, k_residual_add -- the layer around the MoE block.
+//  * k_combine     -- y = sum_r w Y + s Ysh, fixed r order, one rounding
+//                     (k_combine_residual also adds y into the residual);
+//  * k_rmsnorm_quant(_reg), k_residual_add -- the layer around the MoE block.
 //
-// All GEMVs share one scheme: a wave owns R weight rows; every lane streams
-// 16-byte pieces of those rows (global_load_dwordx4, coalesced across the
-// wave, U pieces per row in flight); the token vectors are staged in LDS as
-// fp32 in K-slabs shared by the block's four waves; each lane accumulates in
-// fp32 and the wave reduces at the end.  Weight bytes are read once per token
-// group of up to MT tokens, which is what bounds decode (HBM) throughput.
+// Every GEMV lets a wave own R weight rows, with every lane streaming 16-byte
+// pieces of them (global_load_dwordx4, coalesced across the wave), accumulating
+// in fp32, and the wave reducing at the end.  The rows kernel for larger token
+// groups stages the tokens in LDS as fp32 K-slabs shared by the block's four
+// waves; the expert GEMVs and the decode rows kernel keep each lane's token
+// pieces in registers instead.  Weight bytes are read once per token group of
+// up to MT tokens, which is what bounds decode (HBM) throughput.
 #include <hip/hip_ext.h>
+
+#include <type_traits>
 
 #include "common.hpp"
 #include "kernels.hpp"
@@ -642,7 +647,90 @@ __global__ __launch_bounds__(kThreads) void k_combine_residual(CombineArgs a, fl
   h[(size_t)t * a.hidden + n] += Elem<TY>::quant(y);
 }
 
+// ============================================================ decode rows GEMV
+// Token groups of up to four with weights and tokens of one type: the FFN
+// GEMVs' scheme instead of the LDS slab -- one row per wave, each lane holding
+// its 16-byte pieces of the token vectors in registers and issuing all of its
+// weight loads before the first FMA, so a launch is one memory round trip
+// deep (the slab kernel waits for the tokens to reach LDS first, and its four
+// rows per wave leave most CUs idle on a 2048-row matrix).
+template <typename TW, int MT, int NCH>
+__global__ __launch_bounds__(kThreads) void k_rows_gemv_reg(RowsArgs a) {
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const int ntot = a.nrows[0] + a.nrows[1] + a.nrows[2];
+  const int row = blockIdx.x * kWaves + wave;
+  const int t0 = blockIdx.y * MT;
+  const int mt = min(MT, a.T - t0);
+  if (mt <= 0 || row >= ntot) return;
+  const TW* xs[MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) xs[m] = reinterpret_cast<const TW*>(a.x) + (size_t)(t0 + min(m, mt - 1)) * a.ldx + a.x_off;
+  int j = row, src = 0;
+  if (j >= a.nrows[0]) { j -= a.nrows[0]; src = 1; if (j >= a.nrows[1]) { j -= a.nrows[1]; src = 2; } }
+  const TW* const rows[1] = {reinterpret_cast<const TW*>(a.w[src]) + (size_t)j * a.K};
+  const bool rv[1] = {true};
+  float acc[1][MT];
+#pragma unroll
+  for (int m = 0; m < MT; ++m) acc[0][m] = 0.0f;
+  wave_rows_dot<TW, 1, MT, NCH>(rows, rv, xs, mt, a.K / Elem<TW>::kPer16B, lane, acc);
+#pragma unroll
+  for (int m = 0; m < MT; ++m) acc[0][m] = wave_sum(acc[0][m]);
+  if (lane < MT) {
+    float v = 0.0f;
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+      if (m == lane) v = acc[0][m];
+    if (lane < mt) {
+      float* o = a.out + (size_t)(t0 + lane) * a.ldo + a.o_off + row;
+      *o = a.add ? *o + v : v;
+    }
+  }
+}
+
 // ============================================================ harness ops
+// RMSNorm of one token per block with the row held in registers: each thread
+// loads its VPT 16-byte pieces at once (one memory round trip, where a strided
+// loop waits for every element in turn), sums their squares in piece order,
+// and the waves reduce in a fixed order.  H % 4 == 0, H <= 4 * VPT * kThreads.
+template <typename TQ, int VPT>
+__global__ __launch_bounds__(kThreads) void k_rmsnorm_quant_reg(const float* h, void* out, int H, float eps) {
+  const int t = blockIdx.x;
+  const float4* v = reinterpret_cast<const float4*>(h + (size_t)t * H);
+  const int n4 = H / 4;
+  __shared__ float red[kWaves];
+  float4 r[VPT];
+#pragma unroll
+  for (int u = 0; u < VPT; ++u) {
+    const int i = threadIdx.x + u * kThreads;
+    r[u] = i < n4 ? v[i] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  }
+  float s = 0.0f;
+#pragma unroll
+  for (int u = 0; u < VPT; ++u) {
+    s = fmaf(r[u].x, r[u].x, s);
+    s = fmaf(r[u].y, r[u].y, s);
+    s = fmaf(r[u].z, r[u].z, s);
+    s = fmaf(r[u].w, r[u].w, s);
+  }
+  s = wave_sum(s);
+  if (threadIdx.x % kWave == 0) red[threadIdx.x / kWave] = s;
+  __syncthreads();
+  float tot = 0.0f;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) tot += red[w];
+  const float inv = 1.0f / sqrtf(tot / (float)H + eps);
+  TQ* o = reinterpret_cast<TQ*>(out) + (size_t)t * H;
+#pragma unroll
+  for (int u = 0; u < VPT; ++u) {
+    const int i = threadIdx.x + u * kThreads;
+    if (i >= n4) continue;
+    Elem<TQ>::store(o, 4 * i, r[u].x * inv);
+    Elem<TQ>::store(o, 4 * i + 1, r[u].y * inv);
+    Elem<TQ>::store(o, 4 * i + 2, r[u].z * inv);
+    Elem<TQ>::store(o, 4 * i + 3, r[u].w * inv);
+  }
+}
+
 template <typename TQ>
 __global__ __launch_bounds__(kThreads) void k_rmsnorm_quant(const float* h, void* out, int H, float eps) {
   const int t = blockIdx.x;
@@ -667,9 +755,32 @@ __global__ __launch_bounds__(kThreads) void k_residual_add(float* h, const void*
 }
 
 // ============================================================ launchers
+template <typename TW, int MT>
+static void rows_reg_launch(const RowsArgs& a, int ntot, hipStream_t s) {
+  const dim3 grid((ntot + kWaves - 1) / kWaves, (a.T + MT - 1) / MT);
+  const int pieces = a.K / Elem<TW>::kPer16B;
+  if (pieces <= kWave) k_rows_gemv_reg<TW, MT, 1><<<grid, kThreads, 0, s>>>(a);
+  else if (pieces <= 2 * kWave) k_rows_gemv_reg<TW, MT, 2><<<grid, kThreads, 0, s>>>(a);
+  else k_rows_gemv_reg<TW, MT, 4><<<grid, kThreads, 0, s>>>(a);
+}
+
 template <typename TW, typename TX>
 static void rows_dispatch(const RowsArgs& a, hipStream_t s) {
   const int ntot = a.nrows[0] + a.nrows[1] + a.nrows[2];
+  if constexpr (std::is_same<TW, TX>::value) {
+    // decode-sized groups over 16-byte aligned rows and tokens: registers, no LDS
+    constexpr int EPC = Elem<TW>::kPer16B;
+    bool aligned = a.K % EPC == 0 && a.ldx % EPC == 0 && a.x_off % EPC == 0 &&
+                   reinterpret_cast<uintptr_t>(a.x) % 16 == 0;
+    for (int i = 0; i < 3; ++i)
+      if (a.nrows[i] > 0) aligned = aligned && reinterpret_cast<uintptr_t>(a.w[i]) % 16 == 0;
+    if (aligned && a.relu_in == 0 && a.T <= 4 && ntot > 0) {
+      if (a.T >= 4) rows_reg_launch<TW, 4>(a, ntot, s);
+      else if (a.T >= 2) rows_reg_launch<TW, 2>(a, ntot, s);
+      else rows_reg_launch<TW, 1>(a, ntot, s);
+      return;
+    }
+  }
   const int rows_per_block = kWaves * 4;
   const int mt = a.T >= 4 ? 4 : (a.T >= 2 ? 2 : 1);
   dim3 grid((ntot + rows_per_block - 1) / rows_per_block, (a.T + mt - 1) / mt);
@@ -815,9 +926,21 @@ void launch_combine_residual(const CombineArgs& a, float* h, int T, int dtype, h
   else k_combine_residual<float><<<grid, kThreads, 0, s>>>(a, h);
 }
 
+template <typename TQ>
+static void rmsnorm_dispatch(const float* h, void* out, int T, int H, hipStream_t s) {
+  const int n4 = H / 4;
+  if (H % 4 == 0 && reinterpret_cast<uintptr_t>(h) % 16 == 0 && n4 <= 4 * kThreads) {
+    if (n4 <= kThreads) k_rmsnorm_quant_reg<TQ, 1><<<T, kThreads, 0, s>>>(h, out, H, 1e-6f);
+    else if (n4 <= 2 * kThreads) k_rmsnorm_quant_reg<TQ, 2><<<T, kThreads, 0, s>>>(h, out, H, 1e-6f);
+    else k_rmsnorm_quant_reg<TQ, 4><<<T, kThreads, 0, s>>>(h, out, H, 1e-6f);
+  } else {
+    k_rmsnorm_quant<TQ><<<T, kThreads, 0, s>>>(h, out, H, 1e-6f);
+  }
+}
+
 void launch_rmsnorm_quant(const float* h, void* out, int T, int H, int dtype, hipStream_t s) {
-  if (dtype == 1) k_rmsnorm_quant<bf16_t><<<T, kThreads, 0, s>>>(h, out, H, 1e-6f);
-  else k_rmsnorm_quant<float><<<T, kThreads, 0, s>>>(h, out, H, 1e-6f);
+  if (dtype == 1) rmsnorm_dispatch<bf16_t>(h, out, T, H, s);
+  else rmsnorm_dispatch<float>(h, out, T, H, s);
 }
 
 void launch_residual_add(float* h, const void* y, int n, int dtype, hipStream_t s) {
