@@ -199,6 +199,9 @@ void launch_residual_add(float* h, const void* y, int n, int dtype, hipStream_t 
 void launch_topk(const TopkArgs& a, hipStream_t s);
 void launch_plan_spec(const PlanArgs& a, hipStream_t s);
 void launch_plan_precise(const PlanArgs& a, hipStream_t s);
+// the router's top-k and the precise plan in one launch (T * k <= kFusedRouteMaxPairs)
+constexpr int kFusedRouteMaxPairs = 64;
+void launch_route_plan(const TopkArgs& tk, const PlanArgs& a, hipStream_t s);
 void launch_state_init(CacheState st, int L, int C, int E, hipStream_t s);
 void launch_warm(CacheState st, int layer, int C, int E, const int32_t* d_experts, int n, hipStream_t s);
 

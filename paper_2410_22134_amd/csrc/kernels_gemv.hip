@@ -612,20 +612,45 @@ void launch_dequant_q4(const DequantArgs& a, hipStream_t s) {
 }
 
 // ============================================================ combine
+// y[t][n] = sum_r w[t][r] Y[t][r][n] + s[t] sum_k Ysh[k][t][n], r and k in
+// order, one rounding.  Every operand of the element is loaded before the
+// first product (up to kMaxK ranks and 8 split-K slices), so the kernel waits
+// for one memory round trip instead of one per term.
+__device__ __forceinline__ float combine_value(const CombineArgs& a, int t, int n) {
+  constexpr int kSplitRegs = 8;
+  float wv[kMaxK], yv[kMaxK], sv[kSplitRegs];
+#pragma unroll
+  for (int r = 0; r < kMaxK; ++r) {
+    const bool in = r < a.top_k;
+    wv[r] = in ? a.w[t * a.top_k + r] : 0.0f;
+    yv[r] = in ? a.Y[((size_t)t * a.top_k + r) * a.hidden + n] : 0.0f;
+  }
+  const int split = a.Ysh ? a.ysh_split : 0;
+#pragma unroll
+  for (int k = 0; k < kSplitRegs; ++k)
+    sv[k] = k < split ? a.Ysh[(size_t)k * a.ysh_split_stride + (size_t)t * a.hidden + n] : 0.0f;
+  float y = 0.0f;
+#pragma unroll
+  for (int r = 0; r < kMaxK; ++r)
+    if (r < a.top_k) y += wv[r] * yv[r];
+  if (a.Ysh) {
+    float ysh = 0.0f;
+#pragma unroll
+    for (int k = 0; k < kSplitRegs; ++k)
+      if (k < split) ysh += sv[k];
+    for (int k = kSplitRegs; k < split; ++k) ysh += a.Ysh[(size_t)k * a.ysh_split_stride + (size_t)t * a.hidden + n];
+    const float s = a.sscale ? a.sscale[t] : 1.0f;
+    y += s * ysh;
+  }
+  return y;
+}
+
 template <typename TY>
 __global__ __launch_bounds__(kThreads) void k_combine(CombineArgs a) {
   const int t = blockIdx.y;
   const int n = blockIdx.x * kThreads + threadIdx.x;
   if (n >= a.hidden) return;
-  float y = 0.0f;
-  for (int r = 0; r < a.top_k; ++r) y += a.w[t * a.top_k + r] * a.Y[((size_t)t * a.top_k + r) * a.hidden + n];
-  if (a.Ysh) {
-    float ysh = 0.0f;
-    for (int k = 0; k < a.ysh_split; ++k) ysh += a.Ysh[(size_t)k * a.ysh_split_stride + (size_t)t * a.hidden + n];
-    const float s = a.sscale ? a.sscale[t] : 1.0f;
-    y += s * ysh;
-  }
-  Elem<TY>::store(reinterpret_cast<TY*>(a.y), t * a.hidden + n, y);
+  Elem<TY>::store(reinterpret_cast<TY*>(a.y), t * a.hidden + n, combine_value(a, t, n));
 }
 
 // Combine and residual add in one launch (the layer loop's combine -> h += y):
@@ -635,14 +660,7 @@ __global__ __launch_bounds__(kThreads) void k_combine_residual(CombineArgs a, fl
   const int t = blockIdx.y;
   const int n = blockIdx.x * kThreads + threadIdx.x;
   if (n >= a.hidden) return;
-  float y = 0.0f;
-  for (int r = 0; r < a.top_k; ++r) y += a.w[t * a.top_k + r] * a.Y[((size_t)t * a.top_k + r) * a.hidden + n];
-  if (a.Ysh) {
-    float ysh = 0.0f;
-    for (int k = 0; k < a.ysh_split; ++k) ysh += a.Ysh[(size_t)k * a.ysh_split_stride + (size_t)t * a.hidden + n];
-    const float s = a.sscale ? a.sscale[t] : 1.0f;
-    y += s * ysh;
-  }
+  const float y = combine_value(a, t, n);
   Elem<TY>::store(reinterpret_cast<TY*>(a.y), t * a.hidden + n, y);
   h[(size_t)t * a.hidden + n] += Elem<TY>::quant(y);
 }

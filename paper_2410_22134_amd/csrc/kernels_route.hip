@@ -14,7 +14,8 @@
 //  * k_plan_precise  -- precise plan of the routed layer (Alg. 2
 //                       PushPreciseExperts, Sec. "Reordered Inference"):
 //                       hit/miss, order, victim slots, counters, followed by the
-//                       token permutation grouping (t, r) pairs by position.
+//                       token permutation grouping (t, r) pairs by position;
+//                       k_route_plan runs the top-k first in the same block.
 //
 // Both plans run in one workgroup: the counting phases use all 256 threads,
 // the sequential LRU walk runs in wave 0 with one lane per slot (for slot
@@ -32,10 +33,8 @@ enum {
 };
 
 // ============================================================ top-k
-__global__ __launch_bounds__(256) void k_topk(TopkArgs a) {
-  const int lane = threadIdx.x % kWave;
-  const int t = blockIdx.x * 4 + threadIdx.x / kWave;
-  if (t >= a.T) return;
+// Token t by one wave (lane = expert); ids_copy (LDS, may be null) also gets the ids.
+__device__ __forceinline__ void topk_token(const TopkArgs& a, int t, int lane, int32_t* ids_copy) {
   const bool valid = lane < a.E;
   float z = -INFINITY;
   if (valid) z = a.logits[(size_t)t * a.ld + lane] + (a.bias ? a.bias[lane] : 0.0f);
@@ -45,7 +44,10 @@ __global__ __launch_bounds__(256) void k_topk(TopkArgs a) {
     const uint64_t kmax = wave_max_u64(key);
     const int e = 63 - (int)(uint32_t)(kmax & 0xFFFFFFFFu);
     if (lane == e) { myrank = r; key = 0ull; }
-    if (lane == 0) a.ids[t * a.k + r] = e;
+    if (lane == 0) {
+      a.ids[t * a.k + r] = e;
+      if (ids_copy) ids_copy[t * a.k + r] = e;
+    }
   }
   if (a.want_weights) {
     const float zmax = wave_max(valid ? z : -INFINITY);
@@ -57,6 +59,12 @@ __global__ __launch_bounds__(256) void k_topk(TopkArgs a) {
       a.sscale[t] = 1.0f / (1.0f + expf(-u));
     }
   }
+}
+
+__global__ __launch_bounds__(256) void k_topk(TopkArgs a) {
+  const int t = blockIdx.x * 4 + threadIdx.x / kWave;
+  if (t >= a.T) return;
+  topk_token(a, t, threadIdx.x % kWave, nullptr);
 }
 
 // ============================================================ plan helpers
@@ -355,14 +363,26 @@ __global__ __launch_bounds__(256) void k_predict_plan(PredictPlanArgs p) {
 }
 
 // ============================================================ precise plan + permutation
-__global__ __launch_bounds__(256) void k_plan_precise(PlanArgs a) {
-  __shared__ int cnt_e[kMaxE], pos_of[kMaxE], order[kMaxE], offs[kMaxE + 1], fill[kMaxE];
-  __shared__ int n_pos;
+struct PreciseLds {
+  int cnt_e[kMaxE], pos_of[kMaxE], order[kMaxE], offs[kMaxE + 1], fill[kMaxE];
+  int n_pos;
+  int wave_cnt[4][kMaxE];
+};
+
+// The precise plan over the routed ids `ids` [T x k] (global, or LDS when the
+// top-k ran in the same block).  All 256 threads of the block enter.
+__device__ __forceinline__ void plan_precise_body(const PlanArgs& a, const int32_t* ids, PreciseLds& sh) {
+  int* cnt_e = sh.cnt_e;
+  int* pos_of = sh.pos_of;
+  int* order = sh.order;
+  int* offs = sh.offs;
+  int* fill = sh.fill;
+  int& n_pos = sh.n_pos;
   const int tid = threadIdx.x, lane = tid % kWave;
   const int npairs = a.T * a.k;
   if (tid < kMaxE) { cnt_e[tid] = 0; fill[tid] = 0; }
   __syncthreads();
-  for (int i = tid; i < npairs; i += 256) atomicAdd(&cnt_e[a.ids[i]], 1);
+  for (int i = tid; i < npairs; i += 256) atomicAdd(&cnt_e[ids[i]], 1);
   __syncthreads();
 
   WaveState w;
@@ -456,12 +476,12 @@ __global__ __launch_bounds__(256) void k_plan_precise(PlanArgs a) {
   // lanes with the same position are found with six ballots (one per bit of the
   // position), which gives each pair its rank among the earlier lanes; the waves'
   // counts are then prefixed through LDS.
-  __shared__ int wave_cnt[4][kMaxE];
+  int (&wave_cnt)[4][kMaxE] = sh.wave_cnt;
   const int wave = tid / kWave;
   const uint64_t lt_mask = (1ull << lane) - 1ull;
   for (int base = 0; base < npairs; base += 256) {
     const int i = base + tid;
-    const int pos = i < npairs ? pos_of[a.ids[i]] : -1;
+    const int pos = i < npairs ? pos_of[ids[i]] : -1;
     for (int e = tid; e < 4 * kMaxE; e += 256) (&wave_cnt[0][0])[e] = 0;
     uint64_t same = __ballot(pos >= 0);
 #pragma unroll
@@ -487,6 +507,21 @@ __global__ __launch_bounds__(256) void k_plan_precise(PlanArgs a) {
     __threadfence_system();
     a.rec->done = 1;
   }
+}
+
+__global__ __launch_bounds__(256) void k_plan_precise(PlanArgs a) {
+  __shared__ PreciseLds sh;
+  plan_precise_body(a, a.ids, sh);
+}
+
+// Decode-sized steps: the router's top-k and the precise plan in one block
+// (one launch and no global round trip between them).  T * k <= kFusedRouteMaxPairs.
+__global__ __launch_bounds__(256) void k_route_plan(TopkArgs tk, PlanArgs a) {
+  __shared__ int32_t ids_l[kFusedRouteMaxPairs];
+  __shared__ PreciseLds sh;
+  for (int t = threadIdx.x / kWave; t < tk.T; t += 4) topk_token(tk, t, threadIdx.x % kWave, ids_l);
+  __syncthreads();
+  plan_precise_body(a, ids_l, sh);
 }
 
 // ============================================================ state init / warm start
@@ -517,6 +552,7 @@ void launch_topk(const TopkArgs& a, hipStream_t s) {
 void launch_plan_spec(const PlanArgs& a, hipStream_t s) { k_plan_spec<<<1, 256, 0, s>>>(a); }
 void launch_predict_plan(const PredictPlanArgs& p, hipStream_t s) { k_predict_plan<<<1, 256, 0, s>>>(p); }
 void launch_plan_precise(const PlanArgs& a, hipStream_t s) { k_plan_precise<<<1, 256, 0, s>>>(a); }
+void launch_route_plan(const TopkArgs& tk, const PlanArgs& a, hipStream_t s) { k_route_plan<<<1, 256, 0, s>>>(tk, a); }
 void launch_state_init(CacheState st, int L, int C, int E, hipStream_t s) {
   int n = L * (C > E ? C : E);
   if (n < L * kCounters) n = L * kCounters;

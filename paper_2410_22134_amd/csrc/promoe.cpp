@@ -1288,12 +1288,15 @@ static int route_impl(promoe_ctx* c, int layer, const void* d_x, int T, int32_t*
   const bool sg = c->cfg.shared_gate && c->Ish > 0;
   tk.sgate_col = sg ? c->E : -1;
   tk.sscale = sg ? d_shared_scale : nullptr;
-  launch_topk(tk, s);
-  LAUNCHCHK("route topk");
   int64_t r;
   rc = new_record(c, 1, PROMOE_PRIO_HIGH, &r);
   if (rc) return rc;
-  launch_plan_precise(plan_args(c, layer, d_ids, T, r), s);
+  if ((int64_t)T * c->K <= kFusedRouteMaxPairs) {
+    launch_route_plan(tk, plan_args(c, layer, d_ids, T, r), s);
+  } else {
+    launch_topk(tk, s);
+    launch_plan_precise(plan_args(c, layer, d_ids, T, r), s);
+  }
   hipError_t le = hipGetLastError();
   if (le == hipSuccess) le = hipEventRecord(c->rec_ev[r % kRecRing], s);
   bool early_ffn = false, lazy = false;
