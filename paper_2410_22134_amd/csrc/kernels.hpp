@@ -142,6 +142,8 @@ struct PlanArgs {
   int32_t* d_perm;       // [T*k]
   int32_t* d_pos_of;     // [64] scratch
   int32_t* d_npos;       // [1] precise plan: resident positions (reordered: they come first)
+  int host_done;         // 1: end with a system-scope fence and the record's done word (the
+                         // host polls it); 0: neither (the host waits on the plan's event)
 };
 
 // Predictor tail and spec plan in one block (steps of at most kFusedPredMaxT
@@ -158,6 +160,8 @@ struct PredictPlanArgs {
   int32_t* pred_ids;    // [T x k] out
 };
 void launch_predict_plan(const PredictPlanArgs& p, hipStream_t s);
+// launch_route_plan with the prediction of predict_plan as a second block
+void launch_route_plan_predict(const TopkArgs& tk, const PlanArgs& a, const PredictPlanArgs& p, hipStream_t s);
 
 // Expand 4-bit experts into dense bf16 [Wg | Wu | Wd] copies (the MFMA GEMM's
 // operand type: each weight (code - 8) * scale is rounded to bf16).
@@ -170,6 +174,11 @@ constexpr int kStageExperts = 8;
 void launch_dequant_q4(const DequantArgs& a, hipStream_t s);
 
 void launch_rows_gemv(const RowsArgs& a, int wdtype, int xdtype, hipStream_t s);
+// Batch-1 bf16 rows GEMV over x = q(rms(h)) computed in the kernel, bit for bit
+// launch_rmsnorm_quant then launch_rows_gemv; out = (add_src ? add_src : 0) +
+// dot; x_out (or null) receives x.  a.x is unused.  Returns false, launching
+// nothing, where the separate kernels would not take their register paths.
+bool launch_rows_gemv_norm(const RowsArgs& a, const float* h, const float* add_src, void* x_out, hipStream_t s);
 // Launches one pass of the GEMV kernels over the jobs (a copy of `a` is
 // adjusted per pass; `a` is unchanged).  max_tokens = most pairs of any job.
 // With ev0/ev1 set, the launch records them itself at the kernel's start and

@@ -705,6 +705,91 @@ __global__ __launch_bounds__(kThreads) void k_rows_gemv_reg(RowsArgs a) {
   }
 }
 
+// ============================================================ batch-1 rows GEMV over q(rms(h))
+// The RMSNorm that feeds a batch-1 rows GEMV folded into it.  Each block forms
+// x = q(rms(h)) once, as k_rmsnorm_quant_reg does (thread t sums the squares of
+// its VPT pieces t + 256 u in order, the waves' sums -- lane 0's -- are added in
+// order, each thread stores its pieces of x rounded to bf16), but into LDS; its
+// waves then take their x pieces from there and form the dot in
+// k_rows_gemv_reg's order (pieces lane + 64 u, u ascending).  The result is bit
+// for bit the two kernels', with one launch and one dependent kernel fewer; the
+// weight loads are issued first and overlap the norm.  add_src: out = add_src
+// + dot (a second residual buffer, so no block reads a row of h that another
+// has already updated); x_out: block 0 also stores x.
+template <int VPT, int NCH>
+__global__ __launch_bounds__(kThreads) void k_rows_gemv_norm(RowsArgs a, const float* h, float eps,
+                                                             const float* add_src, bf16_t* x_out) {
+  __shared__ __attribute__((aligned(16))) bf16_t xs[4 * VPT * kThreads];
+  __shared__ float red[kWaves];
+  const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+  const int ntot = a.nrows[0] + a.nrows[1] + a.nrows[2];
+  const int row = blockIdx.x * kWaves + wave;
+  const bool has_row = row < ntot;
+  const int H = a.K, nch = H / 8, n4 = H / 4;
+  uint4 wr[NCH];
+  if (has_row) {
+    int j = row, src = 0;
+    if (j >= a.nrows[0]) { j -= a.nrows[0]; src = 1; if (j >= a.nrows[1]) { j -= a.nrows[1]; src = 2; } }
+    const bf16_t* wrow = reinterpret_cast<const bf16_t*>(a.w[src]) + (size_t)j * H;
+#pragma unroll
+    for (int u = 0; u < NCH; ++u) {
+      const int c = lane + u * kWave;
+      wr[u] = c < nch ? ld16_stream(wrow + (size_t)c * 8) : make_uint4(0, 0, 0, 0);
+    }
+  }
+  const float4* h4 = reinterpret_cast<const float4*>(h);
+  float4 r[VPT];
+#pragma unroll
+  for (int u = 0; u < VPT; ++u) {
+    const int i = tid + u * kThreads;
+    r[u] = i < n4 ? h4[i] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  }
+  float sq = 0.0f;
+#pragma unroll
+  for (int u = 0; u < VPT; ++u) {
+    sq = fmaf(r[u].x, r[u].x, sq);
+    sq = fmaf(r[u].y, r[u].y, sq);
+    sq = fmaf(r[u].z, r[u].z, sq);
+    sq = fmaf(r[u].w, r[u].w, sq);
+  }
+  sq = wave_sum(sq);
+  if (lane == 0) red[wave] = sq;
+  __syncthreads();
+  float tot = 0.0f;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) tot += red[w];
+  const float inv = 1.0f / sqrtf(tot / (float)H + eps);
+#pragma unroll
+  for (int u = 0; u < VPT; ++u) {
+    const int i = tid + u * kThreads;
+    if (i < n4) {
+      const bf16_t q0 = f32_to_bf16(r[u].x * inv), q1 = f32_to_bf16(r[u].y * inv);
+      const bf16_t q2 = f32_to_bf16(r[u].z * inv), q3 = f32_to_bf16(r[u].w * inv);
+      const uint2 q = make_uint2((uint32_t)q0 | ((uint32_t)q1 << 16), (uint32_t)q2 | ((uint32_t)q3 << 16));
+      *reinterpret_cast<uint2*>(&xs[4 * i]) = q;
+      if (x_out && blockIdx.x == 0) *reinterpret_cast<uint2*>(x_out + 4 * (size_t)i) = q;
+    }
+  }
+  __syncthreads();
+  if (!has_row) return;
+  float acc = 0.0f;
+#pragma unroll
+  for (int u = 0; u < NCH; ++u) {
+    const int c = lane + u * kWave;
+    float xf[8], wf[8];
+    const uint4 xq = c < nch ? *reinterpret_cast<const uint4*>(&xs[8 * c]) : make_uint4(0, 0, 0, 0);
+    unpack16(xq, xf);
+    unpack16(wr[u], wf);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc = fmaf(wf[e], xf[e], acc);
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) {
+    float* o = a.out + a.o_off + row;
+    *o = add_src ? add_src[row] + acc : acc;
+  }
+}
+
 // ============================================================ harness ops
 // RMSNorm of one token per block with the row held in registers: each thread
 // loads its VPT 16-byte pieces at once (one memory round trip, where a strided
@@ -942,6 +1027,34 @@ void launch_combine_residual(const CombineArgs& a, float* h, int T, int dtype, h
   dim3 grid((a.hidden + kThreads - 1) / kThreads, T);
   if (dtype == 1) k_combine_residual<bf16_t><<<grid, kThreads, 0, s>>>(a, h);
   else k_combine_residual<float><<<grid, kThreads, 0, s>>>(a, h);
+}
+
+template <int VPT>
+static void rows_norm_launch(const RowsArgs& a, int ntot, int pieces, const float* h, const float* add_src,
+                             bf16_t* x_out, hipStream_t s) {
+  const dim3 grid((ntot + kWaves - 1) / kWaves);
+  if (pieces <= kWave) k_rows_gemv_norm<VPT, 1><<<grid, kThreads, 0, s>>>(a, h, 1e-6f, add_src, x_out);
+  else if (pieces <= 2 * kWave) k_rows_gemv_norm<VPT, 2><<<grid, kThreads, 0, s>>>(a, h, 1e-6f, add_src, x_out);
+  else if (pieces <= 4 * kWave) k_rows_gemv_norm<VPT, 4><<<grid, kThreads, 0, s>>>(a, h, 1e-6f, add_src, x_out);
+  else k_rows_gemv_norm<VPT, 8><<<grid, kThreads, 0, s>>>(a, h, 1e-6f, add_src, x_out);
+}
+
+bool launch_rows_gemv_norm(const RowsArgs& a, const float* h, const float* add_src, void* x_out, hipStream_t s) {
+  // exactly the cases where the separate kernels take their register paths
+  // (launch_rmsnorm_quant and rows_dispatch), so the results agree bit for bit
+  const int ntot = a.nrows[0] + a.nrows[1] + a.nrows[2];
+  const int H = a.K, n4 = H / 4, pieces = H / 8;
+  auto al16 = [](const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 == 0; };
+  bool ok = a.T == 1 && ntot > 0 && H % 8 == 0 && n4 <= 4 * kThreads && a.relu_in == 0 && al16(h) &&
+            (!x_out || al16(x_out));
+  for (int i = 0; i < 3; ++i)
+    if (a.nrows[i] > 0) ok = ok && al16(a.w[i]);
+  if (!ok) return false;
+  bf16_t* xo = static_cast<bf16_t*>(x_out);
+  if (n4 <= kThreads) rows_norm_launch<1>(a, ntot, pieces, h, add_src, xo, s);
+  else if (n4 <= 2 * kThreads) rows_norm_launch<2>(a, ntot, pieces, h, add_src, xo, s);
+  else rows_norm_launch<4>(a, ntot, pieces, h, add_src, xo, s);
+  return true;
 }
 
 template <typename TQ>

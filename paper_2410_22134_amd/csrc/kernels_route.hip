@@ -178,19 +178,17 @@ __device__ __forceinline__ void plan_spec_body(const PlanArgs& a, const int32_t*
   }
   __syncthreads();
   if (a.ids) {
-    if (tid < a.E && votes[tid] > 0) {
-      const int ve = votes[tid], be = best[tid];
+    // rank of each voted expert by (votes desc, best rank asc, id asc): one
+    // wave, lane = expert, counting the larger keys (key order = that order)
+    if (tid < kWave) {
+      const int ve = lane < a.E ? votes[lane] : 0, be = lane < a.E ? best[lane] : kMaxK;
+      const uint32_t key = ve > 0 ? ((uint32_t)ve << 12) | ((uint32_t)(15 - be) << 6) | (uint32_t)(63 - lane) : 0u;
       int rank = 0;
-      for (int j = 0; j < a.E; ++j) {
-        const int vj = votes[j], bj = best[j];
-        rank += (vj > ve) || (vj == ve && bj < be) || (vj == ve && bj == be && j < tid);
-      }
-      if (rank < a.C) Q[rank] = tid;
-    }
-    if (tid == 0) {
-      int nv = 0;
-      for (int j = 0; j < a.E; ++j) nv += votes[j] > 0;
-      nq = min(nv, a.C);
+#pragma unroll
+      for (int j = 0; j < kWave; ++j) rank += __shfl(key, j, kWave) > key ? 1 : 0;
+      if (ve > 0 && rank < a.C) Q[rank] = lane;
+      const uint64_t voted = __ballot(ve > 0);
+      if (lane == 0) nq = min(__popcll(voted), a.C);
     }
   } else if (tid == 0) {
     nq = a.rec->n_q_in;
@@ -256,8 +254,10 @@ __device__ __forceinline__ void plan_spec_body(const PlanArgs& a, const int32_t*
     rec->n_hit = 0;
     rec->predicted = a.ids ? 1 : 0;
     rec->fill_budget = budget;
-    __threadfence_system();
-    rec->done = 1;
+    if (a.host_done) {
+      __threadfence_system();
+      rec->done = 1;
+    }
   }
 }
 
@@ -271,59 +271,78 @@ __global__ __launch_bounds__(256) void k_plan_spec(PlanArgs a) {
 // q[t][e] = W2[e] . relu(h[t]) (fp32 accumulation; or q = h when the
 // predictor is one layer), each token's top-k by (q desc, id asc) as k_topk
 // orders them, written out and kept in LDS, then the spec plan of the vote.
-__global__ __launch_bounds__(256) void k_predict_plan(PredictPlanArgs p) {
-  __shared__ float hs[kFusedPredMaxT * kFusedPredMaxHidden];
-  __shared__ float qs[kFusedPredMaxT * kMaxE];
-  __shared__ int32_t ids_l[kFusedPredMaxT * kMaxK];
-  __shared__ SpecLds sh;
+struct PredictLds {
+  float hs[kFusedPredMaxT * kFusedPredMaxHidden];
+  float qs[kFusedPredMaxT * kMaxE];
+  int32_t ids_l[kFusedPredMaxT * kMaxK];
+  SpecLds sh;
+};
+
+__device__ __forceinline__ void predict_plan_body(const PredictPlanArgs& p, PredictLds& L) {
+  float* hs = L.hs;
+  float* qs = L.qs;
+  int32_t* ids_l = L.ids_l;
   const PlanArgs& a = p.plan;
   const int tid = threadIdx.x, lane = tid % kWave, wv = tid / kWave;
   const int T = a.T, E = a.E, k = a.k, Ph = p.Ph;
   if (Ph > 0) {
+    // four threads per expert: thread q of expert e takes the 16-byte chunks
+    // q, q + 4, ... of its row; with bf16 weights every chunk is loaded before
+    // the hidden activations are staged, so the two loads overlap
+    const int n8 = Ph / 8;  // Ph % 8 == 0
+    const int e = tid >> 2, q = tid & 3;
+    constexpr int kChunks = kFusedPredMaxHidden / 8 / 4;
+    uint4 wq[kChunks];
+    if (p.w2_bf16) {
+      const uint4* row = reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(p.w2) + (size_t)(e < E ? e : 0) * Ph);
+#pragma unroll
+      for (int u = 0; u < kChunks; ++u) {
+        const int j8 = q + 4 * u;
+        wq[u] = (e < E && j8 < n8) ? row[j8] : make_uint4(0, 0, 0, 0);
+      }
+    }
     for (int i = tid; i < T * Ph; i += 256) {
       const int t = i / Ph, j = i - t * Ph;
       hs[i] = fmaxf(p.h[(size_t)t * p.ldh + j], 0.0f);
     }
     __syncthreads();
-    // four threads per expert: thread q of expert e takes the 16-byte chunks
-    // q, q + 4, ... of its row, eight loads in flight at a time, then the four
-    // partial sums meet by two shuffles
-    const int n8 = Ph / 8;  // Ph % 8 == 0
-    const int e = tid >> 2, q = tid & 3;
     float acc[kFusedPredMaxT];
 #pragma unroll
     for (int t = 0; t < kFusedPredMaxT; ++t) acc[t] = 0.0f;
     if (e < E) {
-      for (int base = q; base < n8; base += 32) {
-        float wj[8][8];
+      if (p.w2_bf16) {
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int j8 = base + 4 * u;
-          if (p.w2_bf16) {
-            const uint4 w = j8 < n8 ? reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(p.w2) + (size_t)e * Ph)[j8]
-                                    : make_uint4(0, 0, 0, 0);
-            const uint32_t q4[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              wj[u][2 * i] = __uint_as_float(q4[i] << 16);
-              wj[u][2 * i + 1] = __uint_as_float(q4[i] & 0xFFFF0000u);
-            }
-          } else {
-            const float* w = static_cast<const float*>(p.w2) + (size_t)e * Ph + j8 * 8;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) wj[u][i] = j8 < n8 ? w[i] : 0.0f;
-          }
-        }
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          const int j8 = base + 4 * u;
+        for (int u = 0; u < kChunks; ++u) {
+          const int j8 = q + 4 * u;
           if (j8 >= n8) break;
+          const uint32_t q4[4] = {wq[u].x, wq[u].y, wq[u].z, wq[u].w};
+          float wj[8];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            wj[2 * i] = __uint_as_float(q4[i] << 16);
+            wj[2 * i + 1] = __uint_as_float(q4[i] & 0xFFFF0000u);
+          }
 #pragma unroll
           for (int t = 0; t < kFusedPredMaxT; ++t) {
             if (t < T) {
               const float* h = hs + t * Ph + j8 * 8;
 #pragma unroll
-              for (int i = 0; i < 8; ++i) acc[t] = fmaf(wj[u][i], h[i], acc[t]);
+              for (int i = 0; i < 8; ++i) acc[t] = fmaf(wj[i], h[i], acc[t]);
+            }
+          }
+        }
+      } else {
+        for (int j8 = q; j8 < n8; j8 += 4) {
+          const float* w = static_cast<const float*>(p.w2) + (size_t)e * Ph + j8 * 8;
+          float wj[8];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) wj[i] = w[i];
+#pragma unroll
+          for (int t = 0; t < kFusedPredMaxT; ++t) {
+            if (t < T) {
+              const float* h = hs + t * Ph + j8 * 8;
+#pragma unroll
+              for (int i = 0; i < 8; ++i) acc[t] = fmaf(wj[i], h[i], acc[t]);
             }
           }
         }
@@ -359,7 +378,12 @@ __global__ __launch_bounds__(256) void k_predict_plan(PredictPlanArgs p) {
     }
   }
   __syncthreads();
-  plan_spec_body(a, ids_l, sh);
+  plan_spec_body(a, ids_l, L.sh);
+}
+
+__global__ __launch_bounds__(256) void k_predict_plan(PredictPlanArgs p) {
+  __shared__ PredictLds L;
+  predict_plan_body(p, L);
 }
 
 // ============================================================ precise plan + permutation
@@ -503,7 +527,7 @@ __device__ __forceinline__ void plan_precise_body(const PlanArgs& a, const int32
     if (tid < kMaxE) fill[tid] += wave_cnt[0][tid] + wave_cnt[1][tid] + wave_cnt[2][tid] + wave_cnt[3][tid];
     __syncthreads();
   }
-  if (tid == 0) {
+  if (tid == 0 && a.host_done) {
     __threadfence_system();
     a.rec->done = 1;
   }
@@ -522,6 +546,29 @@ __global__ __launch_bounds__(256) void k_route_plan(TopkArgs tk, PlanArgs a) {
   for (int t = threadIdx.x / kWave; t < tk.T; t += 4) topk_token(tk, t, threadIdx.x % kWave, ids_l);
   __syncthreads();
   plan_precise_body(a, ids_l, sh);
+}
+
+// The same, with the layer's prediction as a second block: its second layer,
+// top-k and the spec plan of the target layer (disjoint cache state; the plan
+// records are the route's and the prediction's), so the prediction needs no
+// launch or stream of its own.
+union RoutePredictLds {
+  struct {
+    int32_t ids_l[kFusedRouteMaxPairs];
+    PreciseLds sh;
+  } route;
+  PredictLds pred;
+};
+
+__global__ __launch_bounds__(256) void k_route_plan_predict(TopkArgs tk, PlanArgs a, PredictPlanArgs p) {
+  __shared__ RoutePredictLds L;
+  if (blockIdx.x == 1) {
+    predict_plan_body(p, L.pred);
+    return;
+  }
+  for (int t = threadIdx.x / kWave; t < tk.T; t += 4) topk_token(tk, t, threadIdx.x % kWave, L.route.ids_l);
+  __syncthreads();
+  plan_precise_body(a, L.route.ids_l, L.route.sh);
 }
 
 // ============================================================ state init / warm start
@@ -553,6 +600,9 @@ void launch_plan_spec(const PlanArgs& a, hipStream_t s) { k_plan_spec<<<1, 256, 
 void launch_predict_plan(const PredictPlanArgs& p, hipStream_t s) { k_predict_plan<<<1, 256, 0, s>>>(p); }
 void launch_plan_precise(const PlanArgs& a, hipStream_t s) { k_plan_precise<<<1, 256, 0, s>>>(a); }
 void launch_route_plan(const TopkArgs& tk, const PlanArgs& a, hipStream_t s) { k_route_plan<<<1, 256, 0, s>>>(tk, a); }
+void launch_route_plan_predict(const TopkArgs& tk, const PlanArgs& a, const PredictPlanArgs& p, hipStream_t s) {
+  k_route_plan_predict<<<2, 256, 0, s>>>(tk, a, p);
+}
 void launch_state_init(CacheState st, int L, int C, int E, hipStream_t s) {
   int n = L * (C > E ? C : E);
   if (n < L * kCounters) n = L * kCounters;

@@ -76,6 +76,8 @@ constexpr int kArrivalGroup = kCopyStreams;
 // Resident experts per FFN launch, for steps larger than decode (as many as
 // one 4-bit staging batch).
 constexpr int kResidentGroup = 8;
+// Expert jobs with at least this many token pairs run on the MFMA GEMM.
+constexpr int kGemmMinTokens = 16;
 
 class HipEngine : public CopyEngine {
  public:
@@ -240,8 +242,11 @@ struct promoe_ctx {
   size_t lazy_prof0[kRecRing] = {}, lazy_nprof[kRecRing] = {};  // its launch's profiling entries
   bool route_lazy = false;                  // the latest route is lazy
   int64_t n_lazy_routes = 0;
-  // promoe_stack_step: the FFN call's combine also adds y into fuse_h
+  // promoe_stack_step: the FFN call's combine also adds y into fuse_h, and
+  // the route computes x = q(rms(x_from_h)) inside its gate GEMV (batch 1)
   float* fuse_h = nullptr;
+  const float* x_from_h = nullptr;
+  float* d_h2 = nullptr;  // second residual buffer of the batch-1 layer loop
   // first predictor rows computed by a route's gate launch (layer, input, T)
   int pred_rows_layer = -1;
   const void* pred_rows_x = nullptr;
@@ -553,6 +558,7 @@ PlanArgs plan_args(promoe_ctx* c, int layer, const int32_t* ids, int T, int64_t 
   a.d_perm = c->d_perm;
   a.d_pos_of = c->d_pos_of;
   a.d_npos = c->d_npos;
+  a.host_done = 1;
   return a;
 }
 
@@ -609,6 +615,17 @@ int launch_gate_rows(promoe_ctx* c, int layer, const void* d_x, int T, bool with
   a.ldo = c->ld_logits;
   a.o_off = gate ? 0 : c->pred_col;  // the row groups land in consecutive columns
   if (a.nrows[0] + a.nrows[1] + a.nrows[2] == 0) return PROMOE_OK;
+  if (c->x_from_h) {
+    // x = q(rms(h)) for this input: in the gate GEMV where it can be (batch 1,
+    // bf16), else first on its own
+    const float* h = c->x_from_h;
+    c->x_from_h = nullptr;
+    if (c->dt == PROMOE_BF16 && launch_rows_gemv_norm(a, h, nullptr, const_cast<void*>(d_x), s)) {
+      LAUNCHCHK("gate rows");
+      return PROMOE_OK;
+    }
+    launch_rmsnorm_quant(h, const_cast<void*>(d_x), T, c->H, c->dt, s);
+  }
   if (c->dt == PROMOE_BF16 && T >= 64 && c->H % 64 == 0) {
     // prefill-sized: gate and predictor rows on MFMA, the single shared-gate row as a GEMV
     RowsGemmArgs g{};
@@ -755,7 +772,7 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
                o_act = take((size_t)c->eb * T * Kk * c->I), o_Y = take(sizeof(float) * (size_t)T * Kk * H),
                o_actsh = take((size_t)c->eb * T * std::max(c->Ish, 1)),
                o_Ysh = take(sizeof(float) * (size_t)kMaxSplit * T * H),
-               o_u = take((size_t)c->eb * T * H);
+               o_u = take((size_t)c->eb * T * H), o_h2 = take(sizeof(float) * (size_t)T * H);
   hipError_t e = hipMalloc(&c->dmem, off);
   if (e != hipSuccess) {
     delete c;
@@ -785,6 +802,7 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   c->d_act_sh = b + o_actsh;
   c->d_Ysh = reinterpret_cast<float*>(b + o_Ysh);
   c->d_u = b + o_u;
+  c->d_h2 = reinterpret_cast<float*>(b + o_h2);
   if (c->q4 && gemm_supported(c->I, c->H) && gemm_supported(c->H, c->I)) {
     e = hipMalloc(&c->d_stage, (size_t)kStageExperts * 3 * c->I * c->H * sizeof(bf16_t));
     if (e != hipSuccess) {
@@ -1257,6 +1275,25 @@ static int route_impl(promoe_ctx* c, int layer, const void* d_x, int T, int32_t*
     c->last_route_t = now;
     c->have_route_t = true;
   }
+  if (c->x_from_h && c->gate_layer == layer && c->gate_x == d_x && c->gate_T == T) {
+    // gate logits already computed on this input: x itself still to be formed
+    launch_rmsnorm_quant(c->x_from_h, const_cast<void*>(d_x), T, c->H, c->dt, s);
+    c->x_from_h = nullptr;
+  }
+  // A route that will not wait for its plan (lazy, below) has the host take the
+  // record in on the plan's event: the kernel skips the fence and done word
+  // that a host poll needs, which sit on the path to the expert launches.  Its
+  // prediction, if it brings one, runs as a second block of the plan kernel
+  // (every expert is resident, so the spec plan has nothing to start early).
+  const bool in_order = (c->cfg.flags & (PROMOE_FLAG_NO_REORDER | PROMOE_FLAG_NO_PREEMPT)) != 0;
+  const bool lazy_plan = c->all_resident() && !h_order && !n_order && !in_order && (int64_t)T * c->K <= 64 &&
+                         T < kGemmMinTokens && !c->noalloc_call;
+  const int target = layer + c->D;
+  const bool pred_in_plan = lazy_plan && with_predict && c->D > 0 && target < c->L && c->lw[layer].pw1 &&
+                            !(c->cfg.flags & PROMOE_FLAG_NO_PREFETCH) && T <= kFusedPredMaxT &&
+                            c->Ph <= kFusedPredMaxHidden &&
+                            (c->Ph == 0 || reinterpret_cast<uintptr_t>(c->lw[layer].pw2) % 16 == 0) &&
+                            (int64_t)T * c->K <= kFusedRouteMaxPairs;
   if (!(c->gate_layer == layer && c->gate_x == d_x && c->gate_T == T)) {
     // With a look-ahead the layer's prediction follows its route on the same
     // input: its first predictor rows ride in the gate launch, and the side
@@ -1266,7 +1303,7 @@ static int route_impl(promoe_ctx* c, int layer, const void* d_x, int T, int32_t*
     rc = launch_gate_rows(c, layer, d_x, T, with_pred, s);
     if (rc) return rc;
     c->pred_rows_layer = -1;
-    if (with_pred) {
+    if (with_pred && !pred_in_plan) {
       HIPCHK(hipEventRecord(c->pred_in, s));
       c->pred_rows_layer = layer;
       c->pred_rows_x = d_x;
@@ -1288,17 +1325,45 @@ static int route_impl(promoe_ctx* c, int layer, const void* d_x, int T, int32_t*
   const bool sg = c->cfg.shared_gate && c->Ish > 0;
   tk.sgate_col = sg ? c->E : -1;
   tk.sscale = sg ? d_shared_scale : nullptr;
-  int64_t r;
+  int64_t r, r_spec = -1;
   rc = new_record(c, 1, PROMOE_PRIO_HIGH, &r);
   if (rc) return rc;
-  if ((int64_t)T * c->K <= kFusedRouteMaxPairs) {
-    launch_route_plan(tk, plan_args(c, layer, d_ids, T, r), s);
+  if (pred_in_plan && (rc = new_record(c, 0, PROMOE_PRIO_LOW, &r_spec))) {
+    publish(c, r);
+    return rc;
+  }
+  if (pred_in_plan) {
+    PlanArgs pa = plan_args(c, layer, d_ids, T, r);
+    pa.host_done = 0;
+    PredictPlanArgs pp{};
+    int32_t* pids = d_pred_ids ? d_pred_ids : c->d_pred_ids;
+    pp.plan = plan_args(c, target, pids, T, r_spec);
+    pp.plan.host_done = 0;
+    if (c->cfg.flags & PROMOE_FLAG_FILL_BY_DEADLINE) pp.plan.fill_budget = deadline_fill_budget(c);
+    pp.h = c->d_logits + c->pred_col;
+    pp.ldh = c->ld_logits;
+    pp.Ph = c->Ph;
+    pp.w2 = c->lw[layer].pw2;
+    pp.w2_bf16 = c->dt == PROMOE_BF16;
+    pp.pred_ids = pids;
+    launch_route_plan_predict(tk, pa, pp, s);
+    c->pred_rows_layer = -1;
+  } else if ((int64_t)T * c->K <= kFusedRouteMaxPairs) {
+    PlanArgs pa = plan_args(c, layer, d_ids, T, r);
+    pa.host_done = lazy_plan ? 0 : 1;
+    launch_route_plan(tk, pa, s);
   } else {
     launch_topk(tk, s);
     launch_plan_precise(plan_args(c, layer, d_ids, T, r), s);
   }
   hipError_t le = hipGetLastError();
   if (le == hipSuccess) le = hipEventRecord(c->rec_ev[r % kRecRing], s);
+  if (r_spec >= 0) {
+    // the prediction's record completes with the same kernel
+    if (le == hipSuccess) le = hipEventRecord(c->rec_ev[r_spec % kRecRing], s);
+    publish(c, r_spec);
+    c->lw[target].planned = true;
+  }
   bool early_ffn = false, lazy = false;
   if (le == hipSuccess) {
     rc = early_resident_launch(c, layer, d_x, T, s, r, &early_ffn);
@@ -1306,7 +1371,7 @@ static int route_impl(promoe_ctx* c, int layer, const void* d_x, int T, int32_t*
     // caller does not ask for the order, so the plan is taken in later
     lazy = !rc && early_ffn && c->all_resident() && !h_order && !n_order;
     // the prediction's launches (on the side stream) fill the host's wait for the plan
-    if (!rc && with_predict)
+    if (!rc && with_predict && !pred_in_plan)
       rc = predict_launch(c, layer, d_x, T, d_pred_ids, nullptr, nullptr, s, true, false, !lazy);
     if (rc) {
       publish(c, r);
@@ -1416,7 +1481,6 @@ namespace {
 // kSharedJob), waiting first for copies `wait01` (chunks 0-1 of every job) and
 // then `wait2` (chunk 2).  Jobs with >= kGemmMinTokens pairs go to the MFMA
 // GEMM (bf16, tile-aligned shapes), the rest to the GEMV kernels.
-constexpr int kGemmMinTokens = 16;
 
 int ffn_launch_one(promoe_ctx* c, FfnArgs a, const std::vector<int>& jobs, hipStream_t s, const CopyWait& wait01,
                    const CopyWait& wait2, bool gemm, const bf16_t* stage = nullptr) {
@@ -2006,21 +2070,51 @@ int promoe_stack_step(promoe_ctx* c, float* d_h, int T, void* d_x, void* d_y, in
   int rc = check_tokens(c, T);
   if (rc) return rc;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  // Batch 1: the two RMSNorms of a layer run inside the attention surrogate's
+  // GEMV and the gate GEMV (bit for bit the separate kernels), the attention
+  // GEMV writing the updated residual into the other of two buffers.
+  const bool fold = T == 1 && c->dt == PROMOE_BF16 && !(predict && c->D == 0);
+  float* hb[2] = {d_h, c->d_h2};
+  int cur = 0;
   for (int l = 0; l < c->L; ++l) {
-    if ((rc = promoe_attn_surrogate(c, l, d_h, T, d_x, stream))) return rc;
+    if (fold) {
+      c->last_stream = s;
+      bool x_ready = false;
+      if (c->lw[l].attn) {
+        RowsArgs a{};
+        a.w[0] = c->lw[l].attn;
+        a.nrows[0] = c->H;
+        a.K = c->H;
+        a.T = T;
+        a.out = hb[cur ^ 1];
+        a.ldo = c->H;
+        if (launch_rows_gemv_norm(a, hb[cur], hb[cur], nullptr, s)) {
+          LAUNCHCHK("attn surrogate");
+          cur ^= 1;
+        } else {
+          if ((rc = promoe_attn_surrogate(c, l, hb[cur], T, d_x, stream))) return rc;
+          x_ready = true;
+        }
+      }
+      if (!x_ready) c->x_from_h = hb[cur];
+    } else if ((rc = promoe_attn_surrogate(c, l, d_h, T, d_x, stream))) {
+      return rc;
+    }
     if (predict && c->D == 0) {
       if ((rc = promoe_predict(c, l, d_x, T, d_pred_ids, nullptr, nullptr, stream))) return rc;
       rc = route_impl(c, l, d_x, T, d_ids, d_w, d_shared_scale, nullptr, nullptr, s, false, nullptr);
     } else {
       rc = route_impl(c, l, d_x, T, d_ids, d_w, d_shared_scale, nullptr, nullptr, s, predict != 0, d_pred_ids);
     }
+    c->x_from_h = nullptr;
     if (rc) return rc;
     // the combine also does the residual add
-    c->fuse_h = d_h;
+    c->fuse_h = hb[cur];
     rc = promoe_expert_ffn(c, l, d_x, T, d_ids, d_w, d_shared_scale, d_y, stream);
     c->fuse_h = nullptr;
     if (rc) return rc;
   }
+  if (cur) HIPCHK(hipMemcpyAsync(d_h, c->d_h2, sizeof(float) * (size_t)T * c->H, hipMemcpyDeviceToDevice, s));
   return PROMOE_OK;
 }
 
