@@ -1282,14 +1282,15 @@ static int route_impl(promoe_ctx* c, int layer, const void* d_x, int T, int32_t*
   }
   // A route that will not wait for its plan (lazy, below) has the host take the
   // record in on the plan's event: the kernel skips the fence and done word
-  // that a host poll needs, which sit on the path to the expert launches.  Its
-  // prediction, if it brings one, runs as a second block of the plan kernel
-  // (every expert is resident, so the spec plan has nothing to start early).
+  // that a host poll needs, which sit on the path to the expert launches.  A
+  // decode-sized route that brings its layer's prediction runs it as a second
+  // block of the plan kernel: no side stream to fork and join, and the host
+  // still sees the precise plan as soon as its block has written it.
   const bool in_order = (c->cfg.flags & (PROMOE_FLAG_NO_REORDER | PROMOE_FLAG_NO_PREEMPT)) != 0;
   const bool lazy_plan = c->all_resident() && !h_order && !n_order && !in_order && (int64_t)T * c->K <= 64 &&
                          T < kGemmMinTokens && !c->noalloc_call;
   const int target = layer + c->D;
-  const bool pred_in_plan = lazy_plan && with_predict && c->D > 0 && target < c->L && c->lw[layer].pw1 &&
+  const bool pred_in_plan = with_predict && c->D > 0 && target < c->L && c->lw[layer].pw1 &&
                             !(c->cfg.flags & PROMOE_FLAG_NO_PREFETCH) && T <= kFusedPredMaxT &&
                             c->Ph <= kFusedPredMaxHidden &&
                             (c->Ph == 0 || reinterpret_cast<uintptr_t>(c->lw[layer].pw2) % 16 == 0) &&
@@ -1334,11 +1335,11 @@ static int route_impl(promoe_ctx* c, int layer, const void* d_x, int T, int32_t*
   }
   if (pred_in_plan) {
     PlanArgs pa = plan_args(c, layer, d_ids, T, r);
-    pa.host_done = 0;
+    pa.host_done = lazy_plan ? 0 : 1;
     PredictPlanArgs pp{};
     int32_t* pids = d_pred_ids ? d_pred_ids : c->d_pred_ids;
     pp.plan = plan_args(c, target, pids, T, r_spec);
-    pp.plan.host_done = 0;
+    pp.plan.host_done = lazy_plan ? 0 : 1;
     if (c->cfg.flags & PROMOE_FLAG_FILL_BY_DEADLINE) pp.plan.fill_budget = deadline_fill_budget(c);
     pp.h = c->d_logits + c->pred_col;
     pp.ldh = c->ld_logits;
