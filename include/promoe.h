@@ -281,15 +281,20 @@ int promoe_route(promoe_ctx* ctx, int layer, const void* d_x, int T, int32_t* d_
 
 /* promoe_route of `layer` followed by promoe_predict of the same layer on the
  * same input (d_pred_ids as there; Q is not returned), in one call: the
- * predictor's first rows ride in the gate launch, and its other kernels are
- * launched while the host waits for the precise plan, so the prediction adds
- * next to no host time to the step.  The predictor runs beside the layer's
- * experts with no device-side join: the spec plan that ends it is awaited on
- * the host by the context's next promoe_route, promoe_route_predict,
- * promoe_predict, promoe_prefetch or promoe_sync call, before that call queues
- * anything (without a spec plan, e.g. with PROMOE_FLAG_NO_PREFETCH, the
- * layer's promoe_expert_ffn call joins the side stream into `stream` after its
- * last launch).  d_pred_ids is complete once such a call has returned.
+ * predictor's first rows ride in the gate launch.  For steps of up to 8 tokens
+ * whose routed pairs (T * k) number at most 64 (and predictor width at most
+ * 1024), the rest of the prediction -- second layer, top-k and the spec plan
+ * of layer+lookahead -- runs as a second block of the route's plan kernel on
+ * `stream`: the host still reads the precise plan as soon as its block has
+ * written it, and d_pred_ids is complete when that kernel is.  Otherwise the
+ * predictor's other kernels run on the library's side stream, launched while
+ * the host waits for the precise plan, with no device-side join: the spec
+ * plan that ends them is awaited on the host by the context's next
+ * promoe_route, promoe_route_predict, promoe_predict, promoe_prefetch or
+ * promoe_sync call, before that call queues anything (without a spec plan,
+ * e.g. with PROMOE_FLAG_NO_PREFETCH, the layer's promoe_expert_ffn call joins
+ * the side stream into `stream` after its last launch); there d_pred_ids is
+ * complete once such a call has returned.
  * Needs cfg.lookahead >= 1 (with 0 the prediction plans the routed layer
  * itself and must come first), else PROMOE_EINVAL.  Results are those of the
  * two calls made in that order. */
