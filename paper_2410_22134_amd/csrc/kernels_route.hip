@@ -222,6 +222,9 @@ __device__ __forceinline__ void plan_spec_body(const PlanArgs& a, const int32_t*
   // The list's hits first (Alg. 2 counts them as it pushes the list), then its
   // fills (the worker of Alg. 1 replaces a slot only when a copy starts): no
   // fill evicts a member of the list.
+  // lane i keeps list member i's record entries, stored at the end one
+  // coalesced store per field (the record lives in host memory)
+  int my_e = 0, my_s = -1, my_f = 0, my_v = -1;
   for (int i = 0; i < nq; ++i) {
     const int e = Q[i];
     const int s_res = __shfl(w.slot_of, e, kWave);
@@ -229,7 +232,7 @@ __device__ __forceinline__ void plan_spec_body(const PlanArgs& a, const int32_t*
       ++clock;
       if (lane == s_res) w.stamp = clock;
       cnt[CNT_SPEC_RESIDENT]++;
-      if (lane == 0) { rec->expert[i] = e; rec->slot[i] = s_res; rec->flag[i] = 0; rec->victim[i] = -1; rec->after[i] = -1; }
+      if (lane == i) { my_e = e; my_s = s_res; my_f = 0; my_v = -1; }
     }
   }
   int fills = 0;
@@ -238,15 +241,22 @@ __device__ __forceinline__ void plan_spec_body(const PlanArgs& a, const int32_t*
     if (__shfl(w.slot_of, e, kWave) >= 0) continue;
     const int v = (budget >= 0 && fills >= budget) ? -1 : spare_victim_slot(a, lane, w, spare);
     if (v < 0) {
-      if (lane == 0) { rec->expert[i] = e; rec->slot[i] = -1; rec->flag[i] = 0; rec->victim[i] = -1; rec->after[i] = -1; }
+      if (lane == i) { my_e = e; my_s = -1; my_f = 0; my_v = -1; }
       continue;
     }
     ++fills;
     const int old = fill_slot(a, lane, w, e, v, true, clock, fseq, cnt);
     cnt[CNT_SPEC_ISSUED]++;
-    if (lane == 0) { rec->expert[i] = e; rec->slot[i] = v; rec->flag[i] = 1; rec->victim[i] = old; rec->after[i] = -1; }
+    if (lane == i) { my_e = e; my_s = v; my_f = 1; my_v = old; }
   }
   store_state(a, lane, w, clock, fseq, cnt);
+  if (lane < nq) {
+    rec->expert[lane] = my_e;
+    rec->slot[lane] = my_s;
+    rec->flag[lane] = my_f;
+    rec->victim[lane] = my_v;
+    rec->after[lane] = -1;
+  }
   if (lane == 0) {
     rec->kind = 0;
     rec->layer = a.layer;
@@ -443,8 +453,11 @@ __device__ __forceinline__ void plan_precise_body(const PlanArgs& a, const int32
     __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_wave_barrier();
 
+    // lane `pos` keeps position pos's record entries; they are stored at the
+    // end, one coalesced store per field (the record lives in host memory)
     PlanRecord* rec = a.rec;
     int n_hit = 0;
+    int my_e = 0, my_s = 0, my_f = 0, my_v = -1, my_a = -1;
     for (int pos = 0; pos < np; ++pos) {
       const int e = order[pos];
       // reordered: positions below nh are the resident members; id order: resident now
@@ -456,8 +469,7 @@ __device__ __forceinline__ void plan_precise_body(const PlanArgs& a, const int32
         if (lane == s) { w.stamp = clock; w.spec_unused = 0; }
         cnt[CNT_HIT]++;
         if (was_spec) cnt[CNT_SPEC_USED]++;
-        if (lane == 0) { rec->expert[pos] = e; rec->slot[pos] = s; rec->flag[pos] = 0; rec->victim[pos] = -1; rec->after[pos] = -1; }
-        if (lane == 0) a.d_order_slot[pos] = s;
+        if (lane == pos) { my_e = e; my_s = s; my_f = 0; my_v = -1; my_a = -1; }
       } else {
         const int v = victim_slot(a, lane, w);
         const int old = fill_slot(a, lane, w, e, v, false, clock, fseq, cnt);
@@ -465,26 +477,38 @@ __device__ __forceinline__ void plan_precise_body(const PlanArgs& a, const int32
         // an earlier member must finish reading the slot; a later one was never read
         const int po = old >= 0 ? pos_of[old] : -1;
         const int after = po < pos ? po : -1;
-        if (lane == 0) { rec->expert[pos] = e; rec->slot[pos] = v; rec->flag[pos] = 1; rec->victim[pos] = old; rec->after[pos] = after; }
-        if (lane == 0) a.d_order_slot[pos] = v;
+        if (lane == pos) { my_e = e; my_s = v; my_f = 1; my_v = old; my_a = after; }
       }
     }
     cnt[CNT_PREC] += np;
     store_state(a, lane, w, clock, fseq, cnt);
     if (lane == 0) a.st.pred_mask[a.layer] = 0ull;
+    // pair offsets of the positions: an exclusive prefix sum across the wave
+    const int my_c = lane < np ? cnt_e[order[lane]] : 0;
+    int incl = my_c;
+#pragma unroll
+    for (int o = 1; o < kWave; o <<= 1) {
+      const int t = __shfl_up(incl, o, kWave);
+      if (lane >= o) incl += t;
+    }
+    const int excl = incl - my_c;
+    const int total = __shfl(incl, kWave - 1, kWave);
+    if (lane < np) {
+      rec->expert[lane] = my_e;
+      rec->slot[lane] = my_s;
+      rec->flag[lane] = my_f;
+      rec->victim[lane] = my_v;
+      rec->after[lane] = my_a;
+      rec->count[lane] = my_c;
+      rec->offset[lane] = excl;
+      a.d_order_slot[lane] = my_s;
+      a.d_offsets[lane] = excl;
+      offs[lane] = excl;
+    }
     if (lane == 0) {
-      int o = 0;
-      for (int pos = 0; pos < np; ++pos) {
-        offs[pos] = o;
-        const int c = cnt_e[order[pos]];
-        rec->count[pos] = c;
-        rec->offset[pos] = o;
-        a.d_offsets[pos] = o;
-        o += c;
-      }
-      offs[np] = o;
-      rec->offset[np] = o;
-      a.d_offsets[np] = o;
+      offs[np] = total;
+      rec->offset[np] = total;
+      a.d_offsets[np] = total;
       rec->kind = 1;
       rec->layer = a.layer;
       rec->n = np;
