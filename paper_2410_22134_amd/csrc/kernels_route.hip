@@ -107,6 +107,21 @@ __device__ __forceinline__ void store_state(const PlanArgs& a, int lane, const W
   }
 }
 
+// A layer's cache state as wave 0 of a plan holds it, loaded at the start of
+// a kernel so that its loads overlap the work before the plan (the top-k, the
+// predictor's second layer) instead of following it.
+struct PlanState {
+  WaveState w;
+  uint32_t clock, fseq;
+  int64_t cnt[kCounters];
+  uint64_t pred_mask;
+};
+
+__device__ __forceinline__ void load_plan_state(const PlanArgs& a, int lane, PlanState& ps) {
+  load_state(a, lane, ps.w, ps.clock, ps.fseq, ps.cnt);
+  ps.pred_mask = a.st.pred_mask[a.layer];
+}
+
 // Lowest-index free slot, else the least recently stamped one (stamps are
 // unique), among the slots that are not pinned.
 __device__ __forceinline__ int victim_slot(const PlanArgs& a, int lane, const WaveState& w) {
@@ -160,7 +175,8 @@ struct SpecLds {
 // The spec plan over the predicted ids `ids` [T x k] (global or LDS; a.ids
 // non-null marks the plan as a prediction), or over the caller's list in the
 // record when a.ids is null.  All 256 threads of the block enter.
-__device__ __forceinline__ void plan_spec_body(const PlanArgs& a, const int32_t* ids, SpecLds& sh) {
+__device__ __forceinline__ void plan_spec_body(const PlanArgs& a, const int32_t* ids, SpecLds& sh,
+                                               const PlanState* pre = nullptr) {
   int* votes = sh.votes;
   int* best = sh.best;
   int* Q = sh.Q;
@@ -200,7 +216,15 @@ __device__ __forceinline__ void plan_spec_body(const PlanArgs& a, const int32_t*
   WaveState w;
   uint32_t clock, fseq;
   int64_t cnt[kCounters];
-  load_state(a, lane, w, clock, fseq, cnt);
+  if (pre) {
+    w = pre->w;
+    clock = pre->clock;
+    fseq = pre->fseq;
+#pragma unroll
+    for (int i = 0; i < kCounters; ++i) cnt[i] = pre->cnt[i];
+  } else {
+    load_state(a, lane, w, clock, fseq, cnt);
+  }
   PlanRecord* rec = a.rec;
   // Host-given lists are never limited; a predicted plan fills at most fill_budget slots.
   const int budget = a.ids ? a.fill_budget : -1;
@@ -294,6 +318,8 @@ __device__ __forceinline__ void predict_plan_body(const PredictPlanArgs& p, Pred
   int32_t* ids_l = L.ids_l;
   const PlanArgs& a = p.plan;
   const int tid = threadIdx.x, lane = tid % kWave, wv = tid / kWave;
+  PlanState ps;
+  if (tid < kWave) load_plan_state(a, lane, ps);
   const int T = a.T, E = a.E, k = a.k, Ph = p.Ph;
   if (Ph > 0) {
     // four threads per expert: thread q of expert e takes the 16-byte chunks
@@ -388,7 +414,7 @@ __device__ __forceinline__ void predict_plan_body(const PredictPlanArgs& p, Pred
     }
   }
   __syncthreads();
-  plan_spec_body(a, ids_l, L.sh);
+  plan_spec_body(a, ids_l, L.sh, &ps);
 }
 
 __global__ __launch_bounds__(256) void k_predict_plan(PredictPlanArgs p) {
@@ -405,7 +431,8 @@ struct PreciseLds {
 
 // The precise plan over the routed ids `ids` [T x k] (global, or LDS when the
 // top-k ran in the same block).  All 256 threads of the block enter.
-__device__ __forceinline__ void plan_precise_body(const PlanArgs& a, const int32_t* ids, PreciseLds& sh) {
+__device__ __forceinline__ void plan_precise_body(const PlanArgs& a, const int32_t* ids, PreciseLds& sh,
+                                                  const PlanState* pre = nullptr) {
   int* cnt_e = sh.cnt_e;
   int* pos_of = sh.pos_of;
   int* order = sh.order;
@@ -423,13 +450,24 @@ __device__ __forceinline__ void plan_precise_body(const PlanArgs& a, const int32
   uint32_t clock, fseq;
   int64_t cnt[kCounters];
   if (tid < kWave) {
-    load_state(a, lane, w, clock, fseq, cnt);
+    uint64_t pred_mask;
+    if (pre) {
+      w = pre->w;
+      clock = pre->clock;
+      fseq = pre->fseq;
+#pragma unroll
+      for (int i = 0; i < kCounters; ++i) cnt[i] = pre->cnt[i];
+      pred_mask = pre->pred_mask;
+    } else {
+      load_state(a, lane, w, clock, fseq, cnt);
+      pred_mask = a.st.pred_mask[a.layer];
+    }
     const bool used = lane < a.E && cnt_e[lane] > 0;
     const bool res = used && w.slot_of >= 0;
     const uint32_t fs = __shfl(w.fetch, w.slot_of >= 0 ? w.slot_of : 0, kWave);
     const uint64_t hmask = __ballot(res);
     const uint64_t mmask = __ballot(used && !res);
-    cnt[CNT_PRED_CORRECT] += __popcll(a.st.pred_mask[a.layer] & (hmask | mmask));
+    cnt[CNT_PRED_CORRECT] += __popcll(pred_mask & (hmask | mmask));
     const int nh = __popcll(hmask), np = nh + __popcll(mmask);
     int rank = -1;
     if (!a.reorder) {
@@ -567,9 +605,11 @@ __global__ __launch_bounds__(256) void k_plan_precise(PlanArgs a) {
 __global__ __launch_bounds__(256) void k_route_plan(TopkArgs tk, PlanArgs a) {
   __shared__ int32_t ids_l[kFusedRouteMaxPairs];
   __shared__ PreciseLds sh;
+  PlanState ps;
+  if (threadIdx.x < kWave) load_plan_state(a, threadIdx.x, ps);
   for (int t = threadIdx.x / kWave; t < tk.T; t += 4) topk_token(tk, t, threadIdx.x % kWave, ids_l);
   __syncthreads();
-  plan_precise_body(a, ids_l, sh);
+  plan_precise_body(a, ids_l, sh, &ps);
 }
 
 // The same, with the layer's prediction as a second block: its second layer,
@@ -590,9 +630,11 @@ __global__ __launch_bounds__(256) void k_route_plan_predict(TopkArgs tk, PlanArg
     predict_plan_body(p, L.pred);
     return;
   }
+  PlanState ps;
+  if (threadIdx.x < kWave) load_plan_state(a, threadIdx.x, ps);
   for (int t = threadIdx.x / kWave; t < tk.T; t += 4) topk_token(tk, t, threadIdx.x % kWave, L.route.ids_l);
   __syncthreads();
-  plan_precise_body(a, L.route.ids_l, L.route.sh);
+  plan_precise_body(a, L.route.ids_l, L.route.sh, &ps);
 }
 
 // ============================================================ state init / warm start
