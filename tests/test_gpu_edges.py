@@ -480,3 +480,50 @@ def test_stack_step_all_resident_lazy_routes(T):
         assert t_b["k_bytes"][:2] == t_a["k_bytes"][:2]
     finally:
         m.close()
+
+
+# The batch-1 layer loop at the model shapes' hidden and predictor widths: the
+# RMSNorms folded into the attention and gate GEMVs (hidden 2048, 4096 and 3584
+# take different register layouts there) and the prediction inside the plan
+# kernel (predictor width 512) must give the separate calls' residual stream,
+# plans and counters bit for bit -- with part of the experts cached, and for
+# the DeepSeek shape also with every expert resident (lazy routes).
+STACK_SHAPES = [
+    ("c2_deepseek16b", configs.C2.with_(n_layers=3), None),
+    ("c2_deepseek16b_all_resident", configs.C2.with_(n_layers=3), "all"),
+    ("c4_mixtral_int4", configs.C4.with_(n_layers=3, weight_format="int4", lookahead=1), None),
+    ("c5_qwen2_57b_int4", configs.C5.with_(n_layers=3, weight_format="int4"), None),
+]
+
+
+@pytest.mark.parametrize("name,cfg,slots", STACK_SHAPES, ids=[c[0] for c in STACK_SHAPES])
+def test_stack_step_model_shapes(name, cfg, slots):
+    _log("stack_step shape", name)
+    if slots == "all":
+        cfg = cfg.with_(slots=cfg.n_experts)
+    m = SyntheticModel(cfg, max_tokens=1, gen_threads=8)
+    try:
+        st = Stack(m, 1)
+        runs = []
+        for native in (False, True):
+            m.open(spec_fill_limit=1)
+            hs, plans = [], []
+            for step in range(3):
+                h0 = torch.from_numpy(sm.stack_input(cfg, 960 + step, 1)).cuda()
+                hs.append(pu.to_np(st.step(h0, native=native)).copy())
+                plans.append([(m.ctx.last_plan(l, 0)["slot"], m.ctx.last_plan(l, 1)["slot"])
+                              for l in range(cfg.n_layers)])
+            runs.append((hs, plans, [m.ctx.stats(l) for l in range(cfg.n_layers)], m.ctx.stats(-1)))
+        (h_a, p_a, s_a, t_a), (h_b, p_b, s_b, t_b) = runs
+        if slots == "all":
+            assert t_b["lazy_routes"] == 3 * cfg.n_layers and t_a["miss"] == 0
+        for i, (a, b) in enumerate(zip(h_a, h_b)):
+            assert np.array_equal(a, b), ("step", i, int((a != b).sum()))
+        assert p_a == p_b
+        for l, (a, b) in enumerate(zip(s_a, s_b)):
+            for c in ocache.COUNTERS:
+                assert a[c] == b[c], (l, c)
+        if slots == "all":  # with copies in flight it depends on their timing
+            assert t_a["pred_in_time"] == t_b["pred_in_time"]
+    finally:
+        m.close()
