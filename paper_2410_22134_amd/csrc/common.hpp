@@ -57,27 +57,71 @@ __device__ __forceinline__ float wave_sum(float v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
   return v;
 }
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
-  return v;
+// Wave-wide max / min through DPP row operations (no LDS round trips): quad
+// permutations and row rotations reduce each row of 16 lanes, two row
+// broadcasts carry rows 0-2 into row 3, and lane 63's result is read out as a
+// scalar, so every lane gets it.  The whole wave must be active.  Max and min
+// are exact in any order, so the result equals a butterfly's.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  // lanes outside the row mask, or whose source is invalid, keep their own value
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)v, (int)v, kCtrl, kRowMask, 0xf, false);
 }
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t v) {
+  return ((uint64_t)dpp_u32<kCtrl, kRowMask>((uint32_t)(v >> 32)) << 32) | dpp_u32<kCtrl, kRowMask>((uint32_t)v);
+}
+__device__ __forceinline__ uint64_t lane63_u64(uint64_t v) {
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, 63);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), 63);
+  return ((uint64_t)hi << 32) | lo;
+}
+enum : int {
+  kDppQuadXor1 = 0xB1,  // quad_perm [1,0,3,2]
+  kDppQuadXor2 = 0x4E,  // quad_perm [2,3,0,1]
+  kDppRowRor4 = 0x124,
+  kDppRowRor8 = 0x128,
+  kDppRowBcast15 = 0x142,  // lane 15 of a row into the next row (rows 1 and 3 by mask 0xa)
+  kDppRowBcast31 = 0x143,  // lane 31 into rows 2 and 3 (mask 0xc)
+};
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    uint64_t w = __shfl_xor(v, o, kWave);
-    v = w > v ? w : v;
-  }
-  return v;
+  uint64_t t;
+  t = dpp_u64<kDppQuadXor1, 0xf>(v); v = t > v ? t : v;
+  t = dpp_u64<kDppQuadXor2, 0xf>(v); v = t > v ? t : v;
+  t = dpp_u64<kDppRowRor4, 0xf>(v); v = t > v ? t : v;
+  t = dpp_u64<kDppRowRor8, 0xf>(v); v = t > v ? t : v;
+  t = dpp_u64<kDppRowBcast15, 0xa>(v); v = t > v ? t : v;
+  t = dpp_u64<kDppRowBcast31, 0xc>(v); v = t > v ? t : v;
+  return lane63_u64(v);
 }
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    uint64_t w = __shfl_xor(v, o, kWave);
-    v = w < v ? w : v;
-  }
-  return v;
+  uint64_t t;
+  t = dpp_u64<kDppQuadXor1, 0xf>(v); v = t < v ? t : v;
+  t = dpp_u64<kDppQuadXor2, 0xf>(v); v = t < v ? t : v;
+  t = dpp_u64<kDppRowRor4, 0xf>(v); v = t < v ? t : v;
+  t = dpp_u64<kDppRowRor8, 0xf>(v); v = t < v ? t : v;
+  t = dpp_u64<kDppRowBcast15, 0xa>(v); v = t < v ? t : v;
+  t = dpp_u64<kDppRowBcast31, 0xc>(v); v = t < v ? t : v;
+  return lane63_u64(v);
 }
+__device__ __forceinline__ float wave_max(float v) {
+  float t;
+  t = __uint_as_float(dpp_u32<kDppQuadXor1, 0xf>(__float_as_uint(v))); v = fmaxf(v, t);
+  t = __uint_as_float(dpp_u32<kDppQuadXor2, 0xf>(__float_as_uint(v))); v = fmaxf(v, t);
+  t = __uint_as_float(dpp_u32<kDppRowRor4, 0xf>(__float_as_uint(v))); v = fmaxf(v, t);
+  t = __uint_as_float(dpp_u32<kDppRowRor8, 0xf>(__float_as_uint(v))); v = fmaxf(v, t);
+  t = __uint_as_float(dpp_u32<kDppRowBcast15, 0xa>(__float_as_uint(v))); v = fmaxf(v, t);
+  t = __uint_as_float(dpp_u32<kDppRowBcast31, 0xc>(__float_as_uint(v))); v = fmaxf(v, t);
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+// Value of lane j (j wave-uniform) as a scalar; v_readlane ignores EXEC.
+__device__ __forceinline__ int lane_value(int v, int j) { return __builtin_amdgcn_readlane(v, j); }
+__device__ __forceinline__ uint32_t lane_value(uint32_t v, int j) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, j);
+}
+// A value every lane holds alike (e.g. read from one LDS word) as a scalar.
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
 // Order-preserving map of an fp32 to uint32 (larger float -> larger key).
 __device__ __forceinline__ uint32_t f32_order_key(float f) {
   uint32_t u = __float_as_uint(f);

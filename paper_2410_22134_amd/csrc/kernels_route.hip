@@ -147,8 +147,8 @@ __device__ __forceinline__ int spare_victim_slot(const PlanArgs& a, int lane, co
 // Give slot v to expert e: evict its occupant (counted), fill, stamp.
 __device__ __forceinline__ int fill_slot(const PlanArgs& a, int lane, WaveState& w, int e, int v, bool speculative,
                                          uint32_t& clock, uint32_t& fseq, int64_t (&cnt)[kCounters]) {
-  const int old = __shfl(w.slot_expert, v, kWave);
-  const int old_unused = __shfl(w.spec_unused, v, kWave);
+  const int old = lane_value(w.slot_expert, v);
+  const int old_unused = lane_value(w.spec_unused, v);
   if (old >= 0) {
     cnt[CNT_EVICT]++;
     if (old_unused) cnt[CNT_SPEC_WASTED]++;
@@ -199,11 +199,11 @@ __device__ __forceinline__ void plan_spec_body(const PlanArgs& a, const int32_t*
     if (tid < kWave) {
       const int ve = lane < a.E ? votes[lane] : 0, be = lane < a.E ? best[lane] : kMaxK;
       const uint32_t key = ve > 0 ? ((uint32_t)ve << 12) | ((uint32_t)(15 - be) << 6) | (uint32_t)(63 - lane) : 0u;
-      int rank = 0;
-#pragma unroll
-      for (int j = 0; j < kWave; ++j) rank += __shfl(key, j, kWave) > key ? 1 : 0;
-      if (ve > 0 && rank < a.C) Q[rank] = lane;
+      // only voted lanes can hold a larger key (the others' key is 0)
       const uint64_t voted = __ballot(ve > 0);
+      int rank = 0;
+      for (uint64_t m = voted; m; m &= m - 1) rank += lane_value(key, __builtin_ctzll(m)) > key ? 1 : 0;
+      if (ve > 0 && rank < a.C) Q[rank] = lane;
       if (lane == 0) nq = min(__popcll(voted), a.C);
     }
   } else if (tid == 0) {
@@ -250,8 +250,8 @@ __device__ __forceinline__ void plan_spec_body(const PlanArgs& a, const int32_t*
   // coalesced store per field (the record lives in host memory)
   int my_e = 0, my_s = -1, my_f = 0, my_v = -1;
   for (int i = 0; i < nq; ++i) {
-    const int e = Q[i];
-    const int s_res = __shfl(w.slot_of, e, kWave);
+    const int e = uniform(Q[i]);
+    const int s_res = lane_value(w.slot_of, e);
     if (s_res >= 0) {
       ++clock;
       if (lane == s_res) w.stamp = clock;
@@ -261,8 +261,8 @@ __device__ __forceinline__ void plan_spec_body(const PlanArgs& a, const int32_t*
   }
   int fills = 0;
   for (int i = 0; i < nq; ++i) {
-    const int e = Q[i];
-    if (__shfl(w.slot_of, e, kWave) >= 0) continue;
+    const int e = uniform(Q[i]);
+    if (lane_value(w.slot_of, e) >= 0) continue;
     const int v = (budget >= 0 && fills >= budget) ? -1 : spare_victim_slot(a, lane, w, spare);
     if (v < 0) {
       if (lane == i) { my_e = e; my_s = -1; my_f = 0; my_v = -1; }
@@ -337,9 +337,25 @@ __device__ __forceinline__ void predict_plan_body(const PredictPlanArgs& p, Pred
         wq[u] = (e < E && j8 < n8) ? row[j8] : make_uint4(0, 0, 0, 0);
       }
     }
-    for (int i = tid; i < T * Ph; i += 256) {
-      const int t = i / Ph, j = i - t * Ph;
-      hs[i] = fmaxf(p.h[(size_t)t * p.ldh + j], 0.0f);
+    {
+      // every load of the hidden activations is issued before the first LDS store
+      constexpr int kPer = kFusedPredMaxT * kFusedPredMaxHidden / 256;
+      const int n = T * Ph;
+      float hv[kPer];
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int i = tid + 256 * u;
+        hv[u] = 0.0f;
+        if (i < n) {
+          const int t = i / Ph, j = i - t * Ph;
+          hv[u] = p.h[(size_t)t * p.ldh + j];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kPer; ++u) {
+        const int i = tid + 256 * u;
+        if (i < n) hs[i] = fmaxf(hv[u], 0.0f);
+      }
     }
     __syncthreads();
     float acc[kFusedPredMaxT];
@@ -469,22 +485,22 @@ __device__ __forceinline__ void plan_precise_body(const PlanArgs& a, const int32
     const uint64_t mmask = __ballot(used && !res);
     cnt[CNT_PRED_CORRECT] += __popcll(pred_mask & (hmask | mmask));
     const int nh = __popcll(hmask), np = nh + __popcll(mmask);
+    // rank among the hits by (fetch sequence, id): one scalar read per hit
+    int hit_rank = 0;
+    for (uint64_t m = hmask; m; m &= m - 1) {
+      const int j = __builtin_ctzll(m);
+      const uint32_t fj = lane_value(fs, j);
+      if (fj < fs || (fj == fs && j < lane)) ++hit_rank;
+    }
     int rank = -1;
     if (!a.reorder) {
       // id order; every member is classified at its turn in the walk below
       const uint64_t umask = __ballot(used);
       if (used) rank = __popcll(umask & ((1ull << lane) - 1ull));
     } else if (res) {
-      rank = 0;
-      for (int j = 0; j < kWave; ++j) {
-        const uint32_t fj = __shfl(fs, j, kWave);
-        if (((hmask >> j) & 1ull) && (fj < fs || (fj == fs && j < lane))) ++rank;
-      }
+      rank = hit_rank;
     } else if (used) {
       rank = nh + __popcll(mmask & ((1ull << lane) - 1ull));
-    } else {
-      // keep the shuffle loop uniform across the wave
-      for (int j = 0; j < kWave; ++j) (void)__shfl(fs, j, kWave);
     }
     pos_of[lane] = rank;
     if (rank >= 0) order[rank] = lane;
@@ -497,13 +513,13 @@ __device__ __forceinline__ void plan_precise_body(const PlanArgs& a, const int32
     int n_hit = 0;
     int my_e = 0, my_s = 0, my_f = 0, my_v = -1, my_a = -1;
     for (int pos = 0; pos < np; ++pos) {
-      const int e = order[pos];
+      const int e = uniform(order[pos]);
       // reordered: positions below nh are the resident members; id order: resident now
-      const int s = __shfl(w.slot_of, e, kWave);
+      const int s = lane_value(w.slot_of, e);
       if (s >= 0) {
         ++n_hit;
         ++clock;
-        const int was_spec = __shfl(w.spec_unused, s, kWave);
+        const int was_spec = lane_value(w.spec_unused, s);
         if (lane == s) { w.stamp = clock; w.spec_unused = 0; }
         cnt[CNT_HIT]++;
         if (was_spec) cnt[CNT_SPEC_USED]++;
@@ -521,16 +537,14 @@ __device__ __forceinline__ void plan_precise_body(const PlanArgs& a, const int32
     cnt[CNT_PREC] += np;
     store_state(a, lane, w, clock, fseq, cnt);
     if (lane == 0) a.st.pred_mask[a.layer] = 0ull;
-    // pair offsets of the positions: an exclusive prefix sum across the wave
+    // pair offsets of the positions: an exclusive prefix sum over the np positions
     const int my_c = lane < np ? cnt_e[order[lane]] : 0;
-    int incl = my_c;
-#pragma unroll
-    for (int o = 1; o < kWave; o <<= 1) {
-      const int t = __shfl_up(incl, o, kWave);
-      if (lane >= o) incl += t;
+    int excl = 0, total = 0;
+    for (int j = 0; j < np; ++j) {
+      const int c = lane_value(my_c, j);
+      if (j < lane) excl += c;
+      total += c;
     }
-    const int excl = incl - my_c;
-    const int total = __shfl(incl, kWave - 1, kWave);
     if (lane < np) {
       rec->expert[lane] = my_e;
       rec->slot[lane] = my_s;
