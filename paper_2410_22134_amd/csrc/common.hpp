@@ -84,16 +84,6 @@ enum : int {
   kDppRowBcast15 = 0x142,  // lane 15 of a row into the next row (rows 1 and 3 by mask 0xa)
   kDppRowBcast31 = 0x143,  // lane 31 into rows 2 and 3 (mask 0xc)
 };
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-  uint64_t t;
-  t = dpp_u64<kDppQuadXor1, 0xf>(v); v = t > v ? t : v;
-  t = dpp_u64<kDppQuadXor2, 0xf>(v); v = t > v ? t : v;
-  t = dpp_u64<kDppRowRor4, 0xf>(v); v = t > v ? t : v;
-  t = dpp_u64<kDppRowRor8, 0xf>(v); v = t > v ? t : v;
-  t = dpp_u64<kDppRowBcast15, 0xa>(v); v = t > v ? t : v;
-  t = dpp_u64<kDppRowBcast31, 0xc>(v); v = t > v ? t : v;
-  return lane63_u64(v);
-}
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
   uint64_t t;
   t = dpp_u64<kDppQuadXor1, 0xf>(v); v = t < v ? t : v;
@@ -103,6 +93,27 @@ __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) {
   t = dpp_u64<kDppRowBcast15, 0xa>(v); v = t < v ? t : v;
   t = dpp_u64<kDppRowBcast31, 0xc>(v); v = t < v ? t : v;
   return lane63_u64(v);
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  uint32_t t;
+  t = dpp_u32<kDppQuadXor1, 0xf>(v); v = t > v ? t : v;
+  t = dpp_u32<kDppQuadXor2, 0xf>(v); v = t > v ? t : v;
+  t = dpp_u32<kDppRowRor4, 0xf>(v); v = t > v ? t : v;
+  t = dpp_u32<kDppRowRor8, 0xf>(v); v = t > v ? t : v;
+  t = dpp_u32<kDppRowBcast15, 0xa>(v); v = t > v ? t : v;
+  t = dpp_u32<kDppRowBcast31, 0xc>(v); v = t > v ? t : v;
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, 63);
+}
+// One round of a wave's top-k: among the candidate lanes, the one with the
+// largest key, ties to the lower lane (a 64-bit key (key << 32 | 63 - lane)
+// orders them the same way); it stops being a candidate.  At least one lane
+// must be a candidate.
+__device__ __forceinline__ int wave_pick_max(uint32_t key, bool& cand) {
+  const uint32_t kmax = wave_max_u32(cand ? key : 0u);
+  const uint64_t tie = __ballot(cand && key == kmax);
+  const int e = (int)__builtin_ctzll(tie);
+  if ((int)(threadIdx.x % kWave) == e) cand = false;
+  return e;
 }
 __device__ __forceinline__ float wave_max(float v) {
   float t;
@@ -119,8 +130,6 @@ __device__ __forceinline__ int lane_value(int v, int j) { return __builtin_amdgc
 __device__ __forceinline__ uint32_t lane_value(uint32_t v, int j) {
   return (uint32_t)__builtin_amdgcn_readlane((int)v, j);
 }
-// A value every lane holds alike (e.g. read from one LDS word) as a scalar.
-__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 // Order-preserving map of an fp32 to uint32 (larger float -> larger key).
 __device__ __forceinline__ uint32_t f32_order_key(float f) {

@@ -87,6 +87,9 @@ struct CombineArgs {
 constexpr int kCounters = 10;
 
 // Per-layer logical cache state on the device.
+constexpr int kFusedPredMaxT = 8;
+constexpr int kFusedPredMaxHidden = 1024;
+
 struct CacheState {
   int32_t* slot_expert;  // [L*C]
   int32_t* slot_of;      // [L*E]
@@ -98,6 +101,9 @@ struct CacheState {
   int64_t* counters;     // [L*kCounters]: prec_access hit miss spec_issued spec_resident spec_used
                          // spec_wasted evict pred_n pred_correct
   uint64_t* pred_mask;   // [L]: experts of the layer's last prediction not yet routed
+  float* pred_xq;        // [L * kFusedPredMaxT * kMaxE]: predictor logits of a target layer, passed
+                         // between the blocks of a fused prediction
+  uint32_t* pred_xcnt;   // [L]: blocks of that prediction finished (0 between launches)
 };
 
 // Plan record written by the plan kernels into host-mapped memory.
@@ -146,10 +152,12 @@ struct PlanArgs {
                          // host polls it); 0: neither (the host waits on the plan's event)
 };
 
-// Predictor tail and spec plan in one block (steps of at most kFusedPredMaxT
-// tokens, predictor hidden width at most kFusedPredMaxHidden, a multiple of 8).
-constexpr int kFusedPredMaxT = 8;
-constexpr int kFusedPredMaxHidden = 1024;
+// Predictor tail and spec plan in one launch (steps of at most kFusedPredMaxT
+// tokens, predictor hidden width at most kFusedPredMaxHidden, a multiple of 8):
+// the second layer's rows are spread over blocks of kPredExpertsPerBlock
+// experts; the block that finishes last runs the top-k and the spec plan.
+constexpr int kPredExpertsPerBlock = 8;
+__host__ __device__ inline int pred_blocks(int E, int Ph) { return Ph > 0 ? (E + kPredExpertsPerBlock - 1) / kPredExpertsPerBlock : 1; }
 struct PredictPlanArgs {
   PlanArgs plan;        // plan.ids: the predicted-ids output (marks a prediction)
   const float* h;       // [T x ldh] first-layer outputs before relu, or the logits when Ph == 0

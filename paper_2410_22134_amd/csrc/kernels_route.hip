@@ -38,12 +38,12 @@ __device__ __forceinline__ void topk_token(const TopkArgs& a, int t, int lane, i
   const bool valid = lane < a.E;
   float z = -INFINITY;
   if (valid) z = a.logits[(size_t)t * a.ld + lane] + (a.bias ? a.bias[lane] : 0.0f);
-  uint64_t key = valid ? (((uint64_t)f32_order_key(z) << 32) | (uint32_t)(63 - lane)) : 0ull;
+  const uint32_t key = f32_order_key(z);
+  bool cand = valid;
   int myrank = -1;
   for (int r = 0; r < a.k; ++r) {
-    const uint64_t kmax = wave_max_u64(key);
-    const int e = 63 - (int)(uint32_t)(kmax & 0xFFFFFFFFu);
-    if (lane == e) { myrank = r; key = 0ull; }
+    const int e = wave_pick_max(key, cand);
+    if (lane == e) myrank = r;
     if (lane == 0) {
       a.ids[t * a.k + r] = e;
       if (ids_copy) ids_copy[t * a.k + r] = e;
@@ -184,6 +184,7 @@ __device__ __forceinline__ void plan_spec_body(const PlanArgs& a, const int32_t*
   const int tid = threadIdx.x, lane = tid % kWave;
   if (tid < kMaxE) { votes[tid] = 0; best[tid] = kMaxK; }
   __syncthreads();
+  uint64_t voted = 0, listed = 0;  // wave 0: experts voted for; the list's members (prediction)
   if (a.ids) {
     const int n = a.T * a.k;
     for (int i = tid; i < n; i += 256) {
@@ -200,10 +201,11 @@ __device__ __forceinline__ void plan_spec_body(const PlanArgs& a, const int32_t*
       const int ve = lane < a.E ? votes[lane] : 0, be = lane < a.E ? best[lane] : kMaxK;
       const uint32_t key = ve > 0 ? ((uint32_t)ve << 12) | ((uint32_t)(15 - be) << 6) | (uint32_t)(63 - lane) : 0u;
       // only voted lanes can hold a larger key (the others' key is 0)
-      const uint64_t voted = __ballot(ve > 0);
+      voted = __ballot(ve > 0);
       int rank = 0;
       for (uint64_t m = voted; m; m &= m - 1) rank += lane_value(key, __builtin_ctzll(m)) > key ? 1 : 0;
       if (ve > 0 && rank < a.C) Q[rank] = lane;
+      listed = __ballot(ve > 0 && rank < a.C);  // the first min(voted, C): Q
       if (lane == 0) nq = min(__popcll(voted), a.C);
     }
   } else if (tid == 0) {
@@ -229,18 +231,13 @@ __device__ __forceinline__ void plan_spec_body(const PlanArgs& a, const int32_t*
   // Host-given lists are never limited; a predicted plan fills at most fill_budget slots.
   const int budget = a.ids ? a.fill_budget : -1;
   if (a.ids) {  // a prediction: remembered until the layer's route scores it
-    uint64_t m = 0;
-    for (int i = 0; i < nq; ++i) m |= 1ull << Q[i];
-    if (lane == 0) a.st.pred_mask[a.layer] = m;
+    if (lane == 0) a.st.pred_mask[a.layer] = listed;
     cnt[CNT_PRED_N] += nq;
   }
   // Experts no fill may evict: every expert the prediction votes for (of which
   // Q is the first C), or the caller's whole list.
-  uint64_t spare = 0;
-  if (a.ids) {
-    if (lane < a.E && votes[lane] > 0) spare = 1ull << lane;
-    spare = __ballot(spare != 0);
-  } else {
+  uint64_t spare = voted;
+  if (!a.ids) {
     for (int i = 0; i < nq; ++i) spare |= 1ull << Q[i];
   }
   // The list's hits first (Alg. 2 counts them as it pushes the list), then its
@@ -249,8 +246,9 @@ __device__ __forceinline__ void plan_spec_body(const PlanArgs& a, const int32_t*
   // lane i keeps list member i's record entries, stored at the end one
   // coalesced store per field (the record lives in host memory)
   int my_e = 0, my_s = -1, my_f = 0, my_v = -1;
+  const int q_lane = lane < nq ? Q[lane] : 0;  // list member i in lane i
   for (int i = 0; i < nq; ++i) {
-    const int e = uniform(Q[i]);
+    const int e = lane_value(q_lane, i);
     const int s_res = lane_value(w.slot_of, e);
     if (s_res >= 0) {
       ++clock;
@@ -261,7 +259,7 @@ __device__ __forceinline__ void plan_spec_body(const PlanArgs& a, const int32_t*
   }
   int fills = 0;
   for (int i = 0; i < nq; ++i) {
-    const int e = uniform(Q[i]);
+    const int e = lane_value(q_lane, i);
     if (lane_value(w.slot_of, e) >= 0) continue;
     const int v = (budget >= 0 && fills >= budget) ? -1 : spare_victim_slot(a, lane, w, spare);
     if (v < 0) {
@@ -300,40 +298,54 @@ __global__ __launch_bounds__(256) void k_plan_spec(PlanArgs a) {
   plan_spec_body(a, a.ids, sh);
 }
 
-// ============================================================ predictor tail + spec plan, one block
+// ============================================================ predictor tail + spec plan
 // For a step of at most kFusedPredMaxT tokens: the predictor's second layer
 // q[t][e] = W2[e] . relu(h[t]) (fp32 accumulation; or q = h when the
 // predictor is one layer), each token's top-k by (q desc, id asc) as k_topk
 // orders them, written out and kept in LDS, then the spec plan of the vote.
+//
+// The rows of W2 are spread over pred_blocks(E, Ph) blocks of
+// kPredExpertsPerBlock experts each, so that their loads run on that many CUs
+// (one CU alone streams the ~128 KB of a 64 x 1024 bf16 W2 at a few tens of
+// GB/s).  Each block writes its logits to the target layer's exchange buffer
+// and counts itself in with a device-scope atomic after a release fence; the
+// block that counts last acquires, reads every logit back, resets the count
+// and runs the top-k and the plan.  No block waits on another.
+constexpr int kPredThreadsPerExpert = 256 / kPredExpertsPerBlock;  // 32: lanes of one wave
+
 struct PredictLds {
   float hs[kFusedPredMaxT * kFusedPredMaxHidden];
   float qs[kFusedPredMaxT * kMaxE];
   int32_t ids_l[kFusedPredMaxT * kMaxK];
   SpecLds sh;
+  int last;
 };
 
-__device__ __forceinline__ void predict_plan_body(const PredictPlanArgs& p, PredictLds& L) {
+// blk: this block's index among the prediction's pred_blocks(E, Ph) blocks.
+__device__ __forceinline__ void predict_plan_body(const PredictPlanArgs& p, PredictLds& L, int blk) {
   float* hs = L.hs;
   float* qs = L.qs;
   int32_t* ids_l = L.ids_l;
   const PlanArgs& a = p.plan;
   const int tid = threadIdx.x, lane = tid % kWave, wv = tid / kWave;
-  PlanState ps;
+  PlanState ps;  // used by the block that runs the plan; loaded early by every block
   if (tid < kWave) load_plan_state(a, lane, ps);
   const int T = a.T, E = a.E, k = a.k, Ph = p.Ph;
+  const int nblk = pred_blocks(E, Ph);
   if (Ph > 0) {
-    // four threads per expert: thread q of expert e takes the 16-byte chunks
-    // q, q + 4, ... of its row; with bf16 weights every chunk is loaded before
-    // the hidden activations are staged, so the two loads overlap
+    // kPredThreadsPerExpert threads per expert: thread q of expert e takes
+    // the 16-byte chunks q, q + 32, ... of its row; with bf16 weights every
+    // chunk is loaded before the hidden activations are staged
     const int n8 = Ph / 8;  // Ph % 8 == 0
-    const int e = tid >> 2, q = tid & 3;
-    constexpr int kChunks = kFusedPredMaxHidden / 8 / 4;
+    const int el = tid / kPredThreadsPerExpert, q = tid % kPredThreadsPerExpert;
+    const int e = blk * kPredExpertsPerBlock + el;
+    constexpr int kChunks = kFusedPredMaxHidden / 8 / kPredThreadsPerExpert;
     uint4 wq[kChunks];
     if (p.w2_bf16) {
       const uint4* row = reinterpret_cast<const uint4*>(static_cast<const bf16_t*>(p.w2) + (size_t)(e < E ? e : 0) * Ph);
 #pragma unroll
       for (int u = 0; u < kChunks; ++u) {
-        const int j8 = q + 4 * u;
+        const int j8 = q + kPredThreadsPerExpert * u;
         wq[u] = (e < E && j8 < n8) ? row[j8] : make_uint4(0, 0, 0, 0);
       }
     }
@@ -365,7 +377,7 @@ __device__ __forceinline__ void predict_plan_body(const PredictPlanArgs& p, Pred
       if (p.w2_bf16) {
 #pragma unroll
         for (int u = 0; u < kChunks; ++u) {
-          const int j8 = q + 4 * u;
+          const int j8 = q + kPredThreadsPerExpert * u;
           if (j8 >= n8) break;
           const uint32_t q4[4] = {wq[u].x, wq[u].y, wq[u].z, wq[u].w};
           float wj[8];
@@ -384,7 +396,7 @@ __device__ __forceinline__ void predict_plan_body(const PredictPlanArgs& p, Pred
           }
         }
       } else {
-        for (int j8 = q; j8 < n8; j8 += 4) {
+        for (int j8 = q; j8 < n8; j8 += kPredThreadsPerExpert) {
           const float* w = static_cast<const float*>(p.w2) + (size_t)e * Ph + j8 * 8;
           float wj[8];
 #pragma unroll
@@ -404,25 +416,50 @@ __device__ __forceinline__ void predict_plan_body(const PredictPlanArgs& p, Pred
     for (int t = 0; t < kFusedPredMaxT; ++t) {
       if (t < T) {
         float v = acc[t];
-        v += __shfl_xor(v, 1, kWave);
-        v += __shfl_xor(v, 2, kWave);
+#pragma unroll
+        for (int o = 1; o < kPredThreadsPerExpert; o <<= 1) v += __shfl_xor(v, o, kWave);
         if (q == 0 && e < E) qs[t * kMaxE + e] = v;
       }
+    }
+    __syncthreads();
+    if (nblk > 1) {
+      float* xq = a.st.pred_xq + (size_t)a.layer * kFusedPredMaxT * kMaxE;
+      uint32_t* xcnt = a.st.pred_xcnt + a.layer;
+      if (tid < kWave) {
+        for (int i = lane; i < T * kPredExpertsPerBlock; i += kWave) {
+          const int t = i / kPredExpertsPerBlock, ee = blk * kPredExpertsPerBlock + i % kPredExpertsPerBlock;
+          if (ee < E) xq[t * kMaxE + ee] = qs[t * kMaxE + ee];
+        }
+        __threadfence();  // release: this wave's logit stores before the count
+        uint32_t prev = 0;
+        if (lane == 0) prev = atomicAdd(xcnt, 1u);
+        prev = lane_value(prev, 0);
+        if (lane == 0) L.last = prev == (uint32_t)(nblk - 1) ? 1 : 0;
+      }
+      __syncthreads();
+      if (!L.last) return;
+      if (tid < kWave) {
+        __threadfence();  // acquire: every block's logits
+        for (int i = lane; i < T * E; i += kWave) {
+          const int t = i / E, ee = i - t * E;
+          qs[t * kMaxE + ee] = xq[t * kMaxE + ee];
+        }
+        if (lane == 0) atomicExch(xcnt, 0u);  // every block has counted: ready for the next launch
+      }
+      __syncthreads();
     }
   } else {
     for (int i = tid; i < T * E; i += 256) {
       const int t = i / E, e = i - t * E;
       qs[t * kMaxE + e] = p.h[(size_t)t * p.ldh + e];
     }
+    __syncthreads();
   }
-  __syncthreads();
   for (int t = wv; t < T; t += 4) {
-    const bool valid = lane < E;
-    uint64_t key = valid ? (((uint64_t)f32_order_key(qs[t * kMaxE + lane]) << 32) | (uint32_t)(63 - lane)) : 0ull;
+    bool cand = lane < E;
+    const uint32_t key = cand ? f32_order_key(qs[t * kMaxE + lane]) : 0u;
     for (int r = 0; r < k; ++r) {
-      const uint64_t kmax = wave_max_u64(key);
-      const int e = 63 - (int)(uint32_t)(kmax & 0xFFFFFFFFu);
-      if (lane == e) key = 0ull;
+      const int e = wave_pick_max(key, cand);
       if (lane == 0) {
         ids_l[t * k + r] = e;
         p.pred_ids[t * k + r] = e;
@@ -435,7 +472,7 @@ __device__ __forceinline__ void predict_plan_body(const PredictPlanArgs& p, Pred
 
 __global__ __launch_bounds__(256) void k_predict_plan(PredictPlanArgs p) {
   __shared__ PredictLds L;
-  predict_plan_body(p, L);
+  predict_plan_body(p, L, blockIdx.x);
 }
 
 // ============================================================ precise plan + permutation
@@ -512,8 +549,9 @@ __device__ __forceinline__ void plan_precise_body(const PlanArgs& a, const int32
     PlanRecord* rec = a.rec;
     int n_hit = 0;
     int my_e = 0, my_s = 0, my_f = 0, my_v = -1, my_a = -1;
+    const int ord_lane = lane < np ? order[lane] : 0;  // the expert at position lane
     for (int pos = 0; pos < np; ++pos) {
-      const int e = uniform(order[pos]);
+      const int e = lane_value(ord_lane, pos);
       // reordered: positions below nh are the resident members; id order: resident now
       const int s = lane_value(w.slot_of, e);
       if (s >= 0) {
@@ -529,7 +567,7 @@ __device__ __forceinline__ void plan_precise_body(const PlanArgs& a, const int32
         const int old = fill_slot(a, lane, w, e, v, false, clock, fseq, cnt);
         cnt[CNT_MISS]++;
         // an earlier member must finish reading the slot; a later one was never read
-        const int po = old >= 0 ? pos_of[old] : -1;
+        const int po = old >= 0 ? lane_value(rank, old) : -1;
         const int after = po < pos ? po : -1;
         if (lane == pos) { my_e = e; my_s = v; my_f = 1; my_v = old; my_a = after; }
       }
@@ -538,7 +576,7 @@ __device__ __forceinline__ void plan_precise_body(const PlanArgs& a, const int32
     store_state(a, lane, w, clock, fseq, cnt);
     if (lane == 0) a.st.pred_mask[a.layer] = 0ull;
     // pair offsets of the positions: an exclusive prefix sum over the np positions
-    const int my_c = lane < np ? cnt_e[order[lane]] : 0;
+    const int my_c = lane < np ? cnt_e[ord_lane] : 0;
     int excl = 0, total = 0;
     for (int j = 0; j < np; ++j) {
       const int c = lane_value(my_c, j);
@@ -640,8 +678,8 @@ union RoutePredictLds {
 
 __global__ __launch_bounds__(256) void k_route_plan_predict(TopkArgs tk, PlanArgs a, PredictPlanArgs p) {
   __shared__ RoutePredictLds L;
-  if (blockIdx.x == 1) {
-    predict_plan_body(p, L.pred);
+  if (blockIdx.x >= 1) {
+    predict_plan_body(p, L.pred, blockIdx.x - 1);
     return;
   }
   PlanState ps;
@@ -656,7 +694,7 @@ __global__ void k_state_init(CacheState st, int L, int C, int E) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < L * C) { st.slot_expert[i] = -1; st.stamp[i] = 0u; st.fetch_seq[i] = 0u; st.spec_unused[i] = 0; }
   if (i < L * E) st.slot_of[i] = -1;
-  if (i < L) { st.clock[i] = (uint32_t)(C - 1); st.fseq[i] = 0u; st.pred_mask[i] = 0ull; }
+  if (i < L) { st.clock[i] = (uint32_t)(C - 1); st.fseq[i] = 0u; st.pred_mask[i] = 0ull; st.pred_xcnt[i] = 0u; }
   if (i < L * kCounters) st.counters[i] = 0;
 }
 
@@ -677,11 +715,13 @@ void launch_topk(const TopkArgs& a, hipStream_t s) {
   k_topk<<<(a.T + 3) / 4, 256, 0, s>>>(a);
 }
 void launch_plan_spec(const PlanArgs& a, hipStream_t s) { k_plan_spec<<<1, 256, 0, s>>>(a); }
-void launch_predict_plan(const PredictPlanArgs& p, hipStream_t s) { k_predict_plan<<<1, 256, 0, s>>>(p); }
+void launch_predict_plan(const PredictPlanArgs& p, hipStream_t s) {
+  k_predict_plan<<<pred_blocks(p.plan.E, p.Ph), 256, 0, s>>>(p);
+}
 void launch_plan_precise(const PlanArgs& a, hipStream_t s) { k_plan_precise<<<1, 256, 0, s>>>(a); }
 void launch_route_plan(const TopkArgs& tk, const PlanArgs& a, hipStream_t s) { k_route_plan<<<1, 256, 0, s>>>(tk, a); }
 void launch_route_plan_predict(const TopkArgs& tk, const PlanArgs& a, const PredictPlanArgs& p, hipStream_t s) {
-  k_route_plan_predict<<<2, 256, 0, s>>>(tk, a, p);
+  k_route_plan_predict<<<1 + pred_blocks(p.plan.E, p.Ph), 256, 0, s>>>(tk, a, p);
 }
 void launch_state_init(CacheState st, int L, int C, int E, hipStream_t s) {
   int n = L * (C > E ? C : E);

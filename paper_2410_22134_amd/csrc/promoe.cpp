@@ -764,6 +764,7 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
                o_su = take(sizeof(int32_t) * L * C), o_clock = take(sizeof(uint32_t) * L),
                o_fseq = take(sizeof(uint32_t) * L), o_cnt = take(sizeof(int64_t) * L * kCounters),
                o_pmask = take(sizeof(uint64_t) * L),
+               o_pxq = take(sizeof(float) * L * kFusedPredMaxT * kMaxE), o_pxc = take(sizeof(uint32_t) * L),
                o_logits = take(sizeof(float) * (size_t)T * c->ld_logits), o_predq = take(sizeof(float) * (size_t)T * E),
                o_pids = take(sizeof(int32_t) * (size_t)T * Kk), o_oslot = take(sizeof(int32_t) * 64),
                o_offs = take(sizeof(int32_t) * 65), o_perm = take(sizeof(int32_t) * (size_t)T * Kk),
@@ -788,6 +789,8 @@ int promoe_create(const promoe_config* cfg, void* d_cache, size_t cache_bytes, p
   c->st.fseq = reinterpret_cast<uint32_t*>(b + o_fseq);
   c->st.counters = reinterpret_cast<int64_t*>(b + o_cnt);
   c->st.pred_mask = reinterpret_cast<uint64_t*>(b + o_pmask);
+  c->st.pred_xq = reinterpret_cast<float*>(b + o_pxq);
+  c->st.pred_xcnt = reinterpret_cast<uint32_t*>(b + o_pxc);
   c->d_logits = reinterpret_cast<float*>(b + o_logits);
   c->d_predq = reinterpret_cast<float*>(b + o_predq);
   c->d_pred_ids = reinterpret_cast<int32_t*>(b + o_pids);
