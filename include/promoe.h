@@ -284,8 +284,9 @@ int promoe_route(promoe_ctx* ctx, int layer, const void* d_x, int T, int32_t* d_
  * predictor's first rows ride in the gate launch.  For steps of up to 8 tokens
  * whose routed pairs (T * k) number at most 64 (and predictor width at most
  * 1024), the rest of the prediction -- second layer, top-k and the spec plan
- * of layer+lookahead -- runs as a second block of the route's plan kernel on
- * `stream`: the host still reads the precise plan as soon as its block has
+ * of layer+lookahead -- runs in further blocks of the route's plan kernel on
+ * `stream` (the second layer's rows spread over them, the block that finishes
+ * last taking the top-k and the plan): the host still reads the precise plan as soon as its block has
  * written it, and d_pred_ids is complete when that kernel is.  Otherwise the
  * predictor's other kernels run on the library's side stream, launched while
  * the host waits for the precise plan, with no device-side join: the spec
