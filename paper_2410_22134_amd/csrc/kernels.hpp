@@ -186,7 +186,12 @@ void launch_rows_gemv(const RowsArgs& a, int wdtype, int xdtype, hipStream_t s);
 // launch_rmsnorm_quant then launch_rows_gemv; out = (add_src ? add_src : 0) +
 // dot; x_out (or null) receives x.  a.x is unused.  Returns false, launching
 // nothing, where the separate kernels would not take their register paths.
-bool launch_rows_gemv_norm(const RowsArgs& a, const float* h, const float* add_src, void* x_out, hipStream_t s);
+// With ca (batch 1, bf16, H <= 2048, one shared slice), h is the residual
+// before the previous layer's MoE output: the kernel forms y = combine(ca) and
+// h' = h + q(y) as launch_combine_residual would, uses h' in place of h and
+// of add_src, and stores y to ca->y; h' is not written.
+bool launch_rows_gemv_norm(const RowsArgs& a, const float* h, const float* add_src, void* x_out, hipStream_t s,
+                           const CombineArgs* ca = nullptr);
 // Launches one pass of the GEMV kernels over the jobs (a copy of `a` is
 // adjusted per pass; `a` is unchanged).  max_tokens = most pairs of any job.
 // With ev0/ev1 set, the launch records them itself at the kernel's start and

@@ -616,8 +616,31 @@ void launch_dequant_q4(const DequantArgs& a, hipStream_t s) {
 // order, one rounding.  Every operand of the element is loaded before the
 // first product (up to kMaxK ranks and 8 split-K slices), so the kernel waits
 // for one memory round trip instead of one per term.
+constexpr int kSplitRegs = 8;
+// The combine's arithmetic over operands already loaded: y = sum_r w[r] Y[r]
+// (r < top_k, in order), then, with a shared expert, y += s * ysh where ysh
+// sums the slices sv[k < min(split, kSplitRegs)] in order and `more` adds any
+// later slices.  Every combine goes through here, so all of them round alike.
+template <typename More>
+__device__ __forceinline__ float combine_terms(const float (&wv)[kMaxK], const float (&yv)[kMaxK], int top_k,
+                                               bool has_sh, const float (&sv)[kSplitRegs], int split, float s,
+                                               More more) {
+  float y = 0.0f;
+#pragma unroll
+  for (int r = 0; r < kMaxK; ++r)
+    if (r < top_k) y += wv[r] * yv[r];
+  if (has_sh) {
+    float ysh = 0.0f;
+#pragma unroll
+    for (int k = 0; k < kSplitRegs; ++k)
+      if (k < split) ysh += sv[k];
+    ysh = more(ysh);
+    y += s * ysh;
+  }
+  return y;
+}
+
 __device__ __forceinline__ float combine_value(const CombineArgs& a, int t, int n) {
-  constexpr int kSplitRegs = 8;
   float wv[kMaxK], yv[kMaxK], sv[kSplitRegs];
 #pragma unroll
   for (int r = 0; r < kMaxK; ++r) {
@@ -629,20 +652,11 @@ __device__ __forceinline__ float combine_value(const CombineArgs& a, int t, int 
 #pragma unroll
   for (int k = 0; k < kSplitRegs; ++k)
     sv[k] = k < split ? a.Ysh[(size_t)k * a.ysh_split_stride + (size_t)t * a.hidden + n] : 0.0f;
-  float y = 0.0f;
-#pragma unroll
-  for (int r = 0; r < kMaxK; ++r)
-    if (r < a.top_k) y += wv[r] * yv[r];
-  if (a.Ysh) {
-    float ysh = 0.0f;
-#pragma unroll
-    for (int k = 0; k < kSplitRegs; ++k)
-      if (k < split) ysh += sv[k];
+  const float s = a.Ysh && a.sscale ? a.sscale[t] : 1.0f;
+  return combine_terms(wv, yv, a.top_k, a.Ysh != nullptr, sv, split, s, [&](float ysh) {
     for (int k = kSplitRegs; k < split; ++k) ysh += a.Ysh[(size_t)k * a.ysh_split_stride + (size_t)t * a.hidden + n];
-    const float s = a.sscale ? a.sscale[t] : 1.0f;
-    y += s * ysh;
-  }
-  return y;
+    return ysh;
+  });
 }
 
 template <typename TY>
@@ -716,10 +730,18 @@ __global__ __launch_bounds__(kThreads) void k_rows_gemv_reg(RowsArgs a) {
 // weight loads are issued first and overlap the norm.  add_src: out = add_src
 // + dot (a second residual buffer, so no block reads a row of h that another
 // has already updated); x_out: block 0 also stores x.
-template <int VPT, int NCH>
+//
+// CMB: h is the residual before the previous layer's MoE output is added; each
+// block first forms that output y = combine(ca) and h' = h + q(y) for the
+// whole token, as k_combine_residual would (same operands, same arithmetic),
+// then works on h' as above, with out = h' + dot; block 0 stores y to ca.y.
+// The combine launch and its dependent-launch gap are gone; h' itself is
+// never written (only out, which is h' plus the GEMV).
+template <int VPT, int NCH, bool CMB>
 __global__ __launch_bounds__(kThreads) void k_rows_gemv_norm(RowsArgs a, const float* h, float eps,
-                                                             const float* add_src, bf16_t* x_out) {
+                                                             const float* add_src, bf16_t* x_out, CombineArgs ca) {
   __shared__ __attribute__((aligned(16))) bf16_t xs[4 * VPT * kThreads];
+  __shared__ __attribute__((aligned(16))) float hs[CMB ? 4 * VPT * kThreads : 4];
   __shared__ float red[kWaves];
   const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
   const int ntot = a.nrows[0] + a.nrows[1] + a.nrows[2];
@@ -743,6 +765,49 @@ __global__ __launch_bounds__(kThreads) void k_rows_gemv_norm(RowsArgs a, const f
   for (int u = 0; u < VPT; ++u) {
     const int i = tid + u * kThreads;
     r[u] = i < n4 ? h4[i] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  }
+  if constexpr (CMB) {
+    // batch 1: Y rows r * H, one shared slice (the launcher checks both)
+    const bool has_sh = ca.Ysh != nullptr;
+    float wv[kMaxK];
+#pragma unroll
+    for (int k = 0; k < kMaxK; ++k) wv[k] = k < ca.top_k ? ca.w[k] : 0.0f;
+    const float sc = has_sh && ca.sscale ? ca.sscale[0] : 1.0f;
+    float4 yq[VPT][kMaxK], sq4[VPT];
+    const float4* Y4 = reinterpret_cast<const float4*>(ca.Y);
+    const float4* S4 = reinterpret_cast<const float4*>(ca.Ysh);
+#pragma unroll
+    for (int u = 0; u < VPT; ++u) {
+      const int i = tid + u * kThreads;
+#pragma unroll
+      for (int k = 0; k < kMaxK; ++k)
+        yq[u][k] = i < n4 && k < ca.top_k ? Y4[(size_t)k * n4 + i] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      sq4[u] = i < n4 && has_sh ? S4[i] : make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    }
+#pragma unroll
+    for (int u = 0; u < VPT; ++u) {
+      const int i = tid + u * kThreads;
+      if (i >= n4) continue;
+      float hv[4] = {r[u].x, r[u].y, r[u].z, r[u].w};
+      bf16_t yb[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        float yv[kMaxK], sv[kSplitRegs];
+#pragma unroll
+        for (int k = 0; k < kMaxK; ++k) yv[k] = c == 0 ? yq[u][k].x : c == 1 ? yq[u][k].y : c == 2 ? yq[u][k].z : yq[u][k].w;
+        sv[0] = c == 0 ? sq4[u].x : c == 1 ? sq4[u].y : c == 2 ? sq4[u].z : sq4[u].w;
+#pragma unroll
+        for (int k = 1; k < kSplitRegs; ++k) sv[k] = 0.0f;
+        const float y = combine_terms(wv, yv, ca.top_k, has_sh, sv, 1, sc, [](float v) { return v; });
+        yb[c] = f32_to_bf16(y);
+        hv[c] += Elem<bf16_t>::quant(y);
+      }
+      r[u] = make_float4(hv[0], hv[1], hv[2], hv[3]);
+      *reinterpret_cast<float4*>(&hs[4 * i]) = r[u];
+      if (blockIdx.x == 0)
+        *reinterpret_cast<uint2*>(static_cast<bf16_t*>(ca.y) + 4 * (size_t)i) =
+            make_uint2((uint32_t)yb[0] | ((uint32_t)yb[1] << 16), (uint32_t)yb[2] | ((uint32_t)yb[3] << 16));
+    }
   }
   float sq = 0.0f;
 #pragma unroll
@@ -786,7 +851,8 @@ __global__ __launch_bounds__(kThreads) void k_rows_gemv_norm(RowsArgs a, const f
   acc = wave_sum(acc);
   if (lane == 0) {
     float* o = a.out + a.o_off + row;
-    *o = add_src ? add_src[row] + acc : acc;
+    if constexpr (CMB) *o = hs[row] + acc;
+    else *o = add_src ? add_src[row] + acc : acc;
   }
 }
 
@@ -1029,17 +1095,20 @@ void launch_combine_residual(const CombineArgs& a, float* h, int T, int dtype, h
   else k_combine_residual<float><<<grid, kThreads, 0, s>>>(a, h);
 }
 
-template <int VPT>
+template <int VPT, bool CMB>
 static void rows_norm_launch(const RowsArgs& a, int ntot, int pieces, const float* h, const float* add_src,
-                             bf16_t* x_out, hipStream_t s) {
+                             bf16_t* x_out, const CombineArgs& ca, hipStream_t s) {
   const dim3 grid((ntot + kWaves - 1) / kWaves);
-  if (pieces <= kWave) k_rows_gemv_norm<VPT, 1><<<grid, kThreads, 0, s>>>(a, h, 1e-6f, add_src, x_out);
-  else if (pieces <= 2 * kWave) k_rows_gemv_norm<VPT, 2><<<grid, kThreads, 0, s>>>(a, h, 1e-6f, add_src, x_out);
-  else if (pieces <= 4 * kWave) k_rows_gemv_norm<VPT, 4><<<grid, kThreads, 0, s>>>(a, h, 1e-6f, add_src, x_out);
-  else k_rows_gemv_norm<VPT, 8><<<grid, kThreads, 0, s>>>(a, h, 1e-6f, add_src, x_out);
+  if (pieces <= kWave) k_rows_gemv_norm<VPT, 1, CMB><<<grid, kThreads, 0, s>>>(a, h, 1e-6f, add_src, x_out, ca);
+  else if (pieces <= 2 * kWave)
+    k_rows_gemv_norm<VPT, 2, CMB><<<grid, kThreads, 0, s>>>(a, h, 1e-6f, add_src, x_out, ca);
+  else if (pieces <= 4 * kWave)
+    k_rows_gemv_norm<VPT, 4, CMB><<<grid, kThreads, 0, s>>>(a, h, 1e-6f, add_src, x_out, ca);
+  else k_rows_gemv_norm<VPT, 8, CMB><<<grid, kThreads, 0, s>>>(a, h, 1e-6f, add_src, x_out, ca);
 }
 
-bool launch_rows_gemv_norm(const RowsArgs& a, const float* h, const float* add_src, void* x_out, hipStream_t s) {
+bool launch_rows_gemv_norm(const RowsArgs& a, const float* h, const float* add_src, void* x_out, hipStream_t s,
+                           const CombineArgs* ca) {
   // exactly the cases where the separate kernels take their register paths
   // (launch_rmsnorm_quant and rows_dispatch), so the results agree bit for bit
   const int ntot = a.nrows[0] + a.nrows[1] + a.nrows[2];
@@ -1049,11 +1118,24 @@ bool launch_rows_gemv_norm(const RowsArgs& a, const float* h, const float* add_s
             (!x_out || al16(x_out));
   for (int i = 0; i < 3; ++i)
     if (a.nrows[i] > 0) ok = ok && al16(a.w[i]);
+  // the combine folded in: bf16 y, one shared slice, the token held in at most
+  // two float4 pieces per thread (its Y rows in registers)
+  if (ca)
+    ok = ok && n4 <= 2 * kThreads && ca->hidden == H && ca->top_k >= 1 && ca->top_k <= kMaxK && al16(ca->Y) &&
+         (!ca->Ysh || (ca->ysh_split == 1 && al16(ca->Ysh))) && reinterpret_cast<uintptr_t>(ca->y) % 8 == 0;
   if (!ok) return false;
   bf16_t* xo = static_cast<bf16_t*>(x_out);
-  if (n4 <= kThreads) rows_norm_launch<1>(a, ntot, pieces, h, add_src, xo, s);
-  else if (n4 <= 2 * kThreads) rows_norm_launch<2>(a, ntot, pieces, h, add_src, xo, s);
-  else rows_norm_launch<4>(a, ntot, pieces, h, add_src, xo, s);
+  const CombineArgs none{};
+  if (ca) {
+    if (n4 <= kThreads) rows_norm_launch<1, true>(a, ntot, pieces, h, add_src, xo, *ca, s);
+    else rows_norm_launch<2, true>(a, ntot, pieces, h, add_src, xo, *ca, s);
+  } else if (n4 <= kThreads) {
+    rows_norm_launch<1, false>(a, ntot, pieces, h, add_src, xo, none, s);
+  } else if (n4 <= 2 * kThreads) {
+    rows_norm_launch<2, false>(a, ntot, pieces, h, add_src, xo, none, s);
+  } else {
+    rows_norm_launch<4, false>(a, ntot, pieces, h, add_src, xo, none, s);
+  }
   return true;
 }
 

@@ -247,6 +247,11 @@ struct promoe_ctx {
   float* fuse_h = nullptr;
   const float* x_from_h = nullptr;
   float* d_h2 = nullptr;  // second residual buffer of the batch-1 layer loop
+  // defer_combine: the FFN call leaves its combine (into fuse_h) pending for
+  // the next layer's attention GEMV to fold in
+  bool defer_combine = false, has_pending = false;
+  CombineArgs pending{};
+  float* pending_h = nullptr;
   // first predictor rows computed by a route's gate launch (layer, input, T)
   int pred_rows_layer = -1;
   const void* pred_rows_x = nullptr;
@@ -1936,8 +1941,16 @@ static int expert_ffn_run(promoe_ctx* c, int layer, int T, const float* d_w, con
   ca.y = d_y;
   ca.hidden = c->H;
   ca.top_k = c->K;
-  if (c->fuse_h) launch_combine_residual(ca, c->fuse_h, T, c->dt, s);
-  else launch_combine(ca, T, c->dt, s);
+  if (c->fuse_h && c->defer_combine) {
+    // the layer loop folds this combine into the next layer's first kernel
+    c->pending = ca;
+    c->pending_h = c->fuse_h;
+    c->has_pending = true;
+  } else if (c->fuse_h) {
+    launch_combine_residual(ca, c->fuse_h, T, c->dt, s);
+  } else {
+    launch_combine(ca, T, c->dt, s);
+  }
   LAUNCHCHK("combine");
   // a prediction the route launched on the side stream: later work on s follows it
   HIPCHK(pred_join(c, s));
@@ -2080,6 +2093,13 @@ int promoe_stack_step(promoe_ctx* c, float* d_h, int T, void* d_x, void* d_y, in
   const bool fold = T == 1 && c->dt == PROMOE_BF16 && !(predict && c->D == 0);
   float* hb[2] = {d_h, c->d_h2};
   int cur = 0;
+  // a pending combine, launched on its own (adding into its residual buffer)
+  auto flush_combine = [&]() {
+    if (!c->has_pending) return;
+    launch_combine_residual(c->pending, c->pending_h, T, c->dt, s);
+    c->has_pending = false;
+  };
+  c->has_pending = false;
   for (int l = 0; l < c->L; ++l) {
     if (fold) {
       c->last_stream = s;
@@ -2092,14 +2112,20 @@ int promoe_stack_step(promoe_ctx* c, float* d_h, int T, void* d_x, void* d_y, in
         a.T = T;
         a.out = hb[cur ^ 1];
         a.ldo = c->H;
-        if (launch_rows_gemv_norm(a, hb[cur], hb[cur], nullptr, s)) {
+        // the previous layer's combine folded in when it is pending on hb[cur]
+        const bool cmb = c->has_pending && c->pending_h == hb[cur];
+        if (!cmb) flush_combine();
+        if (launch_rows_gemv_norm(a, hb[cur], hb[cur], nullptr, s, cmb ? &c->pending : nullptr)) {
           LAUNCHCHK("attn surrogate");
           cur ^= 1;
+          c->has_pending = false;
         } else {
+          flush_combine();
           if ((rc = promoe_attn_surrogate(c, l, hb[cur], T, d_x, stream))) return rc;
           x_ready = true;
         }
       }
+      flush_combine();
       if (!x_ready) c->x_from_h = hb[cur];
     } else if ((rc = promoe_attn_surrogate(c, l, d_h, T, d_x, stream))) {
       return rc;
@@ -2112,12 +2138,19 @@ int promoe_stack_step(promoe_ctx* c, float* d_h, int T, void* d_x, void* d_y, in
     }
     c->x_from_h = nullptr;
     if (rc) return rc;
-    // the combine also does the residual add
+    // the combine also does the residual add; with a next layer whose
+    // attention GEMV can fold it in, it is left pending for that launch
     c->fuse_h = hb[cur];
+    c->defer_combine = fold && l + 1 < c->L && c->lw[l + 1].attn != nullptr;
     rc = promoe_expert_ffn(c, l, d_x, T, d_ids, d_w, d_shared_scale, d_y, stream);
     c->fuse_h = nullptr;
-    if (rc) return rc;
+    c->defer_combine = false;
+    if (rc) {
+      c->has_pending = false;
+      return rc;
+    }
   }
+  flush_combine();
   if (cur) HIPCHK(hipMemcpyAsync(d_h, c->d_h2, sizeof(float) * (size_t)T * c->H, hipMemcpyDeviceToDevice, s));
   return PROMOE_OK;
 }
