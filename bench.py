@@ -83,10 +83,12 @@ def read_traffic(kernel):
     missing or was taken on a different kernel source."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "traffic_counters.txt")
-    src = os.path.join(ROOT, "paper_2410_22134_amd", "csrc", "kernels_gemv.hip")
+    csrc = os.path.join(ROOT, "paper_2410_22134_amd", "csrc")
     if not os.path.exists(path):
         return None, None
-    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    # the GEMV kernels' source and the device helpers they inline
+    src = b"".join(open(os.path.join(csrc, f), "rb").read() for f in ("kernels_gemv.hip", "common.hpp"))
+    digest = hashlib.sha256(src).hexdigest()[:16]
     for line in open(path):
         f = line.split()
         if len(f) >= 4 and f[0] == "traffic" and f[1] == kernel:

@@ -52,11 +52,6 @@ __device__ __forceinline__ void unpack16(const uint4& c, float (&w)[4]) {
 __device__ __forceinline__ float silu(float u) { return u / (1.0f + expf(-u)); }
 
 // ---------------------------------------------------------------- wave ops
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
-}
 // Wave-wide max / min through DPP row operations (no LDS round trips): quad
 // permutations and row rotations reduce each row of 16 lanes, two row
 // broadcasts carry rows 0-2 into row 3, and lane 63's result is read out as a
@@ -123,6 +118,24 @@ __device__ __forceinline__ float wave_max(float v) {
   t = __uint_as_float(dpp_u32<kDppRowRor8, 0xf>(__float_as_uint(v))); v = fmaxf(v, t);
   t = __uint_as_float(dpp_u32<kDppRowBcast15, 0xa>(__float_as_uint(v))); v = fmaxf(v, t);
   t = __uint_as_float(dpp_u32<kDppRowBcast31, 0xc>(__float_as_uint(v))); v = fmaxf(v, t);
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+// Wave-wide sum in a fixed order: quads, then pairs of quads, then the whole
+// row of 16 (row rotations), then rows 0+1 into row 1 and rows 0..3 into row 3
+// (row broadcasts, lanes outside the row mask adding 0); lane 63's sum is
+// returned to every lane, so all lanes hold the same bits.  The whole wave
+// must be active.
+template <int kCtrl, int kRowMask>
+__device__ __forceinline__ float dpp_f32_or0(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), kCtrl, kRowMask, 0xf, false));
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  v += dpp_f32_or0<kDppQuadXor1, 0xf>(v);
+  v += dpp_f32_or0<kDppQuadXor2, 0xf>(v);
+  v += dpp_f32_or0<kDppRowRor4, 0xf>(v);
+  v += dpp_f32_or0<kDppRowRor8, 0xf>(v);
+  v += dpp_f32_or0<kDppRowBcast15, 0xa>(v);
+  v += dpp_f32_or0<kDppRowBcast31, 0xc>(v);
   return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
 }
 // Value of lane j (j wave-uniform) as a scalar; v_readlane ignores EXEC.

@@ -53,11 +53,13 @@ def test_prediction_metrics():
 
 
 def test_traffic_summary_is_tied_to_the_kernel_source():
-    # the summary's figures are used only while the GEMV source still hashes to
-    # the digest recorded with them; a changed kernel reports no traffic
+    # the summary's figures are used only while the GEMV source (and the device
+    # helpers it inlines) still hashes to the digest recorded with them; a
+    # changed kernel reports no traffic
     import hashlib
-    src = os.path.join(ROOT, "paper_2410_22134_amd", "csrc", "kernels_gemv.hip")
-    digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    csrc = os.path.join(ROOT, "paper_2410_22134_amd", "csrc")
+    src = b"".join(open(os.path.join(csrc, f), "rb").read() for f in ("kernels_gemv.hip", "common.hpp"))
+    digest = hashlib.sha256(src).hexdigest()[:16]
     line = [l.split() for l in open(os.path.join(ROOT, "profiles", "traffic_counters.txt"))
             if l.startswith("traffic k_ffn_gateup")][0]
     traffic, ratio = bench.read_traffic("k_ffn_gateup")
