@@ -168,7 +168,7 @@ struct PredictPlanArgs {
   int32_t* pred_ids;    // [T x k] out
 };
 void launch_predict_plan(const PredictPlanArgs& p, hipStream_t s);
-// launch_route_plan with the prediction of predict_plan as a second block
+// launch_route_plan with the prediction of predict_plan in blocks 1 .. pred_blocks(E, Ph)
 void launch_route_plan_predict(const TopkArgs& tk, const PlanArgs& a, const PredictPlanArgs& p, hipStream_t s);
 
 // Expand 4-bit experts into dense bf16 [Wg | Wu | Wd] copies (the MFMA GEMM's

@@ -2,10 +2,10 @@
 //
 //  * k_topk          -- per token one wave, one lane per expert (E <= 64):
 //                       softmax and top-k by (logit desc, id asc) from k rounds
-//                       of a wave max over 64-bit keys (order-preserving logit
-//                       bits, then 63 - id), renormalised weights, the shared
-//                       expert's sigmoid gate.  Used by the router and, ids
-//                       only, by the predictor.
+//                       of a DPP wave max over order-preserving logit bits and a
+//                       ballot of the lanes holding it (lowest id first),
+//                       renormalised weights, the shared expert's sigmoid gate.
+//                       Used by the router and, ids only, by the predictor.
 //  * k_plan_spec     -- speculative plan of a target layer (Alg. 2
 //                       PushPredictedExperts): integer vote over the tokens'
 //                       predicted ids, then the LRU plan: the list's resident
@@ -20,8 +20,10 @@
 // Both plans run in one workgroup: the counting phases use all 256 threads,
 // the sequential LRU walk runs in wave 0 with one lane per slot (for slot
 // state) and one lane per expert (for slot_of), so every victim search is one
-// wave-wide argmin.  The plans write a record into host-mapped memory for the
-// copy scheduler.
+// wave-wide argmin and every lookup one scalar lane read.  The plans write a
+// record into host-mapped memory for the copy scheduler.  k_predict_plan and
+// k_route_plan_predict spread the predictor's second layer over several
+// blocks, the last of which to finish runs the top-k and the spec plan.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -664,10 +666,10 @@ __global__ __launch_bounds__(256) void k_route_plan(TopkArgs tk, PlanArgs a) {
   plan_precise_body(a, ids_l, sh, &ps);
 }
 
-// The same, with the layer's prediction as a second block: its second layer,
-// top-k and the spec plan of the target layer (disjoint cache state; the plan
-// records are the route's and the prediction's), so the prediction needs no
-// launch or stream of its own.
+// The same, with the layer's prediction in blocks 1 .. pred_blocks(E, Ph): its
+// second layer, top-k and the spec plan of the target layer (disjoint cache
+// state; the plan records are the route's and the prediction's), so the
+// prediction needs no launch or stream of its own.
 union RoutePredictLds {
   struct {
     int32_t ids_l[kFusedRouteMaxPairs];
