@@ -183,7 +183,10 @@ typedef struct promoe_stats {
                              on the host: every expert of every layer resident (slots ==
                              experts, each layer's initial cache full), the resident launch
                              covering the step, and no order asked for; their plans are
-                             taken in once complete (stats, sync and later routes) */
+                             taken in once complete (stats, sync and later routes).  At
+                             one token such a route's prediction runs in front of the
+                             row tiles of its resident gate/up launch, which the gate/up
+                             launch timing (k_ms[0]) then includes */
 } promoe_stats;
 
 typedef struct promoe_plan {

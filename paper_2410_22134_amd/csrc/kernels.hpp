@@ -198,6 +198,11 @@ bool launch_rows_gemv_norm(const RowsArgs& a, const float* h, const float* add_s
 // end (hipExtLaunchKernelGGL: kernel execution time, as a profiler sees it).
 void launch_ffn(const FfnArgs& a, int pass, int max_tokens, int dtype, hipStream_t s, hipEvent_t ev0 = nullptr,
                 hipEvent_t ev1 = nullptr);
+// launch_ffn's gate/up pass of a one-token step (dense bf16 experts) with the
+// blocks of launch_predict_plan(p) in front of its row tiles; false, launching
+// nothing, when the step or the prediction is not of that kind.
+bool launch_ffn_gateup_pred(const FfnArgs& a, const PredictPlanArgs& p, int dtype, hipStream_t s,
+                            hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 // Grouped MFMA GEMM (bf16) for the same passes; needs N % 128 == 0 and K % 64 == 0.
 bool gemm_supported(int N, int K);
 int gemm_shared_down_split(int T, int H);  // split-K slices of the shared down GEMM

@@ -22,6 +22,7 @@
 
 #include "common.hpp"
 #include "kernels.hpp"
+#include "plan_device.hpp"
 
 namespace promoe {
 
@@ -172,8 +173,8 @@ struct Job {
 // Everything a block needs from the kernel arguments, read before any branch so
 // the scalar loads issue together.
 template <typename TW>
-__device__ __forceinline__ Job<TW> job_of(const FfnArgs& a, int nrows) {
-  const FfnJob jd = a.jobs[blockIdx.y];
+__device__ __forceinline__ Job<TW> job_of(const FfnArgs& a, int nrows, int by) {
+  const FfnJob jd = a.jobs[by];
   Job<TW> jb;
   jb.pos = jd.pos;
   jb.W = reinterpret_cast<const TW*>(jd.w);
@@ -250,11 +251,12 @@ __device__ __forceinline__ void wave_rows_dot(const TW* const (&rows)[R], const 
 }
 
 // pass 1: act[q][i] = q(silu(Wg[i] . x_t) * (Wu[i] . x_t)) for the wave's RW rows i
+// (row tile bx of job by)
 template <typename TW, int MT, int NCH, int RW>
-__global__ __launch_bounds__(kThreads) void k_ffn_gateup(FfnArgs a) {
+__device__ __forceinline__ void ffn_gateup_body(const FfnArgs& a, int bx, int by) {
   constexpr int R = 2 * RW;
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-  const Job<TW> jb = job_of<TW>(a, -1);
+  const Job<TW> jb = job_of<TW>(a, -1, by);
   const int H = a.hidden, I = jb.I, T = a.T, top_k = a.top_k;
   const int32_t* perm = a.perm;
   void* act_r = a.act;
@@ -265,7 +267,7 @@ __global__ __launch_bounds__(kThreads) void k_ffn_gateup(FfnArgs a) {
                "s"(jb.q0), "s"(jb.q1), "s"(jb.r1), "s"(jb.pos));
   const bool shared = jb.pos == kSharedJob;
   TW* act = reinterpret_cast<TW*>(shared ? act_s : act_r);
-  const int i0 = jb.r0 + (blockIdx.x * kBlockWaves + wave) * RW;
+  const int i0 = jb.r0 + (bx * kBlockWaves + wave) * RW;
   if (i0 >= jb.r1) return;
   const TW* rows[R];
   bool rv[R];
@@ -308,11 +310,35 @@ __global__ __launch_bounds__(kThreads) void k_ffn_gateup(FfnArgs a) {
   }
 }
 
+template <typename TW, int MT, int NCH, int RW>
+__global__ __launch_bounds__(kThreads) void k_ffn_gateup(FfnArgs a) {
+  ffn_gateup_body<TW, MT, NCH, RW>(a, blockIdx.x, blockIdx.y);
+}
+
+// The resident gate/up launch of a batch-1 route whose plan the host does not
+// wait for, carrying that route's prediction: blocks [0, pred_blocks) run the
+// predictor's second layer, top-k and spec plan as k_predict_plan's blocks do
+// (dispatched first, beside the GEMV's row tiles), the rest are the row tiles
+// of k_ffn_gateup<bf16, 1, NCH, 1>, numbered row tile fastest.  The
+// prediction then no longer lengthens the chain of dependent launches.
+template <int NCH>
+__global__ __launch_bounds__(kThreads) void k_ffn_gateup_pred(FfnArgs a, PredictPlanArgs p, int tiles_x) {
+  __shared__ PredictLds<1> L;
+  const int nblk = pred_blocks(p.plan.E, p.Ph);
+  const int b = blockIdx.x;
+  if (b < nblk) {
+    predict_plan_body<1>(p, L, b);
+    return;
+  }
+  const int g = b - nblk;
+  ffn_gateup_body<bf16_t, 1, NCH, 1>(a, g % tiles_x, g / tiles_x);
+}
+
 // pass 2: Y[pair][n] = Wd[n] . act[q] for the wave's RW rows n
 template <typename TW, int MT, int NCH, int RW>
 __global__ __launch_bounds__(kThreads) void k_ffn_down(FfnArgs a) {
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-  const Job<TW> jb = job_of<TW>(a, a.hidden);
+  const Job<TW> jb = job_of<TW>(a, a.hidden, blockIdx.y);
   const int H = a.hidden, I = jb.I;
   const void* act_r = a.act;
   const void* act_s = a.act_sh;
@@ -477,7 +503,7 @@ template <int MT, int RW, int NCH>
 __global__ __launch_bounds__(kThreads) void k_ffn_gateup_q4(FfnArgs a) {
   constexpr int R = 2 * RW;
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-  const Job<bf16_t> jb = job_of<bf16_t>(a, -1);
+  const Job<bf16_t> jb = job_of<bf16_t>(a, -1, blockIdx.y);
   const int H = a.hidden, I = jb.I, T = a.T, top_k = a.top_k;
   const int32_t* perm = a.perm;
   bf16_t* act = reinterpret_cast<bf16_t*>(a.act);
@@ -534,7 +560,7 @@ __global__ __launch_bounds__(kThreads) void k_ffn_gateup_q4(FfnArgs a) {
 template <int MT, int RW, int NCH>
 __global__ __launch_bounds__(kThreads) void k_ffn_down_q4(FfnArgs a) {
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-  const Job<bf16_t> jb = job_of<bf16_t>(a, a.hidden);
+  const Job<bf16_t> jb = job_of<bf16_t>(a, a.hidden, blockIdx.y);
   const int H = a.hidden, I = jb.I;
   const bf16_t* actb = reinterpret_cast<const bf16_t*>(a.act);
   float* Y = a.Y;
@@ -1059,6 +1085,30 @@ static void ffn_dispatch(const FfnArgs& in, int pass, hipStream_t s, hipEvent_t 
     constexpr int NCH = MT == 2 ? 4 : (MT == 4 ? 2 : 1);
     ffn_launch_nch<TW, MT, NCH>(a, pass, grid, s, ev0, ev1);
   }
+}
+
+template <int NCH>
+static void ffn_launch_pred(const FfnArgs& a, const PredictPlanArgs& p, int tiles_x, int grid, hipStream_t s,
+                            hipEvent_t ev0, hipEvent_t ev1) {
+  if (ev0) hipExtLaunchKernelGGL(k_ffn_gateup_pred<NCH>, dim3(grid), dim3(kThreads), 0, s, ev0, ev1, 0, a, p, tiles_x);
+  else k_ffn_gateup_pred<NCH><<<grid, kThreads, 0, s>>>(a, p, tiles_x);
+}
+
+bool launch_ffn_gateup_pred(const FfnArgs& in, const PredictPlanArgs& p, int dtype, hipStream_t s, hipEvent_t ev0,
+                            hipEvent_t ev1) {
+  // batch-1 dense bf16 gate/up rows only, and a prediction of one token
+  if (in.q4 || dtype != 1 || in.T != 1 || p.plan.T != 1 || p.Ph > kFusedPredMaxHidden) return false;
+  FfnArgs a;
+  if (gemv_jobs(in, 0, a) == 0 || a.piece_rows <= 0) return false;
+  const int tiles_x = (a.piece_rows + kBlockWaves - 1) / kBlockWaves;  // one row pair per wave
+  const int grid = pred_blocks(p.plan.E, p.Ph) + tiles_x * a.n_jobs;
+  // as ffn_dispatch<bf16_t, 1> picks NCH for the gate/up pass
+  const int per_lane = (a.hidden / Elem<bf16_t>::kPer16B + kWave - 1) / kWave;
+  if (per_lane <= 1) ffn_launch_pred<1>(a, p, tiles_x, grid, s, ev0, ev1);
+  else if (per_lane == 2) ffn_launch_pred<2>(a, p, tiles_x, grid, s, ev0, ev1);
+  else if (per_lane == 3) ffn_launch_pred<3>(a, p, tiles_x, grid, s, ev0, ev1);
+  else ffn_launch_pred<4>(a, p, tiles_x, grid, s, ev0, ev1);
+  return true;
 }
 
 void launch_ffn(const FfnArgs& a, int pass, int max_tokens, int dtype, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {

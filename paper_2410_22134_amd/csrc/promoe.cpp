@@ -252,6 +252,9 @@ struct promoe_ctx {
   bool defer_combine = false, has_pending = false;
   CombineArgs pending{};
   float* pending_h = nullptr;
+  // a lazy batch-1 route's prediction, to ride in its resident gate/up launch
+  bool ride_pred = false;
+  PredictPlanArgs ride{};
   // first predictor rows computed by a route's gate launch (layer, input, T)
   int pred_rows_layer = -1;
   const void* pred_rows_x = nullptr;
@@ -1341,6 +1344,12 @@ static int route_impl(promoe_ctx* c, int layer, const void* d_x, int T, int32_t*
     publish(c, r);
     return rc;
   }
+  // A lazy one-token route (every expert resident, nobody waiting on the plan)
+  // has its prediction ride in the resident gate/up launch that follows the
+  // plan kernel, beside that launch's row tiles, instead of in the plan
+  // kernel, where the prediction's chain outlasts the plan's and holds back
+  // the expert launches.
+  const bool ride = pred_in_plan && lazy_plan && T == 1 && c->dt == PROMOE_BF16 && !c->q4;
   if (pred_in_plan) {
     PlanArgs pa = plan_args(c, layer, d_ids, T, r);
     pa.host_done = lazy_plan ? 0 : 1;
@@ -1355,7 +1364,13 @@ static int route_impl(promoe_ctx* c, int layer, const void* d_x, int T, int32_t*
     pp.w2 = c->lw[layer].pw2;
     pp.w2_bf16 = c->dt == PROMOE_BF16;
     pp.pred_ids = pids;
-    launch_route_plan_predict(tk, pa, pp, s);
+    if (ride) {
+      launch_route_plan(tk, pa, s);
+      c->ride = pp;
+      c->ride_pred = true;
+    } else {
+      launch_route_plan_predict(tk, pa, pp, s);
+    }
     c->pred_rows_layer = -1;
   } else if ((int64_t)T * c->K <= kFusedRouteMaxPairs) {
     PlanArgs pa = plan_args(c, layer, d_ids, T, r);
@@ -1367,7 +1382,7 @@ static int route_impl(promoe_ctx* c, int layer, const void* d_x, int T, int32_t*
   }
   hipError_t le = hipGetLastError();
   if (le == hipSuccess) le = hipEventRecord(c->rec_ev[r % kRecRing], s);
-  if (r_spec >= 0) {
+  if (r_spec >= 0 && !ride) {
     // the prediction's record completes with the same kernel
     if (le == hipSuccess) le = hipEventRecord(c->rec_ev[r_spec % kRecRing], s);
     publish(c, r_spec);
@@ -1376,6 +1391,22 @@ static int route_impl(promoe_ctx* c, int layer, const void* d_x, int T, int32_t*
   bool early_ffn = false, lazy = false;
   if (le == hipSuccess) {
     rc = early_resident_launch(c, layer, d_x, T, s, r, &early_ffn);
+    if (ride && !rc) {
+      // the resident launch carried the prediction, or it runs on its own now;
+      // its record completes with that launch
+      if (c->ride_pred) launch_predict_plan(c->ride, s);
+      c->ride_pred = false;
+      le = hipGetLastError();
+      if (le == hipSuccess) le = hipEventRecord(c->rec_ev[r_spec % kRecRing], s);
+      if (le != hipSuccess) rc = fail_hip(le, "prediction");
+    }
+  }
+  if (ride) {
+    c->ride_pred = false;
+    publish(c, r_spec);
+    c->lw[target].planned = true;
+  }
+  if (le == hipSuccess) {
     // every expert resident: the resident launch covers the step, and the
     // caller does not ask for the order, so the plan is taken in later
     lazy = !rc && early_ffn && c->all_resident() && !h_order && !n_order;
@@ -1746,7 +1777,10 @@ static int early_resident_launch(promoe_ctx* c, int layer, const void* d_x, int 
         e1 = prof_event(c);
         c->prof_pending.push_back(ProfEntry{e0, e1, pass, 0.0, 0.0});
       }
-      launch_ffn(a, pass, T, c->dt, s, e0, e1);
+      if (pass == 0 && c->ride_pred && launch_ffn_gateup_pred(a, c->ride, c->dt, s, e0, e1))
+        c->ride_pred = false;
+      else
+        launch_ffn(a, pass, T, c->dt, s, e0, e1);
       LAUNCHCHK("early ffn");
     }
   }
