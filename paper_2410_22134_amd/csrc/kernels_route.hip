@@ -207,8 +207,23 @@ __device__ __forceinline__ void plan_precise_body(const PlanArgs& a, const int32
       a.d_npos[0] = n_hit;
       n_pos = np;
     }
+    if (npairs <= kWave) {
+      // every pair in one lane of this wave: its rank among the earlier pairs of
+      // its position (six ballots, as below) and the position's offset from the
+      // lane that holds it; the same places as the tiled loop below
+      const int pos = lane < npairs ? pos_of[ids[lane]] : -1;
+      const int off = __shfl(excl, pos >= 0 ? pos : 0, kWave);
+      uint64_t same = __ballot(pos >= 0);
+#pragma unroll
+      for (int bit = 0; bit < 6; ++bit) {
+        const bool on = pos >= 0 && ((pos >> bit) & 1);
+        const uint64_t bal = __ballot(on);
+        same &= on ? bal : ~bal;
+      }
+      if (pos >= 0) a.d_perm[off + __popcll(same & ((1ull << lane) - 1ull))] = lane;
+    }
   }
-  __syncthreads();
+  if (npairs > kWave) __syncthreads();
 
   // Permutation: pairs in (t, r) order are placed into their position's range,
   // keeping (t, r) order inside a range.  Tiles of 256 pairs; inside a wave the
@@ -218,7 +233,7 @@ __device__ __forceinline__ void plan_precise_body(const PlanArgs& a, const int32
   int (&wave_cnt)[4][kMaxE] = sh.wave_cnt;
   const int wave = tid / kWave;
   const uint64_t lt_mask = (1ull << lane) - 1ull;
-  for (int base = 0; base < npairs; base += 256) {
+  for (int base = 0; npairs > kWave && base < npairs; base += 256) {
     const int i = base + tid;
     const int pos = i < npairs ? pos_of[ids[i]] : -1;
     for (int e = tid; e < 4 * kMaxE; e += 256) (&wave_cnt[0][0])[e] = 0;
