@@ -7,6 +7,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <map>
+#include <random>
 #include <string>
 #include <vector>
 
@@ -505,6 +506,196 @@ void test_high_merge_exhaustive() {
           }
 }
 
+
+// A copy engine with several independent FIFO queues whose copies take random
+// times, moving the bytes when a copy completes: what a reader finds in a slot
+// is what has landed by the time it reads.
+struct DataEngine : CopyEngine {
+  int nq = 2;
+  double now = 0.0;
+  std::mt19937_64 rng;
+  struct Copy {
+    double end;
+    uint8_t* dst;
+    const uint8_t* src;
+    size_t bytes;
+    bool landed;
+  };
+  std::vector<Copy> log;
+  std::vector<double> q_end;
+  std::map<int64_t, double> compute_done;
+  explicit DataEngine(int queues, uint64_t seed) : nq(queues), rng(seed), q_end(queues, 0.0) {}
+  int queues() const override { return nq; }
+  void issue(int64_t seq, void* dst, const void* src, size_t bytes, int64_t after, int queue) override {
+    if ((int64_t)log.size() != seq || queue < 0 || queue >= nq) std::abort();
+    double start = std::max(now, q_end[queue]);
+    if (after >= 0) {
+      auto it = compute_done.find(after);
+      start = std::max(start, it == compute_done.end() ? 1e30 : it->second);
+    }
+    const double end = start + 0.05 + std::uniform_real_distribution<double>(0.0, 1.0)(rng) * (double)bytes / 4.0;
+    q_end[queue] = end;
+    log.push_back({end, static_cast<uint8_t*>(dst), static_cast<const uint8_t*>(src), bytes, false});
+  }
+  // move the bytes of every copy that has completed by time t, in completion order
+  void land(double t) {
+    std::vector<size_t> due;
+    for (size_t i = 0; i < log.size(); ++i)
+      if (!log[i].landed && log[i].end <= t) due.push_back(i);
+    std::sort(due.begin(), due.end(), [&](size_t a, size_t b) {
+      return log[a].end < log[b].end || (log[a].end == log[b].end && a < b);
+    });
+    for (size_t i : due) {
+      std::memcpy(log[i].dst, log[i].src, log[i].bytes);
+      log[i].landed = true;
+    }
+  }
+  bool done(int64_t seq) override {
+    land(now);
+    return log[seq].end <= now;
+  }
+  void wait(int64_t seq) override {
+    now = std::max(now, log[seq].end);
+    land(now);
+  }
+};
+
+// The library's protocol over random plans and timings: speculative plans
+// (assign + push_low), the worker's pumping, and routes that read the layer's
+// routed slots -- at once when no copy into them is pending (the early resident
+// launch), else after the host has purged the layer's low work, issued the
+// rest at high priority and waited, on each queue, for the latest copy
+// ready_seq names (the compute stream's event waits).  Every read must find the
+// bytes of the expert the plan put in the slot, and no copy may land in a slot
+// before a read of its previous contents that the plan ordered first.
+void test_random_protocol() {
+  const int L = 2, C = 3, E = 6;
+  const size_t chunk = 8, sub = 4;
+  for (uint64_t seed = 1; seed <= 300; ++seed) {
+    const int window = 1 + (int)(seed % 2);
+    const size_t merge = seed % 3 == 0 ? 16 : 0;
+    DataEngine eng(1 + (int)(seed % 3 != 1), seed);
+    std::vector<uint8_t> host((size_t)L * E * 3 * chunk), cache((size_t)L * C * 3 * chunk, 0xEE);
+    for (size_t i = 0; i < host.size(); ++i) host[i] = (uint8_t)(i * 7 + 3);
+    Prefetcher pf(L, C, E, chunk, sub, window, cache.data(), &eng, merge);
+    for (int l = 0; l < L; ++l)
+      for (int e = 0; e < E; ++e) pf.set_host(l, e, host.data() + ((size_t)l * E + e) * 3 * chunk);
+    std::vector<std::vector<int>> owner(L, std::vector<int>(C));
+    for (int l = 0; l < L; ++l)
+      for (int s2 = 0; s2 < C; ++s2) {
+        owner[l][s2] = s2;
+        std::memcpy(cache.data() + ((size_t)l * C + s2) * 3 * chunk, pf.host(l, s2), 3 * chunk);
+        pf.mark_resident(l, s2, s2);
+      }
+    std::mt19937_64& rng = eng.rng;
+    auto rnd = [&](int n) { return (int)(rng() % (uint64_t)n); };
+    int64_t tok = 0;
+    double gpu = 0.0;  // the compute stream's clock
+    bool bad = false;
+    auto slot_of = [&](int l, int e) {
+      for (int s2 = 0; s2 < C; ++s2)
+        if (owner[l][s2] == e) return s2;
+      return -1;
+    };
+    auto read = [&](int l, int s2, double t) {
+      eng.land(t);
+      const uint8_t* got = cache.data() + ((size_t)l * C + s2) * 3 * chunk;
+      if (std::memcmp(got, pf.host(l, owner[l][s2]), 3 * chunk) != 0 && !bad) {
+        std::printf("  seed %llu: layer %d slot %d read at %.3f does not hold expert %d\n",
+                    (unsigned long long)seed, l, s2, t, owner[l][s2]);
+        bad = true;
+      }
+    };
+    for (int step = 0; step < 60 && !bad; ++step) {
+      // a speculative plan for a random layer
+      const int lt = rnd(L);
+      std::vector<int> pred;
+      for (int n = 1 + rnd(2); (int)pred.size() < n;) {
+        const int e = rnd(E);
+        if (std::find(pred.begin(), pred.end(), e) == pred.end()) pred.push_back(e);
+      }
+      for (int e : pred) {
+        int s2 = slot_of(lt, e);
+        if (s2 < 0) {
+          std::vector<int> cand;
+          for (int v = 0; v < C; ++v)
+            if (std::find(pred.begin(), pred.end(), owner[lt][v]) == pred.end()) cand.push_back(v);
+          if (cand.empty()) continue;
+          s2 = cand[rnd((int)cand.size())];
+          owner[lt][s2] = e;
+          pf.assign(lt, s2, e);
+        }
+        pf.push_low(lt, s2);
+      }
+      // the worker runs for a while
+      for (int k = rnd(4); k > 0; --k) {
+        pf.pump();
+        eng.now += 0.3 * rnd(4);
+        pf.retire();
+      }
+      // a route of a random layer
+      const int lr = rnd(L);
+      std::vector<int> routed;
+      for (int n = 1 + rnd(2); (int)routed.size() < n;) {
+        const int e = rnd(E);
+        if (std::find(routed.begin(), routed.end(), e) == routed.end()) routed.push_back(e);
+      }
+      pf.retire();
+      std::vector<int> early_slots, late_slots;
+      for (int e : routed) {
+        const int s2 = slot_of(lr, e);
+        if (s2 >= 0 && pf.ready_seq(lr, s2, 2) == -1) early_slots.push_back(s2);
+      }
+      const double t_early = std::max(gpu, eng.now);
+      for (int s2 : early_slots) read(lr, s2, t_early);
+      if (!early_slots.empty()) gpu = t_early + 0.01;
+      pf.purge_low(lr);
+      for (int e : routed) {
+        int s2 = slot_of(lr, e);
+        if (s2 >= 0 && std::find(early_slots.begin(), early_slots.end(), s2) != early_slots.end()) continue;
+        if (s2 < 0) {
+          std::vector<int> cand;
+          for (int v = 0; v < C; ++v) {
+            bool used = false;
+            for (int r2 : routed) used = used || owner[lr][v] == r2;
+            if (!used) cand.push_back(v);
+          }
+          s2 = cand[rnd((int)cand.size())];
+          owner[lr][s2] = e;
+          pf.assign(lr, s2, e);
+        }
+        pf.issue_high(lr, s2);
+        late_slots.push_back(s2);
+      }
+      // the early launch's reads are recorded once the plan is read (after the fills above)
+      if (!early_slots.empty()) {
+        eng.compute_done[tok] = gpu;
+        for (int s2 : early_slots) pf.set_last_read(lr, s2, tok);
+        ++tok;
+      }
+      if (!late_slots.empty()) {
+        std::vector<int64_t> need(eng.nq, -1);
+        for (int s2 : late_slots) {
+          const int64_t n = pf.ready_seq(lr, s2, 2);
+          CHECK(n != -2);
+          const int q = pf.queue_of(lr, s2);
+          need[q] = std::max(need[q], n);
+        }
+        double t = std::max(gpu, eng.now);
+        for (int q = 0; q < eng.nq; ++q)
+          if (need[q] >= 0) t = std::max(t, eng.log[need[q]].end);
+        for (int s2 : late_slots) read(lr, s2, t);
+        gpu = t + 0.01;
+        eng.compute_done[tok] = gpu;
+        for (int s2 : late_slots) pf.set_last_read(lr, s2, tok);
+        ++tok;
+      }
+      eng.now += 0.2 * rnd(3);
+      pf.retire();
+    }
+    CHECK(!bad);
+  }
+}
 }  // namespace
 
 int main(int argc, char** argv) {
@@ -531,6 +722,7 @@ int main(int argc, char** argv) {
   test_capacity_wrap();
   test_high_merge();
   test_high_merge_exhaustive();
+  test_random_protocol();
   std::printf(failures ? "FAILED %d\n" : "ALL OK\n", failures);
   return failures ? 1 : 0;
 }
