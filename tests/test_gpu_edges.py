@@ -30,6 +30,15 @@ def _log(*a):
     print(*a, flush=True)
 
 
+def _step_diff(i, a, b):
+    """What differs between two runs' residuals after step i: the count of
+    unequal elements, the largest difference and the first unequal row."""
+    ne = a != b
+    rows = np.nonzero(ne.any(axis=1))[0] if a.ndim == 2 else np.nonzero(ne)[0]
+    return ("step", i, "unequal", int(ne.sum()), "max_abs", float(np.abs(a - b).max()),
+            "first_row", int(rows[0]) if rows.size else -1)
+
+
 @pytest.mark.parametrize("T", [1, 5, 13, 77, 130])
 def test_ragged_token_counts(T):
     cfg = SMALL
@@ -432,7 +441,7 @@ def test_stack_step_in_one_call(T, lookahead):
             runs.append((hs, plans, [m.ctx.stats(l) for l in range(cfg.n_layers)]))
         (h_a, p_a, s_a), (h_b, p_b, s_b) = runs
         for i, (a, b) in enumerate(zip(h_a, h_b)):
-            assert np.array_equal(a, b), ("step", i)
+            assert np.array_equal(a, b), _step_diff(i, a, b)
         assert p_a == p_b
         for l, (a, b) in enumerate(zip(s_a, s_b)):
             for c in ocache.COUNTERS:
@@ -469,7 +478,7 @@ def test_stack_step_all_resident_lazy_routes(T):
         assert t_a["lazy_routes"] == 0 and t_b["lazy_routes"] == 14 * cfg.n_layers, (t_a["lazy_routes"],
                                                                                      t_b["lazy_routes"])
         for i, (a, b) in enumerate(zip(h_a, h_b)):
-            assert np.array_equal(a, b), ("step", i)
+            assert np.array_equal(a, b), _step_diff(i, a, b)
         assert p_a == p_b
         for l, (a, b) in enumerate(zip(s_a, s_b)):
             for c in ocache.COUNTERS:
